@@ -1,0 +1,130 @@
+/*
+ * gnn.h -- C ABI of libgnn.so, an MI355X (gfx950) implementation of the
+ * interaction-network edge classifier used by GNN-based track finding.
+ *
+ * Paper section 2.1 ("ExaTrkX") places this step in the pipeline: an
+ * interaction network classifies the edges of the hit graph and its per-edge
+ * scores go on to the connected-components step.  Section 2.3 describes the
+ * custom service backend's contract (hits x raw features in); section 1
+ * gives the event scale (about 300k nodes and 1M edges).  This library takes
+ * one hit graph in and returns one score per edge.
+ *
+ * Model (the paper prints no architecture; this is the workload's definition):
+ *   every MLP is two Linear layers, each followed by LayerNorm and ReLU;
+ *   h0 = MLP_node_enc(x);  e0 = MLP_edge_enc([h_src; h_dst]);
+ *   T times: e = MLP_edge([h_src; h_dst; e]);  agg_in(v) = sum of e over
+ *            edges into v; agg_out(v) = sum over edges out of v;
+ *            h = MLP_node([h; agg_in; agg_out]);
+ *   z = w . LNReLU(W [h_src; h_dst; e] + b) + c;  score = sigmoid(z).
+ *
+ * Every pointer argument of gnn_infer* / gnn_debug_* is a DEVICE pointer on
+ * the handle's device, except where noted.  All calls are thread-safe; one
+ * handle may run concurrently on several streams (its weights are read-only
+ * and every call allocates its own stream-ordered workspace).
+ */
+#ifndef GNN_H
+#define GNN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+#define GNN_OK 0
+#define GNN_E_INVALID_ARG (-1) /* null pointer, bad count, bad dims           */
+#define GNN_E_NO_DEVICE (-2)   /* no HIP device visible                        */
+#define GNN_E_OOM (-3)         /* device or host allocation failed             */
+#define GNN_E_INDEX (-4)       /* edge index out of range (validation on)      */
+#define GNN_E_HIP (-5)         /* a HIP runtime call or kernel launch failed   */
+#define GNN_E_UNSUPPORTED (-6) /* dims or device this build does not support   */
+
+/* ---- model description ------------------------------------------------- */
+#define GNN_FP32 0 /* weights and activations fp32                           */
+#define GNN_BF16 1 /* weights and activations bf16, fp32 accumulation, fp32
+                      LayerNorm statistics, fp32 segment sums               */
+
+#define GNN_VALIDATE_INDICES 1u /* check every index is in [0, n_nodes) before
+                                   computing; costs one host synchronisation */
+
+typedef struct gnn_dims {
+  uint32_t struct_size;     /* = sizeof(gnn_dims) (ABI versioning)              */
+  int32_t in_features;      /* F: raw features per node, 1..16 (3 for hits)     */
+  int32_t hidden;           /* H: 64 or 128                                     */
+  int32_t n_iters;          /* T: message-passing iterations, 0..64             */
+  int32_t n_mp_weight_sets; /* 1 = one edge MLP and one node MLP shared by all
+                               iterations; T = one pair per iteration          */
+  int32_t dtype;            /* GNN_FP32 or GNN_BF16                             */
+  float ln_eps;             /* LayerNorm epsilon (1e-5)                         */
+  uint32_t flags;           /* GNN_VALIDATE_INDICES or 0                        */
+} gnn_dims;
+
+typedef struct gnn_handle gnn_handle;
+
+/* Number of floats in the packed weight blob for `dims`, 0 if dims invalid.
+ * Blob order (fp32; W is [out][in] row-major, PyTorch Linear convention):
+ *   node_enc (F->H->H), edge_enc (2H->H->H),
+ *   n_mp_weight_sets x [edge_mlp (3H->H->H), node_mlp (3H->H->H)],
+ *   edge_cls (3H->H->1).
+ * A hidden layer stores W, b, gamma, beta; the classifier's last layer
+ * stores W[1][H] and b[1]. */
+size_t gnn_weight_count(const gnn_dims *dims);
+
+/* Validate dims, convert and upload the HOST fp32 blob `weights` (copied;
+ * the caller may free it on return) to the current HIP device.  Returns NULL
+ * on error (see gnn_last_error): GNN_E_INVALID_ARG for bad dims or NULL
+ * pointers, GNN_E_NO_DEVICE, GNN_E_UNSUPPORTED for a device that is not
+ * gfx950 or dims outside the supported set, GNN_E_OOM. */
+gnn_handle *gnn_create(const float *weights, const gnn_dims *dims);
+
+/* Score every edge of one hit graph (paper section 2.1: one score per edge).
+ *   node_feat   [n_nodes][F] fp32, row-major
+ *   edge_index  [2][n_edges] int32: row 0 = source, row 1 = destination;
+ *               never modified; self-loops and duplicate edges are allowed
+ *   edge_scores [n_edges] fp32 output, sigmoid scores in input edge order
+ * Asynchronous on `stream` (0 = the null stream): inputs must stay valid
+ * and outputs untouched until the stream passes this work.  Results are
+ * bitwise deterministic for a given input.  Returns GNN_OK with no writes
+ * when n_edges == 0; GNN_E_INVALID_ARG for n_nodes == 0 < n_edges, negative
+ * counts, counts above INT32_MAX or NULL pointers.  An index outside
+ * [0, n_nodes) is reported as GNN_E_INDEX when GNN_VALIDATE_INDICES is set;
+ * otherwise it is clamped into range (no fault, meaningless scores). */
+int gnn_infer(gnn_handle *h, const float *node_feat, const int32_t *edge_index,
+              int64_t n_nodes, int64_t n_edges, float *edge_scores, hipStream_t stream);
+
+/* As gnn_infer, writing the pre-sigmoid logits z instead of the scores. */
+int gnn_infer_logits(gnn_handle *h, const float *node_feat, const int32_t *edge_index,
+                     int64_t n_nodes, int64_t n_edges, float *edge_logits,
+                     hipStream_t stream);
+
+/* Waits for the device, then frees everything the handle owns.  NULL-safe. */
+void gnn_destroy(gnn_handle *h);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *gnn_last_error(void);
+
+/* ---- test hooks ---------------------------------------------------------
+ * Destination- and source-sorted CSR of edge_index, as the inference path
+ * builds it: row_ptr_in [n_nodes+1], perm_in [n_edges] (edge ids with
+ * dst == v in ascending id order at row_ptr_in[v] .. row_ptr_in[v+1]-1),
+ * and the same by source.  Any output pointer may be NULL. */
+int gnn_debug_csr(gnn_handle *h, const int32_t *edge_index, int64_t n_nodes, int64_t n_edges,
+                  int32_t *row_ptr_in, int32_t *perm_in, int32_t *row_ptr_out,
+                  int32_t *perm_out, hipStream_t stream);
+
+/* Run the encoders and the first `stop_iter` message-passing iterations and
+ * copy out, as fp32 in input order, h [n_nodes][H] and e [n_edges][H] and,
+ * for stop_iter >= 1, the aggregates of the last iteration run
+ * [n_nodes][H] each.  Any output pointer may be NULL. */
+int gnn_debug_stages(gnn_handle *h, const float *node_feat, const int32_t *edge_index,
+                     int64_t n_nodes, int64_t n_edges, int32_t stop_iter, float *h_out,
+                     float *e_out, float *agg_in_out, float *agg_out_out, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GNN_H */
