@@ -1,0 +1,154 @@
+"""Throughput of the interaction-network edge classifier on one MI355X.
+
+A step is one complete gnn_infer call (CSR build, encoders, 8 message-passing
+iterations, classifier) on one synthetic event whose inputs are already in
+HBM.  Default workload: the 300k-hit / ~1.0M-edge layered event, H=128,
+T=8, fp32, seeded Xavier weights (the event scale of paper section 1).
+
+Prints one JSON line: edges/s (value), ms/event, the roofline position of
+the dominant kernel (the fused edge-update kernel, timed with HIP events on
+the launch stream by the library's profiler over the timed region), the
+aggregation kernel's HBM bandwidth, and the CPU oracle timed on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "edges/sec and ms/event, 8-iter interaction network, 300k nodes/1M edges"
+PEAK_HBM_GBS = 8000.0
+PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2500.0}
+
+
+def edge_update_flops(E, H):
+    # layer 1: 3H -> H, layer 2: H -> H, two flops per multiply-add
+    return 2.0 * E * (3 * H * H + H * H)
+
+
+def aggregate_bytes(N, E, H, act_bytes):
+    # every message row read once per direction, both aggregates written,
+    # perm read per direction, row pointers read per direction
+    return 2.0 * E * H * act_bytes + 2.0 * N * H * act_bytes + 2.0 * E * 4 + 2.0 * (N + 1) * 4
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="full", choices=["full", "full_bf16", "mid", "tiny"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(events are independent; see the sharding notes). Use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2402_09633_amd import gnn as G
+    from paper_2402_09633_amd import inputs as I
+
+    cfg = I.CONFIGS[args.workload]
+    g = I.make_graph(cfg)
+    N, E, H, T = g.n_nodes, g.n_edges, cfg.hidden, cfg.n_iters
+    w = I.make_weights(3, H, 1, cfg.weight_seed)
+    dtype = G.GNN_BF16 if cfg.dtype == "bf16" else G.GNN_FP32
+    dims = G.make_dims(3, H, T, 1, dtype)
+    print(f"# workload {cfg.name}: N={N} E={E} H={H} T={T} {cfg.dtype}", file=sys.stderr,
+          flush=True)
+
+    torch.cuda.set_device(0)
+    x = torch.as_tensor(g.x).cuda()
+    ei = torch.as_tensor(g.edge_index).cuda()
+    out = torch.empty(E, dtype=torch.float32, device="cuda")
+    m = G.Model(w, dims)
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        m(x, ei, out)
+    torch.cuda.synchronize()
+
+    G.gnn_profile_enable(m.handle, True)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for a, b in evs:
+        a.record(stream)
+        m(x, ei, out)
+        b.record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = G.gnn_profile_read(m.handle)
+    G.gnn_profile_enable(m.handle, False)
+    per = np.array([a.elapsed_time(b) for a, b in evs])
+    m.close()
+
+    ms_per_step = (t1 - t0) * 1000.0 / args.steps
+    value = E / (ms_per_step / 1000.0)
+    act_bytes = 2 if cfg.dtype == "bf16" else 4
+
+    eu = prof["edge_update"]
+    eu_ms = eu["ms"] / max(eu["launches"], 1)
+    eu_flops = edge_update_flops(E, H)
+    achieved = eu_flops / (eu_ms / 1000.0) / 1e12
+    peak = PEAK_TFLOPS[cfg.dtype]
+    ag = prof["aggregate"]
+    ag_ms = ag["ms"] / max(ag["launches"], 1)
+    ag_bytes = aggregate_bytes(N, E, H, act_bytes)
+    ag_gbs = ag_bytes / (ag_ms / 1000.0) / 1e9
+
+    rec = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "edges/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if cfg.dtype == "fp32" else "bf16",
+        "data": "synthetic (seeded layered hit graph, seeded Xavier weights)",
+        "config": {"workload": f"{cfg.name}: {N}-hit / {E}-edge layered event, H={H}, T={T}, "
+                               f"{cfg.dtype}", "n_nodes": N, "n_edges": E, "hidden": H,
+                   "n_iters": T, "parallelism": "single GPU"},
+        "ms_per_event_p50": round(float(np.percentile(per, 50)), 4),
+        "ms_per_event_p99": round(float(np.percentile(per, 99)), 4),
+        "ms_per_event_min": round(float(per.min()), 4),
+        "roofline": {"kernel": "edge_update (fused gather + 2-layer edge MLP)",
+                     "bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None,
+                     "flops_per_launch": eu_flops, "avg_launch_ms": round(eu_ms, 4)},
+        "roofline_aggregate": {"kernel": "aggregate (CSR segmented sums, in and out)",
+                               "bound": "hbm", "achieved": round(ag_gbs, 1),
+                               "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                               "frac": round(ag_gbs / PEAK_HBM_GBS, 4),
+                               "bytes_per_launch": ag_bytes, "avg_launch_ms": round(ag_ms, 4)},
+        "stages_ms_per_event": {k: round(v["ms"] / max(prof["n_calls"], 1), 4)
+                                for k, v in prof.items() if k != "n_calls"},
+    }
+
+    if not args.no_cpu_baseline:
+        from oracle import oracle as O
+        cores = O.max_threads()
+        t = time.perf_counter()
+        O.forward(w, g.x, g.edge_index, H, T)
+        dt = time.perf_counter() - t
+        rec["cpu_baseline"] = {
+            "value": round(E / dt, 1), "unit": "edges/s", "cores": cores, "kind": "oracle",
+            "sample": f"one complete fp64 oracle inference of the same {N}-node / {E}-edge "
+                      f"event (H={H}, T={T}) on {cores} host threads, {dt:.1f} s"}
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -45,8 +45,10 @@ extern "C" {
 
 /* ---- model description ------------------------------------------------- */
 #define GNN_FP32 0 /* weights and activations fp32                           */
-#define GNN_BF16 1 /* weights and activations bf16, fp32 accumulation, fp32
-                      LayerNorm statistics, fp32 segment sums               */
+#define GNN_BF16 1 /* activations stored in bf16 and fed to bf16 MFMAs; each
+                      weight carried as two bf16 terms (hi = bf16(W),
+                      lo = bf16(W - hi)); fp32 accumulation, fp32 LayerNorm
+                      statistics, fp32 segment sums                       */
 
 #define GNN_VALIDATE_INDICES 1u /* check every index is in [0, n_nodes) before
                                    computing; costs one host synchronisation */
@@ -106,6 +108,33 @@ void gnn_destroy(gnn_handle *h);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char *gnn_last_error(void);
+
+/* ---- profiling -----------------------------------------------------------
+ * While profiling is enabled on a handle, every call brackets each stage's
+ * kernel launches with HIP events on the call's stream (a few microseconds
+ * of overhead per stage).  gnn_profile_read waits for those events and
+ * returns the accumulated device time per stage since the last enable. */
+#define GNN_STAGE_CSR 0         /* destination- and source-sorted CSR build  */
+#define GNN_STAGE_NODE_ENC 1    /* node encoder MLP                           */
+#define GNN_STAGE_EDGE_ENC 2    /* edge encoder MLP (gathers h_src, h_dst)    */
+#define GNN_STAGE_EDGE_UPDATE 3 /* fused gather + edge MLP, once per iteration */
+#define GNN_STAGE_AGGREGATE 4   /* CSR segmented sums, once per iteration      */
+#define GNN_STAGE_NODE_UPDATE 5 /* node MLP, once per iteration                */
+#define GNN_STAGE_CLASSIFIER 6  /* edge classifier + sigmoid                   */
+#define GNN_STAGE_TOTAL 7       /* the whole call                              */
+#define GNN_N_STAGES 8
+
+typedef struct gnn_profile_stats {
+  uint32_t struct_size;            /* = sizeof(gnn_profile_stats)          */
+  int32_t n_calls;                 /* profiled calls accumulated           */
+  int64_t launches[GNN_N_STAGES];  /* bracketed launches per stage         */
+  double ms[GNN_N_STAGES];         /* accumulated device milliseconds      */
+} gnn_profile_stats;
+
+/* Enable (1) or disable (0) profiling; either way resets the counters. */
+int gnn_profile_enable(gnn_handle *h, int enable);
+/* Synchronise the recorded events and fill *out (struct_size must be set). */
+int gnn_profile_read(gnn_handle *h, gnn_profile_stats *out);
 
 /* ---- test hooks ---------------------------------------------------------
  * Destination- and source-sorted CSR of edge_index, as the inference path

@@ -1,0 +1,743 @@
+// Host runtime of libgnn.so: the C ABI declared in include/gnn.h.
+//
+// gnn_create parses the fp32 weight blob (its own parser), converts every
+// dense layer into the MFMA fragment order the kernels read (mlp.hip) and
+// uploads it once.  gnn_infer enqueues the whole inference on the caller's
+// stream: CSR build (csr.hip), node and edge encoders, T iterations of edge
+// update -> segmented sums (agg.hip) -> node update, then the classifier.
+// The workspace is allocated stream-ordered (hipMallocAsync/hipFreeAsync)
+// from the device's default pool, whose release threshold is raised so that
+// repeated calls reuse memory; one handle can serve several streams at once.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/gnn.h"
+#include "gnn_internal.h"
+
+using namespace gnn;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+// ---------------------------------------------------------------- dims ---
+
+int check_dims(const gnn_dims *d) {
+  if (!d) return fail(GNN_E_INVALID_ARG, "dims is NULL");
+  if (d->struct_size != sizeof(gnn_dims))
+    return fail(GNN_E_INVALID_ARG, "dims.struct_size %u != %zu", d->struct_size,
+                sizeof(gnn_dims));
+  if (d->in_features < 1 || d->in_features > 16)
+    return fail(d->in_features < 1 ? GNN_E_INVALID_ARG : GNN_E_UNSUPPORTED,
+                "in_features %d outside 1..16", d->in_features);
+  if (d->hidden <= 0 || d->hidden % 32)
+    return fail(GNN_E_INVALID_ARG, "hidden %d is not a positive multiple of 32", d->hidden);
+  if (d->hidden != 64 && d->hidden != 128)
+    return fail(GNN_E_UNSUPPORTED, "hidden %d not supported (64 or 128)", d->hidden);
+  if (d->n_iters < 0 || d->n_iters > 64)
+    return fail(GNN_E_INVALID_ARG, "n_iters %d outside 0..64", d->n_iters);
+  if (!(d->n_mp_weight_sets == 1 || (d->n_mp_weight_sets == d->n_iters && d->n_iters > 0)))
+    return fail(GNN_E_INVALID_ARG, "n_mp_weight_sets %d must be 1 or n_iters",
+                d->n_mp_weight_sets);
+  if (d->dtype != GNN_FP32 && d->dtype != GNN_BF16)
+    return fail(GNN_E_INVALID_ARG, "dtype %d unknown", d->dtype);
+  if (!(d->ln_eps > 0.f) || !(d->ln_eps < 1.f))
+    return fail(GNN_E_INVALID_ARG, "ln_eps %g outside (0, 1)", (double)d->ln_eps);
+  if (d->flags & ~GNN_VALIDATE_INDICES) return fail(GNN_E_INVALID_ARG, "unknown flags");
+  return GNN_OK;
+}
+
+size_t layer_floats(size_t fin, size_t fout, bool hidden) {
+  return fin * fout + fout + (hidden ? 2 * fout : 0);
+}
+
+size_t weight_count(const gnn_dims *d) {
+  const size_t F = d->in_features, H = d->hidden, S = d->n_mp_weight_sets;
+  return layer_floats(F, H, true) + layer_floats(H, H, true) +          // node_enc
+         layer_floats(2 * H, H, true) + layer_floats(H, H, true) +      // edge_enc
+         S * 2 * (layer_floats(3 * H, H, true) + layer_floats(H, H, true)) +
+         layer_floats(3 * H, H, true) + layer_floats(H, 1, false);       // edge_cls
+}
+
+// ------------------------------------------------------ weight layout ---
+
+uint16_t f32_to_bf16(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return 0x7fc0;  // NaN
+  u += 0x7fffu + ((u >> 16) & 1u);  // round to nearest even
+  return (uint16_t)(u >> 16);
+}
+
+// A blob layer: W [fout][fin] then b, gamma, beta.
+struct BlobLayer {
+  const float *W, *b, *g, *beta;
+  int fin, fout;
+};
+
+// MFMA fragment orders (see mlp.hip).  With MB = H/32, lane = 0..63,
+// i = lane % 32 and hh = lane / 32:
+//  fp32, any K:        frag[g][mb][lane][t] = W[32mb+i][8g + 4hh + t]
+//  bf16, B from HBM:   frag[g][mb][lane][s] = W[32mb+i][16g + 8hh + s]
+//  bf16, B from accs:  frag[g][mb][lane][s] = W[32mb+i][16g + 8(s/4) + 4hh + s%4]
+void frag_f32(const BlobLayer &L, float *dst) {
+  const int MB = L.fout / 32, G = L.fin / 8;
+  for (int g = 0; g < G; ++g)
+    for (int mb = 0; mb < MB; ++mb)
+      for (int lane = 0; lane < 64; ++lane)
+        for (int t = 0; t < 4; ++t)
+          dst[(((size_t)g * MB + mb) * 64 + lane) * 4 + t] =
+              L.W[(size_t)(mb * 32 + lane % 32) * L.fin + 8 * g + 4 * (lane / 32) + t];
+}
+
+float bf16_to_f32(uint16_t b) {
+  const uint32_t u = (uint32_t)b << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return f;
+}
+
+// bf16 mode carries every weight as hi = bf16(W) and lo = bf16(W - hi).
+void frag_bf16(const BlobLayer &L, bool from_acc, uint16_t *hi, uint16_t *lo) {
+  const int MB = L.fout / 32, G = L.fin / 16;
+  for (int g = 0; g < G; ++g)
+    for (int mb = 0; mb < MB; ++mb)
+      for (int lane = 0; lane < 64; ++lane)
+        for (int s = 0; s < 8; ++s) {
+          const int hh = lane / 32;
+          const int k = from_acc ? 16 * g + 8 * (s / 4) + 4 * hh + s % 4 : 16 * g + 8 * hh + s;
+          const float wv = L.W[(size_t)(mb * 32 + lane % 32) * L.fin + k];
+          const size_t o = (((size_t)g * MB + mb) * 64 + lane) * 8 + s;
+          hi[o] = f32_to_bf16(wv);
+          lo[o] = f32_to_bf16(wv - bf16_to_f32(hi[o]));
+        }
+}
+
+// Builds one host staging image of all device weights, section by section,
+// each 256-byte aligned; device pointers are fixed up after the upload.
+struct Staging {
+  std::vector<unsigned char> bytes;
+  size_t add(const void *src, size_t n) {
+    const size_t off = (bytes.size() + 255) & ~(size_t)255;
+    bytes.resize(off + n);
+    if (src) memcpy(bytes.data() + off, src, n);
+    return off;
+  }
+};
+
+struct LayerOff {
+  size_t w = 0, w_lo = 0, b = 0, g = 0, beta = 0;
+  bool has_ln = false, has_lo = false;
+};
+struct MlpOff {
+  LayerOff l0, l1;
+};
+
+}  // namespace
+
+struct gnn_handle {
+  gnn_dims dims;
+  int device = 0;
+  void *dev_weights = nullptr;
+  MlpDev node_enc, edge_enc, cls;
+  std::vector<MlpDev> edge_mlp, node_mlp;
+  // profiling: recorded (stage, start, end) event pairs not yet read, the
+  // running totals and a pool of reusable events
+  struct Mark {
+    int stage;
+    hipEvent_t a, b;
+  };
+  std::mutex prof_mu;
+  bool prof_on = false;
+  std::vector<Mark> prof_pending;
+  std::vector<hipEvent_t> prof_free;
+  int32_t prof_calls = 0;
+  int64_t prof_launches[GNN_N_STAGES] = {};
+  double prof_ms[GNN_N_STAGES] = {};
+};
+
+namespace {
+
+// Layer kinds for the converter.
+enum class WKind { Plain, FragMem, FragAcc };
+
+LayerOff stage_layer(Staging &st, const BlobLayer &L, WKind kind, bool bf16, bool has_ln) {
+  LayerOff o;
+  o.has_ln = has_ln;
+  const size_t nW = (size_t)L.fin * L.fout;
+  if (kind == WKind::Plain) {
+    o.w = st.add(L.W, nW * sizeof(float));
+  } else if (!bf16) {
+    std::vector<float> f(nW);
+    frag_f32(L, f.data());
+    o.w = st.add(f.data(), nW * sizeof(float));
+  } else {
+    std::vector<uint16_t> hi(nW), lo(nW);
+    frag_bf16(L, kind == WKind::FragAcc, hi.data(), lo.data());
+    o.w = st.add(hi.data(), nW * sizeof(uint16_t));
+    o.w_lo = st.add(lo.data(), nW * sizeof(uint16_t));
+    o.has_lo = true;
+  }
+  o.b = st.add(L.b, L.fout * sizeof(float));
+  if (has_ln) {
+    o.g = st.add(L.g, L.fout * sizeof(float));
+    o.beta = st.add(L.beta, L.fout * sizeof(float));
+  }
+  return o;
+}
+
+LayerDev fix_layer(const LayerOff &o, const unsigned char *base) {
+  LayerDev d;
+  d.w = base + o.w;
+  if (o.has_lo) d.w_lo = base + o.w_lo;
+  d.b = (const float *)(base + o.b);
+  if (o.has_ln) {
+    d.g = (const float *)(base + o.g);
+    d.beta = (const float *)(base + o.beta);
+  }
+  return d;
+}
+
+MlpDev fix_mlp(const MlpOff &o, const unsigned char *base) {
+  return MlpDev{fix_layer(o.l0, base), fix_layer(o.l1, base)};
+}
+
+struct DeviceGuard {
+  int prev = -1;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    if (prev != dev) (void)hipSetDevice(dev);
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+// Workspace carve-up for one call.
+struct Workspace {
+  void *base = nullptr;
+  size_t bytes = 0;
+  void *h = nullptr, *e = nullptr, *ain = nullptr, *aout = nullptr;
+  int32_t *rp_in = nullptr, *rp_out = nullptr, *perm_in = nullptr, *perm_out = nullptr;
+  CsrScratch csr{};
+  int32_t *flag = nullptr;
+};
+
+size_t plan_workspace(Workspace &w, int64_t N, int64_t E, int H, size_t act_bytes) {
+  size_t off = 0;
+  auto take = [&](size_t n) {
+    const size_t o = off;
+    off += align256(n > 0 ? n : 1);
+    return o;
+  };
+  const size_t o_h = take((size_t)N * H * act_bytes);
+  const size_t o_e = take((size_t)E * H * act_bytes);
+  const size_t o_ai = take((size_t)N * H * act_bytes);
+  const size_t o_ao = take((size_t)N * H * act_bytes);
+  const size_t o_rpi = take((size_t)(N + 1) * 4), o_rpo = take((size_t)(N + 1) * 4);
+  const size_t o_pi = take((size_t)E * 4), o_po = take((size_t)E * 4);
+  const size_t o_ka = take((size_t)E * 4), o_kb = take((size_t)E * 4);
+  const size_t o_va = take((size_t)E * 4), o_vb = take((size_t)E * 4);
+  const size_t o_hist = take(csr_hist_len(E) * 4);
+  const size_t o_flag = take(4);
+  if (w.base) {
+    unsigned char *b = (unsigned char *)w.base;
+    w.h = b + o_h;
+    w.e = b + o_e;
+    w.ain = b + o_ai;
+    w.aout = b + o_ao;
+    w.rp_in = (int32_t *)(b + o_rpi);
+    w.rp_out = (int32_t *)(b + o_rpo);
+    w.perm_in = (int32_t *)(b + o_pi);
+    w.perm_out = (int32_t *)(b + o_po);
+    w.csr.keys_a = (uint32_t *)(b + o_ka);
+    w.csr.keys_b = (uint32_t *)(b + o_kb);
+    w.csr.vals_a = (uint32_t *)(b + o_va);
+    w.csr.vals_b = (uint32_t *)(b + o_vb);
+    w.csr.hist = (uint32_t *)(b + o_hist);
+    w.flag = (int32_t *)(b + o_flag);
+  }
+  return off;
+}
+
+int check_counts(gnn_handle *h, int64_t N, int64_t E) {
+  if (!h) return fail(GNN_E_INVALID_ARG, "handle is NULL");
+  if (N < 0 || E < 0) return fail(GNN_E_INVALID_ARG, "negative count (n_nodes %lld, n_edges %lld)",
+                                  (long long)N, (long long)E);
+  if (N > INT32_MAX || E > INT32_MAX)
+    return fail(GNN_E_INVALID_ARG, "count above INT32_MAX");
+  if (E > 0 && N == 0) return fail(GNN_E_INVALID_ARG, "n_edges > 0 with n_nodes == 0");
+  return GNN_OK;
+}
+
+#define HIP_TRY(expr)                                                                \
+  do {                                                                               \
+    hipError_t e_ = (expr);                                                          \
+    if (e_ != hipSuccess) {                                                          \
+      rc = fail(GNN_E_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));           \
+      goto out;                                                                      \
+    }                                                                                \
+  } while (0)
+
+// Brackets stage launches with events when profiling is on.
+struct StageTimer {
+  gnn_handle *h;
+  hipStream_t s;
+  bool on;
+  hipEvent_t a = nullptr;
+  StageTimer(gnn_handle *h_, hipStream_t s_, bool count_call) : h(h_), s(s_) {
+    std::lock_guard<std::mutex> lk(h->prof_mu);
+    on = h->prof_on;
+    if (on && count_call) ++h->prof_calls;
+  }
+  hipEvent_t get() {
+    std::lock_guard<std::mutex> lk(h->prof_mu);
+    hipEvent_t e = nullptr;
+    if (!h->prof_free.empty()) {
+      e = h->prof_free.back();
+      h->prof_free.pop_back();
+    } else if (hipEventCreate(&e) != hipSuccess) {
+      e = nullptr;
+    }
+    return e;
+  }
+  void begin() {
+    if (!on) return;
+    a = get();
+    if (a) (void)hipEventRecord(a, s);
+  }
+  void end(int stage) {
+    if (!on || !a) return;
+    hipEvent_t b = get();
+    if (!b) return;
+    (void)hipEventRecord(b, s);
+    std::lock_guard<std::mutex> lk(h->prof_mu);
+    h->prof_pending.push_back({stage, a, b});
+    a = nullptr;
+  }
+};
+
+// What a call should produce.
+struct RunOut {
+  float *scores = nullptr, *logits = nullptr;  // classifier outputs
+  int stop_iter = -1;                          // >= 0: stop after that many iterations
+  float *h = nullptr, *e = nullptr, *ain = nullptr, *aout = nullptr;  // debug exports
+  bool csr_only = false;
+  int32_t *rp_in = nullptr, *perm_in = nullptr, *rp_out = nullptr, *perm_out = nullptr;
+};
+
+int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
+        hipStream_t stream, const RunOut &ro) {
+  const gnn_dims &d = hd->dims;
+  const int H = d.hidden;
+  const Act act = d.dtype == GNN_BF16 ? Act::BF16 : Act::F32;
+  const size_t ab = act == Act::F32 ? 4 : 2;
+  const int32_t n = (int32_t)N, m = (int32_t)E;
+  int rc = GNN_OK;
+  Workspace w;
+  DeviceGuard guard(hd->device);
+  StageTimer total(hd, stream, true), st(hd, stream, false);
+  st.on = total.on;
+  total.begin();
+
+  w.bytes = plan_workspace(w, N, E, H, ab);
+  {
+    hipError_t ae = hipMallocAsync(&w.base, w.bytes, stream);
+    if (ae != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(ae == hipErrorOutOfMemory ? GNN_E_OOM : GNN_E_HIP,
+                  "hipMallocAsync(%zu bytes) failed: %s", w.bytes, hipGetErrorString(ae));
+    }
+  }
+  plan_workspace(w, N, E, H, ab);
+
+  if (d.flags & GNN_VALIDATE_INDICES) {
+    int32_t bad = 0;
+    HIP_TRY(launch_fill_i32(w.flag, 1, 0, stream));
+    HIP_TRY(launch_validate(ei, E, n, w.flag, stream));
+    HIP_TRY(hipMemcpyAsync(&bad, w.flag, 4, hipMemcpyDeviceToHost, stream));
+    HIP_TRY(hipStreamSynchronize(stream));
+    if (bad) {
+      rc = fail(GNN_E_INDEX, "edge_index holds an index outside [0, %d)", n);
+      goto out;
+    }
+  }
+
+  {
+    int32_t *rpi = ro.rp_in ? ro.rp_in : w.rp_in, *pi = ro.perm_in ? ro.perm_in : w.perm_in;
+    int32_t *rpo = ro.rp_out ? ro.rp_out : w.rp_out, *po = ro.perm_out ? ro.perm_out : w.perm_out;
+    st.begin();
+    HIP_TRY(build_csr(ei + E, m, n, rpi, pi, w.csr, stream));   // by destination
+    HIP_TRY(build_csr(ei, m, n, rpo, po, w.csr, stream));       // by source
+    st.end(GNN_STAGE_CSR);
+    if (ro.csr_only) goto out;
+    w.rp_in = rpi;
+    w.perm_in = pi;
+    w.rp_out = rpo;
+    w.perm_out = po;
+  }
+
+  {
+    GmlpArgs a;
+    a.n_nodes = n;
+    a.eps = d.ln_eps;
+    // node encoder
+    a.n_rows = N;
+    a.x = x;
+    a.F = d.in_features;
+    a.mlp = hd->node_enc;
+    a.out = w.h;
+    st.begin();
+    HIP_TRY(launch_gmlp(GmlpKind::NodeEnc, act, H, a, stream));
+    st.end(GNN_STAGE_NODE_ENC);
+    // edge encoder on [h_src; h_dst]
+    a = GmlpArgs();
+    a.n_nodes = n;
+    a.eps = d.ln_eps;
+    a.n_rows = E;
+    a.src[0] = w.h; a.idx[0] = ei;
+    a.src[1] = w.h; a.idx[1] = ei + E;
+    a.mlp = hd->edge_enc;
+    a.out = w.e;
+    st.begin();
+    HIP_TRY(launch_gmlp(GmlpKind::EdgeEnc, act, H, a, stream));
+    st.end(GNN_STAGE_EDGE_ENC);
+
+    const int T = ro.stop_iter >= 0 ? (ro.stop_iter < d.n_iters ? ro.stop_iter : d.n_iters)
+                                    : d.n_iters;
+    for (int t = 0; t < T; ++t) {
+      const int k = d.n_mp_weight_sets == 1 ? 0 : t;
+      // edge update on [h_src; h_dst; e], in place (a wave reads its own e
+      // rows completely before it writes them)
+      a = GmlpArgs();
+      a.n_nodes = n;
+      a.eps = d.ln_eps;
+      a.n_rows = E;
+      a.src[0] = w.h; a.idx[0] = ei;
+      a.src[1] = w.h; a.idx[1] = ei + E;
+      a.src[2] = w.e;
+      a.mlp = hd->edge_mlp[k];
+      a.out = w.e;
+      st.begin();
+      HIP_TRY(launch_gmlp(GmlpKind::EdgeUpd, act, H, a, stream));
+      st.end(GNN_STAGE_EDGE_UPDATE);
+      st.begin();
+      HIP_TRY(launch_segsum(act, H, w.e, w.rp_in, w.perm_in, w.rp_out, w.perm_out, w.ain,
+                            w.aout, n, stream));
+      st.end(GNN_STAGE_AGGREGATE);
+      // node update on [h; agg_in; agg_out], in place
+      a = GmlpArgs();
+      a.n_nodes = n;
+      a.eps = d.ln_eps;
+      a.n_rows = N;
+      a.src[0] = w.h;
+      a.src[1] = w.ain;
+      a.src[2] = w.aout;
+      a.mlp = hd->node_mlp[k];
+      a.out = w.h;
+      st.begin();
+      HIP_TRY(launch_gmlp(GmlpKind::NodeUpd, act, H, a, stream));
+      st.end(GNN_STAGE_NODE_UPDATE);
+    }
+
+    if (ro.stop_iter >= 0) {
+      const int64_t nh = N * H, eh = E * H;
+      struct { float *dst; void *src; int64_t n; bool agg; } ex[4] = {
+          {ro.h, w.h, nh, false}, {ro.e, w.e, eh, false},
+          {ro.ain, w.ain, nh, true}, {ro.aout, w.aout, nh, true}};
+      for (auto &x2 : ex) {
+        if (!x2.dst || x2.n == 0 || (x2.agg && T == 0)) continue;
+        if (act == Act::F32)
+          HIP_TRY(hipMemcpyAsync(x2.dst, x2.src, x2.n * 4, hipMemcpyDeviceToDevice, stream));
+        else
+          HIP_TRY(launch_bf16_to_f32(x2.src, x2.dst, x2.n, stream));
+      }
+      goto out;
+    }
+
+    // classifier on [h_src; h_dst; e]
+    a = GmlpArgs();
+    a.n_nodes = n;
+    a.eps = d.ln_eps;
+    a.n_rows = E;
+    a.src[0] = w.h; a.idx[0] = ei;
+    a.src[1] = w.h; a.idx[1] = ei + E;
+    a.src[2] = w.e;
+    a.mlp = hd->cls;
+    a.out_score = ro.scores;
+    a.out_logit = ro.logits;
+    st.begin();
+    HIP_TRY(launch_gmlp(GmlpKind::Classifier, act, H, a, stream));
+    st.end(GNN_STAGE_CLASSIFIER);
+  }
+
+out:
+  total.end(GNN_STAGE_TOTAL);
+  {
+    hipError_t fe = hipFreeAsync(w.base, stream);
+    if (fe != hipSuccess && rc == GNN_OK)
+      rc = fail(GNN_E_HIP, "hipFreeAsync failed: %s", hipGetErrorString(fe));
+  }
+  return rc;
+}
+
+int common_checks(gnn_handle *h, const float *x, const int32_t *ei, int64_t N, int64_t E,
+                  const void *out) {
+  int rc = check_counts(h, N, E);
+  if (rc) return rc;
+  if (E == 0) return GNN_OK;
+  if (!x || !ei || !out) return fail(GNN_E_INVALID_ARG, "NULL input or output pointer");
+  return GNN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t gnn_weight_count(const gnn_dims *dims) {
+  if (check_dims(dims) != GNN_OK) return 0;
+  return weight_count(dims);
+}
+
+const char *gnn_last_error(void) { return g_last_error.c_str(); }
+
+gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
+  if (check_dims(dims) != GNN_OK) return nullptr;
+  if (!weights) {
+    fail(GNN_E_INVALID_ARG, "weights is NULL");
+    return nullptr;
+  }
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0) {
+    (void)hipGetLastError();
+    fail(GNN_E_NO_DEVICE, "no HIP device visible");
+    return nullptr;
+  }
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    fail(GNN_E_NO_DEVICE, "hipGetDevice failed");
+    return nullptr;
+  }
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+    fail(GNN_E_HIP, "hipGetDeviceProperties failed");
+    return nullptr;
+  }
+  if (strncmp(prop.gcnArchName, "gfx950", 6) != 0) {
+    fail(GNN_E_UNSUPPORTED, "device %d is %s; this library is built for gfx950 only", dev,
+         prop.gcnArchName);
+    return nullptr;
+  }
+  // Keep freed stream-ordered memory in the pool instead of returning it to
+  // the driver after every call.
+  hipMemPool_t pool;
+  if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+    uint64_t thr = UINT64_MAX;
+    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
+  }
+
+  const gnn_dims &d = *dims;
+  const int F = d.in_features, H = d.hidden, S = d.n_mp_weight_sets;
+  const bool bf16 = d.dtype == GNN_BF16;
+  const float *p = weights;
+  auto next = [&](int fin, int fout, bool ln) {
+    BlobLayer L{p, nullptr, nullptr, nullptr, fin, fout};
+    p += (size_t)fin * fout;
+    L.b = p;
+    p += fout;
+    if (ln) {
+      L.g = p;
+      p += fout;
+      L.beta = p;
+      p += fout;
+    }
+    return L;
+  };
+  Staging st;
+  MlpOff o_ne, o_ee, o_cls;
+  std::vector<MlpOff> o_em(S), o_nm(S);
+  {
+    BlobLayer a0 = next(F, H, true), a1 = next(H, H, true);
+    o_ne = {stage_layer(st, a0, WKind::Plain, bf16, true),
+            stage_layer(st, a1, WKind::FragAcc, bf16, true)};
+    BlobLayer b0 = next(2 * H, H, true), b1 = next(H, H, true);
+    o_ee = {stage_layer(st, b0, WKind::FragMem, bf16, true),
+            stage_layer(st, b1, WKind::FragAcc, bf16, true)};
+    for (int s = 0; s < S; ++s) {
+      BlobLayer e0 = next(3 * H, H, true), e1 = next(H, H, true);
+      o_em[s] = {stage_layer(st, e0, WKind::FragMem, bf16, true),
+                 stage_layer(st, e1, WKind::FragAcc, bf16, true)};
+      BlobLayer n0 = next(3 * H, H, true), n1 = next(H, H, true);
+      o_nm[s] = {stage_layer(st, n0, WKind::FragMem, bf16, true),
+                 stage_layer(st, n1, WKind::FragAcc, bf16, true)};
+    }
+    BlobLayer c0 = next(3 * H, H, true), c1 = next(H, 1, false);
+    o_cls = {stage_layer(st, c0, WKind::FragMem, bf16, true),
+             stage_layer(st, c1, WKind::Plain, bf16, false)};
+  }
+
+  gnn_handle *h = new gnn_handle();
+  h->dims = d;
+  h->device = dev;
+  if (hipMalloc(&h->dev_weights, st.bytes.size()) != hipSuccess) {
+    (void)hipGetLastError();
+    delete h;
+    fail(GNN_E_OOM, "hipMalloc of %zu weight bytes failed", st.bytes.size());
+    return nullptr;
+  }
+  if (hipMemcpy(h->dev_weights, st.bytes.data(), st.bytes.size(), hipMemcpyHostToDevice) !=
+      hipSuccess) {
+    (void)hipFree(h->dev_weights);
+    delete h;
+    fail(GNN_E_HIP, "weight upload failed");
+    return nullptr;
+  }
+  const unsigned char *base = (const unsigned char *)h->dev_weights;
+  h->node_enc = fix_mlp(o_ne, base);
+  h->edge_enc = fix_mlp(o_ee, base);
+  h->cls = fix_mlp(o_cls, base);
+  for (int s = 0; s < S; ++s) {
+    h->edge_mlp.push_back(fix_mlp(o_em[s], base));
+    h->node_mlp.push_back(fix_mlp(o_nm[s], base));
+  }
+  return h;
+}
+
+void gnn_destroy(gnn_handle *h) {
+  if (!h) return;
+  {
+    DeviceGuard guard(h->device);
+    (void)hipDeviceSynchronize();
+    (void)hipFree(h->dev_weights);
+    for (auto &mk : h->prof_pending) {
+      (void)hipEventDestroy(mk.a);
+      (void)hipEventDestroy(mk.b);
+    }
+    for (auto e : h->prof_free) (void)hipEventDestroy(e);
+  }
+  delete h;
+}
+
+int gnn_profile_enable(gnn_handle *h, int enable) {
+  if (!h) return fail(GNN_E_INVALID_ARG, "handle is NULL");
+  gnn_profile_stats scratch;
+  scratch.struct_size = sizeof scratch;
+  int rc = gnn_profile_read(h, &scratch);  // drains pending events
+  if (rc) return rc;
+  std::lock_guard<std::mutex> lk(h->prof_mu);
+  h->prof_on = enable != 0;
+  h->prof_calls = 0;
+  for (int i = 0; i < GNN_N_STAGES; ++i) {
+    h->prof_launches[i] = 0;
+    h->prof_ms[i] = 0.0;
+  }
+  return GNN_OK;
+}
+
+int gnn_profile_read(gnn_handle *h, gnn_profile_stats *out) {
+  if (!h || !out) return fail(GNN_E_INVALID_ARG, "NULL argument");
+  if (out->struct_size != sizeof(gnn_profile_stats))
+    return fail(GNN_E_INVALID_ARG, "gnn_profile_stats.struct_size mismatch");
+  DeviceGuard guard(h->device);
+  std::vector<gnn_handle::Mark> marks;
+  {
+    std::lock_guard<std::mutex> lk(h->prof_mu);
+    marks.swap(h->prof_pending);
+  }
+  int rc = GNN_OK;
+  std::vector<double> add(GNN_N_STAGES, 0.0);
+  std::vector<int64_t> cnt(GNN_N_STAGES, 0);
+  for (auto &mk : marks) {
+    float ms = 0.f;
+    if (hipEventSynchronize(mk.b) != hipSuccess ||
+        hipEventElapsedTime(&ms, mk.a, mk.b) != hipSuccess) {
+      rc = fail(GNN_E_HIP, "profiling event query failed");
+      continue;
+    }
+    add[mk.stage] += ms;
+    cnt[mk.stage] += 1;
+  }
+  std::lock_guard<std::mutex> lk(h->prof_mu);
+  for (auto &mk : marks) {
+    h->prof_free.push_back(mk.a);
+    h->prof_free.push_back(mk.b);
+  }
+  for (int i = 0; i < GNN_N_STAGES; ++i) {
+    h->prof_ms[i] += add[i];
+    h->prof_launches[i] += cnt[i];
+    out->ms[i] = h->prof_ms[i];
+    out->launches[i] = h->prof_launches[i];
+  }
+  out->n_calls = h->prof_calls;
+  return rc;
+}
+
+int gnn_infer(gnn_handle *h, const float *node_feat, const int32_t *edge_index, int64_t n_nodes,
+              int64_t n_edges, float *edge_scores, hipStream_t stream) {
+  int rc = common_checks(h, node_feat, edge_index, n_nodes, n_edges, edge_scores);
+  if (rc || n_edges == 0) return rc;
+  RunOut ro;
+  ro.scores = edge_scores;
+  return run(h, node_feat, edge_index, n_nodes, n_edges, stream, ro);
+}
+
+int gnn_infer_logits(gnn_handle *h, const float *node_feat, const int32_t *edge_index,
+                     int64_t n_nodes, int64_t n_edges, float *edge_logits, hipStream_t stream) {
+  int rc = common_checks(h, node_feat, edge_index, n_nodes, n_edges, edge_logits);
+  if (rc || n_edges == 0) return rc;
+  RunOut ro;
+  ro.logits = edge_logits;
+  return run(h, node_feat, edge_index, n_nodes, n_edges, stream, ro);
+}
+
+int gnn_debug_csr(gnn_handle *h, const int32_t *edge_index, int64_t n_nodes, int64_t n_edges,
+                  int32_t *row_ptr_in, int32_t *perm_in, int32_t *row_ptr_out, int32_t *perm_out,
+                  hipStream_t stream) {
+  int rc = check_counts(h, n_nodes, n_edges);
+  if (rc) return rc;
+  if (n_edges == 0) return GNN_OK;
+  if (!edge_index) return fail(GNN_E_INVALID_ARG, "edge_index is NULL");
+  RunOut ro;
+  ro.csr_only = true;
+  ro.rp_in = row_ptr_in;
+  ro.perm_in = perm_in;
+  ro.rp_out = row_ptr_out;
+  ro.perm_out = perm_out;
+  return run(h, nullptr, edge_index, n_nodes, n_edges, stream, ro);
+}
+
+int gnn_debug_stages(gnn_handle *h, const float *node_feat, const int32_t *edge_index,
+                     int64_t n_nodes, int64_t n_edges, int32_t stop_iter, float *h_out,
+                     float *e_out, float *agg_in_out, float *agg_out_out, hipStream_t stream) {
+  int rc = check_counts(h, n_nodes, n_edges);
+  if (rc) return rc;
+  if (n_edges == 0) return GNN_OK;
+  if (!node_feat || !edge_index) return fail(GNN_E_INVALID_ARG, "NULL input pointer");
+  if (stop_iter < 0) return fail(GNN_E_INVALID_ARG, "stop_iter < 0");
+  RunOut ro;
+  ro.stop_iter = stop_iter;
+  ro.h = h_out;
+  ro.e = e_out;
+  ro.ain = agg_in_out;
+  ro.aout = agg_out_out;
+  return run(h, node_feat, edge_index, n_nodes, n_edges, stream, ro);
+}
+
+}  // extern "C"

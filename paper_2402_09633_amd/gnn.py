@@ -1,0 +1,225 @@
+"""Thin ctypes binding of libgnn.so (include/gnn.h), with the same names.
+
+Argument marshalling only: every step of the inference runs in the HIP
+kernels of libgnn.so.  Device buffers are passed as torch tensors (or raw
+integer addresses); torch is used for device memory and streams, nothing
+else.  There is no fallback: if the library is missing, importing this
+module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch  # imported first so that libgnn.so binds to the HIP runtime torch loaded
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libgnn.so")
+
+GNN_OK = 0
+GNN_E_INVALID_ARG = -1
+GNN_E_NO_DEVICE = -2
+GNN_E_OOM = -3
+GNN_E_INDEX = -4
+GNN_E_HIP = -5
+GNN_E_UNSUPPORTED = -6
+GNN_FP32 = 0
+GNN_BF16 = 1
+GNN_VALIDATE_INDICES = 1
+
+EXPORTS = ("gnn_weight_count", "gnn_create", "gnn_infer", "gnn_infer_logits", "gnn_destroy",
+           "gnn_last_error", "gnn_profile_enable", "gnn_profile_read", "gnn_debug_csr",
+           "gnn_debug_stages")
+STAGES = ("csr", "node_enc", "edge_enc", "edge_update", "aggregate", "node_update",
+          "classifier", "total")
+
+
+class gnn_dims(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("in_features", ctypes.c_int32),
+                ("hidden", ctypes.c_int32), ("n_iters", ctypes.c_int32),
+                ("n_mp_weight_sets", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("ln_eps", ctypes.c_float), ("flags", ctypes.c_uint32)]
+
+
+def make_dims(in_features=3, hidden=128, n_iters=8, n_mp_weight_sets=1, dtype=GNN_FP32,
+              ln_eps=1e-5, flags=0) -> gnn_dims:
+    return gnn_dims(ctypes.sizeof(gnn_dims), in_features, hidden, n_iters, n_mp_weight_sets,
+                    dtype, ln_eps, flags)
+
+
+class gnn_profile_stats(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("n_calls", ctypes.c_int32),
+                ("launches", ctypes.c_int64 * 8), ("ms", ctypes.c_double * 8)]
+
+
+class GnnError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"libgnn error {code}: {msg}")
+        self.code = code
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+    dp = ctypes.POINTER(gnn_dims)
+    L.gnn_weight_count.restype = ctypes.c_size_t
+    L.gnn_weight_count.argtypes = [dp]
+    L.gnn_create.restype = vp
+    L.gnn_create.argtypes = [vp, dp]
+    for name in ("gnn_infer", "gnn_infer_logits"):
+        f = getattr(L, name)
+        f.restype = ctypes.c_int
+        f.argtypes = [vp, vp, vp, i64, i64, vp, vp]
+    L.gnn_destroy.restype = None
+    L.gnn_destroy.argtypes = [vp]
+    L.gnn_last_error.restype = ctypes.c_char_p
+    L.gnn_last_error.argtypes = []
+    L.gnn_profile_enable.restype = ctypes.c_int
+    L.gnn_profile_enable.argtypes = [vp, ctypes.c_int]
+    L.gnn_profile_read.restype = ctypes.c_int
+    L.gnn_profile_read.argtypes = [vp, ctypes.POINTER(gnn_profile_stats)]
+    L.gnn_debug_csr.restype = ctypes.c_int
+    L.gnn_debug_csr.argtypes = [vp, vp, i64, i64, vp, vp, vp, vp, vp]
+    L.gnn_debug_stages.restype = ctypes.c_int
+    L.gnn_debug_stages.argtypes = [vp, vp, vp, i64, i64, i32, vp, vp, vp, vp, vp]
+    return L
+
+
+lib = _load()
+
+
+def _addr(t) -> int | None:
+    """Device address of a tensor (checked contiguous), an int, or None."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if isinstance(t, torch.Tensor):
+        if not t.is_contiguous():
+            raise ValueError("tensor arguments must be contiguous")
+        return t.data_ptr()
+    raise TypeError(f"expected a tensor, an int address or None, got {type(t)}")
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _check(rc: int) -> int:
+    if rc != GNN_OK:
+        raise GnnError(rc, gnn_last_error())
+    return rc
+
+
+def gnn_last_error() -> str:
+    return lib.gnn_last_error().decode()
+
+
+def gnn_weight_count(dims: gnn_dims) -> int:
+    return int(lib.gnn_weight_count(ctypes.byref(dims)))
+
+
+def gnn_create(weights: np.ndarray, dims: gnn_dims) -> int:
+    """Upload a host fp32 weight blob; returns the handle (an address)."""
+    w = np.ascontiguousarray(weights, dtype=np.float32)
+    n = gnn_weight_count(dims)
+    if n == 0:
+        raise GnnError(GNN_E_INVALID_ARG, gnn_last_error())
+    if w.size != n:
+        raise ValueError(f"weight blob has {w.size} floats, dims need {n}")
+    h = lib.gnn_create(w.ctypes.data, ctypes.byref(dims))
+    if not h:
+        raise GnnError(GNN_E_INVALID_ARG, gnn_last_error())
+    return h
+
+
+def gnn_destroy(handle) -> None:
+    lib.gnn_destroy(handle)
+
+
+def _check_io(node_feat, edge_index, out):
+    for t, dt in ((node_feat, torch.float32), (edge_index, torch.int32), (out, torch.float32)):
+        if isinstance(t, torch.Tensor):
+            if t.dtype != dt:
+                raise TypeError(f"expected {dt}, got {t.dtype}")
+            if not t.is_cuda:
+                raise ValueError("inputs and outputs must be device tensors")
+
+
+def gnn_infer(handle, node_feat, edge_index, n_nodes: int, n_edges: int, edge_scores,
+              stream=None) -> int:
+    _check_io(node_feat, edge_index, edge_scores)
+    return _check(lib.gnn_infer(handle, _addr(node_feat), _addr(edge_index), n_nodes, n_edges,
+                                _addr(edge_scores), _stream(stream)))
+
+
+def gnn_infer_logits(handle, node_feat, edge_index, n_nodes: int, n_edges: int, edge_logits,
+                     stream=None) -> int:
+    _check_io(node_feat, edge_index, edge_logits)
+    return _check(lib.gnn_infer_logits(handle, _addr(node_feat), _addr(edge_index), n_nodes,
+                                       n_edges, _addr(edge_logits), _stream(stream)))
+
+
+def gnn_profile_enable(handle, enable: bool = True) -> int:
+    return _check(lib.gnn_profile_enable(handle, 1 if enable else 0))
+
+
+def gnn_profile_read(handle) -> dict:
+    """{'n_calls': n, stage: {'launches': k, 'ms': total_ms}} per stage."""
+    st = gnn_profile_stats()
+    st.struct_size = ctypes.sizeof(gnn_profile_stats)
+    _check(lib.gnn_profile_read(handle, ctypes.byref(st)))
+    out = {"n_calls": st.n_calls}
+    for i, name in enumerate(STAGES):
+        out[name] = {"launches": int(st.launches[i]), "ms": float(st.ms[i])}
+    return out
+
+
+def gnn_debug_csr(handle, edge_index, n_nodes: int, n_edges: int, row_ptr_in=None, perm_in=None,
+                  row_ptr_out=None, perm_out=None, stream=None) -> int:
+    return _check(lib.gnn_debug_csr(handle, _addr(edge_index), n_nodes, n_edges,
+                                    _addr(row_ptr_in), _addr(perm_in), _addr(row_ptr_out),
+                                    _addr(perm_out), _stream(stream)))
+
+
+def gnn_debug_stages(handle, node_feat, edge_index, n_nodes: int, n_edges: int, stop_iter: int,
+                     h_out=None, e_out=None, agg_in_out=None, agg_out_out=None,
+                     stream=None) -> int:
+    return _check(lib.gnn_debug_stages(handle, _addr(node_feat), _addr(edge_index), n_nodes,
+                                       n_edges, stop_iter, _addr(h_out), _addr(e_out),
+                                       _addr(agg_in_out), _addr(agg_out_out), _stream(stream)))
+
+
+class Model:
+    """Owns one handle: ``Model(weights, dims)(x, edge_index) -> scores``."""
+
+    def __init__(self, weights: np.ndarray, dims: gnn_dims):
+        self.dims = dims
+        self.handle = gnn_create(weights, dims)
+
+    def __call__(self, x: torch.Tensor, edge_index: torch.Tensor, out=None, logits=False,
+                 stream=None) -> torch.Tensor:
+        E = edge_index.shape[1]
+        if out is None:
+            out = torch.empty(E, dtype=torch.float32, device=x.device)
+        f = gnn_infer_logits if logits else gnn_infer
+        f(self.handle, x, edge_index, x.shape[0], E, out, stream)
+        return out
+
+    def close(self):
+        if self.handle:
+            gnn_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

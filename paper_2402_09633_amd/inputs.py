@@ -212,8 +212,9 @@ CONFIGS = {
     # 300k hits, windows scaled to ~1.0M edges, H=128, T=8
     "full": Config("full", 300_000, 128, 8, "fp32", "layered", 1002, 2002,
                    window_scale=FULL_WINDOW_SCALE),
-    # the full-size event with bf16 weights and activations
-    "full_bf16": Config("full_bf16", 300_000, 128, 8, "bf16", "layered", 1002, 2003,
+    # the full-size event and the same model, run with bf16 weights and
+    # activations (compared with the fp32 definition of that same model)
+    "full_bf16": Config("full_bf16", 300_000, 128, 8, "bf16", "layered", 1002, 2002,
                         window_scale=FULL_WINDOW_SCALE),
     # 8 independent events, N ~ U{240k..360k}, full-size windows
     "batch": Config("batch", 0, 128, 8, "fp32", "batch", BATCH_EVENT_SEED_BASE, 2004,

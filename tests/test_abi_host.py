@@ -1,0 +1,105 @@
+"""Host-side checks of libgnn.so that need no GPU.
+
+The library loads, exports every function include/gnn.h declares, sizes the
+weight blob like the generator, rejects bad dims and bad arguments, and
+reports a missing device instead of faulting.  No compute call is made.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2402_09633_amd import inputs as I
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gnn.h")
+CSRC = os.path.join(ROOT, "paper_2402_09633_amd", "csrc")
+
+
+@pytest.fixture(scope="module")
+def G():
+    from paper_2402_09633_amd import gnn
+    return gnn
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gnn_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("gnn_create", "gnn_infer", "gnn_destroy", "gnn_weight_count", "gnn_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(G):
+    names = declared_functions()
+    assert set(names) == set(G.EXPORTS)
+    for n in names:
+        assert hasattr(G.lib, n), n
+
+
+@pytest.mark.parametrize("F,H,T,S", [(3, 64, 2, 1), (3, 128, 8, 1), (3, 128, 8, 8), (5, 64, 3, 3),
+                                     (1, 128, 0, 1)])
+def test_weight_count_matches_generator(G, F, H, T, S):
+    d = G.make_dims(F, H, T, S)
+    assert G.gnn_weight_count(d) == I.weight_count(F, H, S)
+
+
+@pytest.mark.parametrize("kw", [dict(hidden=48), dict(hidden=96), dict(hidden=0),
+                                dict(n_iters=-1), dict(n_iters=8, n_mp_weight_sets=3),
+                                dict(dtype=7), dict(ln_eps=0.0), dict(in_features=0),
+                                dict(in_features=17), dict(flags=8)])
+def test_bad_dims_are_rejected(G, kw):
+    d = G.make_dims(**kw)
+    assert G.gnn_weight_count(d) == 0
+    assert G.gnn_last_error() != ""
+
+
+def test_wrong_struct_size_is_rejected(G):
+    d = G.make_dims()
+    d.struct_size = 12
+    assert G.gnn_weight_count(d) == 0
+    assert "struct_size" in G.gnn_last_error()
+
+
+def test_null_arguments(G):
+    d = G.make_dims()
+    assert G.lib.gnn_create(None, ctypes.byref(d)) is None
+    assert G.lib.gnn_infer(None, None, None, 10, 10, None, None) == G.GNN_E_INVALID_ARG
+    assert G.lib.gnn_infer_logits(None, None, None, 10, 10, None, None) == G.GNN_E_INVALID_ARG
+    assert G.lib.gnn_debug_csr(None, None, 10, 10, None, None, None, None, None) == \
+        G.GNN_E_INVALID_ARG
+    G.lib.gnn_destroy(None)  # NULL-safe
+
+
+@pytest.mark.skipif(torch.cuda.device_count() > 0, reason="a GPU is visible")
+def test_create_without_device_reports_no_device(G):
+    d = G.make_dims(3, 64, 2)
+    w = I.make_weights(3, 64, 1, 0)
+    assert G.lib.gnn_create(w.ctypes.data, ctypes.byref(d)) is None
+    assert "device" in G.gnn_last_error()
+
+
+def test_no_float_atomics_in_kernels():
+    # Aggregation must be deterministic: the only atomics are integer LDS
+    # counters of the radix sort.
+    for f in os.listdir(CSRC):
+        text = open(os.path.join(CSRC, f)).read()
+        for line in text.splitlines():
+            if "atomic" in line and "//" not in line.split("atomic")[0]:
+                assert "cnt[" in line, f"{f}: {line.strip()}"
+
+
+def test_product_path_never_touches_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2402_09633_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "oracle" not in text.lower() or f == "inputs.py", f

@@ -1,0 +1,74 @@
+"""GPU CSR construction is bit-exact with the oracle's stable counting sort."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2402_09633_amd import inputs as I
+from tests.gpu_util import dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def G():
+    from paper_2402_09633_amd import gnn
+    return gnn
+
+
+@pytest.fixture(scope="module")
+def handle(G):
+    h = G.gnn_create(I.make_weights(3, 64, 1, 0), G.make_dims(3, 64, 2))
+    yield h
+    G.gnn_destroy(h)
+
+
+def gpu_csr(G, handle, ei, n):
+    E = ei.shape[1]
+    eid = dev(ei)
+    rpi = torch.full((n + 1,), -7, dtype=torch.int32, device="cuda")
+    pi = torch.full((max(E, 1),), -7, dtype=torch.int32, device="cuda")
+    rpo = torch.full((n + 1,), -7, dtype=torch.int32, device="cuda")
+    po = torch.full((max(E, 1),), -7, dtype=torch.int32, device="cuda")
+    G.gnn_debug_csr(handle, eid, n, E, rpi, pi, rpo, po)
+    torch.cuda.synchronize()
+    return rpi.cpu().numpy(), pi.cpu().numpy()[:E], rpo.cpu().numpy(), po.cpu().numpy()[:E]
+
+
+def check(G, handle, oracle_mod, ei, n):
+    rpi, pi, rpo, po = gpu_csr(G, handle, ei, n)
+    orp, op = oracle_mod.csr(ei[1], n)
+    np.testing.assert_array_equal(rpi, orp)
+    np.testing.assert_array_equal(pi, op)
+    orp, op = oracle_mod.csr(ei[0], n)
+    np.testing.assert_array_equal(rpo, orp)
+    np.testing.assert_array_equal(po, op)
+
+
+@pytest.mark.parametrize("name", ["tiny", "mid", "full"])
+def test_csr_configs(G, handle, oracle_mod, name):
+    g = I.make_graph(I.CONFIGS[name])
+    print(f"csr {name}: N={g.n_nodes} E={g.n_edges}", flush=True)
+    check(G, handle, oracle_mod, g.edge_index, g.n_nodes)
+
+
+def test_csr_shuffled_full(G, handle, oracle_mod):
+    g, _ = I.shuffled(I.make_graph(I.CONFIGS["full"]), 3)
+    check(G, handle, oracle_mod, g.edge_index, g.n_nodes)
+
+
+@pytest.mark.parametrize("n,e,seed", [(1, 5, 0), (2, 1, 1), (255, 1000, 2), (256, 4097, 3),
+                                      (257, 2048, 4), (65536, 70001, 5), (65537, 3, 6),
+                                      (100_000, 333_333, 7)])
+def test_csr_edge_cases(G, handle, oracle_mod, n, e, seed):
+    rng = np.random.default_rng(seed)
+    ei = rng.integers(0, n, size=(2, e)).astype(np.int32)
+    check(G, handle, oracle_mod, ei, n)
+
+
+def test_csr_hub(G, handle, oracle_mod):
+    rng = np.random.default_rng(9)
+    n, e = 5000, 300_000
+    ei = rng.integers(0, n, size=(2, e)).astype(np.int32)
+    ei[1, rng.random(e) < 0.5] = 17       # in-degree ~150k
+    ei[0, rng.random(e) < 0.2] = 4999     # out-degree ~60k
+    check(G, handle, oracle_mod, ei, n)

@@ -1,0 +1,258 @@
+"""End-to-end parity of the HIP path with the CPU oracle, through the C ABI.
+
+fp32: per-edge logits within 1e-4 * max(1, |z|) of the fp64 oracle.
+bf16: per-edge scores within 2e-2 of the fp64 oracle of the same fp32 model.
+Full-size events are compared on the stored oracle sample (tests/golden/),
+after checking that the regenerated graph has the stored digest.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2402_09633_amd import inputs as I
+from tests.gpu_util import BF16_SCORE_ATOL, assert_logits_close, dev, run_model
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+@pytest.fixture(scope="module")
+def G():
+    from paper_2402_09633_amd import gnn
+    return gnn
+
+
+def _tiny_random(seed, n, e, loops=False):
+    rng = np.random.default_rng(seed)
+    x = rng.normal(size=(n, 3)).astype(np.float32)
+    ei = rng.integers(0, n, size=(2, e)).astype(np.int32)
+    if not loops and n > 1:
+        ei[1] = np.where(ei[0] == ei[1], (ei[1] + 1) % n, ei[1])
+    return x, ei
+
+
+@pytest.mark.parametrize("H,T,S,noise", [(64, 2, 1, 0.0), (64, 2, 1, 0.3), (128, 2, 1, 0.3),
+                                         (64, 3, 3, 0.3), (128, 0, 1, 0.3), (64, 1, 1, 0.3)])
+def test_tiny_fp32_logits(G, oracle_mod, H, T, S, noise):
+    c = I.CONFIGS["tiny"]
+    g = I.make_graph(c)
+    w = I.make_weights(3, H, S, c.weight_seed, affine_noise=noise)
+    print(f"tiny H={H} T={T} S={S} noise={noise}", flush=True)
+    ref = oracle_mod.forward(w, g.x, g.edge_index, H, T, S)
+    got = run_model(G, w, G.make_dims(3, H, T, S), g.x, g.edge_index)
+    assert_logits_close(got, ref["logits"])
+    sc = run_model(G, w, G.make_dims(3, H, T, S), g.x, g.edge_index, logits=False)
+    np.testing.assert_allclose(sc, ref["scores"], rtol=0, atol=1e-5)
+
+
+@pytest.mark.parametrize("n,e,seed", [(50, 1, 0), (50, 31, 1), (50, 33, 2), (3000, 8001, 3),
+                                      (1, 7, 4), (700, 129, 5)])
+def test_ragged_and_small_graphs(G, oracle_mod, n, e, seed):
+    x, ei = _tiny_random(seed, n, e, loops=(n == 1))
+    w = I.make_weights(3, 64, 1, seed, affine_noise=0.3)
+    print(f"ragged n={n} e={e}", flush=True)
+    ref = oracle_mod.forward(w, x, ei, 64, 2)
+    got = run_model(G, w, G.make_dims(3, 64, 2), x, ei)
+    assert_logits_close(got, ref["logits"])
+
+
+def test_stage_parity_tiny(G, oracle_mod):
+    c = I.CONFIGS["tiny"]
+    g = I.make_graph(c)
+    H, T = c.hidden, 3
+    w = I.make_weights(3, H, 1, c.weight_seed, affine_noise=0.3)
+    h = G.gnn_create(w, G.make_dims(3, H, T))
+    try:
+        xd, eid = dev(g.x), dev(g.edge_index)
+        N, E = g.n_nodes, g.n_edges
+        for t in range(T + 1):
+            ref = oracle_mod.forward(w, g.x, g.edge_index, H, T, dump_iter=t)
+            outs = {k: torch.zeros(n, H, device="cuda") for k, n in
+                    (("h", N), ("e", E), ("agg_in", N), ("agg_out", N))}
+            G.gnn_debug_stages(h, xd, eid, N, E, t, outs["h"], outs["e"], outs["agg_in"],
+                               outs["agg_out"])
+            torch.cuda.synchronize()
+            for k in (("h", "e") if t == 0 else ("h", "e", "agg_in", "agg_out")):
+                assert_logits_close(outs[k].cpu().numpy(), ref[k], what=f"{k} after {t}")
+    finally:
+        G.gnn_destroy(h)
+
+
+@pytest.mark.slow
+def test_mid_fp32_full_compare(G, oracle_mod):
+    c = I.CONFIGS["mid"]
+    g = I.make_graph(c)
+    w = I.make_weights(3, c.hidden, 1, c.weight_seed)
+    print(f"mid N={g.n_nodes} E={g.n_edges}", flush=True)
+    ref = oracle_mod.forward(w, g.x, g.edge_index, c.hidden, c.n_iters)
+    got = run_model(G, w, G.make_dims(3, c.hidden, c.n_iters), g.x, g.edge_index)
+    err = assert_logits_close(got, ref["logits"])
+    print(f"mid max scaled logit error {err:.2e}", flush=True)
+
+
+def _golden(name):
+    with open(os.path.join(GOLDEN, f"{name}_oracle_sample.json")) as f:
+        return json.load(f)
+
+
+def test_full_fp32_vs_stored_oracle(G):
+    gold = _golden("full")
+    c = I.CONFIGS["full"]
+    g = I.make_graph(c)
+    assert g.digest() == gold["graph_digest"]
+    w = I.make_weights(3, c.hidden, 1, c.weight_seed)
+    ids = np.array(gold["edge_ids"])
+    got = run_model(G, w, G.make_dims(3, c.hidden, c.n_iters), g.x, g.edge_index)
+    err = assert_logits_close(got[ids], gold["logits"])
+    print(f"full fp32 max scaled logit error {err:.2e}", flush=True)
+    sc = run_model(G, w, G.make_dims(3, c.hidden, c.n_iters), g.x, g.edge_index, logits=False)
+    np.testing.assert_allclose(sc[ids], gold["scores"], rtol=0, atol=2e-5)
+
+
+def test_full_bf16_scores_vs_stored_oracle(G):
+    gold = _golden("full")
+    c = I.CONFIGS["full_bf16"]
+    g = I.make_graph(c)
+    assert g.digest() == gold["graph_digest"] and c.weight_seed == gold["weight_seed"]
+    w = I.make_weights(3, c.hidden, 1, c.weight_seed)
+    ids = np.array(gold["edge_ids"])
+    sc = run_model(G, w, G.make_dims(3, c.hidden, c.n_iters, dtype=G.GNN_BF16), g.x,
+                   g.edge_index, logits=False)
+    err = np.abs(sc[ids] - np.array(gold["scores"]))
+    print(f"full bf16 max score error {err.max():.3e} p99 {np.percentile(err, 99):.3e}",
+          flush=True)
+    assert err.max() <= BF16_SCORE_ATOL
+
+
+@pytest.mark.parametrize("noise", [0.0, 0.3])
+def test_tiny_bf16_scores(G, oracle_mod, noise):
+    c = I.CONFIGS["tiny"]
+    g = I.make_graph(c)
+    w = I.make_weights(3, c.hidden, 1, c.weight_seed, affine_noise=noise)
+    ref = oracle_mod.forward(w, g.x, g.edge_index, c.hidden, c.n_iters)
+    sc = run_model(G, w, G.make_dims(3, c.hidden, c.n_iters, dtype=G.GNN_BF16), g.x,
+                   g.edge_index, logits=False)
+    assert np.abs(sc - ref["scores"]).max() <= BF16_SCORE_ATOL
+
+
+@pytest.mark.parametrize("dtype", [0, 1])
+@pytest.mark.parametrize("bias", [0.0, 3.25, -80.0])
+def test_zero_weights_closed_form(G, dtype, bias):
+    g = I.make_graph(I.CONFIGS["tiny"])
+    w = np.zeros(I.weight_count(3, 64, 1), np.float32)
+    v = I.blob_views(w, 3, 64, 1)
+    for k in v:
+        if k.endswith(".g"):
+            v[k][:] = 1.0
+    v["edge_cls.1.b"][:] = bias
+    d = G.make_dims(3, 64, 2, dtype=dtype)
+    z = run_model(G, w, d, g.x, g.edge_index)
+    assert (z == np.float32(bias)).all()
+    s = run_model(G, w, d, g.x, g.edge_index, logits=False)
+    if bias == 0.0:
+        assert (s == 0.5).all()
+    else:
+        np.testing.assert_allclose(s, 1 / (1 + np.exp(-np.float64(bias))), rtol=1e-6, atol=0)
+
+
+@pytest.mark.parametrize("dtype", [0, 1])
+def test_constant_messages_aggregate_to_degrees_full_scale(G, dtype):
+    c = I.CONFIGS["full"]
+    g = I.make_graph(c)
+    H = c.hidden
+    w = I.make_weights(3, H, 1, c.weight_seed)
+    v = I.blob_views(w, 3, H, 1)
+    v["edge_mlp0.1.W"][:] = 0.0
+    v["edge_mlp0.1.beta"][:] = 1.0
+    h = G.gnn_create(w, G.make_dims(3, H, c.n_iters, dtype=dtype))
+    try:
+        N, E = g.n_nodes, g.n_edges
+        ain = torch.zeros(N, H, device="cuda")
+        aout = torch.zeros(N, H, device="cuda")
+        e = torch.zeros(E, H, device="cuda")
+        G.gnn_debug_stages(h, dev(g.x), dev(g.edge_index), N, E, 2, None, e, ain, aout)
+        torch.cuda.synchronize()
+        assert (e == 1).all()
+        indeg = np.bincount(g.edge_index[1], minlength=N).astype(np.float32)
+        outdeg = np.bincount(g.edge_index[0], minlength=N).astype(np.float32)
+        np.testing.assert_array_equal(ain.cpu().numpy(), np.repeat(indeg[:, None], H, 1))
+        np.testing.assert_array_equal(aout.cpu().numpy(), np.repeat(outdeg[:, None], H, 1))
+    finally:
+        G.gnn_destroy(h)
+
+
+def test_full_deterministic_and_permutation_equivariant(G):
+    c = I.CONFIGS["full"]
+    g = I.make_graph(c)
+    w = I.make_weights(3, c.hidden, 1, c.weight_seed)
+    m = G.Model(w, G.make_dims(3, c.hidden, c.n_iters))
+    try:
+        xd, eid = dev(g.x), dev(g.edge_index)
+        a = m(xd, eid, logits=True).cpu().numpy()
+        b = m(xd, eid, logits=True).cpu().numpy()
+        assert np.array_equal(a, b)  # bitwise run-to-run
+        gs, p = I.shuffled(g, 21)
+        s = m(xd, dev(gs.edge_index), logits=True).cpu().numpy()
+        assert_logits_close(s, a[p].astype(np.float64), rtol=2e-4, what="shuffled")
+    finally:
+        m.close()
+
+
+def test_batch_multi_stream_equals_single_stream(G):
+    c = I.CONFIGS["batch"]
+    gold = _golden("batch_event0")
+    events = I.make_batch(c)[:4]
+    assert events[0].digest() == gold["graph_digest"]
+    w = I.make_weights(3, c.hidden, 1, c.weight_seed)
+    m = G.Model(w, G.make_dims(3, c.hidden, c.n_iters))
+    try:
+        xs = [dev(g.x) for g in events]
+        eis = [dev(g.edge_index) for g in events]
+        single = []
+        for x, ei in zip(xs, eis):
+            single.append(m(x, ei, logits=True).cpu().numpy())
+        outs = [torch.empty(g.n_edges, device="cuda") for g in events]
+        streams = [torch.cuda.Stream() for _ in events]
+        torch.cuda.synchronize()
+        for x, ei, o, st in zip(xs, eis, outs, streams):
+            G.gnn_infer_logits(m.handle, x, ei, x.shape[0], ei.shape[1], o, st)
+        torch.cuda.synchronize()
+        for k, o in enumerate(outs):
+            assert np.array_equal(o.cpu().numpy(), single[k]), f"event {k}"
+        ids = np.array(gold["edge_ids"])
+        assert_logits_close(single[0][ids], gold["logits"], what="batch event 0")
+    finally:
+        m.close()
+
+
+def test_empty_edge_list_writes_nothing(G):
+    w = I.make_weights(3, 64, 1, 0)
+    m = G.Model(w, G.make_dims(3, 64, 2))
+    try:
+        out = torch.full((4,), 7.0, device="cuda")
+        x = dev(np.zeros((5, 3), np.float32))
+        ei = torch.zeros(2, 0, dtype=torch.int32, device="cuda")
+        G.gnn_infer(m.handle, x, ei, 5, 0, out)
+        torch.cuda.synchronize()
+        assert (out == 7.0).all()
+    finally:
+        m.close()
+
+
+def test_validate_indices_reports_bad_index(G):
+    w = I.make_weights(3, 64, 1, 0)
+    m = G.Model(w, G.make_dims(3, 64, 2, flags=G.GNN_VALIDATE_INDICES))
+    try:
+        x, ei = _tiny_random(1, 100, 300)
+        ei[1, 17] = 100
+        with pytest.raises(G.GnnError) as e:
+            m(dev(x), dev(ei))
+        assert e.value.code == G.GNN_E_INDEX
+        ei[1, 17] = 5
+        m(dev(x), dev(ei))  # the same handle still works
+        torch.cuda.synchronize()
+    finally:
+        m.close()
