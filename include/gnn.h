@@ -52,6 +52,13 @@ extern "C" {
 
 #define GNN_VALIDATE_INDICES 1u /* check every index is in [0, n_nodes) before
                                    computing; costs one host synchronisation */
+#define GNN_LITERAL_GATHER 2u   /* fp32: evaluate the first layer of every edge
+                                   MLP per edge on the gathered [h_src; h_dst; e]
+                                   rows instead of the default regrouping
+                                   (W_s h)[src] + (W_d h)[dst] + W_e e with the
+                                   node projections computed once per node; the
+                                   two agree up to fp32 rounding.  bf16 always
+                                   uses the per-edge form. */
 
 typedef struct gnn_dims {
   uint32_t struct_size;     /* = sizeof(gnn_dims) (ABI versioning)              */
@@ -62,7 +69,7 @@ typedef struct gnn_dims {
                                iterations; T = one pair per iteration          */
   int32_t dtype;            /* GNN_FP32 or GNN_BF16                             */
   float ln_eps;             /* LayerNorm epsilon (1e-5)                         */
-  uint32_t flags;           /* GNN_VALIDATE_INDICES or 0                        */
+  uint32_t flags;           /* GNN_VALIDATE_INDICES | GNN_LITERAL_GATHER or 0   */
 } gnn_dims;
 
 typedef struct gnn_handle gnn_handle;

@@ -27,62 +27,81 @@ __device__ __forceinline__ uint32_t clamp_key(int32_t k, int32_t n) {
   return k < 0 ? 0u : (k >= n ? (uint32_t)(n - 1) : (uint32_t)k);
 }
 
-// Pass 0 reads int32 keys from edge_index (clamped); later passes read the
-// previous pass's uint32 keys.
-__global__ __launch_bounds__(RS_THREADS) void rs_upsweep(const int32_t *__restrict__ keys_i32,
-                                                         const uint32_t *__restrict__ keys_u32,
-                                                         int32_t n, int32_t n_nodes, int shift,
-                                                         uint32_t *__restrict__ hist,
-                                                         int32_t ntiles) {
+// The two sorts of one CSR build (by destination, by source) run side by
+// side: blockIdx.y selects the sort, and each sort has its own slice of the
+// scratch buffers.
+struct SortSet {
+  const int32_t *keys_i32[2];   // pass 0: raw indices (clamped here)
+  const uint32_t *keys_in[2];   // later passes
+  const uint32_t *vals_in[2];   // nullptr in pass 0: the value is the item index
+  uint32_t *keys_out[2];
+  uint32_t *vals_out[2];
+  uint32_t *hist[2];            // [RS_RADIX][ntiles] counts, then offsets
+  uint32_t *totals[2];          // [RS_RADIX] per-digit totals (zeroed beforehand)
+};
+
+__device__ __forceinline__ uint32_t load_key(const SortSet &S, int y, int64_t i, int32_t n_nodes) {
+  return S.keys_i32[y] ? clamp_key(S.keys_i32[y][i], n_nodes) : S.keys_in[y][i];
+}
+
+__global__ __launch_bounds__(RS_THREADS) void rs_upsweep(SortSet S, int32_t n, int32_t n_nodes,
+                                                         int shift, int32_t ntiles) {
   __shared__ uint32_t cnt[RS_RADIX];
+  const int y = blockIdx.y;
   cnt[threadIdx.x] = 0;  // RS_THREADS == RS_RADIX
   __syncthreads();
   const int64_t base = (int64_t)blockIdx.x * RS_TILE;
 #pragma unroll
   for (int it = 0; it < RS_ITEMS; ++it) {
     const int64_t i = base + (int64_t)it * RS_THREADS + threadIdx.x;
-    if (i < n) {
-      const uint32_t k = keys_i32 ? clamp_key(keys_i32[i], n_nodes) : keys_u32[i];
-      atomicAdd(&cnt[(k >> shift) & (RS_RADIX - 1)], 1u);
+    if (i < n) atomicAdd(&cnt[(load_key(S, y, i, n_nodes) >> shift) & (RS_RADIX - 1)], 1u);
+  }
+  __syncthreads();
+  const uint32_t c = cnt[threadIdx.x];
+  S.hist[y][(int64_t)threadIdx.x * ntiles + blockIdx.x] = c;
+  if (c) atomicAdd(&S.totals[y][threadIdx.x], c);
+}
+
+// Block d turns row d of the count matrix into exclusive offsets:
+// offs[d][t] = (items with a smaller digit) + (items with digit d in earlier
+// tiles).  Digit-major order is what makes the sort stable.
+__global__ __launch_bounds__(RS_THREADS) void rs_scan_digit(SortSet S, int32_t ntiles) {
+  __shared__ uint32_t part[RS_THREADS];
+  __shared__ uint32_t carry;
+  const int y = blockIdx.y, d = blockIdx.x, t = threadIdx.x;
+  part[t] = t < d ? S.totals[y][t] : 0u;
+  __syncthreads();
+  for (int off = RS_THREADS / 2; off > 0; off >>= 1) {
+    if (t < off) part[t] += part[t + off];
+    __syncthreads();
+  }
+  if (t == 0) carry = part[0];
+  __syncthreads();
+  uint32_t *row = S.hist[y] + (int64_t)d * ntiles;
+  for (int32_t c0 = 0; c0 < ntiles; c0 += RS_THREADS) {
+    const int32_t i = c0 + t;
+    const uint32_t v = i < ntiles ? row[i] : 0u;
+    part[t] = v;
+    __syncthreads();
+    // Hillis-Steele inclusive scan of this chunk.
+    for (int off = 1; off < RS_THREADS; off <<= 1) {
+      const uint32_t u = t >= off ? part[t - off] : 0u;
+      __syncthreads();
+      part[t] += u;
+      __syncthreads();
     }
-  }
-  __syncthreads();
-  hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = cnt[threadIdx.x];
-}
-
-// Exclusive scan, in place, of `len` counters (digit-major: all tiles of
-// digit 0, then digit 1, ...).  One block; thread t scans a contiguous chunk.
-__global__ __launch_bounds__(1024) void rs_scan(uint32_t *__restrict__ a, int32_t len) {
-  __shared__ uint32_t part[1024];
-  const int t = threadIdx.x;
-  const int chunk = (len + 1023) / 1024;
-  const int beg = min(t * chunk, len), end = min(beg + chunk, len);
-  uint32_t s = 0;
-  for (int i = beg; i < end; ++i) s += a[i];
-  part[t] = s;
-  __syncthreads();
-  // Hillis-Steele inclusive scan over the 1024 partial sums.
-  for (int off = 1; off < 1024; off <<= 1) {
-    const uint32_t v = t >= off ? part[t - off] : 0u;
+    if (i < ntiles) row[i] = carry + part[t] - v;
     __syncthreads();
-    part[t] += v;
+    if (t == RS_THREADS - 1) carry += part[t];
     __syncthreads();
-  }
-  uint32_t run = part[t] - s;
-  for (int i = beg; i < end; ++i) {
-    const uint32_t v = a[i];
-    a[i] = run;
-    run += v;
   }
 }
 
-__global__ __launch_bounds__(RS_THREADS) void rs_scatter(
-    const int32_t *__restrict__ keys_i32, const uint32_t *__restrict__ keys_u32,
-    const uint32_t *__restrict__ vals_in, int32_t n, int32_t n_nodes, int shift,
-    const uint32_t *__restrict__ offs, int32_t ntiles, uint32_t *__restrict__ keys_out,
-    uint32_t *__restrict__ vals_out) {
+__global__ __launch_bounds__(RS_THREADS) void rs_scatter(SortSet S, int32_t n, int32_t n_nodes,
+                                                         int shift, int32_t ntiles) {
   __shared__ uint32_t cnt[RS_WAVES][RS_RADIX];
   __shared__ uint32_t base[RS_WAVES][RS_RADIX];
+  const int y = blockIdx.y;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   for (int i = 0; i < RS_WAVES; ++i) cnt[i][threadIdx.x] = 0;
   __syncthreads();
@@ -96,8 +115,8 @@ __global__ __launch_bounds__(RS_THREADS) void rs_scatter(
     const bool ok = i < n;
     uint32_t k = 0, v = 0;
     if (ok) {
-      k = keys_i32 ? clamp_key(keys_i32[i], n_nodes) : keys_u32[i];
-      v = vals_in ? vals_in[i] : (uint32_t)i;
+      k = load_key(S, y, i, n_nodes);
+      v = S.vals_in[y] ? S.vals_in[y][i] : (uint32_t)i;
     }
     key[it] = k;
     val[it] = v;
@@ -119,7 +138,7 @@ __global__ __launch_bounds__(RS_THREADS) void rs_scatter(
   __syncthreads();
   {
     const int d = threadIdx.x;
-    uint32_t run = offs[(int64_t)d * ntiles + blockIdx.x];
+    uint32_t run = S.hist[y][(int64_t)d * ntiles + blockIdx.x];
 #pragma unroll
     for (int i = 0; i < RS_WAVES; ++i) {
       base[i][d] = run;
@@ -134,27 +153,37 @@ __global__ __launch_bounds__(RS_THREADS) void rs_scatter(
       const uint32_t d = (key[it] >> shift) & (RS_RADIX - 1);
       const uint32_t pos = base[w][d] + pre[it];
       if (pos < (uint32_t)n) {  // always true when the ranks are consistent
-        keys_out[pos] = key[it];
-        vals_out[pos] = val[it];
+        S.keys_out[y][pos] = key[it];
+        S.vals_out[y][pos] = val[it];
       }
     }
   }
 }
 
-// row_ptr[v] = number of sorted keys < v, for v in [0, n_nodes].  Thread p
-// (0 <= p <= n) writes every v with skeys[p-1] < v <= skeys[p].
-__global__ void csr_rowptr(const uint32_t *__restrict__ skeys, int32_t n, int32_t n_nodes,
-                           int32_t *__restrict__ row_ptr) {
-  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (p > n) return;
-  const int64_t lo = p == 0 ? 0 : (int64_t)skeys[p - 1] + 1;
-  const int64_t hi = p == n ? n_nodes : min((int64_t)skeys[p], (int64_t)n_nodes);
-  for (int64_t v = lo; v <= hi; ++v) row_ptr[v] = (int32_t)p;
-}
+// row_ptr[v] = number of sorted keys < v (lower bound), v in [0, n_nodes];
+// also copies the sorted values out as the permutation.
+struct CsrOut {
+  const uint32_t *skeys[2];
+  const uint32_t *svals[2];
+  int32_t *row_ptr[2];
+  int32_t *perm[2];
+};
 
-__global__ void copy_u32(const uint32_t *__restrict__ a, int32_t *__restrict__ b, int32_t n) {
+__global__ void csr_finish(CsrOut O, int32_t n, int32_t n_nodes) {
+  const int y = blockIdx.y;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) b[i] = (int32_t)a[i];
+  if (i <= n_nodes) {
+    const uint32_t v = (uint32_t)i;
+    const uint32_t *k = O.skeys[y];
+    int32_t lo = 0, hi = n;
+    while (lo < hi) {
+      const int32_t mid = (int32_t)(((int64_t)lo + hi) >> 1);
+      if (k[mid] < v) lo = mid + 1;
+      else hi = mid;
+    }
+    O.row_ptr[y][i] = lo;
+  }
+  if (i < n) O.perm[y][i] = (int32_t)O.svals[y][i];
 }
 
 __global__ void validate_idx(const int32_t *__restrict__ ei, int64_t n, int32_t n_nodes,
@@ -184,40 +213,56 @@ size_t csr_hist_len(int64_t n_edges) {
   return (size_t)RS_RADIX * (size_t)((n_edges + RS_TILE - 1) / RS_TILE);
 }
 
-hipError_t build_csr(const int32_t *keys, int32_t n, int32_t n_nodes, int32_t *row_ptr,
-                     int32_t *perm, const CsrScratch &s, hipStream_t stream) {
-  // Number of 8-bit digits needed for keys in [0, n_nodes).
+hipError_t build_csr(const int32_t *edge_index, int32_t n, int32_t n_nodes, int32_t *row_ptr_in,
+                     int32_t *perm_in, int32_t *row_ptr_out, int32_t *perm_out,
+                     const CsrScratch &s, hipStream_t stream) {
+  // Number of 8-bit digits needed for keys in [0, n_nodes); at least one
+  // pass so that the sorted arrays are always written.
   int bits = 0;
   while (bits < 31 && ((int64_t)1 << bits) < (int64_t)n_nodes) ++bits;
-  const int passes = (bits + 7) / 8;
+  const int passes = bits > 0 ? (bits + 7) / 8 : 1;
   const int32_t ntiles = (int32_t)((n + RS_TILE - 1) / RS_TILE);
-  const int32_t len = RS_RADIX * ntiles;
+  const size_t hl = csr_hist_len(n);
+  const dim3 grid(ntiles, 2);
 
-  const uint32_t *kin = nullptr, *vin = nullptr;
-  uint32_t *kout = s.keys_a, *vout = s.vals_a;
+  // Sort 0: keys = destinations (row 1), sort 1: keys = sources (row 0).
+  uint32_t *ka[2] = {s.keys_a, s.keys_a + n}, *kb[2] = {s.keys_b, s.keys_b + n};
+  uint32_t *va[2] = {s.vals_a, s.vals_a + n}, *vb[2] = {s.vals_b, s.vals_b + n};
+  fill_i32<<<blocks_for(2 * RS_RADIX * passes, 256), 256, 0, stream>>>(
+      (int32_t *)s.totals, 2 * RS_RADIX * passes, 0);
+  SortSet S{};
+  S.keys_i32[0] = edge_index + n;
+  S.keys_i32[1] = edge_index;
+  for (int y = 0; y < 2; ++y) {
+    S.hist[y] = s.hist + y * hl;
+  }
   for (int p = 0; p < passes; ++p) {
+    for (int y = 0; y < 2; ++y) {
+      S.totals[y] = s.totals + (p * 2 + y) * RS_RADIX;
+      S.keys_out[y] = (p & 1) ? kb[y] : ka[y];
+      S.vals_out[y] = (p & 1) ? vb[y] : va[y];
+    }
     const int shift = 8 * p;
-    const int32_t *k32 = p == 0 ? keys : nullptr;
-    rs_upsweep<<<ntiles, RS_THREADS, 0, stream>>>(k32, kin, n, n_nodes, shift, s.hist, ntiles);
-    rs_scan<<<1, 1024, 0, stream>>>(s.hist, len);
-    rs_scatter<<<ntiles, RS_THREADS, 0, stream>>>(k32, kin, vin, n, n_nodes, shift, s.hist,
-                                                 ntiles, kout, vout);
-    kin = kout;
-    vin = vout;
-    kout = (kout == s.keys_a) ? s.keys_b : s.keys_a;
-    vout = (vout == s.vals_a) ? s.vals_b : s.vals_a;
+    rs_upsweep<<<grid, RS_THREADS, 0, stream>>>(S, n, n_nodes, shift, ntiles);
+    rs_scan_digit<<<dim3(RS_RADIX, 2), RS_THREADS, 0, stream>>>(S, ntiles);
+    rs_scatter<<<grid, RS_THREADS, 0, stream>>>(S, n, n_nodes, shift, ntiles);
+    for (int y = 0; y < 2; ++y) {
+      S.keys_i32[y] = nullptr;
+      S.keys_in[y] = S.keys_out[y];
+      S.vals_in[y] = S.vals_out[y];
+    }
   }
-  if (passes == 0) {
-    // n_nodes == 1: every key is 0 and the order is the identity.
-    rs_upsweep<<<ntiles, RS_THREADS, 0, stream>>>(keys, nullptr, n, n_nodes, 0, s.hist, ntiles);
-    rs_scan<<<1, 1024, 0, stream>>>(s.hist, len);
-    rs_scatter<<<ntiles, RS_THREADS, 0, stream>>>(keys, nullptr, nullptr, n, n_nodes, 0, s.hist,
-                                                 ntiles, s.keys_a, s.vals_a);
-    kin = s.keys_a;
-    vin = s.vals_a;
+  CsrOut O{};
+  for (int y = 0; y < 2; ++y) {
+    O.skeys[y] = S.keys_in[y];
+    O.svals[y] = S.vals_in[y];
   }
-  copy_u32<<<blocks_for(n, 256), 256, 0, stream>>>(vin, perm, n);
-  csr_rowptr<<<blocks_for((int64_t)n + 1, 256), 256, 0, stream>>>(kin, n, n_nodes, row_ptr);
+  O.row_ptr[0] = row_ptr_in;
+  O.perm[0] = perm_in;
+  O.row_ptr[1] = row_ptr_out;
+  O.perm[1] = perm_out;
+  const int64_t m = (int64_t)(n > n_nodes ? n : n_nodes) + 1;
+  csr_finish<<<dim3(blocks_for(m, 256), 2), 256, 0, stream>>>(O, n, n_nodes);
   return hipGetLastError();
 }
 

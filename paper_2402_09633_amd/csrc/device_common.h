@@ -1,0 +1,118 @@
+// Device helpers shared by the MLP kernel files (mlp.hip, factored.hip):
+// vector types, the XCD-aware block remap, index clamping, the stable
+// sigmoid, the LayerNorm/ReLU epilogue on MFMA accumulators and the small-K
+// first layer of the node encoder.
+//
+// Accumulator layout (v_mfma_*_32x32*): for a 32x32 block, lane l holds
+// column n = l % 32 and rows 8*(v/4) + 4*(l/32) + v%4 for v = 0..15.  The
+// kernels put output features on rows and graph rows (edges or nodes) on
+// columns, so lane l holds half of the features of row n and lane l ^ 32 the
+// other half.
+#pragma once
+
+#include "gnn_internal.h"
+
+namespace gnn {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef float f16v __attribute__((ext_vector_type(16)));
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf4 __attribute__((ext_vector_type(4)));
+
+constexpr int WAVES_PER_BLOCK = 4;
+constexpr int ROWS_PER_WAVE = 32;
+constexpr int MAX_F = 16;
+
+// Workgroups are dispatched round-robin over the 8 XCDs of the chip; give
+// each XCD a contiguous range of row tiles so that neighbouring edges, which
+// share gathered node rows, reuse one L2.
+__device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
+  const int q = nblocks >> 3, rmd = nblocks & 7;
+  const int r = bid & 7, k = bid >> 3;
+  return r * q + min(r, rmd) + k;
+}
+
+__device__ __forceinline__ int clamp_idx(int32_t v, int32_t n) {
+  return v < 0 ? 0 : (v >= n ? n - 1 : v);
+}
+
+__device__ __forceinline__ float sigmoidf_stable(float z) {
+  if (z >= 0.f) return 1.f / (1.f + __expf(-z));
+  const float ez = __expf(z);
+  return ez / (1.f + ez);
+}
+
+// Bias + LayerNorm + ReLU over the H = 32*MB features of this lane's row,
+// held half in this lane and half in lane ^ 32.  With add_bias false the
+// bias is already in the accumulators.
+template <int MB>
+__device__ __forceinline__ void bias_ln_relu(f16v (&acc)[MB], const float *__restrict__ b,
+                                             const float *__restrict__ g,
+                                             const float *__restrict__ beta, float eps, int hh,
+                                             bool add_bias) {
+  constexpr float inv_h = 1.0f / (32 * MB);
+  float s = 0.f;
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int f = mb * 32 + 8 * q + 4 * hh;
+      const f4 bb = add_bias ? *(const f4 *)(b + f) : f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        acc[mb][4 * q + t] += bb[t];
+        s += acc[mb][4 * q + t];
+      }
+    }
+  s += __shfl_xor(s, 32);
+  const float mean = s * inv_h;
+  float var = 0.f;
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const float d = acc[mb][v] - mean;
+      var += d * d;
+    }
+  var += __shfl_xor(var, 32);
+  const float rstd = 1.0f / sqrtf(var * inv_h + eps);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int f = mb * 32 + 8 * q + 4 * hh;
+      const f4 gg = *(const f4 *)(g + f);
+      const f4 bt = *(const f4 *)(beta + f);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const float y = (acc[mb][4 * q + t] - mean) * rstd * gg[t] + bt[t];
+        acc[mb][4 * q + t] = fmaxf(y, 0.f);
+      }
+    }
+}
+
+// Layer 1 on VALU for a small input width F (node encoder): the accumulator
+// slots are filled directly with W x + b.
+template <int MB>
+__device__ __forceinline__ void small_k_layer(f16v (&acc)[MB], const float *__restrict__ x,
+                                              int F, int row, const float *__restrict__ W,
+                                              const float *__restrict__ b, int hh) {
+  float xin[MAX_F];
+#pragma unroll
+  for (int k = 0; k < MAX_F; ++k) xin[k] = k < F ? x[(int64_t)row * F + k] : 0.f;
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int f = mb * 32 + 8 * (v / 4) + 4 * hh + (v % 4);
+      float s = b[f];
+#pragma unroll
+      for (int k = 0; k < MAX_F; ++k)
+        if (k < F) s += W[f * F + k] * xin[k];
+      acc[mb][v] = s;
+    }
+}
+
+}  // namespace
+}  // namespace gnn

@@ -57,7 +57,8 @@ int check_dims(const gnn_dims *d) {
     return fail(GNN_E_INVALID_ARG, "dtype %d unknown", d->dtype);
   if (!(d->ln_eps > 0.f) || !(d->ln_eps < 1.f))
     return fail(GNN_E_INVALID_ARG, "ln_eps %g outside (0, 1)", (double)d->ln_eps);
-  if (d->flags & ~GNN_VALIDATE_INDICES) return fail(GNN_E_INVALID_ARG, "unknown flags");
+  if (d->flags & ~(GNN_VALIDATE_INDICES | GNN_LITERAL_GATHER))
+    return fail(GNN_E_INVALID_ARG, "unknown flags");
   return GNN_OK;
 }
 
@@ -149,12 +150,22 @@ struct MlpOff {
 
 }  // namespace
 
+// Extra fp32 weights of the regrouped first layers: stacked projections
+// [W_s; W_d] (2H x H) per edge-side MLP and the W_e column blocks (H x H).
+struct FactDev {
+  const float *proj_ee = nullptr, *proj_cls = nullptr, *we_cls = nullptr;
+  std::vector<const float *> proj_em, we_em;
+  int grid_enc = 0, grid_upd = 0, grid_cls = 0;  // persistent edge-kernel grids
+};
+
 struct gnn_handle {
   gnn_dims dims;
   int device = 0;
+  bool factored = false;
   void *dev_weights = nullptr;
   MlpDev node_enc, edge_enc, cls;
   std::vector<MlpDev> edge_mlp, node_mlp;
+  FactDev fd;
   // profiling: recorded (stage, start, end) event pairs not yet read, the
   // running totals and a pool of reusable events
   struct Mark {
@@ -200,6 +211,33 @@ LayerOff stage_layer(Staging &st, const BlobLayer &L, WKind kind, bool bf16, boo
   return o;
 }
 
+// fp32 fragments of an arbitrary (fout x fin) row-major matrix.
+size_t stage_frag_f32(Staging &st, const std::vector<float> &W, int fout, int fin) {
+  BlobLayer L{W.data(), nullptr, nullptr, nullptr, fin, fout};
+  std::vector<float> f(W.size());
+  frag_f32(L, f.data());
+  return st.add(f.data(), f.size() * sizeof(float));
+}
+
+// [W[:, 0:H]; W[:, H:2H]] as a (2H x H) matrix, W being (H x fin).
+std::vector<float> stacked_projection(const BlobLayer &L, int H) {
+  std::vector<float> P((size_t)2 * H * H);
+  for (int o = 0; o < H; ++o)
+    for (int k = 0; k < H; ++k) {
+      P[(size_t)o * H + k] = L.W[(size_t)o * L.fin + k];
+      P[(size_t)(H + o) * H + k] = L.W[(size_t)o * L.fin + H + k];
+    }
+  return P;
+}
+
+// W[:, 2H:3H] as an (H x H) matrix.
+std::vector<float> third_block(const BlobLayer &L, int H) {
+  std::vector<float> P((size_t)H * H);
+  for (int o = 0; o < H; ++o)
+    for (int k = 0; k < H; ++k) P[(size_t)o * H + k] = L.W[(size_t)o * L.fin + 2 * H + k];
+  return P;
+}
+
 LayerDev fix_layer(const LayerOff &o, const unsigned char *base) {
   LayerDev d;
   d.w = base + o.w;
@@ -235,12 +273,14 @@ struct Workspace {
   void *base = nullptr;
   size_t bytes = 0;
   void *h = nullptr, *e = nullptr, *ain = nullptr, *aout = nullptr;
+  float *pa = nullptr, *pb = nullptr;  // node projections (regrouped fp32 path)
   int32_t *rp_in = nullptr, *rp_out = nullptr, *perm_in = nullptr, *perm_out = nullptr;
   CsrScratch csr{};
   int32_t *flag = nullptr;
 };
 
-size_t plan_workspace(Workspace &w, int64_t N, int64_t E, int H, size_t act_bytes) {
+size_t plan_workspace(Workspace &w, int64_t N, int64_t E, int H, size_t act_bytes,
+                      bool factored) {
   size_t off = 0;
   auto take = [&](size_t n) {
     const size_t o = off;
@@ -253,11 +293,18 @@ size_t plan_workspace(Workspace &w, int64_t N, int64_t E, int H, size_t act_byte
   const size_t o_ao = take((size_t)N * H * act_bytes);
   const size_t o_rpi = take((size_t)(N + 1) * 4), o_rpo = take((size_t)(N + 1) * 4);
   const size_t o_pi = take((size_t)E * 4), o_po = take((size_t)E * 4);
-  const size_t o_ka = take((size_t)E * 4), o_kb = take((size_t)E * 4);
-  const size_t o_va = take((size_t)E * 4), o_vb = take((size_t)E * 4);
-  const size_t o_hist = take(csr_hist_len(E) * 4);
+  const size_t o_ka = take((size_t)E * 8), o_kb = take((size_t)E * 8);
+  const size_t o_va = take((size_t)E * 8), o_vb = take((size_t)E * 8);
+  const size_t o_hist = take(csr_hist_len(E) * 8);
+  const size_t o_tot = take(2 * 256 * 4 * 4);
   const size_t o_flag = take(4);
+  const size_t o_pa = factored ? take((size_t)N * 2 * H * 4) : 0;
+  const size_t o_pb = factored ? take((size_t)N * 2 * H * 4) : 0;
   if (w.base) {
+    if (factored) {
+      w.pa = (float *)((unsigned char *)w.base + o_pa);
+      w.pb = (float *)((unsigned char *)w.base + o_pb);
+    }
     unsigned char *b = (unsigned char *)w.base;
     w.h = b + o_h;
     w.e = b + o_e;
@@ -272,6 +319,7 @@ size_t plan_workspace(Workspace &w, int64_t N, int64_t E, int H, size_t act_byte
     w.csr.vals_a = (uint32_t *)(b + o_va);
     w.csr.vals_b = (uint32_t *)(b + o_vb);
     w.csr.hist = (uint32_t *)(b + o_hist);
+    w.csr.totals = (uint32_t *)(b + o_tot);
     w.flag = (int32_t *)(b + o_flag);
   }
   return off;
@@ -357,7 +405,8 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
   st.on = total.on;
   total.begin();
 
-  w.bytes = plan_workspace(w, N, E, H, ab);
+  const bool fac = hd->factored;
+  w.bytes = plan_workspace(w, N, E, H, ab, fac);
   {
     hipError_t ae = hipMallocAsync(&w.base, w.bytes, stream);
     if (ae != hipSuccess) {
@@ -366,7 +415,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
                   "hipMallocAsync(%zu bytes) failed: %s", w.bytes, hipGetErrorString(ae));
     }
   }
-  plan_workspace(w, N, E, H, ab);
+  plan_workspace(w, N, E, H, ab, fac);
 
   if (d.flags & GNN_VALIDATE_INDICES) {
     int32_t bad = 0;
@@ -384,14 +433,113 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
     int32_t *rpi = ro.rp_in ? ro.rp_in : w.rp_in, *pi = ro.perm_in ? ro.perm_in : w.perm_in;
     int32_t *rpo = ro.rp_out ? ro.rp_out : w.rp_out, *po = ro.perm_out ? ro.perm_out : w.perm_out;
     st.begin();
-    HIP_TRY(build_csr(ei + E, m, n, rpi, pi, w.csr, stream));   // by destination
-    HIP_TRY(build_csr(ei, m, n, rpo, po, w.csr, stream));       // by source
+    HIP_TRY(build_csr(ei, m, n, rpi, pi, rpo, po, w.csr, stream));
     st.end(GNN_STAGE_CSR);
     if (ro.csr_only) goto out;
     w.rp_in = rpi;
     w.perm_in = pi;
     w.rp_out = rpo;
     w.perm_out = po;
+  }
+
+  if (fac) {
+    const FactDev &fd = hd->fd;
+    const int T = ro.stop_iter >= 0 ? (ro.stop_iter < d.n_iters ? ro.stop_iter : d.n_iters)
+                                    : d.n_iters;
+    auto set_of = [&](int t) { return d.n_mp_weight_sets == 1 ? 0 : t; };
+    // node encoder -> h0, projections for the edge encoder (pa) and for the
+    // first edge update, or the classifier when there is no iteration (pb)
+    NodeArgs na;
+    na.n_rows = N;
+    na.x = x;
+    na.F = d.in_features;
+    na.mlp = hd->node_enc;
+    na.proj[0] = fd.proj_ee;
+    na.proj[1] = d.n_iters > 0 ? fd.proj_em[0] : fd.proj_cls;
+    na.nproj = 2;
+    na.h_out = (float *)w.h;
+    na.p_out[0] = w.pa;
+    na.p_out[1] = w.pb;
+    na.eps = d.ln_eps;
+    st.begin();
+    HIP_TRY(launch_node_f32(true, H, na, stream));
+    st.end(GNN_STAGE_NODE_ENC);
+
+    auto edge_args = [&](const float *P, const MlpDev &m) {
+      EdgeArgs ea;
+      ea.n_rows = E;
+      ea.n_nodes = n;
+      ea.src_idx = ei;
+      ea.dst_idx = ei + E;
+      ea.P = P;
+      ea.b1 = m.l0.b;
+      ea.g1 = m.l0.g;
+      ea.beta1 = m.l0.beta;
+      ea.w2 = (const float *)m.l1.w;
+      ea.b2 = m.l1.b;
+      ea.g2 = m.l1.g;
+      ea.beta2 = m.l1.beta;
+      ea.eps = d.ln_eps;
+      return ea;
+    };
+    {
+      EdgeArgs ea = edge_args(w.pa, hd->edge_enc);
+      ea.e_out = (float *)w.e;
+      st.begin();
+      HIP_TRY(launch_edge_f32(EdgeMode::Enc, H, ea, fd.grid_enc, stream));
+      st.end(GNN_STAGE_EDGE_ENC);
+    }
+    for (int t = 0; t < T; ++t) {
+      const int k = set_of(t);
+      EdgeArgs ea = edge_args(w.pb, hd->edge_mlp[k]);
+      ea.e_in = (const float *)w.e;
+      ea.we = fd.we_em[k];
+      ea.e_out = (float *)w.e;  // in place: a wave reads its rows before writing them
+      st.begin();
+      HIP_TRY(launch_edge_f32(EdgeMode::Upd, H, ea, fd.grid_upd, stream));
+      st.end(GNN_STAGE_EDGE_UPDATE);
+      st.begin();
+      HIP_TRY(launch_segsum(act, H, w.e, w.rp_in, w.perm_in, w.rp_out, w.perm_out, w.ain,
+                            w.aout, n, stream));
+      st.end(GNN_STAGE_AGGREGATE);
+      NodeArgs nu;
+      nu.n_rows = N;
+      nu.src[0] = (const float *)w.h;
+      nu.src[1] = (const float *)w.ain;
+      nu.src[2] = (const float *)w.aout;
+      nu.mlp = hd->node_mlp[k];
+      nu.proj[0] = t + 1 < d.n_iters ? fd.proj_em[set_of(t + 1)] : fd.proj_cls;
+      nu.nproj = 1;
+      nu.h_out = (float *)w.h;  // in place: a wave reads its rows before writing them
+      nu.p_out[0] = w.pb;
+      nu.eps = d.ln_eps;
+      st.begin();
+      HIP_TRY(launch_node_f32(false, H, nu, stream));
+      st.end(GNN_STAGE_NODE_UPDATE);
+    }
+    if (ro.stop_iter >= 0) {
+      const int64_t nh = N * H, eh = E * H;
+      struct { float *dst; void *src; int64_t n; bool agg; } ex[4] = {
+          {ro.h, w.h, nh, false}, {ro.e, w.e, eh, false},
+          {ro.ain, w.ain, nh, true}, {ro.aout, w.aout, nh, true}};
+      for (auto &x2 : ex) {
+        if (!x2.dst || x2.n == 0 || (x2.agg && T == 0)) continue;
+        HIP_TRY(hipMemcpyAsync(x2.dst, x2.src, x2.n * 4, hipMemcpyDeviceToDevice, stream));
+      }
+      goto out;
+    }
+    {
+      EdgeArgs ea = edge_args(w.pb, hd->cls);
+      ea.e_in = (const float *)w.e;
+      ea.we = fd.we_cls;
+      ea.g2 = ea.beta2 = nullptr;
+      ea.out_score = ro.scores;
+      ea.out_logit = ro.logits;
+      st.begin();
+      HIP_TRY(launch_edge_f32(EdgeMode::Cls, H, ea, fd.grid_cls, stream));
+      st.end(GNN_STAGE_CLASSIFIER);
+    }
+    goto out;
   }
 
   {
@@ -573,6 +721,9 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
   Staging st;
   MlpOff o_ne, o_ee, o_cls;
   std::vector<MlpOff> o_em(S), o_nm(S);
+  const bool factored = !bf16 && !(d.flags & GNN_LITERAL_GATHER);
+  size_t o_proj_ee = 0, o_proj_cls = 0, o_we_cls = 0;
+  std::vector<size_t> o_proj_em(S), o_we_em(S);
   {
     BlobLayer a0 = next(F, H, true), a1 = next(H, H, true);
     o_ne = {stage_layer(st, a0, WKind::Plain, bf16, true),
@@ -580,10 +731,15 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
     BlobLayer b0 = next(2 * H, H, true), b1 = next(H, H, true);
     o_ee = {stage_layer(st, b0, WKind::FragMem, bf16, true),
             stage_layer(st, b1, WKind::FragAcc, bf16, true)};
+    if (factored) o_proj_ee = stage_frag_f32(st, stacked_projection(b0, H), 2 * H, H);
     for (int s = 0; s < S; ++s) {
       BlobLayer e0 = next(3 * H, H, true), e1 = next(H, H, true);
       o_em[s] = {stage_layer(st, e0, WKind::FragMem, bf16, true),
                  stage_layer(st, e1, WKind::FragAcc, bf16, true)};
+      if (factored) {
+        o_proj_em[s] = stage_frag_f32(st, stacked_projection(e0, H), 2 * H, H);
+        o_we_em[s] = stage_frag_f32(st, third_block(e0, H), H, H);
+      }
       BlobLayer n0 = next(3 * H, H, true), n1 = next(H, H, true);
       o_nm[s] = {stage_layer(st, n0, WKind::FragMem, bf16, true),
                  stage_layer(st, n1, WKind::FragAcc, bf16, true)};
@@ -591,6 +747,10 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
     BlobLayer c0 = next(3 * H, H, true), c1 = next(H, 1, false);
     o_cls = {stage_layer(st, c0, WKind::FragMem, bf16, true),
              stage_layer(st, c1, WKind::Plain, bf16, false)};
+    if (factored) {
+      o_proj_cls = stage_frag_f32(st, stacked_projection(c0, H), 2 * H, H);
+      o_we_cls = stage_frag_f32(st, third_block(c0, H), H, H);
+    }
   }
 
   gnn_handle *h = new gnn_handle();
@@ -616,6 +776,23 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
   for (int s = 0; s < S; ++s) {
     h->edge_mlp.push_back(fix_mlp(o_em[s], base));
     h->node_mlp.push_back(fix_mlp(o_nm[s], base));
+  }
+  h->factored = factored;
+  if (factored) {
+    FactDev &fd = h->fd;
+    fd.proj_ee = (const float *)(base + o_proj_ee);
+    fd.proj_cls = (const float *)(base + o_proj_cls);
+    fd.we_cls = (const float *)(base + o_we_cls);
+    for (int s = 0; s < S; ++s) {
+      fd.proj_em.push_back((const float *)(base + o_proj_em[s]));
+      fd.we_em.push_back((const float *)(base + o_we_em[s]));
+    }
+    int n_cu = 0;
+    if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      n_cu = 256;
+    fd.grid_enc = edge_f32_grid(EdgeMode::Enc, H, n_cu);
+    fd.grid_upd = edge_f32_grid(EdgeMode::Upd, H, n_cu);
+    fd.grid_cls = edge_f32_grid(EdgeMode::Cls, H, n_cu);
   }
   return h;
 }

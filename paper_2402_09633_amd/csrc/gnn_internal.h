@@ -52,6 +52,43 @@ enum class GmlpKind : int { NodeEnc = 0, EdgeEnc = 1, EdgeUpd = 2, NodeUpd = 3, 
 // Every launcher enqueues on `stream` and returns the launch status.
 hipError_t launch_gmlp(GmlpKind kind, Act act, int hidden, const GmlpArgs &a, hipStream_t stream);
 
+// ---- fp32 kernels with the edge MLPs' first layer regrouped per node ----
+// (factored.hip).  P rows are [W_s h_v ; W_d h_v], 2H floats per node.
+struct NodeArgs {
+  int64_t n_rows = 0;
+  const float *x = nullptr;  // encoder: raw features [n_rows][F]
+  int32_t F = 0;
+  const float *src[3] = {nullptr, nullptr, nullptr};  // update: h, agg_in, agg_out
+  MlpDev mlp;
+  const float *proj[2] = {nullptr, nullptr};  // fragments of (2H x H) [W_s; W_d]
+  int32_t nproj = 1;
+  float *h_out = nullptr;                     // [n_rows][H] or nullptr
+  float *p_out[2] = {nullptr, nullptr};       // [n_rows][2H]
+  float eps = 1e-5f;
+};
+
+enum class EdgeMode : int { Enc = 0, Upd = 1, Cls = 2 };
+
+struct EdgeArgs {
+  int64_t n_rows = 0;
+  int32_t n_nodes = 0;
+  const int32_t *src_idx = nullptr, *dst_idx = nullptr;
+  const float *P = nullptr;      // [n_nodes][2H]
+  const float *e_in = nullptr;   // [n_rows][H] (update, classifier)
+  const float *we = nullptr;     // fragments of W_e (H x H)
+  const float *b1 = nullptr, *g1 = nullptr, *beta1 = nullptr;
+  const float *w2 = nullptr;     // fragments of W2 (H x H), or the classifier head [H]
+  const float *b2 = nullptr, *g2 = nullptr, *beta2 = nullptr;
+  float *e_out = nullptr, *out_logit = nullptr, *out_score = nullptr;
+  float eps = 1e-5f;
+};
+
+hipError_t launch_node_f32(bool enc, int hidden, const NodeArgs &a, hipStream_t stream);
+// `grid` = number of persistent workgroups (edge_f32_grid).
+hipError_t launch_edge_f32(EdgeMode mode, int hidden, const EdgeArgs &a, int grid,
+                           hipStream_t stream);
+int edge_f32_grid(EdgeMode mode, int hidden, int n_cu);
+
 // Deterministic CSR segmented sums of the edge rows `e` ([n_edges][H]):
 // agg_in[v] = sum over p in [rp_in[v], rp_in[v+1]) of e[perm_in[p]], in
 // ascending p, and the same for agg_out.  fp32 accumulation in both modes.
@@ -59,15 +96,19 @@ hipError_t launch_segsum(Act act, int hidden, const void *e, const int32_t *rp_i
                          const int32_t *perm_in, const int32_t *rp_out, const int32_t *perm_out,
                          void *agg_in, void *agg_out, int32_t n_nodes, hipStream_t stream);
 
-// Stable CSR of `keys` (n_edges int32 in [0, n_nodes), clamped if not):
-// row_ptr[n_nodes+1] and perm[n_edges] (edge ids, ascending within a row).
+// Stable CSRs of edge_index ([2][n_edges] int32, indices clamped into
+// [0, n_nodes)): by destination (row_ptr_in, perm_in) and by source
+// (row_ptr_out, perm_out); row_ptr has n_nodes+1 entries, perm lists edge
+// ids ascending within each row.  Both sorts run in the same launches.
 struct CsrScratch {
-  uint32_t *keys_a, *keys_b, *vals_a, *vals_b;  // n_edges each
-  uint32_t *hist;                               // csr_hist_len(n_edges)
+  uint32_t *keys_a, *keys_b, *vals_a, *vals_b;  // 2*n_edges each
+  uint32_t *hist;                               // 2*csr_hist_len(n_edges)
+  uint32_t *totals;                             // 2*256*4
 };
 size_t csr_hist_len(int64_t n_edges);
-hipError_t build_csr(const int32_t *keys, int32_t n_edges, int32_t n_nodes, int32_t *row_ptr,
-                     int32_t *perm, const CsrScratch &s, hipStream_t stream);
+hipError_t build_csr(const int32_t *edge_index, int32_t n_edges, int32_t n_nodes,
+                     int32_t *row_ptr_in, int32_t *perm_in, int32_t *row_ptr_out,
+                     int32_t *perm_out, const CsrScratch &s, hipStream_t stream);
 
 // flag <- 1 if any of the 2*n_edges indices lies outside [0, n_nodes).
 hipError_t launch_validate(const int32_t *edge_index, int64_t n_edges, int32_t n_nodes,

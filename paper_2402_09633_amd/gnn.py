@@ -27,6 +27,7 @@ GNN_E_UNSUPPORTED = -6
 GNN_FP32 = 0
 GNN_BF16 = 1
 GNN_VALIDATE_INDICES = 1
+GNN_LITERAL_GATHER = 2
 
 EXPORTS = ("gnn_weight_count", "gnn_create", "gnn_infer", "gnn_infer_logits", "gnn_destroy",
            "gnn_last_error", "gnn_profile_enable", "gnn_profile_read", "gnn_debug_csr",

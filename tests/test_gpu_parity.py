@@ -34,37 +34,46 @@ def _tiny_random(seed, n, e, loops=False):
     return x, ei
 
 
+# fp32 runs both forms of the edge MLPs' first layer: the default regrouping
+# at node level (flags 0) and the per-edge gather (GNN_LITERAL_GATHER = 2).
+PATHS = [0, 2]
+
+
+@pytest.mark.parametrize("flags", PATHS)
 @pytest.mark.parametrize("H,T,S,noise", [(64, 2, 1, 0.0), (64, 2, 1, 0.3), (128, 2, 1, 0.3),
-                                         (64, 3, 3, 0.3), (128, 0, 1, 0.3), (64, 1, 1, 0.3)])
-def test_tiny_fp32_logits(G, oracle_mod, H, T, S, noise):
+                                         (64, 3, 3, 0.3), (128, 0, 1, 0.3), (64, 1, 1, 0.3),
+                                         (128, 4, 4, 0.3)])
+def test_tiny_fp32_logits(G, oracle_mod, H, T, S, noise, flags):
     c = I.CONFIGS["tiny"]
     g = I.make_graph(c)
     w = I.make_weights(3, H, S, c.weight_seed, affine_noise=noise)
-    print(f"tiny H={H} T={T} S={S} noise={noise}", flush=True)
+    print(f"tiny H={H} T={T} S={S} noise={noise} flags={flags}", flush=True)
     ref = oracle_mod.forward(w, g.x, g.edge_index, H, T, S)
-    got = run_model(G, w, G.make_dims(3, H, T, S), g.x, g.edge_index)
+    got = run_model(G, w, G.make_dims(3, H, T, S, flags=flags), g.x, g.edge_index)
     assert_logits_close(got, ref["logits"])
-    sc = run_model(G, w, G.make_dims(3, H, T, S), g.x, g.edge_index, logits=False)
+    sc = run_model(G, w, G.make_dims(3, H, T, S, flags=flags), g.x, g.edge_index, logits=False)
     np.testing.assert_allclose(sc, ref["scores"], rtol=0, atol=1e-5)
 
 
+@pytest.mark.parametrize("flags", PATHS)
 @pytest.mark.parametrize("n,e,seed", [(50, 1, 0), (50, 31, 1), (50, 33, 2), (3000, 8001, 3),
                                       (1, 7, 4), (700, 129, 5)])
-def test_ragged_and_small_graphs(G, oracle_mod, n, e, seed):
+def test_ragged_and_small_graphs(G, oracle_mod, n, e, seed, flags):
     x, ei = _tiny_random(seed, n, e, loops=(n == 1))
     w = I.make_weights(3, 64, 1, seed, affine_noise=0.3)
-    print(f"ragged n={n} e={e}", flush=True)
+    print(f"ragged n={n} e={e} flags={flags}", flush=True)
     ref = oracle_mod.forward(w, x, ei, 64, 2)
-    got = run_model(G, w, G.make_dims(3, 64, 2), x, ei)
+    got = run_model(G, w, G.make_dims(3, 64, 2, flags=flags), x, ei)
     assert_logits_close(got, ref["logits"])
 
 
-def test_stage_parity_tiny(G, oracle_mod):
+@pytest.mark.parametrize("flags", PATHS)
+def test_stage_parity_tiny(G, oracle_mod, flags):
     c = I.CONFIGS["tiny"]
     g = I.make_graph(c)
     H, T = c.hidden, 3
     w = I.make_weights(3, H, 1, c.weight_seed, affine_noise=0.3)
-    h = G.gnn_create(w, G.make_dims(3, H, T))
+    h = G.gnn_create(w, G.make_dims(3, H, T, flags=flags))
     try:
         xd, eid = dev(g.x), dev(g.edge_index)
         N, E = g.n_nodes, g.n_edges
@@ -85,12 +94,19 @@ def test_stage_parity_tiny(G, oracle_mod):
 def test_mid_fp32_full_compare(G, oracle_mod):
     c = I.CONFIGS["mid"]
     g = I.make_graph(c)
-    w = I.make_weights(3, c.hidden, 1, c.weight_seed)
+    w = I.make_weights(3, c.hidden, 1, c.weight_seed, affine_noise=0.1)
     print(f"mid N={g.n_nodes} E={g.n_edges}", flush=True)
     ref = oracle_mod.forward(w, g.x, g.edge_index, c.hidden, c.n_iters)
-    got = run_model(G, w, G.make_dims(3, c.hidden, c.n_iters), g.x, g.edge_index)
-    err = assert_logits_close(got, ref["logits"])
-    print(f"mid max scaled logit error {err:.2e}", flush=True)
+    for flags in PATHS:
+        got = run_model(G, w, G.make_dims(3, c.hidden, c.n_iters, flags=flags), g.x,
+                        g.edge_index)
+        err = assert_logits_close(got, ref["logits"])
+        print(f"mid flags={flags} max scaled logit error {err:.2e}", flush=True)
+    sc = run_model(G, w, G.make_dims(3, c.hidden, c.n_iters, dtype=G.GNN_BF16), g.x,
+                   g.edge_index, logits=False)
+    err = np.abs(sc - ref["scores"])
+    print(f"mid bf16 max score error {err.max():.3e}", flush=True)
+    assert err.max() <= BF16_SCORE_ATOL
 
 
 def _golden(name):
@@ -98,17 +114,19 @@ def _golden(name):
         return json.load(f)
 
 
-def test_full_fp32_vs_stored_oracle(G):
+@pytest.mark.parametrize("flags", PATHS)
+def test_full_fp32_vs_stored_oracle(G, flags):
     gold = _golden("full")
     c = I.CONFIGS["full"]
     g = I.make_graph(c)
     assert g.digest() == gold["graph_digest"]
     w = I.make_weights(3, c.hidden, 1, c.weight_seed)
     ids = np.array(gold["edge_ids"])
-    got = run_model(G, w, G.make_dims(3, c.hidden, c.n_iters), g.x, g.edge_index)
+    dims = G.make_dims(3, c.hidden, c.n_iters, flags=flags)
+    got = run_model(G, w, dims, g.x, g.edge_index)
     err = assert_logits_close(got[ids], gold["logits"])
-    print(f"full fp32 max scaled logit error {err:.2e}", flush=True)
-    sc = run_model(G, w, G.make_dims(3, c.hidden, c.n_iters), g.x, g.edge_index, logits=False)
+    print(f"full fp32 flags={flags} max scaled logit error {err:.2e}", flush=True)
+    sc = run_model(G, w, dims, g.x, g.edge_index, logits=False)
     np.testing.assert_allclose(sc[ids], gold["scores"], rtol=0, atol=2e-5)
 
 
