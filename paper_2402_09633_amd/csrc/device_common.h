@@ -93,25 +93,33 @@ __device__ __forceinline__ void bias_ln_relu(f16v (&acc)[MB], const float *__res
 }
 
 // Layer 1 on VALU for a small input width F (node encoder): the accumulator
-// slots are filled directly with W x + b.
+// slots are filled directly with W x + b.  Wt is W transposed, [F][H], so
+// a lane reads its four consecutive features of one input as a float4.
 template <int MB>
 __device__ __forceinline__ void small_k_layer(f16v (&acc)[MB], const float *__restrict__ x,
-                                              int F, int row, const float *__restrict__ W,
+                                              int F, int row, const float *__restrict__ Wt,
                                               const float *__restrict__ b, int hh) {
-  float xin[MAX_F];
-#pragma unroll
-  for (int k = 0; k < MAX_F; ++k) xin[k] = k < F ? x[(int64_t)row * F + k] : 0.f;
+  constexpr int H = 32 * MB;
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int f = mb * 32 + 8 * (v / 4) + 4 * hh + (v % 4);
-      float s = b[f];
+    for (int q = 0; q < 4; ++q) {
+      const f4 bb = *(const f4 *)(b + mb * 32 + 8 * q + 4 * hh);
 #pragma unroll
-      for (int k = 0; k < MAX_F; ++k)
-        if (k < F) s += W[f * F + k] * xin[k];
-      acc[mb][v] = s;
+      for (int t = 0; t < 4; ++t) acc[mb][4 * q + t] = bb[t];
     }
+  for (int k = 0; k < F; ++k) {
+    const float xk = x[(int64_t)row * F + k];
+    const float *wk = Wt + k * H + 4 * hh;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f4 ww = *(const f4 *)(wk + mb * 32 + 8 * q);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[mb][4 * q + t] += ww[t] * xk;
+      }
+  }
 }
 
 }  // namespace

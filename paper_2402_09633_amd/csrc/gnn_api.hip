@@ -153,9 +153,14 @@ struct MlpOff {
 // Extra fp32 weights of the regrouped first layers: stacked projections
 // [W_s; W_d] (2H x H) per edge-side MLP and the W_e column blocks (H x H).
 struct FactDev {
-  const float *proj_ee = nullptr, *proj_cls = nullptr, *we_cls = nullptr;
-  std::vector<const float *> proj_em, we_em;
-  int grid_enc = 0, grid_upd = 0, grid_cls = 0;  // persistent edge-kernel grids
+  const float *we_cls = nullptr;
+  std::vector<const float *> we_em;
+  // node-kernel fragment streams: encoder (W2 | two projections) and, per
+  // iteration, update (W1 | W2 | projection for the next edge consumer)
+  const float *enc_stream = nullptr;
+  std::vector<const float *> upd_stream;
+  int enc_chunks = 0, upd_chunks = 0;
+  int grid_enc = 0, grid_upd = 0, grid_cls = 0, grid_node = 0;  // persistent grids
 };
 
 struct gnn_handle {
@@ -184,7 +189,7 @@ struct gnn_handle {
 namespace {
 
 // Layer kinds for the converter.
-enum class WKind { Plain, FragMem, FragAcc };
+enum class WKind { Plain, PlainT, FragMem, FragAcc };
 
 LayerOff stage_layer(Staging &st, const BlobLayer &L, WKind kind, bool bf16, bool has_ln) {
   LayerOff o;
@@ -192,6 +197,11 @@ LayerOff stage_layer(Staging &st, const BlobLayer &L, WKind kind, bool bf16, boo
   const size_t nW = (size_t)L.fin * L.fout;
   if (kind == WKind::Plain) {
     o.w = st.add(L.W, nW * sizeof(float));
+  } else if (kind == WKind::PlainT) {
+    std::vector<float> t(nW);  // [in][out]
+    for (int o2 = 0; o2 < L.fout; ++o2)
+      for (int k = 0; k < L.fin; ++k) t[(size_t)k * L.fout + o2] = L.W[(size_t)o2 * L.fin + k];
+    o.w = st.add(t.data(), nW * sizeof(float));
   } else if (!bf16) {
     std::vector<float> f(nW);
     frag_f32(L, f.data());
@@ -219,23 +229,29 @@ size_t stage_frag_f32(Staging &st, const std::vector<float> &W, int fout, int fi
   return st.add(f.data(), f.size() * sizeof(float));
 }
 
-// [W[:, 0:H]; W[:, H:2H]] as a (2H x H) matrix, W being (H x fin).
-std::vector<float> stacked_projection(const BlobLayer &L, int H) {
-  std::vector<float> P((size_t)2 * H * H);
+// Column block W[:, c0:c0+H] of an (H x fin) layer, as an (H x H) matrix.
+std::vector<float> col_block(const BlobLayer &L, int H, int c0) {
+  std::vector<float> P((size_t)H * H);
   for (int o = 0; o < H; ++o)
-    for (int k = 0; k < H; ++k) {
-      P[(size_t)o * H + k] = L.W[(size_t)o * L.fin + k];
-      P[(size_t)(H + o) * H + k] = L.W[(size_t)o * L.fin + H + k];
-    }
+    for (int k = 0; k < H; ++k) P[(size_t)o * H + k] = L.W[(size_t)o * L.fin + c0 + k];
   return P;
 }
 
-// W[:, 2H:3H] as an (H x H) matrix.
-std::vector<float> third_block(const BlobLayer &L, int H) {
-  std::vector<float> P((size_t)H * H);
-  for (int o = 0; o < H; ++o)
-    for (int k = 0; k < H; ++k) P[(size_t)o * H + k] = L.W[(size_t)o * L.fin + 2 * H + k];
-  return P;
+std::vector<float> frag_of(const float *W, int fout, int fin) {
+  BlobLayer L{W, nullptr, nullptr, nullptr, fin, fout};
+  std::vector<float> f((size_t)fout * fin);
+  frag_f32(L, f.data());
+  return f;
+}
+
+void append(std::vector<float> &dst, const std::vector<float> &src) {
+  dst.insert(dst.end(), src.begin(), src.end());
+}
+
+// Fragments of the two projection halves W[:, 0:H] and W[:, H:2H].
+void append_projection(std::vector<float> &dst, const BlobLayer &L, int H) {
+  append(dst, frag_of(col_block(L, H, 0).data(), H, H));
+  append(dst, frag_of(col_block(L, H, H).data(), H, H));
 }
 
 LayerDev fix_layer(const LayerOff &o, const unsigned char *base) {
@@ -454,15 +470,15 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
     na.x = x;
     na.F = d.in_features;
     na.mlp = hd->node_enc;
-    na.proj[0] = fd.proj_ee;
-    na.proj[1] = d.n_iters > 0 ? fd.proj_em[0] : fd.proj_cls;
+    na.wstream = fd.enc_stream;
+    na.nchunks = fd.enc_chunks;
     na.nproj = 2;
     na.h_out = (float *)w.h;
     na.p_out[0] = w.pa;
     na.p_out[1] = w.pb;
     na.eps = d.ln_eps;
     st.begin();
-    HIP_TRY(launch_node_f32(true, H, na, stream));
+    HIP_TRY(launch_node_f32(true, H, na, fd.grid_node, stream));
     st.end(GNN_STAGE_NODE_ENC);
 
     auto edge_args = [&](const float *P, const MlpDev &m) {
@@ -508,13 +524,14 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       nu.src[1] = (const float *)w.ain;
       nu.src[2] = (const float *)w.aout;
       nu.mlp = hd->node_mlp[k];
-      nu.proj[0] = t + 1 < d.n_iters ? fd.proj_em[set_of(t + 1)] : fd.proj_cls;
+      nu.wstream = fd.upd_stream[t];
+      nu.nchunks = fd.upd_chunks;
       nu.nproj = 1;
       nu.h_out = (float *)w.h;  // in place: a wave reads its rows before writing them
       nu.p_out[0] = w.pb;
       nu.eps = d.ln_eps;
       st.begin();
-      HIP_TRY(launch_node_f32(false, H, nu, stream));
+      HIP_TRY(launch_node_f32(false, H, nu, fd.grid_node, stream));
       st.end(GNN_STAGE_NODE_UPDATE);
     }
     if (ro.stop_iter >= 0) {
@@ -722,34 +739,49 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
   MlpOff o_ne, o_ee, o_cls;
   std::vector<MlpOff> o_em(S), o_nm(S);
   const bool factored = !bf16 && !(d.flags & GNN_LITERAL_GATHER);
-  size_t o_proj_ee = 0, o_proj_cls = 0, o_we_cls = 0;
-  std::vector<size_t> o_proj_em(S), o_we_em(S);
+  const int T = d.n_iters;
+  size_t o_we_cls = 0, o_enc_stream = 0;
+  std::vector<size_t> o_we_em(S), o_upd_stream(T);
   {
     BlobLayer a0 = next(F, H, true), a1 = next(H, H, true);
-    o_ne = {stage_layer(st, a0, WKind::Plain, bf16, true),
+    o_ne = {stage_layer(st, a0, WKind::PlainT, bf16, true),
             stage_layer(st, a1, WKind::FragAcc, bf16, true)};
     BlobLayer b0 = next(2 * H, H, true), b1 = next(H, H, true);
     o_ee = {stage_layer(st, b0, WKind::FragMem, bf16, true),
             stage_layer(st, b1, WKind::FragAcc, bf16, true)};
-    if (factored) o_proj_ee = stage_frag_f32(st, stacked_projection(b0, H), 2 * H, H);
+    std::vector<BlobLayer> e0s, n0s, n1s;
     for (int s = 0; s < S; ++s) {
       BlobLayer e0 = next(3 * H, H, true), e1 = next(H, H, true);
       o_em[s] = {stage_layer(st, e0, WKind::FragMem, bf16, true),
                  stage_layer(st, e1, WKind::FragAcc, bf16, true)};
-      if (factored) {
-        o_proj_em[s] = stage_frag_f32(st, stacked_projection(e0, H), 2 * H, H);
-        o_we_em[s] = stage_frag_f32(st, third_block(e0, H), H, H);
-      }
+      if (factored) o_we_em[s] = stage_frag_f32(st, col_block(e0, H, 2 * H), H, H);
       BlobLayer n0 = next(3 * H, H, true), n1 = next(H, H, true);
       o_nm[s] = {stage_layer(st, n0, WKind::FragMem, bf16, true),
                  stage_layer(st, n1, WKind::FragAcc, bf16, true)};
+      e0s.push_back(e0);
+      n0s.push_back(n0);
+      n1s.push_back(n1);
     }
     BlobLayer c0 = next(3 * H, H, true), c1 = next(H, 1, false);
     o_cls = {stage_layer(st, c0, WKind::FragMem, bf16, true),
              stage_layer(st, c1, WKind::Plain, bf16, false)};
     if (factored) {
-      o_proj_cls = stage_frag_f32(st, stacked_projection(c0, H), 2 * H, H);
-      o_we_cls = stage_frag_f32(st, third_block(c0, H), H, H);
+      o_we_cls = stage_frag_f32(st, col_block(c0, H, 2 * H), H, H);
+      // Node encoder stream: W2 | projection for the edge encoder |
+      // projection for the first edge update (the classifier if T == 0).
+      std::vector<float> es = frag_of(a1.W, H, H);
+      append_projection(es, b0, H);
+      append_projection(es, T > 0 ? e0s[0] : c0, H);
+      o_enc_stream = st.add(es.data(), es.size() * sizeof(float));
+      // Node update t: W1 | W2 | projection for edge update t+1 (or the
+      // classifier after the last iteration).
+      for (int t = 0; t < T; ++t) {
+        const int k = S == 1 ? 0 : t;
+        std::vector<float> us = frag_of(n0s[k].W, H, 3 * H);
+        append(us, frag_of(n1s[k].W, H, H));
+        append_projection(us, t + 1 < T ? e0s[S == 1 ? 0 : t + 1] : c0, H);
+        o_upd_stream[t] = st.add(us.data(), us.size() * sizeof(float));
+      }
     }
   }
 
@@ -780,19 +812,20 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
   h->factored = factored;
   if (factored) {
     FactDev &fd = h->fd;
-    fd.proj_ee = (const float *)(base + o_proj_ee);
-    fd.proj_cls = (const float *)(base + o_proj_cls);
     fd.we_cls = (const float *)(base + o_we_cls);
-    for (int s = 0; s < S; ++s) {
-      fd.proj_em.push_back((const float *)(base + o_proj_em[s]));
-      fd.we_em.push_back((const float *)(base + o_we_em[s]));
-    }
+    for (int s = 0; s < S; ++s) fd.we_em.push_back((const float *)(base + o_we_em[s]));
+    fd.enc_stream = (const float *)(base + o_enc_stream);
+    for (int t = 0; t < T; ++t) fd.upd_stream.push_back((const float *)(base + o_upd_stream[t]));
+    const int kg = H / 8;  // k-groups of one H-wide operand; 8 per chunk
+    fd.enc_chunks = (kg + 4 * kg) / 8;
+    fd.upd_chunks = (3 * kg + kg + 2 * kg) / 8;
     int n_cu = 0;
     if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
       n_cu = 256;
     fd.grid_enc = edge_f32_grid(EdgeMode::Enc, H, n_cu);
     fd.grid_upd = edge_f32_grid(EdgeMode::Upd, H, n_cu);
     fd.grid_cls = edge_f32_grid(EdgeMode::Cls, H, n_cu);
+    fd.grid_node = node_f32_grid(n_cu);
   }
   return h;
 }

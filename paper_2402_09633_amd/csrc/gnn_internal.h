@@ -59,8 +59,9 @@ struct NodeArgs {
   const float *x = nullptr;  // encoder: raw features [n_rows][F]
   int32_t F = 0;
   const float *src[3] = {nullptr, nullptr, nullptr};  // update: h, agg_in, agg_out
-  MlpDev mlp;
-  const float *proj[2] = {nullptr, nullptr};  // fragments of (2H x H) [W_s; W_d]
+  MlpDev mlp;                 // biases and LayerNorm parameters; encoder W1 rows
+  const float *wstream = nullptr;  // fragment stream: [W1 (update only)] W2 proj...
+  int32_t nchunks = 0;             // chunks of the stream (8 k-groups each)
   int32_t nproj = 1;
   float *h_out = nullptr;                     // [n_rows][H] or nullptr
   float *p_out[2] = {nullptr, nullptr};       // [n_rows][2H]
@@ -83,7 +84,10 @@ struct EdgeArgs {
   float eps = 1e-5f;
 };
 
-hipError_t launch_node_f32(bool enc, int hidden, const NodeArgs &a, hipStream_t stream);
+hipError_t launch_node_f32(bool enc, int hidden, const NodeArgs &a, int grid,
+                           hipStream_t stream);
+int node_f32_grid(int n_cu);
+int node_stream_chunk_f4(int hidden);
 // `grid` = number of persistent workgroups (edge_f32_grid).
 hipError_t launch_edge_f32(EdgeMode mode, int hidden, const EdgeArgs &a, int grid,
                            hipStream_t stream);
