@@ -335,12 +335,18 @@ __global__ __launch_bounds__(64 * EDGE_WAVES) void edge_f32(EdgeArgs a) {
     return row < a.n_rows ? row : a.n_rows - 1;  // tail lanes recompute the last row
   };
 
-  // The e row of the next unit is requested before the current unit's
-  // stores, so waiting for it never waits for those stores as well.
+  // The next unit's edge indices and e row are requested before the
+  // current unit's stores: vector-memory completions are counted in issue
+  // order, so a load issued after a store can only be waited for together
+  // with that store.
   f4 ev[HAS_E ? G : 1];
-  if constexpr (HAS_E) {
-    if (gw < units) {
-      const float *ep = a.e_in + row_of(gw) * H + 4 * hh;
+  int32_t nsrc = 0, ndst = 0;
+  if (gw < units) {
+    const int64_t r0 = row_of(gw);
+    nsrc = a.src_idx[r0];
+    ndst = a.dst_idx[r0];
+    if constexpr (HAS_E) {
+      const float *ep = a.e_in + r0 * H + 4 * hh;
 #pragma unroll
       for (int g = 0; g < G; ++g) ev[g] = *(const f4 *)(ep + 8 * g);
     }
@@ -351,9 +357,8 @@ __global__ __launch_bounds__(64 * EDGE_WAVES) void edge_f32(EdgeArgs a) {
     asm volatile("" ::: "memory");
     const int64_t row = u * 32 + n;
     const bool valid = row < a.n_rows;
-    const int64_t r = row_of(u);
-    const int64_t s = clamp_idx(a.src_idx[r], a.n_nodes);
-    const int64_t d = clamp_idx(a.dst_idx[r], a.n_nodes);
+    const int64_t s = clamp_idx(nsrc, a.n_nodes);
+    const int64_t d = clamp_idx(ndst, a.n_nodes);
 
     // Layer 1 = P[src][0:H] + P[dst][H:2H] (+ W_e e) + b1.
     f16v acc[MB];
@@ -384,11 +389,18 @@ __global__ __launch_bounds__(64 * EDGE_WAVES) void edge_f32(EdgeArgs a) {
             acc[mb] = __builtin_amdgcn_mfma_f32_32x32x2f32(wb[mb][t], ev[g][t], acc[mb], 0, 0,
                                                            0);
       }
+    }
+    {
       const int64_t un = u + nw;
       if (un < units) {
-        const float *ep = a.e_in + row_of(un) * H + 4 * hh;
+        const int64_t rn = row_of(un);
+        nsrc = a.src_idx[rn];
+        ndst = a.dst_idx[rn];
+        if constexpr (HAS_E) {
+          const float *ep = a.e_in + rn * H + 4 * hh;
 #pragma unroll
-        for (int g = 0; g < G; ++g) ev[g] = *(const f4 *)(ep + 8 * g);
+          for (int g = 0; g < G; ++g) ev[g] = *(const f4 *)(ep + 8 * g);
+        }
       }
     }
     ln_relu_lds<MB>(acc, prm, a.eps, hh);
