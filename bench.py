@@ -25,6 +25,23 @@ METRIC = "edges/sec and ms/event, 8-iter interaction network, 300k nodes/1M edge
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2500.0}
 
+# HBM bytes per launch of the fp32 edge-update kernel on the full event,
+# from rocprofv3 FETCH_SIZE / WRITE_SIZE passes scaled by a plain-copy
+# calibration (profiles/full_fp32_kernels_and_counters.md).  Valid only for
+# the kernel sources they were measured on (hash of the files below).
+TRAFFIC_SOURCES = ["paper_2402_09633_amd/csrc/factored.hip",
+                   "paper_2402_09633_amd/csrc/device_common.h"]
+MEASURED_TRAFFIC = {"c330b264c61fa985": {"edge_update_bytes": 1652e6}}
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
 
 def edge_update_flops(E, H, factored):
     """Multiply-adds x 2 of one edge-update launch.
@@ -47,7 +64,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="full", choices=["full", "full_bf16", "mid", "tiny"])
+    ap.add_argument("--workload", default="full",
+                    choices=["full", "full_bf16", "mid", "tiny", "batch"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--literal", action="store_true",
                     help="evaluate the edge MLPs' first layer per edge (GNN_LITERAL_GATHER)")
@@ -78,6 +96,8 @@ def main():
     from paper_2402_09633_amd import inputs as I
 
     cfg = I.CONFIGS[args.workload]
+    if cfg.kind == "batch":
+        return bench_batch(args, cfg)
     g = I.make_graph(cfg)
     N, E, H, T = g.n_nodes, g.n_edges, cfg.hidden, cfg.n_iters
     w = I.make_weights(3, H, 1, cfg.weight_seed)
@@ -128,6 +148,10 @@ def main():
     ag_bytes = aggregate_bytes(N, E, H, act_bytes)
     ag_gbs = ag_bytes / (ag_ms / 1000.0) / 1e9
 
+    traffic = None
+    if factored and cfg.name == "full":
+        m_t = MEASURED_TRAFFIC.get(kernel_source_hash())
+        traffic = m_t["edge_update_bytes"] if m_t else None
     rec = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -151,7 +175,8 @@ def main():
                                 "weights in LDS)") if factored else
                                ("gmlp edge update (gathers [h_src; h_dst; e], 3H->H->H)"),
                      "bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
-                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None,
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                     "traffic": traffic,
                      "flops_per_launch": eu_flops, "avg_launch_ms": round(eu_ms, 4)},
         "roofline_aggregate": {"kernel": "aggregate (CSR segmented sums, in and out)",
                                "bound": "hbm", "achieved": round(ag_gbs, 1),
@@ -172,6 +197,63 @@ def main():
             "value": round(E / dt, 1), "unit": "edges/s", "cores": cores, "kind": "oracle",
             "sample": f"one complete fp64 oracle inference of the same {N}-node / {E}-edge "
                       f"event (H={H}, T={T}) on {cores} host threads, {dt:.1f} s"}
+    print(json.dumps(rec), flush=True)
+
+
+def bench_batch(args, cfg):
+    """Ragged service batch: 8 independent events, one stream each, one handle."""
+    import numpy as np
+    import torch
+
+    from paper_2402_09633_amd import gnn as G
+    from paper_2402_09633_amd import inputs as I
+
+    events = I.make_batch(cfg)
+    H, T = cfg.hidden, cfg.n_iters
+    w = I.make_weights(3, H, 1, cfg.weight_seed)
+    torch.cuda.set_device(0)
+    m = G.Model(w, G.make_dims(3, H, T))
+    xs = [torch.as_tensor(g.x).cuda() for g in events]
+    eis = [torch.as_tensor(g.edge_index).cuda() for g in events]
+    outs = [torch.empty(g.n_edges, device="cuda") for g in events]
+    streams = [torch.cuda.Stream() for _ in events]
+    total_e = sum(g.n_edges for g in events)
+
+    def one_batch(evs=None):
+        for k, st in enumerate(streams):
+            if evs is not None:
+                evs[k][0].record(st)
+            G.gnn_infer(m.handle, xs[k], eis[k], xs[k].shape[0], eis[k].shape[1], outs[k], st)
+            if evs is not None:
+                evs[k][1].record(st)
+
+    for _ in range(args.warmup):
+        one_batch()
+    torch.cuda.synchronize()
+    samples = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in streams]
+        one_batch(evs)
+        samples.append(evs)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    per = np.array([a.elapsed_time(b) for evs in samples for a, b in evs])
+    m.close()
+    ms_per_batch = (t1 - t0) * 1000.0 / args.steps
+    rec = {
+        "metric": "aggregate edges/sec and p50/p99 ms/event, ragged batch of 8 events on 8 streams",
+        "value": round(total_e / (ms_per_batch / 1000.0), 1), "unit": "edges/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_batch, 4),
+        "higher_is_better": True, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"batch: 8 events, N={[g.n_nodes for g in events]}, "
+                               f"E={[g.n_edges for g in events]}, H={H}, T={T}, fp32"},
+        "ms_per_event_p50": round(float(np.percentile(per, 50)), 3),
+        "ms_per_event_p99": round(float(np.percentile(per, 99)), 3),
+        "note": "per-event times overlap across streams; the aggregate rate is the sum of "
+                "edges over the wall time of the batch",
+    }
     print(json.dumps(rec), flush=True)
 
 

@@ -8,7 +8,11 @@
 // fully coalesced 256/512-byte chunk, sums run in a fixed order (bitwise
 // reproducible, no float atomics), and empty rows are written as zeros.
 // Four rows are loaded before they are added to keep several HBM requests
-// in flight per lane.  Accumulation is fp32 in both storage modes.
+// in flight per lane.  Accumulation is fp32 in both storage modes.  Rows
+// longer than LONG_ROW messages use Neumaier's compensated summation: a hub
+// node can receive 10^5 messages, where a plain fp32 running sum drifts by
+// ~10^-4 relative, while the compensated sum stays within a few ulps of the
+// exact sum at any length.  Either way the order is fixed.
 #include "gnn_internal.h"
 
 namespace gnn {
@@ -18,6 +22,60 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 
 constexpr int THREADS = 256;
+constexpr int LONG_ROW = 32;
+
+// One step of Neumaier summation: s + c carries the running sum.  With
+// COMP false it is a plain sum (c stays 0).
+template <bool COMP>
+__device__ __forceinline__ void nsum(float &s, float &c, float x) {
+  if constexpr (COMP) {
+    const float t = s + x;
+    c += fabsf(s) >= fabsf(x) ? (s - t) + x : (x - t) + s;
+    s = t;
+  } else {
+    s += x;
+  }
+}
+
+template <int H, bool COMP>
+__device__ __forceinline__ void row_sum_f32(const float *__restrict__ base,
+                                            const int32_t *__restrict__ perm, int32_t p,
+                                            int32_t pe, float (&s)[4], float (&c)[4]) {
+  for (; p + 4 <= pe; p += 4) {
+    f4 r[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) r[u] = *(const f4 *)(base + (int64_t)perm[p + u] * H);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) nsum<COMP>(s[k], c[k], r[u][k]);
+  }
+  for (; p < pe; ++p) {
+    const f4 r = *(const f4 *)(base + (int64_t)perm[p] * H);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) nsum<COMP>(s[k], c[k], r[k]);
+  }
+}
+
+template <int H, bool COMP>
+__device__ __forceinline__ void row_sum_bf16(const __bf16 *__restrict__ base,
+                                             const int32_t *__restrict__ perm, int32_t p,
+                                             int32_t pe, float (&s)[8], float (&c)[8]) {
+  for (; p + 4 <= pe; p += 4) {
+    bf8 r[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) r[u] = *(const bf8 *)(base + (int64_t)perm[p + u] * H);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int k = 0; k < 8; ++k) nsum<COMP>(s[k], c[k], (float)r[u][k]);
+  }
+  for (; p < pe; ++p) {
+    const bf8 r = *(const bf8 *)(base + (int64_t)perm[p] * H);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) nsum<COMP>(s[k], c[k], (float)r[k]);
+  }
+}
 
 template <int H>
 __global__ __launch_bounds__(THREADS) void segsum_f32(
@@ -38,20 +96,13 @@ __global__ __launch_bounds__(THREADS) void segsum_f32(
   int32_t p = rp[v];
   const int32_t pe = rp[v + 1];
   const float *base = e + 4 * sub;
-  f4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (; p + 4 <= pe; p += 4) {
-    const int64_t j0 = perm[p], j1 = perm[p + 1], j2 = perm[p + 2], j3 = perm[p + 3];
-    const f4 r0 = *(const f4 *)(base + j0 * H);
-    const f4 r1 = *(const f4 *)(base + j1 * H);
-    const f4 r2 = *(const f4 *)(base + j2 * H);
-    const f4 r3 = *(const f4 *)(base + j3 * H);
-    acc += r0;
-    acc += r1;
-    acc += r2;
-    acc += r3;
-  }
-  for (; p < pe; ++p) acc += *(const f4 *)(base + (int64_t)perm[p] * H);
-  *(f4 *)(dst + v * H + 4 * sub) = acc;
+  float s[4] = {0.f, 0.f, 0.f, 0.f}, c[4] = {0.f, 0.f, 0.f, 0.f};
+  if (pe - p > LONG_ROW)
+    row_sum_f32<H, true>(base, perm, p, pe, s, c);
+  else
+    row_sum_f32<H, false>(base, perm, p, pe, s, c);
+  const f4 res = {s[0] + c[0], s[1] + c[1], s[2] + c[2], s[3] + c[3]};
+  *(f4 *)(dst + v * H + 4 * sub) = res;
 }
 
 template <int H>
@@ -73,24 +124,15 @@ __global__ __launch_bounds__(THREADS) void segsum_bf16(
   int32_t p = rp[v];
   const int32_t pe = rp[v + 1];
   const __bf16 *base = e + 8 * sub;
-  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (; p + 4 <= pe; p += 4) {
-    bf8 r[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) r[u] = *(const bf8 *)(base + (int64_t)perm[p + u] * H);
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int k = 0; k < 8; ++k) acc[k] += (float)r[u][k];
-  }
-  for (; p < pe; ++p) {
-    const bf8 r = *(const bf8 *)(base + (int64_t)perm[p] * H);
-#pragma unroll
-    for (int k = 0; k < 8; ++k) acc[k] += (float)r[k];
-  }
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float c[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (pe - p > LONG_ROW)
+    row_sum_bf16<H, true>(base, perm, p, pe, s, c);
+  else
+    row_sum_bf16<H, false>(base, perm, p, pe, s, c);
   bf8 o;
 #pragma unroll
-  for (int k = 0; k < 8; ++k) o[k] = (__bf16)acc[k];
+  for (int k = 0; k < 8; ++k) o[k] = (__bf16)(s[k] + c[k]);
   *(bf8 *)(dst + v * H + 8 * sub) = o;
 }
 

@@ -274,3 +274,19 @@ def test_validate_indices_reports_bad_index(G):
         torch.cuda.synchronize()
     finally:
         m.close()
+
+
+@pytest.mark.parametrize("flags", PATHS)
+def test_hub_graph_long_segments(G, oracle_mod, flags):
+    # one node receives half of all edges and another sends a fifth of them:
+    # aggregation rows of ~150k and ~60k messages
+    rng = np.random.default_rng(31)
+    n, e = 5000, 300_000
+    x = rng.normal(size=(n, 3)).astype(np.float32)
+    ei = rng.integers(0, n, size=(2, e)).astype(np.int32)
+    ei[1, rng.random(e) < 0.5] = 17
+    ei[0, rng.random(e) < 0.2] = 4999
+    w = I.make_weights(3, 64, 1, 31, affine_noise=0.2)
+    ref = oracle_mod.forward(w, x, ei, 64, 2)
+    got = run_model(G, w, G.make_dims(3, 64, 2, flags=flags), x, ei)
+    assert_logits_close(got, ref["logits"])
