@@ -132,6 +132,18 @@ def main():
     prof = G.gnn_profile_read(m.handle)
     G.gnn_profile_enable(m.handle, False)
     per = np.array([a.elapsed_time(b) for a, b in evs])
+
+    # Next pipeline step, measured on its own: connected components of the
+    # edges scoring above 0.5 (labels = smallest hit id per component).
+    labels = torch.empty(N, dtype=torch.int32, device="cuda")
+    G.gnn_wcc(ei, out, 0.5, N, E, labels)
+    torch.cuda.synchronize()
+    tw = time.perf_counter()
+    for _ in range(5):
+        G.gnn_wcc(ei, out, 0.5, N, E, labels)
+    torch.cuda.synchronize()
+    wcc_ms = (time.perf_counter() - tw) * 1000.0 / 5
+    n_comp = int(torch.unique(labels).numel())
     m.close()
 
     ms_per_step = (t1 - t0) * 1000.0 / args.steps
@@ -185,6 +197,11 @@ def main():
                                "bytes_per_launch": ag_bytes, "avg_launch_ms": round(ag_ms, 4)},
         "stages_ms_per_event": {k: round(v["ms"] / max(prof["n_calls"], 1), 4)
                                 for k, v in prof.items() if k != "n_calls"},
+        "components": {"ms_per_event": round(wcc_ms, 4), "threshold": 0.5,
+                       "n_components": n_comp,
+                       "note": "weakly-connected components of the edges scoring above the "
+                               "threshold, after inference (wall time, host-checked rounds); "
+                               "not part of value"},
     }
 
     if not args.no_cpu_baseline:

@@ -110,6 +110,26 @@ int gnn_infer_logits(gnn_handle *h, const float *node_feat, const int32_t *edge_
                      int64_t n_nodes, int64_t n_edges, float *edge_logits,
                      hipStream_t stream);
 
+/* Track candidates from edge scores (paper section 2.1: the GNN edge scores
+ * are passed to the weakly-connected-components step; section 2.3: one
+ * integer label per space point).  Keeps the edges with
+ * edge_scores[j] > threshold (every edge when edge_scores is NULL), treats
+ * them as undirected and writes labels[v] = the smallest node id of v's
+ * connected component -- unique, so results are bitwise reproducible.
+ *   edge_index [2][n_edges] int32 (device), edge_scores [n_edges] fp32
+ *   (device) or NULL, labels [n_nodes] int32 (device, output).
+ * Runs on the current device; the host checks convergence between rounds,
+ * so the call returns after `stream` has drained.  GNN_E_INVALID_ARG for
+ * bad counts or NULL pointers; out-of-range indices are clamped. */
+int gnn_wcc(const int32_t *edge_index, const float *edge_scores, float threshold,
+            int64_t n_nodes, int64_t n_edges, int32_t *labels, hipStream_t stream);
+
+/* Hits in, labels out: gnn_infer, then gnn_wcc on its scores.  edge_scores
+ * may be NULL (scores then live in a temporary buffer). */
+int gnn_infer_labels(gnn_handle *h, const float *node_feat, const int32_t *edge_index,
+                     int64_t n_nodes, int64_t n_edges, float threshold, float *edge_scores,
+                     int32_t *labels, hipStream_t stream);
+
 /* Waits for the device, then frees everything the handle owns.  NULL-safe. */
 void gnn_destroy(gnn_handle *h);
 

@@ -35,10 +35,18 @@
  * iteration the edge update uses the old h and e, aggregation sums the new
  * e, and the node update uses the old h.
  *
+ * Track candidates (paper section 2.1: the edge scores are passed to the
+ * weakly-connected-components step; section 2.3: the custom backend returns
+ * one integer label per space point): oracle_wcc keeps the edges whose score
+ * exceeds a threshold, treats them as undirected, and labels every node with
+ * the smallest node id of its connected component, found by breadth-first
+ * search.
+ *
  * Every function here is pinned by the CPU tests against something other
  * than itself: a torch-CPU library evaluation of one hidden layer, an
  * incidence-matrix brute force on tiny graphs, closed forms (all-zero
- * weights, constant messages) and invariances (edge order, node labels).
+ * weights, constant messages), invariances (edge order, node labels), and
+ * scipy's connected_components for the labels.
  */
 #include <math.h>
 #include <stdint.h>
@@ -382,4 +390,56 @@ done:
   free(h); free(h2); free(e); free(e2); free(ain); free(aout);
   model_free(&m);
   return rc;
+}
+
+/* Connected components of the undirected graph of kept edges
+ * (score > threshold; all edges when scores is NULL).  labels[v] = smallest
+ * node id in v's component.  Returns -4 for an out-of-range index. */
+int oracle_wcc(long n_nodes, long n_edges, const int32_t *edge_index, const float *scores,
+               float threshold, int32_t *labels) {
+  if (n_nodes < 0 || n_edges < 0) return -1;
+  const int32_t *src = edge_index, *dst = edge_index + n_edges;
+  for (long j = 0; j < n_edges; ++j)
+    if (src[j] < 0 || src[j] >= n_nodes || dst[j] < 0 || dst[j] >= n_nodes) return -4;
+  /* adjacency lists of the kept edges, both directions */
+  long *deg = (long *)calloc((size_t)n_nodes + 1, sizeof(long));
+  for (long j = 0; j < n_edges; ++j)
+    if (!scores || scores[j] > threshold) {
+      deg[src[j] + 1] += 1;
+      deg[dst[j] + 1] += 1;
+    }
+  for (long v = 0; v < n_nodes; ++v) deg[v + 1] += deg[v];
+  int32_t *adj = (int32_t *)malloc(sizeof(int32_t) * (size_t)(deg[n_nodes] > 0 ? deg[n_nodes] : 1));
+  long *fill = (long *)malloc(sizeof(long) * (size_t)(n_nodes > 0 ? n_nodes : 1));
+  for (long v = 0; v < n_nodes; ++v) fill[v] = deg[v];
+  for (long j = 0; j < n_edges; ++j)
+    if (!scores || scores[j] > threshold) {
+      adj[fill[src[j]]++] = dst[j];
+      adj[fill[dst[j]]++] = src[j];
+    }
+  /* BFS from every unlabelled node in increasing id order: the start node
+   * is then the smallest id of its component */
+  int32_t *queue = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n_nodes > 0 ? n_nodes : 1));
+  for (long v = 0; v < n_nodes; ++v) labels[v] = -1;
+  for (long v = 0; v < n_nodes; ++v) {
+    if (labels[v] >= 0) continue;
+    long head = 0, tail = 0;
+    labels[v] = (int32_t)v;
+    queue[tail++] = (int32_t)v;
+    while (head < tail) {
+      const int32_t u = queue[head++];
+      for (long k = deg[u]; k < deg[u + 1]; ++k) {
+        const int32_t w = adj[k];
+        if (labels[w] < 0) {
+          labels[w] = (int32_t)v;
+          queue[tail++] = w;
+        }
+      }
+    }
+  }
+  free(deg);
+  free(adj);
+  free(fill);
+  free(queue);
+  return 0;
 }

@@ -54,6 +54,8 @@ def lib():
         L.oracle_forward.argtypes = [_fp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                      ctypes.c_double, _fp, _ip, ctypes.c_long, ctypes.c_long,
                                      _dp, _dp, ctypes.c_int, _dp, _dp, _dp, _dp]
+        L.oracle_wcc.restype = ctypes.c_int
+        L.oracle_wcc.argtypes = [ctypes.c_long, ctypes.c_long, _ip, _fp, ctypes.c_float, _ip]
         L.oracle_max_threads.restype = ctypes.c_int
         L.oracle_set_threads.argtypes = [ctypes.c_int]
         _lib = L
@@ -129,3 +131,16 @@ def forward(weights, x, edge_index, hidden, n_iters, n_mp_weight_sets=1, eps=1e-
     if rc:
         raise ValueError(f"oracle_forward failed ({rc})")
     return out
+
+
+def wcc(edge_index, n_nodes, scores=None, threshold=0.5):
+    """Component label (smallest node id of the component) of every node, over
+    the undirected graph of edges with score > threshold (all if scores=None)."""
+    ei = np.ascontiguousarray(edge_index, np.int32).reshape(2, -1)
+    sc = None if scores is None else np.ascontiguousarray(scores, np.float32)
+    lab = np.zeros(max(n_nodes, 1), np.int32)
+    rc = lib().oracle_wcc(n_nodes, ei.shape[1], _ptr(ei, _ip), _ptr(sc, _fp), float(threshold),
+                          _ptr(lab, _ip))
+    if rc:
+        raise ValueError(f"oracle_wcc failed ({rc})")
+    return lab[:n_nodes]

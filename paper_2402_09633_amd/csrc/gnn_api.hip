@@ -917,6 +917,76 @@ int gnn_infer_logits(gnn_handle *h, const float *node_feat, const int32_t *edge_
   return run(h, node_feat, edge_index, n_nodes, n_edges, stream, ro);
 }
 
+int gnn_wcc(const int32_t *edge_index, const float *edge_scores, float threshold,
+            int64_t n_nodes, int64_t n_edges, int32_t *labels, hipStream_t stream) {
+  if (n_nodes < 0 || n_edges < 0) return fail(GNN_E_INVALID_ARG, "negative count");
+  if (n_nodes > INT32_MAX || n_edges > INT32_MAX)
+    return fail(GNN_E_INVALID_ARG, "count above INT32_MAX");
+  if (n_edges > 0 && n_nodes == 0) return fail(GNN_E_INVALID_ARG, "n_edges > 0 with n_nodes == 0");
+  if (n_nodes == 0) return GNN_OK;
+  if (!labels || (n_edges > 0 && !edge_index))
+    return fail(GNN_E_INVALID_ARG, "NULL labels or edge_index");
+  const int32_t n = (int32_t)n_nodes;
+  // Hooking onto the smaller root plus full compression converges in a few
+  // rounds on graphs of tracks (and in O(log n) on typical graphs); a call
+  // that has not converged after max_rounds fails instead of returning
+  // partial labels.
+  const int max_rounds = 256;
+  int rc = GNN_OK;
+  bool converged = n_edges == 0;
+  int32_t *changed = nullptr;
+  {
+    hipError_t ae = hipMallocAsync((void **)&changed, sizeof(int32_t), stream);
+    if (ae != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(GNN_E_OOM, "hipMallocAsync failed: %s", hipGetErrorString(ae));
+    }
+  }
+  HIP_TRY(wcc_launch_init(labels, n, stream));
+  for (int r = 0; r < max_rounds && n_edges > 0; ++r) {
+    int32_t host_changed = 0;
+    HIP_TRY(launch_fill_i32(changed, 1, 0, stream));
+    HIP_TRY(wcc_launch_round(edge_index, edge_scores, threshold, n_edges, n, labels, changed,
+                             stream));
+    HIP_TRY(hipMemcpyAsync(&host_changed, changed, sizeof(int32_t), hipMemcpyDeviceToHost,
+                           stream));
+    HIP_TRY(hipStreamSynchronize(stream));
+    if (!host_changed) {
+      converged = true;
+      break;
+    }
+  }
+  if (!converged) rc = fail(GNN_E_UNSUPPORTED, "components did not converge in %d rounds",
+                            max_rounds);
+out:
+  {
+    hipError_t fe = hipFreeAsync(changed, stream);
+    if (fe != hipSuccess && rc == GNN_OK)
+      rc = fail(GNN_E_HIP, "hipFreeAsync failed: %s", hipGetErrorString(fe));
+  }
+  return rc;
+}
+
+int gnn_infer_labels(gnn_handle *h, const float *node_feat, const int32_t *edge_index,
+                     int64_t n_nodes, int64_t n_edges, float threshold, float *edge_scores,
+                     int32_t *labels, hipStream_t stream) {
+  int rc = check_counts(h, n_nodes, n_edges);
+  if (rc) return rc;
+  if (n_nodes > 0 && !labels) return fail(GNN_E_INVALID_ARG, "labels is NULL");
+  float *scores = edge_scores;
+  if (n_edges > 0 && !scores) {
+    hipError_t ae = hipMallocAsync((void **)&scores, (size_t)n_edges * sizeof(float), stream);
+    if (ae != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(GNN_E_OOM, "hipMallocAsync failed: %s", hipGetErrorString(ae));
+    }
+  }
+  rc = gnn_infer(h, node_feat, edge_index, n_nodes, n_edges, scores, stream);
+  if (rc == GNN_OK) rc = gnn_wcc(edge_index, scores, threshold, n_nodes, n_edges, labels, stream);
+  if (scores != edge_scores) (void)hipFreeAsync(scores, stream);
+  return rc;
+}
+
 int gnn_debug_csr(gnn_handle *h, const int32_t *edge_index, int64_t n_nodes, int64_t n_edges,
                   int32_t *row_ptr_in, int32_t *perm_in, int32_t *row_ptr_out, int32_t *perm_out,
                   hipStream_t stream) {

@@ -114,6 +114,14 @@ hipError_t build_csr(const int32_t *edge_index, int32_t n_edges, int32_t n_nodes
                      int32_t *row_ptr_in, int32_t *perm_in, int32_t *row_ptr_out,
                      int32_t *perm_out, const CsrScratch &s, hipStream_t stream);
 
+// Weakly-connected components (wcc.hip): labels <- identity, then rounds of
+// hooking over the kept edges and pointer jumping; `changed` is set to 1 by
+// a round that joined two trees.
+hipError_t wcc_launch_init(int32_t *labels, int32_t n, hipStream_t stream);
+hipError_t wcc_launch_round(const int32_t *edge_index, const float *scores, float threshold,
+                            int64_t n_edges, int32_t n_nodes, int32_t *labels,
+                            int32_t *changed, hipStream_t stream);
+
 // flag <- 1 if any of the 2*n_edges indices lies outside [0, n_nodes).
 hipError_t launch_validate(const int32_t *edge_index, int64_t n_edges, int32_t n_nodes,
                            int32_t *flag, hipStream_t stream);

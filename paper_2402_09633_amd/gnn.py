@@ -29,9 +29,9 @@ GNN_BF16 = 1
 GNN_VALIDATE_INDICES = 1
 GNN_LITERAL_GATHER = 2
 
-EXPORTS = ("gnn_weight_count", "gnn_create", "gnn_infer", "gnn_infer_logits", "gnn_destroy",
-           "gnn_last_error", "gnn_profile_enable", "gnn_profile_read", "gnn_debug_csr",
-           "gnn_debug_stages")
+EXPORTS = ("gnn_weight_count", "gnn_create", "gnn_infer", "gnn_infer_logits", "gnn_wcc",
+           "gnn_infer_labels", "gnn_destroy", "gnn_last_error", "gnn_profile_enable",
+           "gnn_profile_read", "gnn_debug_csr", "gnn_debug_stages")
 STAGES = ("csr", "node_enc", "edge_enc", "edge_update", "aggregate", "node_update",
           "classifier", "total")
 
@@ -74,6 +74,10 @@ def _load():
         f = getattr(L, name)
         f.restype = ctypes.c_int
         f.argtypes = [vp, vp, vp, i64, i64, vp, vp]
+    L.gnn_wcc.restype = ctypes.c_int
+    L.gnn_wcc.argtypes = [vp, vp, ctypes.c_float, i64, i64, vp, vp]
+    L.gnn_infer_labels.restype = ctypes.c_int
+    L.gnn_infer_labels.argtypes = [vp, vp, vp, i64, i64, ctypes.c_float, vp, vp, vp]
     L.gnn_destroy.restype = None
     L.gnn_destroy.argtypes = [vp]
     L.gnn_last_error.restype = ctypes.c_char_p
@@ -166,6 +170,24 @@ def gnn_infer_logits(handle, node_feat, edge_index, n_nodes: int, n_edges: int, 
     _check_io(node_feat, edge_index, edge_logits)
     return _check(lib.gnn_infer_logits(handle, _addr(node_feat), _addr(edge_index), n_nodes,
                                        n_edges, _addr(edge_logits), _stream(stream)))
+
+
+def gnn_wcc(edge_index, edge_scores, threshold: float, n_nodes: int, n_edges: int, labels,
+            stream=None) -> int:
+    """Component labels (smallest node id per component) of the edges scoring
+    above `threshold`; edge_scores may be None (every edge kept)."""
+    for t, dt in ((edge_index, torch.int32), (edge_scores, torch.float32), (labels, torch.int32)):
+        if isinstance(t, torch.Tensor) and t.dtype != dt:
+            raise TypeError(f"expected {dt}, got {t.dtype}")
+    return _check(lib.gnn_wcc(_addr(edge_index), _addr(edge_scores), float(threshold), n_nodes,
+                              n_edges, _addr(labels), _stream(stream)))
+
+
+def gnn_infer_labels(handle, node_feat, edge_index, n_nodes: int, n_edges: int,
+                     threshold: float, edge_scores, labels, stream=None) -> int:
+    return _check(lib.gnn_infer_labels(handle, _addr(node_feat), _addr(edge_index), n_nodes,
+                                       n_edges, float(threshold), _addr(edge_scores),
+                                       _addr(labels), _stream(stream)))
 
 
 def gnn_profile_enable(handle, enable: bool = True) -> int:

@@ -87,9 +87,11 @@ def test_create_without_device_reports_no_device(G):
 
 
 def test_no_float_atomics_in_kernels():
-    # Aggregation must be deterministic: the only atomics are the radix
-    # sort's uint32 digit counters (LDS `cnt`, global `totals`).
-    allowed = ("atomicAdd(&cnt[", "atomicAdd(&S.totals[")
+    # Aggregation must be deterministic: the only atomics are integer ones --
+    # the radix sort's uint32 digit counters (LDS `cnt`, global `totals`) and
+    # the components' int32 parent array (atomicMin, relaxed loads).
+    allowed = ("atomicAdd(&cnt[", "atomicAdd(&S.totals[", "atomicMin(&parent[",
+               "__hip_atomic_load(parent")
     for f in os.listdir(CSRC):
         text = open(os.path.join(CSRC, f)).read()
         for line in text.splitlines():
@@ -98,6 +100,8 @@ def test_no_float_atomics_in_kernels():
                 assert any(a in code for a in allowed), f"{f}: {line.strip()}"
     csr = open(os.path.join(CSRC, "csr.hip")).read()
     assert "uint32_t cnt[" in csr and "uint32_t *totals[2]" in csr
+    wcc = open(os.path.join(CSRC, "wcc.hip")).read()
+    assert "int32_t *parent" in wcc and "float *parent" not in wcc
 
 
 def test_product_path_never_touches_the_oracle():

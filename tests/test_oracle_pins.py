@@ -204,3 +204,42 @@ def test_forward_rejects_bad_indices(oracle_mod):
     w = I.make_weights(3, 8, 1, 17)
     with pytest.raises(ValueError):
         oracle_mod.forward(w, x, ei, 8, 1)
+
+
+def _canonical(labels):
+    """Map any component labelling to 'smallest node id of the component'."""
+    labels = np.asarray(labels)
+    first = {}
+    for v, c in enumerate(labels):
+        first.setdefault(c, v)
+    return np.array([first[c] for c in labels], np.int32)
+
+
+@pytest.mark.parametrize("seed,n,e,thr", [(0, 50, 40, 0.5), (1, 300, 400, 0.3), (2, 1000, 900, 0.7),
+                                          (3, 20, 0, 0.5), (4, 1, 3, 0.5)])
+def test_wcc_matches_scipy(oracle_mod, seed, n, e, thr):
+    from scipy.sparse import coo_matrix
+    from scipy.sparse.csgraph import connected_components
+    rng = np.random.default_rng(seed)
+    ei = rng.integers(0, n, size=(2, e)).astype(np.int32)
+    sc = rng.random(e).astype(np.float32)
+    got = oracle_mod.wcc(ei, n, sc, thr)
+    keep = sc > thr
+    A = coo_matrix((np.ones(keep.sum()), (ei[0, keep], ei[1, keep])), shape=(n, n))
+    _, lab = connected_components(A, directed=True, connection="weak")
+    np.testing.assert_array_equal(got, _canonical(lab))
+    assert (got <= np.arange(n)).all() and (got[got] == got).all()
+
+
+def test_wcc_threshold_and_order_invariance(oracle_mod):
+    rng = np.random.default_rng(5)
+    n, e = 500, 700
+    ei = rng.integers(0, n, size=(2, e)).astype(np.int32)
+    sc = rng.random(e).astype(np.float32)
+    a = oracle_mod.wcc(ei, n, sc, 0.4)
+    keep = sc > 0.4
+    np.testing.assert_array_equal(a, oracle_mod.wcc(ei[:, keep], n))        # pre-filtered
+    p = rng.permutation(e)
+    np.testing.assert_array_equal(a, oracle_mod.wcc(ei[:, p], n, sc[p], 0.4))  # edge order
+    np.testing.assert_array_equal(a, oracle_mod.wcc(ei[::-1].copy(), n, sc, 0.4))  # direction
+    assert (oracle_mod.wcc(ei, n, np.zeros(e, np.float32), 0.5) == np.arange(n)).all()
