@@ -145,6 +145,7 @@ def main():
     wcc_ms = (time.perf_counter() - tw) * 1000.0 / 5
     n_comp = int(torch.unique(labels).numel())
     m.close()
+    filt = bench_filter(G, I, cfg) if cfg.name == "full" else None
 
     ms_per_step = (t1 - t0) * 1000.0 / args.steps
     value = E / (ms_per_step / 1000.0)
@@ -203,6 +204,8 @@ def main():
                                "threshold, after inference (wall time, host-checked rounds); "
                                "not part of value"},
     }
+    if filt:
+        rec["filter"] = filt
 
     if not args.no_cpu_baseline:
         from oracle import oracle as O
@@ -215,6 +218,31 @@ def main():
             "sample": f"one complete fp64 oracle inference of the same {N}-node / {E}-edge "
                       f"event (H={H}, T={T}) on {cores} host threads, {dt:.1f} s"}
     print(json.dumps(rec), flush=True)
+
+
+def bench_filter(G, I, cfg):
+    """The step before the GNN: filter MLP + threshold compaction over the
+    candidate edges of the same hits (wide windows, ~2.1M candidates)."""
+    import torch
+    g = I.layered_graph(cfg.n_nodes, cfg.graph_seed, I.DPHI_MID, I.DZ_MID)
+    f = G.gnn_filter_create(I.make_filter_weights(3, 64, 77), G.make_filter_dims(3, 64))
+    x = torch.as_tensor(g.x).cuda()
+    ei = torch.as_tensor(g.edge_index).cuda()
+    sc = torch.empty(g.n_edges, device="cuda")
+    out = torch.empty(2 * g.n_edges, dtype=torch.int32, device="cuda")
+    kept = G.gnn_filter_apply(f, x, ei, g.n_nodes, g.n_edges, 0.5, sc, out)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    for _ in range(5):
+        kept = G.gnn_filter_apply(f, x, ei, g.n_nodes, g.n_edges, 0.5, sc, out)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t) * 1000.0 / 5
+    G.gnn_filter_destroy(f)
+    return {"ms_per_event": round(ms, 4), "candidates": g.n_edges, "kept": kept,
+            "candidate_edges_per_s": round(g.n_edges / (ms / 1000.0), 1),
+            "note": "filter MLP (2F->64->64->1) + stable compaction at 0.5 on the same hits "
+                    "with the wide windows (wall time incl. the count read-back); not part "
+                    "of value"}
 
 
 def bench_batch(args, cfg):

@@ -110,6 +110,35 @@ int gnn_infer_logits(gnn_handle *h, const float *node_feat, const int32_t *edge_
                      int64_t n_nodes, int64_t n_edges, float *edge_logits,
                      hipStream_t stream);
 
+/* ---- edge filter (the step before the GNN) --------------------------------
+ * Paper section 2.1: after the embedding step a Filtering MLP scores every
+ * candidate edge and applyFiltering keeps the edges above a fixed threshold.
+ * Model: s_j = sigmoid(w . phi(W1 phi(W0 [x_src; x_dst] + b0) + b1) + c),
+ * phi = LayerNorm then ReLU.  Blob (fp32, W [out][in]): layer 0 (2F -> H:
+ * W, b, gamma, beta), layer 1 (H -> H: W, b, gamma, beta), head (H -> 1: W,
+ * b). */
+typedef struct gnn_filter_dims {
+  uint32_t struct_size; /* = sizeof(gnn_filter_dims)          */
+  int32_t in_features;  /* F, 1..16                           */
+  int32_t hidden;       /* H, 64 or 128                        */
+  float ln_eps;         /* LayerNorm epsilon                   */
+} gnn_filter_dims;
+
+typedef struct gnn_filter gnn_filter;
+
+size_t gnn_filter_weight_count(const gnn_filter_dims *dims);
+gnn_filter *gnn_filter_create(const float *weights, const gnn_filter_dims *dims);
+void gnn_filter_destroy(gnn_filter *f);
+
+/* Scores the n_edges candidate edges (edge_scores, [n_edges] fp32 device,
+ * may be NULL) and writes the edges with score > threshold, in input order,
+ * as a contiguous [2][n_kept] int32 edge_index to edge_index_out (device,
+ * room for 2 * n_edges).  *n_kept (host) receives the count, so the call
+ * returns after `stream` has drained. */
+int gnn_filter_apply(gnn_filter *f, const float *node_feat, const int32_t *edge_index,
+                     int64_t n_nodes, int64_t n_edges, float threshold, float *edge_scores,
+                     int32_t *edge_index_out, int64_t *n_kept, hipStream_t stream);
+
 /* Track candidates from edge scores (paper section 2.1: the GNN edge scores
  * are passed to the weakly-connected-components step; section 2.3: one
  * integer label per space point).  Keeps the edges with

@@ -42,6 +42,12 @@
  * the smallest node id of its connected component, found by breadth-first
  * search.
  *
+ * Edge filtering (paper section 2.1: an MLP scores the candidate edges and a
+ * fixed threshold on those scores removes clearly fake ones before the GNN):
+ * oracle_filter evaluates s_j = sigmoid(w . phi(W2 phi(W1 [x_src; x_dst] + b1)
+ * + b2) + c) per candidate edge and keeps, in input order, the edges with
+ * s_j > threshold.
+ *
  * Every function here is pinned by the CPU tests against something other
  * than itself: a torch-CPU library evaluation of one hidden layer, an
  * incidence-matrix brute force on tiny graphs, closed forms (all-zero
@@ -441,5 +447,62 @@ int oracle_wcc(long n_nodes, long n_edges, const int32_t *edge_index, const floa
   free(adj);
   free(fill);
   free(queue);
+  return 0;
+}
+
+long oracle_filter_weight_count(int F, int H) {
+  return layer_floats(2 * F, H, 1) + layer_floats(H, H, 1) + layer_floats(H, 1, 0);
+}
+
+/* Filter scores of every candidate edge (scores, may be NULL) and the ids of
+ * the kept edges in input order (kept, may be NULL; its count is returned
+ * through *n_kept).  Returns 0, -1 for bad arguments, -4 for a bad index. */
+int oracle_filter(const float *weights, int F, int H, double eps, const float *x,
+                  const int32_t *edge_index, long n_nodes, long n_edges, double threshold,
+                  double *scores, int64_t *kept, int64_t *n_kept) {
+  if (F <= 0 || H <= 0 || n_nodes < 0 || n_edges < 0 || (n_edges > 0 && n_nodes == 0)) return -1;
+  const int32_t *src = edge_index, *dst = edge_index + n_edges;
+  for (long j = 0; j < n_edges; ++j)
+    if (src[j] < 0 || src[j] >= n_nodes || dst[j] < 0 || dst[j] >= n_nodes) return -4;
+  double *store = (double *)malloc(sizeof(double) * (size_t)oracle_filter_weight_count(F, H));
+  double *d = store;
+  const float *p = weights;
+  omlp m;
+  olayer head;
+  p = take_layer(&m.l0, p, 2 * F, H, 1, &d);
+  p = take_layer(&m.l1, p, H, H, 1, &d);
+  p = take_layer(&head, p, H, 1, 0, &d);
+  double *sc = (double *)malloc(sizeof(double) * (size_t)(n_edges > 0 ? n_edges : 1));
+#pragma omp parallel
+  {
+    double *a = (double *)malloc(sizeof(double) * (size_t)2 * F);
+    double *tmp = (double *)malloc(sizeof(double) * (size_t)H);
+    double *hid = (double *)malloc(sizeof(double) * (size_t)H);
+#pragma omp for schedule(static)
+    for (long j = 0; j < n_edges; ++j) {
+      for (int k = 0; k < F; ++k) {
+        a[k] = x[(long)src[j] * F + k];
+        a[F + k] = x[(long)dst[j] * F + k];
+      }
+      mlp_hidden(&m, eps, a, tmp, hid);
+      double z;
+      linear(&head, hid, &z);
+      sc[j] = sigmoid(z);
+    }
+    free(a);
+    free(tmp);
+    free(hid);
+  }
+  long cnt = 0;
+  for (long j = 0; j < n_edges; ++j) {
+    if (scores) scores[j] = sc[j];
+    if (sc[j] > threshold) {
+      if (kept) kept[cnt] = j;
+      ++cnt;
+    }
+  }
+  if (n_kept) *n_kept = cnt;
+  free(sc);
+  free(store);
   return 0;
 }

@@ -56,6 +56,12 @@ def lib():
                                      _dp, _dp, ctypes.c_int, _dp, _dp, _dp, _dp]
         L.oracle_wcc.restype = ctypes.c_int
         L.oracle_wcc.argtypes = [ctypes.c_long, ctypes.c_long, _ip, _fp, ctypes.c_float, _ip]
+        L.oracle_filter_weight_count.restype = ctypes.c_long
+        L.oracle_filter_weight_count.argtypes = [ctypes.c_int, ctypes.c_int]
+        L.oracle_filter.restype = ctypes.c_int
+        L.oracle_filter.argtypes = [_fp, ctypes.c_int, ctypes.c_int, ctypes.c_double, _fp, _ip,
+                                    ctypes.c_long, ctypes.c_long, ctypes.c_double, _dp,
+                                    ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64)]
         L.oracle_max_threads.restype = ctypes.c_int
         L.oracle_set_threads.argtypes = [ctypes.c_int]
         _lib = L
@@ -144,3 +150,28 @@ def wcc(edge_index, n_nodes, scores=None, threshold=0.5):
     if rc:
         raise ValueError(f"oracle_wcc failed ({rc})")
     return lab[:n_nodes]
+
+
+def filter_weight_count(F: int, H: int) -> int:
+    return int(lib().oracle_filter_weight_count(F, H))
+
+
+def filter_edges(weights, x, edge_index, hidden, threshold=0.5, eps=1e-5):
+    """Filter-MLP scores of every candidate edge (fp64) and the ids of the
+    edges scoring above `threshold`, in input order."""
+    x = np.ascontiguousarray(x, np.float32)
+    n_nodes, F = x.shape
+    ei = np.ascontiguousarray(edge_index, np.int32).reshape(2, -1)
+    E = ei.shape[1]
+    w = np.ascontiguousarray(weights, np.float32)
+    if w.size != filter_weight_count(F, hidden):
+        raise ValueError("filter weight blob has the wrong size")
+    sc = np.zeros(max(E, 1))
+    kept = np.zeros(max(E, 1), np.int64)
+    nk = ctypes.c_int64(0)
+    rc = lib().oracle_filter(_ptr(w, _fp), F, hidden, float(eps), _ptr(x, _fp), _ptr(ei, _ip),
+                             n_nodes, E, float(threshold), _ptr(sc, _dp),
+                             kept.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), ctypes.byref(nk))
+    if rc:
+        raise ValueError(f"oracle_filter failed ({rc})")
+    return sc[:E], kept[:nk.value]

@@ -122,5 +122,34 @@ __device__ __forceinline__ void small_k_layer(f16v (&acc)[MB], const float *__re
   }
 }
 
+// out[mb] (mb < MB) = sum over k < H of Wf[MB0 + mb][k] * act[k]; Wf holds
+// fragments of an (MBT*32) x H matrix; act is in accumulator order.
+template <int MB, int MBT>
+__device__ __forceinline__ void gemm_acc_f32(f16v (&out)[MB], const f16v (&act)[MB],
+                                             const f4 *__restrict__ wf, int mb0) {
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) out[mb][v] = 0.f;
+  constexpr int G = MB * 4;
+  f4 wb[2][MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) wb[0][mb] = wf[(mb0 + mb) * 64];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const int cur = g & 1, nxt = cur ^ 1;
+    if (g + 1 < G) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) wb[nxt][mb] = wf[((g + 1) * MBT + mb0 + mb) * 64];
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+        out[mb] = __builtin_amdgcn_mfma_f32_32x32x2f32(wb[cur][mb][t], act[g / 4][4 * (g % 4) + t],
+                                                       out[mb], 0, 0, 0);
+  }
+}
+
 }  // namespace
 }  // namespace gnn

@@ -29,35 +29,6 @@ namespace {
 constexpr int NODE_WAVES = 4;
 constexpr int EDGE_WAVES = 8;
 
-// out[mb] (mb < MB) = sum over k < H of Wf[MB0 + mb][k] * act[k]; Wf holds
-// fragments of an (MBT*32) x H matrix; act is in accumulator order.
-template <int MB, int MBT>
-__device__ __forceinline__ void gemm_acc_f32(f16v (&out)[MB], const f16v (&act)[MB],
-                                             const f4 *__restrict__ wf, int mb0) {
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) out[mb][v] = 0.f;
-  constexpr int G = MB * 4;
-  f4 wb[2][MB];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) wb[0][mb] = wf[(mb0 + mb) * 64];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const int cur = g & 1, nxt = cur ^ 1;
-    if (g + 1 < G) {
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) wb[nxt][mb] = wf[((g + 1) * MBT + mb0 + mb) * 64];
-    }
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-        out[mb] = __builtin_amdgcn_mfma_f32_32x32x2f32(wb[cur][mb][t], act[g / 4][4 * (g % 4) + t],
-                                                       out[mb], 0, 0, 0);
-  }
-}
-
 // Layer 1 over the concatenation of three row sources with K = 3H.  A
 // lane's half-row of each source (16 float4) is loaded in one burst, the
 // next source's while the current one is multiplied, so an HBM miss is
@@ -122,7 +93,8 @@ struct WStream {
   const f4 *base;     // fragment stream in global memory
   int nchunks;        // chunks per tile
   f4 (*buf)[CH * MB * 64];
-  int c = 0;          // chunk index within the tile
+  int c = 0;          // chunk index within the tile (position in the stream)
+  int k = 0;          // chunks consumed so far (selects the LDS buffer)
   f4 st[MB];          // staged next chunk (CH*MB*64 f4 / 512 threads = MB each)
   __device__ void fetch(int cc, int tid) {
 #pragma unroll
@@ -136,11 +108,14 @@ struct WStream {
   __device__ const f4 *begin(int tid) {
     __syncthreads();
     fetch((c + 1) % nchunks, tid);
-    return buf[c & 1];
+    return buf[k & 1];
   }
-  // End of a chunk: publish the next one (read by others after the barrier).
+  // End of a chunk: publish the next one (read by others after the barrier)
+  // into the other buffer.  The buffer alternates with every chunk consumed,
+  // also across tiles when a tile has an odd number of chunks.
   __device__ void end(int tid) {
-    commit((c + 1) & 1, tid);
+    commit((k + 1) & 1, tid);
+    ++k;
     c = (c + 1) % nchunks;
   }
 };

@@ -917,6 +917,155 @@ int gnn_infer_logits(gnn_handle *h, const float *node_feat, const int32_t *edge_
   return run(h, node_feat, edge_index, n_nodes, n_edges, stream, ro);
 }
 
+struct gnn_filter {
+  gnn_filter_dims dims;
+  int device = 0;
+  void *dev = nullptr;
+  FilterArgs tmpl;  // weight pointers
+};
+
+namespace {
+int check_filter_dims(const gnn_filter_dims *d) {
+  if (!d) return fail(GNN_E_INVALID_ARG, "dims is NULL");
+  if (d->struct_size != sizeof(gnn_filter_dims))
+    return fail(GNN_E_INVALID_ARG, "gnn_filter_dims.struct_size mismatch");
+  if (d->in_features < 1 || d->in_features > 16)
+    return fail(GNN_E_INVALID_ARG, "in_features %d outside 1..16", d->in_features);
+  if (d->hidden != 64 && d->hidden != 128)
+    return fail(d->hidden > 0 && d->hidden % 32 == 0 ? GNN_E_UNSUPPORTED : GNN_E_INVALID_ARG,
+                "hidden %d not supported (64 or 128)", d->hidden);
+  if (!(d->ln_eps > 0.f) || !(d->ln_eps < 1.f))
+    return fail(GNN_E_INVALID_ARG, "ln_eps outside (0, 1)");
+  return GNN_OK;
+}
+}  // namespace
+
+size_t gnn_filter_weight_count(const gnn_filter_dims *d) {
+  if (check_filter_dims(d)) return 0;
+  const size_t F = d->in_features, H = d->hidden;
+  return layer_floats(2 * F, H, true) + layer_floats(H, H, true) + layer_floats(H, 1, false);
+}
+
+gnn_filter *gnn_filter_create(const float *weights, const gnn_filter_dims *dims) {
+  if (check_filter_dims(dims)) return nullptr;
+  if (!weights) {
+    fail(GNN_E_INVALID_ARG, "weights is NULL");
+    return nullptr;
+  }
+  int ndev = 0, dev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0 || hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    fail(GNN_E_NO_DEVICE, "no HIP device visible");
+    return nullptr;
+  }
+  const int F = dims->in_features, H = dims->hidden;
+  const float *p = weights;
+  auto next = [&](int fin, int fout, bool ln) {
+    BlobLayer L{p, nullptr, nullptr, nullptr, fin, fout};
+    p += (size_t)fin * fout;
+    L.b = p;
+    p += fout;
+    if (ln) {
+      L.g = p;
+      p += fout;
+      L.beta = p;
+      p += fout;
+    }
+    return L;
+  };
+  BlobLayer l0 = next(2 * F, H, true), l1 = next(H, H, true), l2 = next(H, 1, false);
+  Staging st;
+  LayerOff o0 = stage_layer(st, l0, WKind::PlainT, false, true);
+  LayerOff o1 = stage_layer(st, l1, WKind::FragAcc, false, true);
+  LayerOff o2 = stage_layer(st, l2, WKind::Plain, false, false);
+  gnn_filter *f = new gnn_filter();
+  f->dims = *dims;
+  f->device = dev;
+  if (hipMalloc(&f->dev, st.bytes.size()) != hipSuccess ||
+      hipMemcpy(f->dev, st.bytes.data(), st.bytes.size(), hipMemcpyHostToDevice) != hipSuccess) {
+    (void)hipGetLastError();
+    if (f->dev) (void)hipFree(f->dev);
+    delete f;
+    fail(GNN_E_OOM, "filter weight upload failed");
+    return nullptr;
+  }
+  const unsigned char *base = (const unsigned char *)f->dev;
+  LayerDev d0 = fix_layer(o0, base), d1 = fix_layer(o1, base), d2 = fix_layer(o2, base);
+  f->tmpl.F = F;
+  f->tmpl.eps = dims->ln_eps;
+  f->tmpl.w0t = (const float *)d0.w;
+  f->tmpl.b0 = d0.b;
+  f->tmpl.g0 = d0.g;
+  f->tmpl.beta0 = d0.beta;
+  f->tmpl.w1 = (const float *)d1.w;
+  f->tmpl.b1 = d1.b;
+  f->tmpl.g1 = d1.g;
+  f->tmpl.beta1 = d1.beta;
+  f->tmpl.w2 = (const float *)d2.w;
+  f->tmpl.b2 = d2.b;
+  return f;
+}
+
+void gnn_filter_destroy(gnn_filter *f) {
+  if (!f) return;
+  {
+    DeviceGuard guard(f->device);
+    (void)hipDeviceSynchronize();
+    (void)hipFree(f->dev);
+  }
+  delete f;
+}
+
+int gnn_filter_apply(gnn_filter *f, const float *node_feat, const int32_t *edge_index,
+                     int64_t n_nodes, int64_t n_edges, float threshold, float *edge_scores,
+                     int32_t *edge_index_out, int64_t *n_kept, hipStream_t stream) {
+  if (!f) return fail(GNN_E_INVALID_ARG, "filter is NULL");
+  if (n_nodes < 0 || n_edges < 0 || n_nodes > INT32_MAX || n_edges > INT32_MAX)
+    return fail(GNN_E_INVALID_ARG, "bad count");
+  if (n_edges > 0 && n_nodes == 0) return fail(GNN_E_INVALID_ARG, "n_edges > 0 with n_nodes == 0");
+  if (!n_kept) return fail(GNN_E_INVALID_ARG, "n_kept is NULL");
+  *n_kept = 0;
+  if (n_edges == 0) return GNN_OK;
+  if (!node_feat || !edge_index || !edge_index_out)
+    return fail(GNN_E_INVALID_ARG, "NULL input or output pointer");
+  DeviceGuard guard(f->device);
+  const size_t nt = compact_tiles(n_edges);
+  const size_t sc_bytes = edge_scores ? 0 : align256((size_t)n_edges * 4);
+  const size_t bytes = sc_bytes + align256((nt + 1) * 4) + 256;
+  int rc = GNN_OK;
+  unsigned char *ws = nullptr;
+  {
+    hipError_t ae = hipMallocAsync((void **)&ws, bytes, stream);
+    if (ae != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(GNN_E_OOM, "hipMallocAsync failed: %s", hipGetErrorString(ae));
+    }
+  }
+  float *scores = edge_scores ? edge_scores : (float *)ws;
+  int32_t *counts = (int32_t *)(ws + sc_bytes);
+  int32_t *total = counts + nt;
+  int32_t host_total = 0;
+  FilterArgs a = f->tmpl;
+  a.n_edges = n_edges;
+  a.n_nodes = (int32_t)n_nodes;
+  a.x = node_feat;
+  a.edge_index = edge_index;
+  a.scores = scores;
+  HIP_TRY(launch_filter_scores(f->dims.hidden, a, stream));
+  HIP_TRY(launch_compact(scores, edge_index, n_edges, threshold, counts, total, edge_index_out,
+                         stream));
+  HIP_TRY(hipMemcpyAsync(&host_total, total, 4, hipMemcpyDeviceToHost, stream));
+  HIP_TRY(hipStreamSynchronize(stream));
+  *n_kept = host_total;
+out:
+  {
+    hipError_t fe = hipFreeAsync(ws, stream);
+    if (fe != hipSuccess && rc == GNN_OK)
+      rc = fail(GNN_E_HIP, "hipFreeAsync failed: %s", hipGetErrorString(fe));
+  }
+  return rc;
+}
+
 int gnn_wcc(const int32_t *edge_index, const float *edge_scores, float threshold,
             int64_t n_nodes, int64_t n_edges, int32_t *labels, hipStream_t stream) {
   if (n_nodes < 0 || n_edges < 0) return fail(GNN_E_INVALID_ARG, "negative count");

@@ -114,6 +114,27 @@ hipError_t build_csr(const int32_t *edge_index, int32_t n_edges, int32_t n_nodes
                      int32_t *row_ptr_in, int32_t *perm_in, int32_t *row_ptr_out,
                      int32_t *perm_out, const CsrScratch &s, hipStream_t stream);
 
+// Edge filter (filter.hip): scores[j] = sigmoid(MLP([x_src; x_dst])).
+struct FilterArgs {
+  int64_t n_edges = 0;
+  int32_t n_nodes = 0;
+  const float *x = nullptr;  // [n_nodes][F]
+  int32_t F = 0;
+  const int32_t *edge_index = nullptr;
+  const float *w0t = nullptr, *b0 = nullptr, *g0 = nullptr, *beta0 = nullptr;  // W0 as [2F][H]
+  const float *w1 = nullptr, *b1 = nullptr, *g1 = nullptr, *beta1 = nullptr;   // fragments
+  const float *w2 = nullptr, *b2 = nullptr;                                   // head [H], [1]
+  float *scores = nullptr;
+  float eps = 1e-5f;
+};
+hipError_t launch_filter_scores(int hidden, const FilterArgs &a, hipStream_t stream);
+// Stable compaction of the edges with score > threshold into out
+// ([2][total] contiguous); counts has compact_tiles(n) entries.
+size_t compact_tiles(int64_t n);
+hipError_t launch_compact(const float *scores, const int32_t *edge_index, int64_t n,
+                          float threshold, int32_t *counts, int32_t *total, int32_t *out,
+                          hipStream_t stream);
+
 // Weakly-connected components (wcc.hip): labels <- identity, then rounds of
 // hooking over the kept edges and pointer jumping; `changed` is set to 1 by
 // a round that joined two trees.

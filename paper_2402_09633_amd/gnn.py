@@ -29,9 +29,10 @@ GNN_BF16 = 1
 GNN_VALIDATE_INDICES = 1
 GNN_LITERAL_GATHER = 2
 
-EXPORTS = ("gnn_weight_count", "gnn_create", "gnn_infer", "gnn_infer_logits", "gnn_wcc",
-           "gnn_infer_labels", "gnn_destroy", "gnn_last_error", "gnn_profile_enable",
-           "gnn_profile_read", "gnn_debug_csr", "gnn_debug_stages")
+EXPORTS = ("gnn_weight_count", "gnn_create", "gnn_infer", "gnn_infer_logits",
+           "gnn_filter_weight_count", "gnn_filter_create", "gnn_filter_apply",
+           "gnn_filter_destroy", "gnn_wcc", "gnn_infer_labels", "gnn_destroy", "gnn_last_error",
+           "gnn_profile_enable", "gnn_profile_read", "gnn_debug_csr", "gnn_debug_stages")
 STAGES = ("csr", "node_enc", "edge_enc", "edge_update", "aggregate", "node_update",
           "classifier", "total")
 
@@ -47,6 +48,15 @@ def make_dims(in_features=3, hidden=128, n_iters=8, n_mp_weight_sets=1, dtype=GN
               ln_eps=1e-5, flags=0) -> gnn_dims:
     return gnn_dims(ctypes.sizeof(gnn_dims), in_features, hidden, n_iters, n_mp_weight_sets,
                     dtype, ln_eps, flags)
+
+
+class gnn_filter_dims(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("in_features", ctypes.c_int32),
+                ("hidden", ctypes.c_int32), ("ln_eps", ctypes.c_float)]
+
+
+def make_filter_dims(in_features=3, hidden=64, ln_eps=1e-5) -> gnn_filter_dims:
+    return gnn_filter_dims(ctypes.sizeof(gnn_filter_dims), in_features, hidden, ln_eps)
 
 
 class gnn_profile_stats(ctypes.Structure):
@@ -74,6 +84,16 @@ def _load():
         f = getattr(L, name)
         f.restype = ctypes.c_int
         f.argtypes = [vp, vp, vp, i64, i64, vp, vp]
+    fdp = ctypes.POINTER(gnn_filter_dims)
+    L.gnn_filter_weight_count.restype = ctypes.c_size_t
+    L.gnn_filter_weight_count.argtypes = [fdp]
+    L.gnn_filter_create.restype = vp
+    L.gnn_filter_create.argtypes = [vp, fdp]
+    L.gnn_filter_destroy.restype = None
+    L.gnn_filter_destroy.argtypes = [vp]
+    L.gnn_filter_apply.restype = ctypes.c_int
+    L.gnn_filter_apply.argtypes = [vp, vp, vp, i64, i64, ctypes.c_float, vp, vp,
+                                   ctypes.POINTER(ctypes.c_int64), vp]
     L.gnn_wcc.restype = ctypes.c_int
     L.gnn_wcc.argtypes = [vp, vp, ctypes.c_float, i64, i64, vp, vp]
     L.gnn_infer_labels.restype = ctypes.c_int
@@ -170,6 +190,37 @@ def gnn_infer_logits(handle, node_feat, edge_index, n_nodes: int, n_edges: int, 
     _check_io(node_feat, edge_index, edge_logits)
     return _check(lib.gnn_infer_logits(handle, _addr(node_feat), _addr(edge_index), n_nodes,
                                        n_edges, _addr(edge_logits), _stream(stream)))
+
+
+def gnn_filter_weight_count(dims: gnn_filter_dims) -> int:
+    return int(lib.gnn_filter_weight_count(ctypes.byref(dims)))
+
+
+def gnn_filter_create(weights: np.ndarray, dims: gnn_filter_dims) -> int:
+    w = np.ascontiguousarray(weights, dtype=np.float32)
+    n = gnn_filter_weight_count(dims)
+    if n == 0:
+        raise GnnError(GNN_E_INVALID_ARG, gnn_last_error())
+    if w.size != n:
+        raise ValueError(f"filter blob has {w.size} floats, dims need {n}")
+    h = lib.gnn_filter_create(w.ctypes.data, ctypes.byref(dims))
+    if not h:
+        raise GnnError(GNN_E_INVALID_ARG, gnn_last_error())
+    return h
+
+
+def gnn_filter_destroy(handle) -> None:
+    lib.gnn_filter_destroy(handle)
+
+
+def gnn_filter_apply(handle, node_feat, edge_index, n_nodes: int, n_edges: int,
+                     threshold: float, edge_scores, edge_index_out, stream=None) -> int:
+    """Returns n_kept; edge_index_out[: 2 * n_kept] holds the kept edges as [2][n_kept]."""
+    nk = ctypes.c_int64(0)
+    _check(lib.gnn_filter_apply(handle, _addr(node_feat), _addr(edge_index), n_nodes, n_edges,
+                                float(threshold), _addr(edge_scores), _addr(edge_index_out),
+                                ctypes.byref(nk), _stream(stream)))
+    return int(nk.value)
 
 
 def gnn_wcc(edge_index, edge_scores, threshold: float, n_nodes: int, n_edges: int, labels,

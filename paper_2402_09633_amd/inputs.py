@@ -313,3 +313,50 @@ def blob_views(blob: np.ndarray, in_features: int, hidden: int, n_mp_weight_sets
             views[name + ".beta"] = blob[off:off + fout]; off += fout
     assert off == blob.size
     return views
+
+
+# ---------------------------------------------------------- edge filter ---
+
+def filter_layer_shapes(in_features: int, hidden: int):
+    """(name, fan_in, fan_out, hidden_layer) of the edge-filter MLP, in blob
+    order: [x_src; x_dst] (2F) -> H -> H -> 1."""
+    return [("filter.0", 2 * in_features, hidden, True), ("filter.1", hidden, hidden, True),
+            ("filter.2", hidden, 1, False)]
+
+
+def filter_weight_count(in_features: int, hidden: int) -> int:
+    return sum(fin * fout + fout + (2 * fout if hid else 0)
+               for _, fin, fout, hid in filter_layer_shapes(in_features, hidden))
+
+
+def make_filter_weights(in_features: int, hidden: int, seed: int,
+                        affine_noise: float = 0.0) -> np.ndarray:
+    """Packed fp32 filter blob, drawn like make_weights (Xavier W, zero b,
+    gamma 1, beta 0; perturbed b/gamma/beta with affine_noise > 0)."""
+    rng = np.random.default_rng(seed)
+    parts = []
+    for _, fin, fout, hid in filter_layer_shapes(in_features, hidden):
+        a = math.sqrt(6.0 / (fin + fout))
+        parts.append(rng.uniform(-a, a, fin * fout))
+        parts.append(rng.uniform(-affine_noise, affine_noise, fout) if affine_noise > 0
+                     else np.zeros(fout))
+        if hid:
+            if affine_noise > 0:
+                parts.append(rng.uniform(1 - affine_noise, 1 + affine_noise, fout))
+                parts.append(rng.uniform(-affine_noise, affine_noise, fout))
+            else:
+                parts.append(np.ones(fout))
+                parts.append(np.zeros(fout))
+    return np.concatenate(parts).astype(np.float32)
+
+
+def filter_blob_views(blob: np.ndarray, in_features: int, hidden: int) -> dict:
+    views, off = {}, 0
+    for name, fin, fout, hid in filter_layer_shapes(in_features, hidden):
+        views[name + ".W"] = blob[off:off + fin * fout].reshape(fout, fin); off += fin * fout
+        views[name + ".b"] = blob[off:off + fout]; off += fout
+        if hid:
+            views[name + ".g"] = blob[off:off + fout]; off += fout
+            views[name + ".beta"] = blob[off:off + fout]; off += fout
+    assert off == blob.size
+    return views

@@ -111,3 +111,9 @@ def test_product_path_never_touches_the_oracle():
             if f.endswith((".py", ".hip", ".h", ".cpp")):
                 text = open(os.path.join(dirpath, f)).read()
                 assert "oracle" not in text.lower() or f == "inputs.py", f
+
+
+@pytest.mark.parametrize("F,H", [(3, 64), (3, 128), (5, 64)])
+def test_filter_weight_count_matches_generator(G, F, H):
+    assert G.gnn_filter_weight_count(G.make_filter_dims(F, H)) == I.filter_weight_count(F, H)
+    assert G.gnn_filter_weight_count(G.make_filter_dims(F, 96)) == 0

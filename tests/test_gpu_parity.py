@@ -290,3 +290,18 @@ def test_hub_graph_long_segments(G, oracle_mod, flags):
     ref = oracle_mod.forward(w, x, ei, 64, 2)
     got = run_model(G, w, G.make_dims(3, 64, 2, flags=flags), x, ei)
     assert_logits_close(got, ref["logits"])
+
+
+@pytest.mark.parametrize("flags", PATHS)
+def test_hidden64_many_tiles_per_workgroup(G, oracle_mod, flags):
+    # 300k nodes: every persistent node workgroup walks several 256-node
+    # tiles; with H=64 the encoder's weight stream has an odd number of LDS
+    # chunks per tile (regression: the buffer parity must carry across tiles)
+    rng = np.random.default_rng(41)
+    n, e = 300_000, 150_000
+    x = rng.normal(size=(n, 3)).astype(np.float32)
+    ei = rng.integers(0, n, size=(2, e)).astype(np.int32)
+    w = I.make_weights(3, 64, 1, 41, affine_noise=0.2)
+    ref = oracle_mod.forward(w, x, ei, 64, 2)
+    got = run_model(G, w, G.make_dims(3, 64, 2, flags=flags), x, ei)
+    assert_logits_close(got, ref["logits"])

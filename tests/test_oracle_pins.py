@@ -243,3 +243,39 @@ def test_wcc_threshold_and_order_invariance(oracle_mod):
     np.testing.assert_array_equal(a, oracle_mod.wcc(ei[:, p], n, sc[p], 0.4))  # edge order
     np.testing.assert_array_equal(a, oracle_mod.wcc(ei[::-1].copy(), n, sc, 0.4))  # direction
     assert (oracle_mod.wcc(ei, n, np.zeros(e, np.float32), 0.5) == np.arange(n)).all()
+
+
+def _filter_brute(w, x, ei, F, H, eps=1e-5):
+    V = {k: torch.as_tensor(np.asarray(v, np.float64)) for k, v in
+         I.filter_blob_views(np.asarray(w, np.float32), F, H).items()}
+    xx = torch.as_tensor(np.asarray(x, np.float64))
+    a = torch.cat([xx[torch.as_tensor(ei[0], dtype=torch.long)],
+                   xx[torch.as_tensor(ei[1], dtype=torch.long)]], 1)
+    for name in ("filter.0", "filter.1"):
+        y = Fn.linear(a, V[name + ".W"], V[name + ".b"])
+        a = torch.relu(Fn.layer_norm(y, (H,), V[name + ".g"], V[name + ".beta"], eps))
+    return torch.sigmoid(Fn.linear(a, V["filter.2.W"], V["filter.2.b"])[:, 0]).numpy()
+
+
+@pytest.mark.parametrize("H,seed", [(8, 0), (16, 1)])
+def test_filter_matches_brute_force(oracle_mod, H, seed):
+    x, ei = _tiny(seed, 40, 300)
+    w = I.make_filter_weights(3, H, seed, affine_noise=0.3)
+    sc, kept = oracle_mod.filter_edges(w, x, ei, H, 0.5)
+    ref = _filter_brute(w, x, ei, 3, H)
+    np.testing.assert_allclose(sc, ref, rtol=0, atol=1e-13)
+    np.testing.assert_array_equal(kept, np.nonzero(ref > 0.5)[0])
+
+
+def test_filter_closed_forms(oracle_mod):
+    x, ei = _tiny(3, 30, 100)
+    w = np.zeros(I.filter_weight_count(3, 8), np.float32)
+    v = I.filter_blob_views(w, 3, 8)
+    v["filter.0.g"][:] = 1.0
+    v["filter.1.g"][:] = 1.0
+    v["filter.2.b"][:] = 1.5
+    sc, kept = oracle_mod.filter_edges(w, x, ei, 8, 0.5)
+    assert (sc == scipy.special.expit(1.5)).all() and (kept == np.arange(100)).all()
+    sc, kept = oracle_mod.filter_edges(w, x, ei, 8, 0.9)  # sigmoid(1.5) = 0.818 < 0.9
+    assert kept.size == 0
+    assert oracle_mod.filter_edges(w, x, np.zeros((2, 0), np.int32), 8)[1].size == 0
