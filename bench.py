@@ -23,34 +23,59 @@ sys.path.insert(0, ROOT)
 
 METRIC = "edges/sec and ms/event, 8-iter interaction network, 300k nodes/1M edges"
 PEAK_HBM_GBS = 8000.0
-PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2500.0}
+PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2500.0, "fp16": 2500.0}
 
-# HBM bytes per launch of the fp32 edge-update kernel on the full event,
-# from rocprofv3 FETCH_SIZE / WRITE_SIZE passes scaled by a plain-copy
-# calibration (profiles/full_fp32_kernels_and_counters.md).  Valid only for
-# the kernel sources they were measured on (hash of the files below).
-TRAFFIC_SOURCES = ["paper_2402_09633_amd/csrc/factored.hip",
-                   "paper_2402_09633_amd/csrc/device_common.h"]
-MEASURED_TRAFFIC = {"c330b264c61fa985": {"edge_update_bytes": 1652e6}}
+# HBM bytes per launch of the edge-update kernel on the full event, from
+# rocprofv3 FETCH_SIZE / WRITE_SIZE passes scaled by a plain-copy calibration
+# (profiles/full_event_fp32_kernels_and_counters.md).  Valid only for the kernel sources they were measured on
+# (hash of the files of that path).
+TRAFFIC_SOURCES = {
+    "split": ["paper_2402_09633_amd/csrc/split.hip", "paper_2402_09633_amd/csrc/device_common.h"],
+    "fp32_mfma": ["paper_2402_09633_amd/csrc/factored.hip",
+                  "paper_2402_09633_amd/csrc/device_common.h"],
+}
+MEASURED_TRAFFIC = {"1e41d2d9601c09d1": {"edge_update_bytes": 1.666e9},   # edge_split<4,1>
+                    "01db9dfa269e4bf7": {"edge_update_bytes": 1.652e9}}   # edge_f32<4,1>
 
 
-def kernel_source_hash():
+def kernel_source_hash(path):
     import hashlib
     h = hashlib.sha256()
-    for f in TRAFFIC_SOURCES:
+    for f in TRAFFIC_SOURCES[path]:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
 def edge_update_flops(E, H, factored):
-    """Multiply-adds x 2 of one edge-update launch.
+    """Algorithmic multiply-adds x 2 of one edge-update launch (fp32 model).
 
     Per-edge form: layer 1 over [h_src; h_dst; e] (3H -> H) and layer 2
     (H -> H).  Regrouped form: the launch computes W_e e (H -> H) and layer 2;
     the W_s h and W_d h products run once per node inside the node kernel.
     """
     return 2.0 * E * ((1 if factored else 3) * H * H + H * H)
+
+
+def edge_update_bytes(N, E, H):
+    """Algorithmic HBM bytes of one regrouped edge-update launch: e read and
+    written (fp32), both indices per edge, and every node's projection row
+    [W_s h; W_d h] (2H fp32) read once."""
+    return E * (2 * H * 4 + 8) + N * 2 * H * 4
+
+
+def node_update_bytes(N, H):
+    """h, agg_in, agg_out read; h and the projection row written (fp32)."""
+    return N * (3 * H * 4 + H * 4 + 2 * H * 4)
+
+
+def split_mfma_flops(N, E, H):
+    """Matrix-core work the split kernels execute per launch (each partial
+    product counted): the edge update runs 3 fp16 products per fp32 product
+    over W_e e and W2; the node update 6 bf16 products over layer 1 (3H -> H)
+    and 3 fp16 products over layer 2 and the 2H x H projection."""
+    return {"edge_update": 3 * 2.0 * E * 2 * H * H,
+            "node_update": 6 * 2.0 * N * 3 * H * H + 3 * 2.0 * N * 3 * H * H}
 
 
 def aggregate_bytes(N, E, H, act_bytes):
@@ -69,6 +94,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--literal", action="store_true",
                     help="evaluate the edge MLPs' first layer per edge (GNN_LITERAL_GATHER)")
+    ap.add_argument("--fp32-mfma", action="store_true",
+                    help="fp32 products on the fp32 matrix cores (GNN_FP32_MFMA) instead of "
+                         "split fp16/bf16 products")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 3 times (reference "
                          "kernel of known traffic for scaling HBM byte counters)")
@@ -102,9 +130,12 @@ def main():
     N, E, H, T = g.n_nodes, g.n_edges, cfg.hidden, cfg.n_iters
     w = I.make_weights(3, H, 1, cfg.weight_seed)
     dtype = G.GNN_BF16 if cfg.dtype == "bf16" else G.GNN_FP32
-    flags = G.GNN_LITERAL_GATHER if args.literal else 0
+    flags = (G.GNN_LITERAL_GATHER if args.literal else 0) | \
+        (G.GNN_FP32_MFMA if args.fp32_mfma else 0)
     dims = G.make_dims(3, H, T, 1, dtype, flags=flags)
     factored = cfg.dtype == "fp32" and not args.literal
+    split = factored and not args.fp32_mfma
+    path = "split" if split else ("fp32_mfma" if factored else "literal")
     print(f"# workload {cfg.name}: N={N} E={E} H={H} T={T} {cfg.dtype}", file=sys.stderr,
           flush=True)
 
@@ -145,6 +176,22 @@ def main():
     wcc_ms = (time.perf_counter() - tw) * 1000.0 / 5
     n_comp = int(torch.unique(labels).numel())
     m.close()
+    side = None
+    if split:
+        # The same event on the fp32 matrix cores, outside the timed region
+        # (reported for comparison only).
+        m2 = G.Model(w, G.make_dims(3, H, T, 1, dtype, flags=G.GNN_FP32_MFMA))
+        m2(x, ei, out)
+        torch.cuda.synchronize()
+        ts = time.perf_counter()
+        for _ in range(5):
+            m2(x, ei, out)
+        torch.cuda.synchronize()
+        side_ms = (time.perf_counter() - ts) * 1000.0 / 5
+        m2.close()
+        side = {"ms_per_event": round(side_ms, 4), "edges_per_s": round(E / side_ms * 1e3, 1),
+                "note": "same event with GNN_FP32_MFMA (products on the fp32 matrix cores), "
+                        "5 events after the timed region; not part of value"}
     filt = bench_filter(G, I, cfg) if cfg.name == "full" else None
 
     ms_per_step = (t1 - t0) * 1000.0 / args.steps
@@ -154,17 +201,53 @@ def main():
     eu = prof["edge_update"]
     eu_ms = eu["ms"] / max(eu["launches"], 1)
     eu_flops = edge_update_flops(E, H, factored)
-    achieved = eu_flops / (eu_ms / 1000.0) / 1e12
-    peak = PEAK_TFLOPS[cfg.dtype]
     ag = prof["aggregate"]
     ag_ms = ag["ms"] / max(ag["launches"], 1)
     ag_bytes = aggregate_bytes(N, E, H, act_bytes)
     ag_gbs = ag_bytes / (ag_ms / 1000.0) / 1e9
+    nu = prof["node_update"]
+    nu_ms = nu["ms"] / max(nu["launches"], 1)
 
     traffic = None
     if factored and cfg.name == "full":
-        m_t = MEASURED_TRAFFIC.get(kernel_source_hash())
+        m_t = MEASURED_TRAFFIC.get(kernel_source_hash(path))
         traffic = m_t["edge_update_bytes"] if m_t else None
+    if split:
+        eb = edge_update_bytes(N, E, H)
+        gbs = eb / (eu_ms / 1000.0) / 1e9
+        mf = split_mfma_flops(N, E, H)
+        eu_mfma = mf["edge_update"] / (eu_ms / 1000.0) / 1e12
+        roof = {"kernel": "edge_split<4,1> (gathers node projections, W_e e, layer 2; "
+                          "f16x2 weights in LDS)",
+                "bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
+                "bytes_per_launch": eb, "avg_launch_ms": round(eu_ms, 4),
+                "mfma": {"dtype": "fp16", "executed_tflop_per_launch": mf["edge_update"] / 1e12,
+                         "achieved": round(eu_mfma, 1), "peak": PEAK_TFLOPS["fp16"],
+                         "unit": "TFLOP/s", "frac": round(eu_mfma / PEAK_TFLOPS["fp16"], 4),
+                         "fp32_equivalent_tflops": round(eu_flops / (eu_ms / 1000.0) / 1e12, 1)}}
+        nb = node_update_bytes(N, H)
+        nu_gbs = nb / (nu_ms / 1000.0) / 1e9
+        nu_mfma = mf["node_update"] / (nu_ms / 1000.0) / 1e12
+        roof_node = {"kernel": "node_split<4,false,1> (layer 1 bf16x3, layer 2 and the "
+                               "next projection f16x2; weights streamed through LDS)",
+                     "bound": "hbm", "achieved": round(nu_gbs, 1), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(nu_gbs / PEAK_HBM_GBS, 4),
+                     "bytes_per_launch": nb, "avg_launch_ms": round(nu_ms, 4),
+                     "mfma": {"dtype": "bf16/fp16",
+                              "executed_tflop_per_launch": mf["node_update"] / 1e12,
+                              "achieved": round(nu_mfma, 1), "peak": PEAK_TFLOPS["fp16"],
+                              "unit": "TFLOP/s", "frac": round(nu_mfma / PEAK_TFLOPS["fp16"], 4)}}
+    else:
+        achieved = eu_flops / (eu_ms / 1000.0) / 1e12
+        peak = PEAK_TFLOPS[cfg.dtype]
+        roof = {"kernel": ("edge_f32<4,1> (gathers node projections, W_e e, layer 2; "
+                           "weights in LDS)") if factored else
+                          ("gmlp edge update (gathers [h_src; h_dst; e], 3H->H->H)"),
+                "bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": traffic,
+                "flops_per_launch": eu_flops, "avg_launch_ms": round(eu_ms, 4)}
+        roof_node = None
     rec = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -180,17 +263,17 @@ def main():
         "data": "synthetic (seeded layered hit graph, seeded Xavier weights)",
         "config": {"workload": f"{cfg.name}: {N}-hit / {E}-edge layered event, H={H}, T={T}, "
                                f"{cfg.dtype}", "n_nodes": N, "n_edges": E, "hidden": H,
-                   "n_iters": T, "parallelism": "single GPU"},
+                   "n_iters": T, "parallelism": "single GPU",
+                   "products": {"split": "fp32 operands split into fp16 pairs (bf16 triples "
+                                         "for the node MLP's first layer) on the fp16/bf16 "
+                                         "matrix cores, fp32 accumulation",
+                                "fp32_mfma": "fp32 matrix cores",
+                                "literal": "per-edge first layer"}[path]
+                   if cfg.dtype == "fp32" else "bf16 matrix cores"},
         "ms_per_event_p50": round(float(np.percentile(per, 50)), 4),
         "ms_per_event_p99": round(float(np.percentile(per, 99)), 4),
         "ms_per_event_min": round(float(per.min()), 4),
-        "roofline": {"kernel": ("edge_f32<4,1> (gathers node projections, W_e e, layer 2; "
-                                "weights in LDS)") if factored else
-                               ("gmlp edge update (gathers [h_src; h_dst; e], 3H->H->H)"),
-                     "bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
-                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
-                     "traffic": traffic,
-                     "flops_per_launch": eu_flops, "avg_launch_ms": round(eu_ms, 4)},
+        "roofline": roof,
         "roofline_aggregate": {"kernel": "aggregate (CSR segmented sums, in and out)",
                                "bound": "hbm", "achieved": round(ag_gbs, 1),
                                "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -204,6 +287,10 @@ def main():
                                "threshold, after inference (wall time, host-checked rounds); "
                                "not part of value"},
     }
+    if roof_node:
+        rec["roofline_node_update"] = roof_node
+    if side:
+        rec["fp32_mfma_path"] = side
     if filt:
         rec["filter"] = filt
 

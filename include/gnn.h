@@ -59,6 +59,19 @@ extern "C" {
                                    node projections computed once per node; the
                                    two agree up to fp32 rounding.  bf16 always
                                    uses the per-edge form. */
+#define GNN_FP32_MFMA 4u        /* fp32, regrouped form: multiply on the fp32
+                                   matrix cores (v_mfma_f32_32x32x2_f32).  The
+                                   default multiplies fp32 operands split into
+                                   fp16 pairs (x = x1 + x2, per-operand error
+                                   <= 2^-22 |x|; weights pre-scaled by a power
+                                   of two) on the fp16 matrix cores, and the node
+                                   MLP's first layer, whose input holds the
+                                   unbounded aggregates, with operands split
+                                   exactly into bf16 triples; fp32 accumulation
+                                   throughout.  The default needs every
+                                   LayerNorm output bound max|gamma| sqrt(H-1) +
+                                   max|beta| <= 2^15 (fp16 range); weights that
+                                   break it select this path by themselves. */
 
 typedef struct gnn_dims {
   uint32_t struct_size;     /* = sizeof(gnn_dims) (ABI versioning)              */
@@ -69,7 +82,8 @@ typedef struct gnn_dims {
                                iterations; T = one pair per iteration          */
   int32_t dtype;            /* GNN_FP32 or GNN_BF16                             */
   float ln_eps;             /* LayerNorm epsilon (1e-5)                         */
-  uint32_t flags;           /* GNN_VALIDATE_INDICES | GNN_LITERAL_GATHER or 0   */
+  uint32_t flags;           /* OR of GNN_VALIDATE_INDICES, GNN_LITERAL_GATHER,
+                               GNN_FP32_MFMA, or 0                              */
 } gnn_dims;
 
 typedef struct gnn_handle gnn_handle;

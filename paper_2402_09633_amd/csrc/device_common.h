@@ -1,4 +1,5 @@
-// Device helpers shared by the MLP kernel files (mlp.hip, factored.hip):
+// Device helpers shared by the MLP kernel files (mlp.hip, factored.hip,
+// split.hip):
 // vector types, the XCD-aware block remap, index clamping, the stable
 // sigmoid, the LayerNorm/ReLU epilogue on MFMA accumulators and the small-K
 // first layer of the node encoder.
@@ -45,12 +46,14 @@ __device__ __forceinline__ float sigmoidf_stable(float z) {
 
 // Bias + LayerNorm + ReLU over the H = 32*MB features of this lane's row,
 // held half in this lane and half in lane ^ 32.  With add_bias false the
-// bias is already in the accumulators.
+// bias is already in the accumulators.  Accumulators that hold s * y for a
+// power-of-two s (split-precision products) pass bscale = s and eps * s^2:
+// LayerNorm of s * (y + b) with eps s^2 equals LayerNorm of y + b with eps.
 template <int MB>
 __device__ __forceinline__ void bias_ln_relu(f16v (&acc)[MB], const float *__restrict__ b,
                                              const float *__restrict__ g,
                                              const float *__restrict__ beta, float eps, int hh,
-                                             bool add_bias) {
+                                             bool add_bias, float bscale = 1.f) {
   constexpr float inv_h = 1.0f / (32 * MB);
   float s = 0.f;
 #pragma unroll
@@ -61,7 +64,7 @@ __device__ __forceinline__ void bias_ln_relu(f16v (&acc)[MB], const float *__res
       const f4 bb = add_bias ? *(const f4 *)(b + f) : f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        acc[mb][4 * q + t] += bb[t];
+        acc[mb][4 * q + t] += bb[t] * bscale;
         s += acc[mb][4 * q + t];
       }
     }
@@ -89,6 +92,50 @@ __device__ __forceinline__ void bias_ln_relu(f16v (&acc)[MB], const float *__res
         const float y = (acc[mb][4 * q + t] - mean) * rstd * gg[t] + bt[t];
         acc[mb][4 * q + t] = fmaxf(y, 0.f);
       }
+    }
+}
+
+// LayerNorm epilogue with its parameters (b, gamma, beta; H floats each)
+// read from LDS (the bias already multiplied by the accumulators' scale,
+// eps by its square).
+template <int MB>
+__device__ __forceinline__ void ln_relu_lds(f16v (&acc)[MB], const float *prm, float eps, int hh) {
+  constexpr int H = 32 * MB;
+  constexpr float inv_h = 1.0f / H;
+  float s = 0.f;
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f4 bb = *(const f4 *)(prm + mb * 32 + 8 * q + 4 * hh);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        acc[mb][4 * q + t] += bb[t];
+        s += acc[mb][4 * q + t];
+      }
+    }
+  s += __shfl_xor(s, 32);
+  const float mean = s * inv_h;
+  float var = 0.f;
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const float d = acc[mb][v] - mean;
+      var += d * d;
+    }
+  var += __shfl_xor(var, 32);
+  const float rstd = 1.0f / sqrtf(var * inv_h + eps);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int f = mb * 32 + 8 * q + 4 * hh;
+      const f4 gg = *(const f4 *)(prm + H + f);
+      const f4 bt = *(const f4 *)(prm + 2 * H + f);
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        acc[mb][4 * q + t] = fmaxf((acc[mb][4 * q + t] - mean) * rstd * gg[t] + bt[t], 0.f);
     }
 }
 

@@ -228,49 +228,6 @@ __global__ __launch_bounds__(64 * EDGE_WAVES) void node_f32(NodeArgs a) {
   }
 }
 
-// LayerNorm epilogue with its parameters (b, gamma, beta; H floats each)
-// read from LDS.
-template <int MB>
-__device__ __forceinline__ void ln_relu_lds(f16v (&acc)[MB], const float *prm, float eps, int hh) {
-  constexpr int H = 32 * MB;
-  constexpr float inv_h = 1.0f / H;
-  float s = 0.f;
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const f4 bb = *(const f4 *)(prm + mb * 32 + 8 * q + 4 * hh);
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        acc[mb][4 * q + t] += bb[t];
-        s += acc[mb][4 * q + t];
-      }
-    }
-  s += __shfl_xor(s, 32);
-  const float mean = s * inv_h;
-  float var = 0.f;
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const float d = acc[mb][v] - mean;
-      var += d * d;
-    }
-  var += __shfl_xor(var, 32);
-  const float rstd = 1.0f / sqrtf(var * inv_h + eps);
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int f = mb * 32 + 8 * q + 4 * hh;
-      const f4 gg = *(const f4 *)(prm + H + f);
-      const f4 bt = *(const f4 *)(prm + 2 * H + f);
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
-        acc[mb][4 * q + t] = fmaxf((acc[mb][4 * q + t] - mean) * rstd * gg[t] + bt[t], 0.f);
-    }
-}
-
 template <int MB, int MODE>
 __global__ __launch_bounds__(64 * EDGE_WAVES) void edge_f32(EdgeArgs a) {
   constexpr int H = 32 * MB;

@@ -8,6 +8,7 @@
 // The workspace is allocated stream-ordered (hipMallocAsync/hipFreeAsync)
 // from the device's default pool, whose release threshold is raised so that
 // repeated calls reuse memory; one handle can serve several streams at once.
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -57,7 +58,7 @@ int check_dims(const gnn_dims *d) {
     return fail(GNN_E_INVALID_ARG, "dtype %d unknown", d->dtype);
   if (!(d->ln_eps > 0.f) || !(d->ln_eps < 1.f))
     return fail(GNN_E_INVALID_ARG, "ln_eps %g outside (0, 1)", (double)d->ln_eps);
-  if (d->flags & ~(GNN_VALIDATE_INDICES | GNN_LITERAL_GATHER))
+  if (d->flags & ~(GNN_VALIDATE_INDICES | GNN_LITERAL_GATHER | GNN_FP32_MFMA))
     return fail(GNN_E_INVALID_ARG, "unknown flags");
   return GNN_OK;
 }
@@ -128,6 +129,88 @@ void frag_bf16(const BlobLayer &L, bool from_acc, uint16_t *hi, uint16_t *lo) {
         }
 }
 
+// ---- split-precision records (split.hip) ----
+// A record holds the A operands of one 16-wide k-step for all MB = fout/32
+// output blocks, [mb][part][lane][8] 16-bit values; slot j of lane l
+// (hh = l / 32) multiplies input column k(g, hh, j) of row 32 mb + l % 32:
+//   B from HBM:   k = 16 g + 8 hh + j
+//   B from accs:  k = 16 g + 8 (j / 4) + 4 hh + j % 4
+
+uint16_t f16_bits(_Float16 v) {
+  uint16_t b;
+  memcpy(&b, &v, 2);
+  return b;
+}
+
+// Power of two s with max |s W| in [2^13, 2^14) (1 for an all-zero or
+// non-finite W), over the whole (fout x fin) layer.
+float pow2_scale(const BlobLayer &L) {
+  float mx = 0.f;
+  const size_t n = (size_t)L.fout * L.fin;
+  for (size_t i = 0; i < n; ++i) mx = fmaxf(mx, fabsf(L.W[i]));
+  if (!(mx > 0.f) || !std::isfinite(mx)) return 1.f;
+  int e = 0;
+  (void)frexpf(mx, &e);  // mx = m 2^e, m in [0.5, 1)
+  int k = 14 - e;
+  k = k < -40 ? -40 : (k > 40 ? 40 : k);
+  return ldexpf(1.f, k);
+}
+
+// Largest value a LayerNorm/ReLU output of layer L can take:
+// |(y - mean) / sqrt(var + eps)| <= sqrt(H - 1) for every feature.
+double ln_out_bound(const BlobLayer &L) {
+  double b = 0.0;
+  const double r = sqrt((double)L.fout - 1.0);
+  for (int f = 0; f < L.fout; ++f) {
+    const double v = fabs((double)L.g[f]) * r + fabs((double)L.beta[f]);
+    if (!(v <= 1e30)) return INFINITY;
+    b = v > b ? v : b;
+  }
+  return b;
+}
+
+// f16x2 records of s * W[:, c0 : c0 + K]: parts w1 = fp16(sW), w2 = fp16(sW - w1).
+std::vector<uint16_t> rec_f16x2(const BlobLayer &L, int c0, int K, float s, bool from_acc) {
+  const int MB = L.fout / 32, G = K / 16;
+  std::vector<uint16_t> out((size_t)G * MB * 2 * 64 * 8);
+  for (int g = 0; g < G; ++g)
+    for (int mb = 0; mb < MB; ++mb)
+      for (int lane = 0; lane < 64; ++lane)
+        for (int j = 0; j < 8; ++j) {
+          const int hh = lane / 32;
+          const int k = from_acc ? 16 * g + 8 * (j / 4) + 4 * hh + j % 4 : 16 * g + 8 * hh + j;
+          const float wv = s * L.W[(size_t)(mb * 32 + lane % 32) * L.fin + c0 + k];
+          const _Float16 p1 = (_Float16)wv;
+          const _Float16 p2 = (_Float16)(wv - (float)p1);
+          const size_t o = ((((size_t)g * MB + mb) * 2) * 64 + lane) * 8 + j;
+          out[o] = f16_bits(p1);
+          out[o + 64 * 8] = f16_bits(p2);
+        }
+  return out;
+}
+
+// bf16x3 records of W[:, 0:K] with B from HBM: W = w1 + w2 + w3 exactly.
+std::vector<uint16_t> rec_bf16x3(const BlobLayer &L, int K) {
+  const int MB = L.fout / 32, G = K / 16;
+  std::vector<uint16_t> out((size_t)G * MB * 3 * 64 * 8);
+  for (int g = 0; g < G; ++g)
+    for (int mb = 0; mb < MB; ++mb)
+      for (int lane = 0; lane < 64; ++lane)
+        for (int j = 0; j < 8; ++j) {
+          const int k = 16 * g + 8 * (lane / 32) + j;
+          const float wv = L.W[(size_t)(mb * 32 + lane % 32) * L.fin + k];
+          const uint16_t p1 = f32_to_bf16(wv);
+          const float r = wv - bf16_to_f32(p1);
+          const uint16_t p2 = f32_to_bf16(r);
+          const uint16_t p3 = f32_to_bf16(r - bf16_to_f32(p2));
+          const size_t o = ((((size_t)g * MB + mb) * 3) * 64 + lane) * 8 + j;
+          out[o] = p1;
+          out[o + 64 * 8] = p2;
+          out[o + 2 * 64 * 8] = p3;
+        }
+  return out;
+}
+
 // Builds one host staging image of all device weights, section by section,
 // each 256-byte aligned; device pointers are fixed up after the upload.
 struct Staging {
@@ -150,16 +233,25 @@ struct MlpOff {
 
 }  // namespace
 
-// Extra fp32 weights of the regrouped first layers: stacked projections
-// [W_s; W_d] (2H x H) per edge-side MLP and the W_e column blocks (H x H).
+// Extra weights of the regrouped first layers: W_e column blocks (H x H) and
+// the node-kernel streams with the stacked projections [W_s; W_d].  In the
+// split path every matrix is in f16x2 / bf16x3 records and the edge kernels
+// read W2 from records too; in the fp32 path they are fp32 MFMA fragments.
 struct FactDev {
-  const float *we_cls = nullptr;
-  std::vector<const float *> we_em;
-  // node-kernel fragment streams: encoder (W2 | two projections) and, per
+  bool split = false;
+  const void *we_cls = nullptr;
+  std::vector<const void *> we_em;
+  // node-kernel streams: encoder (W2 | two projections) and, per
   // iteration, update (W1 | W2 | projection for the next edge consumer)
-  const float *enc_stream = nullptr;
-  std::vector<const float *> upd_stream;
+  const void *enc_stream = nullptr;
+  std::vector<const void *> upd_stream;
   int enc_chunks = 0, upd_chunks = 0;
+  // split path: W2 records of the edge-side MLPs and the power-of-two scales
+  // (s1: first layer incl. the stored projections; s2: W2)
+  const void *w2_ee = nullptr;
+  std::vector<const void *> w2_em;
+  float s1_ee = 1.f, s2_ee = 1.f, s1_cls = 1.f, s2_ne = 1.f;
+  std::vector<float> s1_em, s2_em, s2_nm;
   int grid_enc = 0, grid_upd = 0, grid_cls = 0, grid_node = 0;  // persistent grids
 };
 
@@ -470,15 +562,17 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
     na.x = x;
     na.F = d.in_features;
     na.mlp = hd->node_enc;
-    na.wstream = fd.enc_stream;
+    na.wstream = (const float *)fd.enc_stream;
     na.nchunks = fd.enc_chunks;
+    na.s2 = fd.s2_ne;
     na.nproj = 2;
     na.h_out = (float *)w.h;
     na.p_out[0] = w.pa;
     na.p_out[1] = w.pb;
     na.eps = d.ln_eps;
     st.begin();
-    HIP_TRY(launch_node_f32(true, H, na, fd.grid_node, stream));
+    HIP_TRY(fd.split ? launch_node_split(true, H, na, fd.grid_node, stream)
+                     : launch_node_f32(true, H, na, fd.grid_node, stream));
     st.end(GNN_STAGE_NODE_ENC);
 
     auto edge_args = [&](const float *P, const MlpDev &m) {
@@ -498,21 +592,35 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       ea.eps = d.ln_eps;
       return ea;
     };
+    auto launch_edge = [&](EdgeMode mode, const EdgeArgs &ea, int grid) {
+      return fd.split ? launch_edge_split(mode, H, ea, grid, stream)
+                      : launch_edge_f32(mode, H, ea, grid, stream);
+    };
     {
       EdgeArgs ea = edge_args(w.pa, hd->edge_enc);
       ea.e_out = (float *)w.e;
+      if (fd.split) {
+        ea.w2 = (const float *)fd.w2_ee;
+        ea.s1 = fd.s1_ee;
+        ea.s2 = fd.s2_ee;
+      }
       st.begin();
-      HIP_TRY(launch_edge_f32(EdgeMode::Enc, H, ea, fd.grid_enc, stream));
+      HIP_TRY(launch_edge(EdgeMode::Enc, ea, fd.grid_enc));
       st.end(GNN_STAGE_EDGE_ENC);
     }
     for (int t = 0; t < T; ++t) {
       const int k = set_of(t);
       EdgeArgs ea = edge_args(w.pb, hd->edge_mlp[k]);
       ea.e_in = (const float *)w.e;
-      ea.we = fd.we_em[k];
+      ea.we = (const float *)fd.we_em[k];
       ea.e_out = (float *)w.e;  // in place: a wave reads its rows before writing them
+      if (fd.split) {
+        ea.w2 = (const float *)fd.w2_em[k];
+        ea.s1 = fd.s1_em[k];
+        ea.s2 = fd.s2_em[k];
+      }
       st.begin();
-      HIP_TRY(launch_edge_f32(EdgeMode::Upd, H, ea, fd.grid_upd, stream));
+      HIP_TRY(launch_edge(EdgeMode::Upd, ea, fd.grid_upd));
       st.end(GNN_STAGE_EDGE_UPDATE);
       st.begin();
       HIP_TRY(launch_segsum(act, H, w.e, w.rp_in, w.perm_in, w.rp_out, w.perm_out, w.ain,
@@ -524,14 +632,16 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       nu.src[1] = (const float *)w.ain;
       nu.src[2] = (const float *)w.aout;
       nu.mlp = hd->node_mlp[k];
-      nu.wstream = fd.upd_stream[t];
+      nu.wstream = (const float *)fd.upd_stream[t];
       nu.nchunks = fd.upd_chunks;
+      nu.s2 = fd.split ? fd.s2_nm[k] : 1.f;
       nu.nproj = 1;
       nu.h_out = (float *)w.h;  // in place: a wave reads its rows before writing them
       nu.p_out[0] = w.pb;
       nu.eps = d.ln_eps;
       st.begin();
-      HIP_TRY(launch_node_f32(false, H, nu, fd.grid_node, stream));
+      HIP_TRY(fd.split ? launch_node_split(false, H, nu, fd.grid_node, stream)
+                       : launch_node_f32(false, H, nu, fd.grid_node, stream));
       st.end(GNN_STAGE_NODE_UPDATE);
     }
     if (ro.stop_iter >= 0) {
@@ -548,12 +658,13 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
     {
       EdgeArgs ea = edge_args(w.pb, hd->cls);
       ea.e_in = (const float *)w.e;
-      ea.we = fd.we_cls;
+      ea.we = (const float *)fd.we_cls;
       ea.g2 = ea.beta2 = nullptr;
+      ea.s1 = fd.s1_cls;
       ea.out_score = ro.scores;
       ea.out_logit = ro.logits;
       st.begin();
-      HIP_TRY(launch_edge_f32(EdgeMode::Cls, H, ea, fd.grid_cls, stream));
+      HIP_TRY(launch_edge(EdgeMode::Cls, ea, fd.grid_cls));
       st.end(GNN_STAGE_CLASSIFIER);
     }
     goto out;
@@ -740,8 +851,10 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
   std::vector<MlpOff> o_em(S), o_nm(S);
   const bool factored = !bf16 && !(d.flags & GNN_LITERAL_GATHER);
   const int T = d.n_iters;
-  size_t o_we_cls = 0, o_enc_stream = 0;
-  std::vector<size_t> o_we_em(S), o_upd_stream(T);
+  size_t o_we_cls = 0, o_enc_stream = 0, o_w2_ee = 0;
+  std::vector<size_t> o_we_em(S), o_upd_stream(T), o_w2_em(S);
+  bool split = false;
+  FactDev fdh;  // scales of the split path (pointers are fixed up below)
   {
     BlobLayer a0 = next(F, H, true), a1 = next(H, H, true);
     o_ne = {stage_layer(st, a0, WKind::PlainT, bf16, true),
@@ -749,29 +862,90 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
     BlobLayer b0 = next(2 * H, H, true), b1 = next(H, H, true);
     o_ee = {stage_layer(st, b0, WKind::FragMem, bf16, true),
             stage_layer(st, b1, WKind::FragAcc, bf16, true)};
-    std::vector<BlobLayer> e0s, n0s, n1s;
+    std::vector<BlobLayer> e0s, e1s, n0s, n1s;
     for (int s = 0; s < S; ++s) {
       BlobLayer e0 = next(3 * H, H, true), e1 = next(H, H, true);
       o_em[s] = {stage_layer(st, e0, WKind::FragMem, bf16, true),
                  stage_layer(st, e1, WKind::FragAcc, bf16, true)};
-      if (factored) o_we_em[s] = stage_frag_f32(st, col_block(e0, H, 2 * H), H, H);
       BlobLayer n0 = next(3 * H, H, true), n1 = next(H, H, true);
       o_nm[s] = {stage_layer(st, n0, WKind::FragMem, bf16, true),
                  stage_layer(st, n1, WKind::FragAcc, bf16, true)};
       e0s.push_back(e0);
+      e1s.push_back(e1);
       n0s.push_back(n0);
       n1s.push_back(n1);
     }
     BlobLayer c0 = next(3 * H, H, true), c1 = next(H, 1, false);
     o_cls = {stage_layer(st, c0, WKind::FragMem, bf16, true),
              stage_layer(st, c1, WKind::Plain, bf16, false)};
+    // The edge consumer of the projections computed after node update t
+    // (t = -1: the node encoder's second projection).
+    auto next_edge_l1 = [&](int t) -> const BlobLayer & {
+      return t + 1 < T ? e0s[S == 1 ? 0 : t + 1] : c0;
+    };
     if (factored) {
+      // Split products need every LayerNorm output that feeds an f16x2
+      // product inside the fp16 range (with a factor 2 to spare).
+      double bound = 0.0;
+      for (const BlobLayer *L : {&a0, &a1, &b0, &b1}) bound = fmax(bound, ln_out_bound(*L));
+      for (int s = 0; s < S; ++s)
+        for (const BlobLayer *L : {&e0s[s], &e1s[s], &n0s[s], &n1s[s]})
+          bound = fmax(bound, ln_out_bound(*L));
+      split = !(d.flags & GNN_FP32_MFMA) && bound <= 32768.0;
+    }
+    if (factored && split) {
+      auto add16 = [&](const std::vector<uint16_t> &v) {
+        return st.add(v.data(), v.size() * sizeof(uint16_t));
+      };
+      auto cat = [](std::vector<uint16_t> &dst, const std::vector<uint16_t> &src) {
+        dst.insert(dst.end(), src.begin(), src.end());
+      };
+      fdh.s1_ee = pow2_scale(b0);
+      fdh.s2_ee = pow2_scale(b1);
+      fdh.s1_cls = pow2_scale(c0);
+      fdh.s2_ne = pow2_scale(a1);
+      for (int s = 0; s < S; ++s) {
+        fdh.s1_em.push_back(pow2_scale(e0s[s]));
+        fdh.s2_em.push_back(pow2_scale(e1s[s]));
+        fdh.s2_nm.push_back(pow2_scale(n1s[s]));
+        o_we_em[s] = add16(rec_f16x2(e0s[s], 2 * H, H, fdh.s1_em[s], false));
+        o_w2_em[s] = add16(rec_f16x2(e1s[s], 0, H, fdh.s2_em[s], true));
+      }
+      o_we_cls = add16(rec_f16x2(c0, 2 * H, H, fdh.s1_cls, false));
+      o_w2_ee = add16(rec_f16x2(b1, 0, H, fdh.s2_ee, true));
+      // Projections of h (B operand from the accumulators), scaled by the
+      // consumer's first-layer scale.
+      auto scale_of = [&](const BlobLayer &L) {
+        if (&L == &c0) return fdh.s1_cls;
+        for (int s = 0; s < S; ++s)
+          if (&L == &e0s[s]) return fdh.s1_em[s];
+        return fdh.s1_ee;
+      };
+      auto proj = [&](std::vector<uint16_t> &dst, const BlobLayer &L) {
+        const float sc = scale_of(L);
+        cat(dst, rec_f16x2(L, 0, H, sc, true));
+        cat(dst, rec_f16x2(L, H, H, sc, true));
+      };
+      std::vector<uint16_t> es = rec_f16x2(a1, 0, H, fdh.s2_ne, true);
+      proj(es, b0);
+      proj(es, next_edge_l1(-1));
+      o_enc_stream = add16(es);
+      for (int t = 0; t < T; ++t) {
+        const int k = S == 1 ? 0 : t;
+        std::vector<uint16_t> us = rec_bf16x3(n0s[k], 3 * H);
+        cat(us, rec_f16x2(n1s[k], 0, H, fdh.s2_nm[k], true));
+        proj(us, next_edge_l1(t));
+        o_upd_stream[t] = add16(us);
+      }
+    } else if (factored) {
+      for (int s = 0; s < S; ++s)
+        o_we_em[s] = stage_frag_f32(st, col_block(e0s[s], H, 2 * H), H, H);
       o_we_cls = stage_frag_f32(st, col_block(c0, H, 2 * H), H, H);
       // Node encoder stream: W2 | projection for the edge encoder |
       // projection for the first edge update (the classifier if T == 0).
       std::vector<float> es = frag_of(a1.W, H, H);
       append_projection(es, b0, H);
-      append_projection(es, T > 0 ? e0s[0] : c0, H);
+      append_projection(es, next_edge_l1(-1), H);
       o_enc_stream = st.add(es.data(), es.size() * sizeof(float));
       // Node update t: W1 | W2 | projection for edge update t+1 (or the
       // classifier after the last iteration).
@@ -779,7 +953,7 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
         const int k = S == 1 ? 0 : t;
         std::vector<float> us = frag_of(n0s[k].W, H, 3 * H);
         append(us, frag_of(n1s[k].W, H, H));
-        append_projection(us, t + 1 < T ? e0s[S == 1 ? 0 : t + 1] : c0, H);
+        append_projection(us, next_edge_l1(t), H);
         o_upd_stream[t] = st.add(us.data(), us.size() * sizeof(float));
       }
     }
@@ -812,19 +986,31 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
   h->factored = factored;
   if (factored) {
     FactDev &fd = h->fd;
-    fd.we_cls = (const float *)(base + o_we_cls);
-    for (int s = 0; s < S; ++s) fd.we_em.push_back((const float *)(base + o_we_em[s]));
-    fd.enc_stream = (const float *)(base + o_enc_stream);
-    for (int t = 0; t < T; ++t) fd.upd_stream.push_back((const float *)(base + o_upd_stream[t]));
-    const int kg = H / 8;  // k-groups of one H-wide operand; 8 per chunk
-    fd.enc_chunks = (kg + 4 * kg) / 8;
-    fd.upd_chunks = (3 * kg + kg + 2 * kg) / 8;
+    fd = fdh;
+    fd.split = split;
+    fd.we_cls = base + o_we_cls;
+    for (int s = 0; s < S; ++s) fd.we_em.push_back(base + o_we_em[s]);
+    fd.enc_stream = base + o_enc_stream;
+    for (int t = 0; t < T; ++t) fd.upd_stream.push_back(base + o_upd_stream[t]);
     int n_cu = 0;
     if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
       n_cu = 256;
-    fd.grid_enc = edge_f32_grid(EdgeMode::Enc, H, n_cu);
-    fd.grid_upd = edge_f32_grid(EdgeMode::Upd, H, n_cu);
-    fd.grid_cls = edge_f32_grid(EdgeMode::Cls, H, n_cu);
+    if (split) {
+      fd.w2_ee = base + o_w2_ee;
+      for (int s = 0; s < S; ++s) fd.w2_em.push_back(base + o_w2_em[s]);
+      fd.enc_chunks = node_split_chunks(true, H, 2);
+      fd.upd_chunks = node_split_chunks(false, H, 1);
+      fd.grid_enc = edge_split_grid(EdgeMode::Enc, H, n_cu);
+      fd.grid_upd = edge_split_grid(EdgeMode::Upd, H, n_cu);
+      fd.grid_cls = edge_split_grid(EdgeMode::Cls, H, n_cu);
+    } else {
+      const int kg = H / 8;  // k-groups of one H-wide operand; 8 per chunk
+      fd.enc_chunks = (kg + 4 * kg) / 8;
+      fd.upd_chunks = (3 * kg + kg + 2 * kg) / 8;
+      fd.grid_enc = edge_f32_grid(EdgeMode::Enc, H, n_cu);
+      fd.grid_upd = edge_f32_grid(EdgeMode::Upd, H, n_cu);
+      fd.grid_cls = edge_f32_grid(EdgeMode::Cls, H, n_cu);
+    }
     fd.grid_node = node_f32_grid(n_cu);
   }
   return h;

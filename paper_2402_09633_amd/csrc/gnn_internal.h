@@ -66,6 +66,7 @@ struct NodeArgs {
   float *h_out = nullptr;                     // [n_rows][H] or nullptr
   float *p_out[2] = {nullptr, nullptr};       // [n_rows][2H]
   float eps = 1e-5f;
+  float s2 = 1.f;  // split kernels: power-of-two scale of the layer-2 weights
 };
 
 enum class EdgeMode : int { Enc = 0, Upd = 1, Cls = 2 };
@@ -82,6 +83,9 @@ struct EdgeArgs {
   const float *b2 = nullptr, *g2 = nullptr, *beta2 = nullptr;
   float *e_out = nullptr, *out_logit = nullptr, *out_score = nullptr;
   float eps = 1e-5f;
+  // split kernels: power-of-two scales of the first layer (W_e and the
+  // stored P rows) and of W2
+  float s1 = 1.f, s2 = 1.f;
 };
 
 hipError_t launch_node_f32(bool enc, int hidden, const NodeArgs &a, int grid,
@@ -92,6 +96,17 @@ int node_stream_chunk_f4(int hidden);
 hipError_t launch_edge_f32(EdgeMode mode, int hidden, const EdgeArgs &a, int grid,
                            hipStream_t stream);
 int edge_f32_grid(EdgeMode mode, int hidden, int n_cu);
+
+// The same kernels with split-precision products on the fp16/bf16 matrix
+// cores (split.hip).  Weights come as f16x2 / bf16x3 records; P rows are
+// stored multiplied by the consumer's s1.
+hipError_t launch_node_split(bool enc, int hidden, const NodeArgs &a, int grid,
+                             hipStream_t stream);
+int node_split_chunks(bool enc, int hidden, int nproj);
+size_t node_split_chunk_bytes(bool enc, int hidden);
+hipError_t launch_edge_split(EdgeMode mode, int hidden, const EdgeArgs &a, int grid,
+                             hipStream_t stream);
+int edge_split_grid(EdgeMode mode, int hidden, int n_cu);
 
 // Deterministic CSR segmented sums of the edge rows `e` ([n_edges][H]):
 // agg_in[v] = sum over p in [rp_in[v], rp_in[v+1]) of e[perm_in[p]], in

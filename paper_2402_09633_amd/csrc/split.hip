@@ -1,0 +1,504 @@
+// fp32 interaction-network kernels whose matrix products run on the fp16 and
+// bf16 matrix cores, with the first Linear layer of every edge-side MLP
+// regrouped per node as in factored.hip.
+//
+// gfx950 multiplies fp16/bf16 16 times faster than fp32 on its matrix cores,
+// so every fp32 product here is evaluated from an exact, or nearly exact,
+// splitting of both operands into low-precision parts, with every partial
+// product accumulated in fp32 (products of the parts are exact in fp32):
+//
+//  f16x2   x = x1 + x2, x1 = fp16(x), x2 = fp16(x - x1), both rounded to
+//          nearest, so |x - x1 - x2| <= 2^-22 |x| (2^-25 absolute once x2 is
+//          subnormal).  W is scaled first by a power of two s chosen on the
+//          host so that max |s W| lies in [2^13, 2^14), split the same way,
+//          and  s W x = w1 x1 + w2 x1 + w1 x2  up to the dropped w2 x2
+//          (<= 2^-22 |sW||x|).  Three v_mfma_f32_32x32x16_f16 replace eight
+//          v_mfma_f32_32x32x2_f32 per 16-wide k-step.  It is used where the
+//          operand is a LayerNorm/ReLU output, bounded by
+//          max_f |gamma_f| sqrt(H-1) + |beta_f|; the handle checks that bound
+//          against the fp16 range when it is created.  The edge kernels keep
+//          both of their H x H matrices in LDS in this form (2 x 64 KB).
+//  bf16x3  x = x1 + x2 + x3 exactly (bf16 has the fp32 exponent range), and
+//          the six partial products w_i x_j with i + j <= 4 are kept; the
+//          dropped ones are below 2^-25 |W||x|.  Used for the node MLP's first
+//          layer, whose input includes the aggregates (sums over up to a
+//          node's whole degree, not bounded by any LayerNorm).
+//
+// An accumulator that holds s * y is never rescaled: the bias is added as
+// s * b and LayerNorm runs with eps * s^2, which gives the LayerNorm of y + b
+// exactly (s is a power of two).  The node kernel stores the projections
+// P = [W_s h; W_d h] already multiplied by the scale of the consuming edge
+// MLP's first layer, which is the scale its W_e part uses too.
+#include "device_common.h"
+
+namespace gnn {
+namespace {
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef float f8 __attribute__((ext_vector_type(8)));
+typedef unsigned u4 __attribute__((ext_vector_type(4)));
+
+constexpr int SW = 8;  // waves per workgroup
+
+__device__ __forceinline__ f8 cat8(const f4 &a, const f4 &b) {
+  return f8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+
+__device__ __forceinline__ void split2(const f8 &x, h8 &x1, h8 &x2) {
+  x1 = __builtin_convertvector(x, h8);
+  x2 = __builtin_convertvector(x - __builtin_convertvector(x1, f8), h8);
+}
+
+// bf16 -> fp32 by placing the 16 bits on top (exact).
+__device__ __forceinline__ f8 widen_bf16(const bf8 &a) {
+  const u4 u = __builtin_bit_cast(u4, a);
+  f8 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    r[2 * i] = __builtin_bit_cast(float, u[i] << 16);
+    r[2 * i + 1] = __builtin_bit_cast(float, u[i] & 0xffff0000u);
+  }
+  return r;
+}
+
+__device__ __forceinline__ void split3(const f8 &x, bf8 &x1, bf8 &x2, bf8 &x3) {
+  x1 = __builtin_convertvector(x, bf8);
+  const f8 r1 = x - widen_bf16(x1);
+  x2 = __builtin_convertvector(r1, bf8);
+  x3 = __builtin_convertvector(r1 - widen_bf16(x2), bf8);
+}
+
+__device__ __forceinline__ f16v mma_h(const h8 &a, const h8 &b, const f16v &c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f16v mma_b(const bf8 &a, const bf8 &b, const f16v &c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Weight records.  One record holds the A operands of one 16-wide k-step for
+// all MB output blocks, laid out [mb][part][lane] (16 bytes per slot), so
+// that lane l reads its parts of block mb at rec[(parts * mb + part) * 64].
+//
+// acc[mb] += (w1 + w2) (x1 + x2) over one k-step, x given split.
+template <int MB>
+__device__ __forceinline__ void step_h(f16v (&acc)[MB], const h8 *rec, const h8 &x1,
+                                       const h8 &x2) {
+  h8 w1[MB], w2[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    w1[mb] = rec[(2 * mb) * 64];
+    w2[mb] = rec[(2 * mb + 1) * 64];
+  }
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = mma_h(w1[mb], x1, acc[mb]);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = mma_h(w2[mb], x1, acc[mb]);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = mma_h(w1[mb], x2, acc[mb]);
+}
+
+template <int MB>
+__device__ __forceinline__ void step_h(f16v (&acc)[MB], const h8 *rec, const f8 &x) {
+  h8 x1, x2;
+  split2(x, x1, x2);
+  step_h<MB>(acc, rec, x1, x2);
+}
+
+// acc[mb] += (w1 + w2 + w3) (x1 + x2 + x3) over one k-step, six products,
+// two output blocks at a time (their weights, 24 registers, are the only
+// ones live).
+template <int MB>
+__device__ __forceinline__ void step_b(f16v (&acc)[MB], const bf8 *rec, const f8 &x) {
+  bf8 x1, x2, x3;
+  split3(x, x1, x2, x3);
+#pragma unroll
+  for (int m0 = 0; m0 < MB; m0 += 2) {
+    bf8 w[3][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int p = 0; p < 3; ++p) w[p][i] = rec[(3 * (m0 + i) + p) * 64];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) acc[m0 + i] = mma_b(w[0][i], x1, acc[m0 + i]);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) acc[m0 + i] = mma_b(w[1][i], x1, acc[m0 + i]);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) acc[m0 + i] = mma_b(w[0][i], x2, acc[m0 + i]);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) acc[m0 + i] = mma_b(w[2][i], x1, acc[m0 + i]);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) acc[m0 + i] = mma_b(w[1][i], x2, acc[m0 + i]);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) acc[m0 + i] = mma_b(w[0][i], x3, acc[m0 + i]);
+  }
+}
+
+// The eight accumulator values a lane supplies as the B operand of k-step
+// g = 2 mb + p when the operand is the previous layer's accumulators: the
+// features 16 g + 8 (j / 4) + 4 hh + j % 4, j = 0..7.
+template <int MB>
+__device__ __forceinline__ f8 acc_x(const f16v (&a)[MB], int g) {
+  const int mb = g / 2, o = 8 * (g % 2);
+  return f8{a[mb][o], a[mb][o + 1], a[mb][o + 2], a[mb][o + 3],
+            a[mb][o + 4], a[mb][o + 5], a[mb][o + 6], a[mb][o + 7]};
+}
+
+template <int MB>
+__device__ __forceinline__ void zero(f16v (&a)[MB]) {
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) a[mb][v] = 0.f;
+}
+
+template <int MB>
+__device__ __forceinline__ void store_rows(float *__restrict__ o, const f16v (&acc)[MB]) {
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f4 val = {acc[mb][4 * q], acc[mb][4 * q + 1], acc[mb][4 * q + 2], acc[mb][4 * q + 3]};
+      *(f4 *)(o + mb * 32 + 8 * q) = val;
+    }
+}
+
+// Weight stream of the node kernel: all records of one tile, cut into chunks
+// of NF4 float4 per thread (NF4 * 8 KB), double-buffered through LDS.  While
+// the waves multiply out of one buffer, the next chunk is fetched from L2
+// into registers and written into the other buffer; one barrier per chunk.
+template <int NF4>
+struct Stream {
+  const f4 *base;
+  int nchunks;
+  f4 *buf;    // 2 x NF4 * 512 float4
+  int c = 0;  // chunk index within the tile's stream
+  int k = 0;  // chunks consumed so far (selects the buffer)
+  f4 st[NF4];
+  __device__ void fetch(int cc, int tid) {
+#pragma unroll
+    for (int i = 0; i < NF4; ++i) st[i] = base[(size_t)cc * NF4 * 512 + i * 512 + tid];
+  }
+  __device__ void commit(int b, int tid) {
+#pragma unroll
+    for (int i = 0; i < NF4; ++i) buf[b * NF4 * 512 + i * 512 + tid] = st[i];
+  }
+  __device__ const f4 *begin(int tid) {
+    __syncthreads();
+    fetch((c + 1) % nchunks, tid);
+    return buf + (k & 1) * NF4 * 512;
+  }
+  __device__ void end(int tid) {
+    commit((k + 1) & 1, tid);
+    ++k;
+    c = (c + 1) % nchunks;
+  }
+};
+
+// Records per chunk: bf16x3 records (3 parts) in the first layer of the
+// node update, f16x2 records (2 parts) after it.  A chunk is 48 KB (MB = 4)
+// in the update and 32 KB in the encoder.
+constexpr int RPC_B = 4;
+template <bool ENC>
+constexpr int rpc_h() { return ENC ? 4 : 6; }
+template <int MB, bool ENC>
+constexpr int node_nf4() { return (ENC ? 4 * 2 : 4 * 3) * MB * 64 / 512; }
+
+template <int MB, bool ENC, int NPROJ>
+__global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
+  constexpr int H = 32 * MB;
+  constexpr int G = H / 16;  // k-steps per H-wide operand
+  constexpr int NF4 = node_nf4<MB, ENC>();
+  constexpr int RPC_H = rpc_h<ENC>();
+  constexpr int REC_H = 2 * MB * 64;  // h8 slots per f16x2 record
+  constexpr int REC_B = 3 * MB * 64;  // bf8 slots per bf16x3 record
+  static_assert(RPC_H * REC_H == NF4 * 512, "f16x2 chunk size");
+  static_assert(ENC || RPC_B * REC_B == NF4 * 512, "bf16x3 chunk size");
+  __shared__ f4 wbuf[2 * NF4 * 512];
+  const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, n = lane & 31;
+  const int wave = tid >> 6;
+  Stream<NF4> ws{(const f4 *)a.wstream, a.nchunks, wbuf};
+  ws.fetch(0, tid);
+  ws.commit(0, tid);
+
+  const float eps2 = a.eps * a.s2 * a.s2;
+  const int blk = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t tiles = (a.n_rows + 32 * SW - 1) / (32 * SW);
+  for (int64_t tile = blk; tile < tiles; tile += gridDim.x) {
+    // Keeps loop-invariant loads inside the loop (hoisted, they would stay
+    // in registers for the whole kernel).
+    asm volatile("" ::: "memory");
+    const int64_t row = tile * 32 * SW + wave * 32 + n;
+    const bool valid = row < a.n_rows;
+    const int64_t r = valid ? row : a.n_rows - 1;
+
+    f16v acc[MB];
+    if constexpr (ENC) {
+      small_k_layer<MB>(acc, a.x, a.F, (int)r, (const float *)a.mlp.l0.w, a.mlp.l0.b, hh);
+      bias_ln_relu<MB>(acc, nullptr, a.mlp.l0.g, a.mlp.l0.beta, a.eps, hh, false);
+    } else {
+      // Layer 1 over [h; agg_in; agg_out]: 3G bf16x3 records.  The node row
+      // slices are loaded LA records ahead into a ring of LA + 1 slots.
+      zero<MB>(acc);
+      constexpr int NREC = 3 * G, LA = 3;
+      auto load_rec = [&](int rec) {
+        const float *p = a.src[rec / G] + r * H + 16 * (rec % G) + 8 * hh;
+        return cat8(*(const f4 *)p, *(const f4 *)(p + 4));
+      };
+      f8 xr[LA + 1];
+#pragma unroll
+      for (int i = 0; i < LA; ++i) xr[i] = load_rec(i);
+      const bf8 *w = nullptr;
+#pragma unroll
+      for (int i = 0; i < NREC; ++i) {
+        if (i + LA < NREC) xr[(i + LA) % (LA + 1)] = load_rec(i + LA);
+        if (i % RPC_B == 0) w = (const bf8 *)ws.begin(tid) + lane;
+        step_b<MB>(acc, w + (i % RPC_B) * REC_B, xr[i % (LA + 1)]);
+        if (i % RPC_B == RPC_B - 1) ws.end(tid);
+      }
+      bias_ln_relu<MB>(acc, a.mlp.l0.b, a.mlp.l0.g, a.mlp.l0.beta, a.eps, hh, true);
+    }
+
+    // The f16x2 records: layer 2, then the projection halves.  Record i of
+    // this part sits in chunk i / RPC_H at slot i % RPC_H.
+    const h8 *wcur = nullptr;
+    auto rec_h = [&](int i) {
+      if (i % RPC_H == 0) wcur = (const h8 *)ws.begin(tid) + lane;
+      return wcur + (i % RPC_H) * REC_H;
+    };
+    auto rec_done = [&](int i) {
+      if (i % RPC_H == RPC_H - 1) ws.end(tid);
+    };
+    f16v hv[MB];
+    zero<MB>(hv);
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      step_h<MB>(hv, rec_h(g), acc_x<MB>(acc, g));
+      rec_done(g);
+    }
+    bias_ln_relu<MB>(hv, a.mlp.l1.b, a.mlp.l1.g, a.mlp.l1.beta, eps2, hh, true, a.s2);
+    if (valid && a.h_out) store_rows<MB>(a.h_out + row * H + 4 * hh, hv);
+    h8 x1[G], x2[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) split2(acc_x<MB>(hv, g), x1[g], x2[g]);
+#pragma unroll
+    for (int p = 0; p < NPROJ; ++p)
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        f16v pv[MB];
+        zero<MB>(pv);
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const int i = G * (1 + 2 * p + half) + g;
+          step_h<MB>(pv, rec_h(i), x1[g], x2[g]);
+          rec_done(i);
+        }
+        if (valid) store_rows<MB>(a.p_out[p] + row * 2 * H + half * H + 4 * hh, pv);
+      }
+  }
+}
+
+template <int MB, int MODE>
+__global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
+  constexpr int H = 32 * MB;
+  constexpr int G = H / 16;
+  constexpr int NR = G * MB * 2 * 64;  // h8 slots of one H x H matrix
+  constexpr bool HAS_E = MODE != (int)EdgeMode::Enc;
+  constexpr bool HAS_L2 = MODE != (int)EdgeMode::Cls;
+  __shared__ h8 lds[(HAS_E ? NR : 0) + (HAS_L2 ? NR : 0)];
+  __shared__ float prm[6 * H];  // s1 b1, gamma1, beta1, s2 b2, gamma2, beta2
+  h8 *lw_e = lds;
+  h8 *lw_2 = lds + (HAS_E ? NR : 0);
+  for (int i = threadIdx.x; i < NR; i += 64 * SW) {
+    if constexpr (HAS_E) lw_e[i] = ((const h8 *)a.we)[i];
+    if constexpr (HAS_L2) lw_2[i] = ((const h8 *)a.w2)[i];
+  }
+  for (int i = threadIdx.x; i < H; i += 64 * SW) {
+    prm[i] = a.b1[i] * a.s1;
+    prm[H + i] = a.g1[i];
+    prm[2 * H + i] = a.beta1[i];
+    if constexpr (HAS_L2) {
+      prm[3 * H + i] = a.b2[i] * a.s2;
+      prm[4 * H + i] = a.g2[i];
+      prm[5 * H + i] = a.beta2[i];
+    } else {
+      prm[3 * H + i] = ((const float *)a.w2)[i];  // classifier head row
+    }
+  }
+  __syncthreads();
+  const float eps1 = a.eps * a.s1 * a.s1, eps2 = a.eps * a.s2 * a.s2;
+
+  const int lane = threadIdx.x & 63, hh = lane >> 5, n = lane & 31;
+  const int blk = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t gw = (int64_t)blk * SW + (threadIdx.x >> 6);
+  const int64_t nw = (int64_t)gridDim.x * SW;
+  const int64_t units = (a.n_rows + 31) / 32;
+  auto row_of = [&](int64_t u) {
+    const int64_t row = u * 32 + n;
+    return row < a.n_rows ? row : a.n_rows - 1;  // tail lanes recompute the last row
+  };
+
+  // The next unit's edge indices and e row are requested before the
+  // current unit's stores (vector-memory completions are counted in issue
+  // order, so a load issued after a store is waited for with that store).
+  f8 ev[HAS_E ? G : 1];
+  auto load_e = [&](int64_t rr) {
+    const float *ep = a.e_in + rr * H + 8 * hh;
+#pragma unroll
+    for (int g = 0; g < G; ++g) ev[g] = cat8(*(const f4 *)(ep + 16 * g), *(const f4 *)(ep + 16 * g + 4));
+  };
+  int32_t nsrc = 0, ndst = 0;
+  if (gw < units) {
+    const int64_t r0 = row_of(gw);
+    nsrc = a.src_idx[r0];
+    ndst = a.dst_idx[r0];
+    if constexpr (HAS_E) load_e(r0);
+  }
+  for (int64_t u = gw; u < units; u += nw) {
+    // Keeps the LDS record reads inside the loop (they are loop-invariant;
+    // hoisted, they would pin every weight in registers).
+    asm volatile("" ::: "memory");
+    const int64_t row = u * 32 + n;
+    const bool valid = row < a.n_rows;
+    const int64_t s = clamp_idx(nsrc, a.n_nodes);
+    const int64_t d = clamp_idx(ndst, a.n_nodes);
+
+    // Layer 1 = s1 (P[src][0:H] + P[dst][H:2H] + W_e e) (+ s1 b1 in the LayerNorm).
+    f16v acc[MB];
+    {
+      const float *ps = a.P + s * 2 * H + 4 * hh;
+      const float *pd = a.P + d * 2 * H + H + 4 * hh;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int f = mb * 32 + 8 * q;
+          const f4 x = *(const f4 *)(ps + f) + *(const f4 *)(pd + f);
+#pragma unroll
+          for (int t = 0; t < 4; ++t) acc[mb][4 * q + t] = x[t];
+        }
+    }
+    if constexpr (HAS_E) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) step_h<MB>(acc, lw_e + g * 2 * MB * 64 + lane, ev[g]);
+    }
+    {
+      const int64_t un = u + nw;
+      if (un < units) {
+        const int64_t rn = row_of(un);
+        nsrc = a.src_idx[rn];
+        ndst = a.dst_idx[rn];
+        if constexpr (HAS_E) load_e(rn);
+      }
+    }
+    ln_relu_lds<MB>(acc, prm, eps1, hh);
+
+    if constexpr (!HAS_L2) {
+      float part = 0.f;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f4 ww = *(const f4 *)(prm + 3 * H + mb * 32 + 8 * q + 4 * hh);
+#pragma unroll
+          for (int t = 0; t < 4; ++t) part += acc[mb][4 * q + t] * ww[t];
+        }
+      part += __shfl_xor(part, 32);
+      if (valid && hh == 0) {
+        const float z = part + a.b2[0];
+        if (a.out_logit) a.out_logit[row] = z;
+        if (a.out_score) a.out_score[row] = sigmoidf_stable(z);
+      }
+    } else {
+      f16v acc2[MB];
+      zero<MB>(acc2);
+#pragma unroll
+      for (int g = 0; g < G; ++g) step_h<MB>(acc2, lw_2 + g * 2 * MB * 64 + lane, acc_x<MB>(acc, g));
+      ln_relu_lds<MB>(acc2, prm + 3 * H, eps2, hh);
+      if (valid) store_rows<MB>(a.e_out + row * H + 4 * hh, acc2);
+    }
+  }
+}
+
+template <int MB>
+hipError_t node_h(bool enc, const NodeArgs &a, int grid, hipStream_t stream) {
+  const int64_t tiles = (a.n_rows + 32 * SW - 1) / (32 * SW);
+  if (tiles <= 0) return hipSuccess;
+  const unsigned nb = (unsigned)(tiles < grid ? tiles : grid);
+  if (enc) {
+    if (a.nproj == 2)
+      node_split<MB, true, 2><<<nb, 64 * SW, 0, stream>>>(a);
+    else
+      node_split<MB, true, 1><<<nb, 64 * SW, 0, stream>>>(a);
+  } else {
+    node_split<MB, false, 1><<<nb, 64 * SW, 0, stream>>>(a);
+  }
+  return hipGetLastError();
+}
+
+template <int MB>
+hipError_t edge_h(EdgeMode mode, const EdgeArgs &a, int grid, hipStream_t stream) {
+  const int64_t units = (a.n_rows + 31) / 32;
+  const int64_t need = (units + SW - 1) / SW;
+  if (need <= 0) return hipSuccess;
+  const unsigned nb = (unsigned)(need < grid ? need : grid);
+  switch (mode) {
+    case EdgeMode::Enc: edge_split<MB, 0><<<nb, 64 * SW, 0, stream>>>(a); break;
+    case EdgeMode::Upd: edge_split<MB, 1><<<nb, 64 * SW, 0, stream>>>(a); break;
+    case EdgeMode::Cls: edge_split<MB, 2><<<nb, 64 * SW, 0, stream>>>(a); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+// Chunks of a node stream: the encoder holds (1 + 2 nproj) f16x2 matrices,
+// the update 3H/16 bf16x3 records and three f16x2 matrices.
+int node_split_chunks(bool enc, int hidden, int nproj) {
+  const int G = hidden / 16;
+  return enc ? (G * (1 + 2 * nproj)) / 4 : (3 * G) / RPC_B + (3 * G) / 6;
+}
+
+size_t node_split_chunk_bytes(bool enc, int hidden) {
+  return (size_t)(enc ? 4 * 2 : 4 * 3) * (hidden / 32) * 64 * 16;
+}
+
+hipError_t launch_node_split(bool enc, int hidden, const NodeArgs &a, int grid,
+                             hipStream_t stream) {
+  if (a.F > MAX_F || a.nproj < 1 || a.nproj > 2 || (!enc && a.nproj != 1) || grid <= 0)
+    return hipErrorInvalidValue;
+  if (a.nchunks != node_split_chunks(enc, hidden, a.nproj)) return hipErrorInvalidValue;
+  switch (hidden) {
+    case 64: return node_h<2>(enc, a, grid, stream);
+    case 128: return node_h<4>(enc, a, grid, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+int edge_split_grid(EdgeMode mode, int hidden, int n_cu) {
+  const void *fn = nullptr;
+  if (hidden == 64)
+    fn = mode == EdgeMode::Enc   ? (const void *)edge_split<2, 0>
+         : mode == EdgeMode::Upd ? (const void *)edge_split<2, 1>
+                                 : (const void *)edge_split<2, 2>;
+  else
+    fn = mode == EdgeMode::Enc   ? (const void *)edge_split<4, 0>
+         : mode == EdgeMode::Upd ? (const void *)edge_split<4, 1>
+                                 : (const void *)edge_split<4, 2>;
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 64 * SW, 0) != hipSuccess ||
+      per_cu < 1)
+    per_cu = 1;
+  return per_cu * (n_cu > 0 ? n_cu : 1);
+}
+
+hipError_t launch_edge_split(EdgeMode mode, int hidden, const EdgeArgs &a, int grid,
+                             hipStream_t stream) {
+  if (grid <= 0) return hipErrorInvalidValue;
+  switch (hidden) {
+    case 64: return edge_h<2>(mode, a, grid, stream);
+    case 128: return edge_h<4>(mode, a, grid, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace gnn

@@ -28,6 +28,7 @@ GNN_FP32 = 0
 GNN_BF16 = 1
 GNN_VALIDATE_INDICES = 1
 GNN_LITERAL_GATHER = 2
+GNN_FP32_MFMA = 4
 
 EXPORTS = ("gnn_weight_count", "gnn_create", "gnn_infer", "gnn_infer_logits",
            "gnn_filter_weight_count", "gnn_filter_create", "gnn_filter_apply",

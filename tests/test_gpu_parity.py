@@ -34,9 +34,11 @@ def _tiny_random(seed, n, e, loops=False):
     return x, ei
 
 
-# fp32 runs both forms of the edge MLPs' first layer: the default regrouping
-# at node level (flags 0) and the per-edge gather (GNN_LITERAL_GATHER = 2).
-PATHS = [0, 2]
+# fp32 runs three kernel sets: the default regrouping of the edge MLPs'
+# first layer at node level with split-precision products on the fp16/bf16
+# matrix cores (flags 0), the same regrouping on the fp32 matrix cores
+# (GNN_FP32_MFMA = 4), and the per-edge gather (GNN_LITERAL_GATHER = 2).
+PATHS = [0, 4, 2]
 
 
 @pytest.mark.parametrize("flags", PATHS)
@@ -305,3 +307,65 @@ def test_hidden64_many_tiles_per_workgroup(G, oracle_mod, flags):
     ref = oracle_mod.forward(w, x, ei, 64, 2)
     got = run_model(G, w, G.make_dims(3, 64, 2, flags=flags), x, ei)
     assert_logits_close(got, ref["logits"])
+
+
+def _hub_free_graph(seed, n=3000, e=12000):
+    rng = np.random.default_rng(seed)
+    x = rng.normal(size=(n, 3)).astype(np.float32)
+    ei = rng.integers(0, n, size=(2, e)).astype(np.int32)
+    return x, ei
+
+
+def test_split_products_take_fp32_mfma_path_outside_fp16_range(G, oracle_mod):
+    # gamma = 5000 on one LayerNorm: its outputs can reach 5000 sqrt(63) > 2^15,
+    # beyond what the fp16 parts of a split product can hold, so the handle
+    # must use the fp32 matrix-core kernels: bitwise the GNN_FP32_MFMA result.
+    x, ei = _hub_free_graph(51)
+    w = I.make_weights(3, 64, 1, 51, affine_noise=0.2)
+    V = I.blob_views(w, 3, 64, 1)
+    V["edge_mlp0.0.g"][:] = 5000.0
+    ref = oracle_mod.forward(w, x, ei, 64, 2)
+    dflt = run_model(G, w, G.make_dims(3, 64, 2), x, ei)
+    f32 = run_model(G, w, G.make_dims(3, 64, 2, flags=G.GNN_FP32_MFMA), x, ei)
+    assert np.array_equal(dflt, f32)
+    assert_logits_close(dflt, ref["logits"])
+
+
+def test_split_products_large_but_in_range_activations(G, oracle_mod):
+    # every gamma and beta times 1000 (gamma ~ 1000, |beta| <= 200): LayerNorm
+    # outputs up to ~1e4, inside the fp16 range of the split parts (the split
+    # path runs).  Logits of O(1) are then differences of O(1e4) terms, so
+    # fp32 itself is off by more than 1e-4 here: the split products must stay
+    # within twice the fp32 matrix-core path's error.
+    x, ei = _hub_free_graph(52)
+    w = I.make_weights(3, 64, 1, 52, affine_noise=0.2)
+    V = I.blob_views(w, 3, 64, 1)
+    for k in V:
+        if k.endswith(".g") or k.endswith(".beta"):
+            V[k][:] *= 1000.0
+    ref = oracle_mod.forward(w, x, ei, 64, 2)["logits"]
+    dflt = run_model(G, w, G.make_dims(3, 64, 2), x, ei)
+    f32 = run_model(G, w, G.make_dims(3, 64, 2, flags=G.GNN_FP32_MFMA), x, ei)
+    assert not np.array_equal(dflt, f32)  # the split kernels ran
+    scale = np.maximum(1.0, np.abs(ref))
+    e_split = float(np.max(np.abs(dflt - ref) / scale))
+    e_f32 = float(np.max(np.abs(f32 - ref) / scale))
+    print(f"large activations: split {e_split:.2e} fp32 mfma {e_f32:.2e}", flush=True)
+    assert e_split <= 2 * e_f32 + 1e-6
+
+
+@pytest.mark.parametrize("H", [64, 128])
+def test_split_products_error_matches_fp32_mfma(G, oracle_mod, H):
+    # The split products are meant to be as accurate as fp32 ones: on the
+    # tiny event their worst logit error stays within twice that of the
+    # fp32 matrix-core path (plus a floor of 1e-6).
+    c = I.CONFIGS["tiny"]
+    g = I.make_graph(c)
+    w = I.make_weights(3, H, 1, c.weight_seed, affine_noise=0.3)
+    ref = oracle_mod.forward(w, g.x, g.edge_index, H, 4)["logits"]
+    def err(flags):
+        z = run_model(G, w, G.make_dims(3, H, 4, flags=flags), g.x, g.edge_index)
+        return float(np.max(np.abs(z - ref) / np.maximum(1.0, np.abs(ref))))
+    e_split, e_f32 = err(0), err(G.GNN_FP32_MFMA)
+    print(f"H={H} split {e_split:.2e} fp32 mfma {e_f32:.2e}", flush=True)
+    assert e_split <= 2 * e_f32 + 1e-6
