@@ -175,6 +175,18 @@ def main():
     torch.cuda.synchronize()
     wcc_ms = (time.perf_counter() - tw) * 1000.0 / 5
     n_comp = int(torch.unique(labels).numel())
+    # The same event with its edge list in a seeded random order (the
+    # generator emits edges grouped by source, which favours the gathers).
+    gs, _ = I.shuffled(g, 7)
+    eis_ = torch.as_tensor(gs.edge_index).cuda()
+    m(x, eis_, out)
+    torch.cuda.synchronize()
+    ts = time.perf_counter()
+    for _ in range(5):
+        m(x, eis_, out)
+    torch.cuda.synchronize()
+    shuf_ms = (time.perf_counter() - ts) * 1000.0 / 5
+    del eis_
     m.close()
     side = None
     if split:
@@ -289,6 +301,10 @@ def main():
     }
     if roof_node:
         rec["roofline_node_update"] = roof_node
+    rec["shuffled_edge_order"] = {
+        "ms_per_event": round(shuf_ms, 4), "edges_per_s": round(E / shuf_ms * 1e3, 1),
+        "note": "same event, edge list in a seeded random order (seed 7), 5 events after the "
+                "timed region; not part of value"}
     if side:
         rec["fp32_mfma_path"] = side
     if filt:
@@ -372,6 +388,25 @@ def bench_batch(args, cfg):
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     per = np.array([a.elapsed_time(b) for evs in samples for a, b in evs])
+
+    # Throughput against the number of concurrent instances (streams): the
+    # 8 events are dealt round-robin onto k streams; one handle throughout.
+    sweep = []
+    for k in (1, 2, 4, 8):
+        def run_k():
+            for i in range(len(events)):
+                st = streams[i % k]
+                G.gnn_infer(m.handle, xs[i], eis[i], xs[i].shape[0], eis[i].shape[1], outs[i],
+                            st)
+        run_k()
+        torch.cuda.synchronize()
+        ts = time.perf_counter()
+        for _ in range(3):
+            run_k()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - ts) * 1000.0 / 3
+        sweep.append({"streams": k, "ms_per_batch": round(ms, 3),
+                      "edges_per_s": round(total_e / (ms / 1000.0), 1)})
     m.close()
     ms_per_batch = (t1 - t0) * 1000.0 / args.steps
     rec = {
@@ -385,6 +420,7 @@ def bench_batch(args, cfg):
         "ms_per_event_p99": round(float(np.percentile(per, 99)), 3),
         "note": "per-event times overlap across streams; the aggregate rate is the sum of "
                 "edges over the wall time of the batch",
+        "instances": sweep,
     }
     print(json.dumps(rec), flush=True)
 

@@ -175,8 +175,10 @@ struct Stream {
   int k = 0;  // chunks consumed so far (selects the buffer)
   f4 st[NF4];
   __device__ void fetch(int cc, int tid) {
+    // a 32-bit byte offset from the uniform base (one register per address)
+    const char *b = (const char *)base + (uint32_t)(cc * NF4 * 512 + tid) * 16u;
 #pragma unroll
-    for (int i = 0; i < NF4; ++i) st[i] = base[(size_t)cc * NF4 * 512 + i * 512 + tid];
+    for (int i = 0; i < NF4; ++i) st[i] = *(const f4 *)(b + i * 512 * 16);
   }
   __device__ void commit(int b, int tid) {
 #pragma unroll
@@ -240,9 +242,15 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
       // slices are loaded LA records ahead into a ring of LA + 1 slots.
       zero<MB>(acc);
       constexpr int NREC = 3 * G, LA = 3;
+      // Addresses are a per-tile scalar base plus one 32-bit lane offset
+      // shared by the three sources: 64-bit per-lane pointers cost the
+      // registers that the look-ahead needs (a spill reload would wait for
+      // every load in flight).
+      const int64_t t0 = tile * 32 * SW;
+      const uint32_t roff = (uint32_t)((r - t0) * H + 8 * hh) * 4u;
       auto load_rec = [&](int rec) {
-        const float *p = a.src[rec / G] + r * H + 16 * (rec % G) + 8 * hh;
-        return cat8(*(const f4 *)p, *(const f4 *)(p + 4));
+        const char *p = (const char *)(a.src[rec / G] + t0 * H) + roff + 64 * (rec % G);
+        return cat8(*(const f4 *)p, *(const f4 *)(p + 16));
       };
       f8 xr[LA + 1];
 #pragma unroll
