@@ -57,23 +57,27 @@ def edge_update_flops(E, H, factored):
     return 2.0 * E * ((1 if factored else 3) * H * H + H * H)
 
 
-def edge_update_bytes(N, E, H):
+def edge_update_bytes(N, E, H, s=4):
     """Algorithmic HBM bytes of one regrouped edge-update launch: e read and
-    written (fp32), both indices per edge, and every node's projection row
-    [W_s h; W_d h] (2H fp32) read once."""
-    return E * (2 * H * 4 + 8) + N * 2 * H * 4
+    written (s bytes per element), both indices per edge, and every node's
+    projection row [W_s h; W_d h] (2H fp32) read once."""
+    return E * (2 * H * s + 8) + N * 2 * H * 4
 
 
-def node_update_bytes(N, H):
-    """h, agg_in, agg_out read; h and the projection row written (fp32)."""
-    return N * (3 * H * 4 + H * 4 + 2 * H * 4)
+def node_update_bytes(N, H, s=4):
+    """h, agg_in, agg_out read and h written (s bytes per element); the
+    projection row written (fp32)."""
+    return N * (4 * H * s + 2 * H * 4)
 
 
-def split_mfma_flops(N, E, H):
-    """Matrix-core work the split kernels execute per launch (each partial
-    product counted): the edge update runs 3 fp16 products per fp32 product
-    over W_e e and W2; the node update 6 bf16 products over layer 1 (3H -> H)
-    and 3 fp16 products over layer 2 and the 2H x H projection."""
+def split_mfma_flops(N, E, H, bf16=False):
+    """Matrix-core work the regrouped kernels execute per launch (each
+    partial product counted).  fp32 split: the edge update runs 3 fp16
+    products per fp32 product over W_e e and W2; the node update 6 bf16
+    products over layer 1 (3H -> H) and 3 fp16 products over layer 2 and the
+    2H x H projection.  bf16 model: 2 products (hi/lo weights) throughout."""
+    if bf16:
+        return {"edge_update": 2 * 2.0 * E * 2 * H * H, "node_update": 2 * 2.0 * N * 6 * H * H}
     return {"edge_update": 3 * 2.0 * E * 2 * H * H,
             "node_update": 6 * 2.0 * N * 3 * H * H + 3 * 2.0 * N * 3 * H * H}
 
@@ -133,9 +137,10 @@ def main():
     flags = (G.GNN_LITERAL_GATHER if args.literal else 0) | \
         (G.GNN_FP32_MFMA if args.fp32_mfma else 0)
     dims = G.make_dims(3, H, T, 1, dtype, flags=flags)
-    factored = cfg.dtype == "fp32" and not args.literal
-    split = factored and not args.fp32_mfma
-    path = "split" if split else ("fp32_mfma" if factored else "literal")
+    factored = not args.literal
+    bf16 = cfg.dtype == "bf16"
+    split = factored and (bf16 or not args.fp32_mfma)
+    path = ("bf16" if bf16 else "split") if split else ("fp32_mfma" if factored else "literal")
     print(f"# workload {cfg.name}: N={N} E={E} H={H} T={T} {cfg.dtype}", file=sys.stderr,
           flush=True)
 
@@ -189,7 +194,7 @@ def main():
     del eis_
     m.close()
     side = None
-    if split:
+    if split and not bf16:
         # The same event on the fp32 matrix cores, outside the timed region
         # (reported for comparison only).
         m2 = G.Model(w, G.make_dims(3, H, T, 1, dtype, flags=G.GNN_FP32_MFMA))
@@ -221,32 +226,37 @@ def main():
     nu_ms = nu["ms"] / max(nu["launches"], 1)
 
     traffic = None
-    if factored and cfg.name == "full":
+    if factored and cfg.name == "full" and path in TRAFFIC_SOURCES:
         m_t = MEASURED_TRAFFIC.get(kernel_source_hash(path))
         traffic = m_t["edge_update_bytes"] if m_t else None
     if split:
-        eb = edge_update_bytes(N, E, H)
+        eb = edge_update_bytes(N, E, H, act_bytes)
         gbs = eb / (eu_ms / 1000.0) / 1e9
-        mf = split_mfma_flops(N, E, H)
+        mf = split_mfma_flops(N, E, H, bf16)
         eu_mfma = mf["edge_update"] / (eu_ms / 1000.0) / 1e12
-        roof = {"kernel": "edge_split<4,1> (gathers node projections, W_e e, layer 2; "
-                          "f16x2 weights in LDS)",
+        mdt = "bf16" if bf16 else "fp16"
+        roof = {"kernel": ("edge_split<4,1,bf16> (gathers node projections, W_e e, layer 2; "
+                           "hi/lo bf16 weights in LDS)") if bf16 else
+                          ("edge_split<4,1> (gathers node projections, W_e e, layer 2; "
+                           "f16x2 weights in LDS)"),
                 "bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "bytes_per_launch": eb, "avg_launch_ms": round(eu_ms, 4),
-                "mfma": {"dtype": "fp16", "executed_tflop_per_launch": mf["edge_update"] / 1e12,
-                         "achieved": round(eu_mfma, 1), "peak": PEAK_TFLOPS["fp16"],
-                         "unit": "TFLOP/s", "frac": round(eu_mfma / PEAK_TFLOPS["fp16"], 4),
+                "mfma": {"dtype": mdt, "executed_tflop_per_launch": mf["edge_update"] / 1e12,
+                         "achieved": round(eu_mfma, 1), "peak": PEAK_TFLOPS[mdt],
+                         "unit": "TFLOP/s", "frac": round(eu_mfma / PEAK_TFLOPS[mdt], 4),
                          "fp32_equivalent_tflops": round(eu_flops / (eu_ms / 1000.0) / 1e12, 1)}}
-        nb = node_update_bytes(N, H)
+        nb = node_update_bytes(N, H, act_bytes)
         nu_gbs = nb / (nu_ms / 1000.0) / 1e9
         nu_mfma = mf["node_update"] / (nu_ms / 1000.0) / 1e12
-        roof_node = {"kernel": "node_split<4,false,1> (layer 1 bf16x3, layer 2 and the "
-                               "next projection f16x2; weights streamed through LDS)",
+        roof_node = {"kernel": ("node_split<4,false,1,bf16> (hi/lo bf16 weights streamed "
+                                "through LDS)") if bf16 else
+                               ("node_split<4,false,1> (layer 1 bf16x3, layer 2 and the "
+                                "next projection f16x2; weights streamed through LDS)"),
                      "bound": "hbm", "achieved": round(nu_gbs, 1), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(nu_gbs / PEAK_HBM_GBS, 4),
                      "bytes_per_launch": nb, "avg_launch_ms": round(nu_ms, 4),
-                     "mfma": {"dtype": "bf16/fp16",
+                     "mfma": {"dtype": "bf16" if bf16 else "bf16/fp16",
                               "executed_tflop_per_launch": mf["node_update"] / 1e12,
                               "achieved": round(nu_mfma, 1), "peak": PEAK_TFLOPS["fp16"],
                               "unit": "TFLOP/s", "frac": round(nu_mfma / PEAK_TFLOPS["fp16"], 4)}}
@@ -280,8 +290,9 @@ def main():
                                          "for the node MLP's first layer) on the fp16/bf16 "
                                          "matrix cores, fp32 accumulation",
                                 "fp32_mfma": "fp32 matrix cores",
-                                "literal": "per-edge first layer"}[path]
-                   if cfg.dtype == "fp32" else "bf16 matrix cores"},
+                                "literal": "per-edge first layer",
+                                "bf16": "bf16 activations on the bf16 matrix cores, hi/lo "
+                                        "bf16 weights, fp32 accumulation"}[path]},
         "ms_per_event_p50": round(float(np.percentile(per, 50)), 4),
         "ms_per_event_p99": round(float(np.percentile(per, 99)), 4),
         "ms_per_event_min": round(float(per.min()), 4),

@@ -52,13 +52,12 @@ extern "C" {
 
 #define GNN_VALIDATE_INDICES 1u /* check every index is in [0, n_nodes) before
                                    computing; costs one host synchronisation */
-#define GNN_LITERAL_GATHER 2u   /* fp32: evaluate the first layer of every edge
-                                   MLP per edge on the gathered [h_src; h_dst; e]
-                                   rows instead of the default regrouping
+#define GNN_LITERAL_GATHER 2u   /* evaluate the first layer of every edge MLP per
+                                   edge on the gathered [h_src; h_dst; e] rows
+                                   instead of the default regrouping
                                    (W_s h)[src] + (W_d h)[dst] + W_e e with the
                                    node projections computed once per node; the
-                                   two agree up to fp32 rounding.  bf16 always
-                                   uses the per-edge form. */
+                                   two agree up to fp32 rounding (both dtypes) */
 #define GNN_FP32_MFMA 4u        /* fp32, regrouped form: multiply on the fp32
                                    matrix cores (v_mfma_f32_32x32x2_f32).  The
                                    default multiplies fp32 operands split into

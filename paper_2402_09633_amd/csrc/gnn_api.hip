@@ -189,6 +189,26 @@ std::vector<uint16_t> rec_f16x2(const BlobLayer &L, int c0, int K, float s, bool
   return out;
 }
 
+// bf16 hi/lo records of W[:, c0 : c0 + K]: hi = bf16(W), lo = bf16(W - hi)
+// (the bf16 model's weights).
+std::vector<uint16_t> rec_bf16x2(const BlobLayer &L, int c0, int K, bool from_acc) {
+  const int MB = L.fout / 32, G = K / 16;
+  std::vector<uint16_t> out((size_t)G * MB * 2 * 64 * 8);
+  for (int g = 0; g < G; ++g)
+    for (int mb = 0; mb < MB; ++mb)
+      for (int lane = 0; lane < 64; ++lane)
+        for (int j = 0; j < 8; ++j) {
+          const int hh = lane / 32;
+          const int k = from_acc ? 16 * g + 8 * (j / 4) + 4 * hh + j % 4 : 16 * g + 8 * hh + j;
+          const float wv = L.W[(size_t)(mb * 32 + lane % 32) * L.fin + c0 + k];
+          const uint16_t hi = f32_to_bf16(wv);
+          const size_t o = ((((size_t)g * MB + mb) * 2) * 64 + lane) * 8 + j;
+          out[o] = hi;
+          out[o + 64 * 8] = f32_to_bf16(wv - bf16_to_f32(hi));
+        }
+  return out;
+}
+
 // bf16x3 records of W[:, 0:K] with B from HBM: W = w1 + w2 + w3 exactly.
 std::vector<uint16_t> rec_bf16x3(const BlobLayer &L, int K) {
   const int MB = L.fout / 32, G = K / 16;
@@ -238,7 +258,8 @@ struct MlpOff {
 // split path every matrix is in f16x2 / bf16x3 records and the edge kernels
 // read W2 from records too; in the fp32 path they are fp32 MFMA fragments.
 struct FactDev {
-  bool split = false;
+  bool split = false;  // split.hip kernels (fp32 split products, or the bf16 model)
+  bool bf16 = false;   // with split: the bf16 model
   const void *we_cls = nullptr;
   std::vector<const void *> we_em;
   // node-kernel streams: encoder (W2 | two projections) and, per
@@ -571,7 +592,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
     na.p_out[1] = w.pb;
     na.eps = d.ln_eps;
     st.begin();
-    HIP_TRY(fd.split ? launch_node_split(true, H, na, fd.grid_node, stream)
+    HIP_TRY(fd.split ? launch_node_split(true, H, na, fd.grid_node, fd.bf16, stream)
                      : launch_node_f32(true, H, na, fd.grid_node, stream));
     st.end(GNN_STAGE_NODE_ENC);
 
@@ -593,7 +614,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       return ea;
     };
     auto launch_edge = [&](EdgeMode mode, const EdgeArgs &ea, int grid) {
-      return fd.split ? launch_edge_split(mode, H, ea, grid, stream)
+      return fd.split ? launch_edge_split(mode, H, ea, grid, fd.bf16, stream)
                       : launch_edge_f32(mode, H, ea, grid, stream);
     };
     {
@@ -640,7 +661,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       nu.p_out[0] = w.pb;
       nu.eps = d.ln_eps;
       st.begin();
-      HIP_TRY(fd.split ? launch_node_split(false, H, nu, fd.grid_node, stream)
+      HIP_TRY(fd.split ? launch_node_split(false, H, nu, fd.grid_node, fd.bf16, stream)
                        : launch_node_f32(false, H, nu, fd.grid_node, stream));
       st.end(GNN_STAGE_NODE_UPDATE);
     }
@@ -651,7 +672,10 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
           {ro.ain, w.ain, nh, true}, {ro.aout, w.aout, nh, true}};
       for (auto &x2 : ex) {
         if (!x2.dst || x2.n == 0 || (x2.agg && T == 0)) continue;
-        HIP_TRY(hipMemcpyAsync(x2.dst, x2.src, x2.n * 4, hipMemcpyDeviceToDevice, stream));
+        if (act == Act::F32)
+          HIP_TRY(hipMemcpyAsync(x2.dst, x2.src, x2.n * 4, hipMemcpyDeviceToDevice, stream));
+        else
+          HIP_TRY(launch_bf16_to_f32(x2.src, x2.dst, x2.n, stream));
       }
       goto out;
     }
@@ -849,7 +873,7 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
   Staging st;
   MlpOff o_ne, o_ee, o_cls;
   std::vector<MlpOff> o_em(S), o_nm(S);
-  const bool factored = !bf16 && !(d.flags & GNN_LITERAL_GATHER);
+  const bool factored = !(d.flags & GNN_LITERAL_GATHER);
   const int T = d.n_iters;
   size_t o_we_cls = 0, o_enc_stream = 0, o_w2_ee = 0;
   std::vector<size_t> o_we_em(S), o_upd_stream(T), o_w2_em(S);
@@ -883,7 +907,7 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
     auto next_edge_l1 = [&](int t) -> const BlobLayer & {
       return t + 1 < T ? e0s[S == 1 ? 0 : t + 1] : c0;
     };
-    if (factored) {
+    if (factored && !bf16) {
       // Split products need every LayerNorm output that feeds an f16x2
       // product inside the fp16 range (with a factor 2 to spare).
       double bound = 0.0;
@@ -893,7 +917,40 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
           bound = fmax(bound, ln_out_bound(*L));
       split = !(d.flags & GNN_FP32_MFMA) && bound <= 32768.0;
     }
-    if (factored && split) {
+    if (factored && bf16) {
+      // The bf16 model on the same kernels: hi/lo bf16 records, no scales.
+      split = true;
+      auto add16 = [&](const std::vector<uint16_t> &v) {
+        return st.add(v.data(), v.size() * sizeof(uint16_t));
+      };
+      auto cat = [](std::vector<uint16_t> &dst, const std::vector<uint16_t> &src) {
+        dst.insert(dst.end(), src.begin(), src.end());
+      };
+      for (int s = 0; s < S; ++s) {
+        fdh.s1_em.push_back(1.f);
+        fdh.s2_em.push_back(1.f);
+        fdh.s2_nm.push_back(1.f);
+        o_we_em[s] = add16(rec_bf16x2(e0s[s], 2 * H, H, false));
+        o_w2_em[s] = add16(rec_bf16x2(e1s[s], 0, H, true));
+      }
+      o_we_cls = add16(rec_bf16x2(c0, 2 * H, H, false));
+      o_w2_ee = add16(rec_bf16x2(b1, 0, H, true));
+      auto proj = [&](std::vector<uint16_t> &dst, const BlobLayer &L) {
+        cat(dst, rec_bf16x2(L, 0, H, true));
+        cat(dst, rec_bf16x2(L, H, H, true));
+      };
+      std::vector<uint16_t> es = rec_bf16x2(a1, 0, H, true);
+      proj(es, b0);
+      proj(es, next_edge_l1(-1));
+      o_enc_stream = add16(es);
+      for (int t = 0; t < T; ++t) {
+        const int k = S == 1 ? 0 : t;
+        std::vector<uint16_t> us = rec_bf16x2(n0s[k], 0, 3 * H, false);
+        cat(us, rec_bf16x2(n1s[k], 0, H, true));
+        proj(us, next_edge_l1(t));
+        o_upd_stream[t] = add16(us);
+      }
+    } else if (factored && split) {
       auto add16 = [&](const std::vector<uint16_t> &v) {
         return st.add(v.data(), v.size() * sizeof(uint16_t));
       };
@@ -988,6 +1045,7 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
     FactDev &fd = h->fd;
     fd = fdh;
     fd.split = split;
+    fd.bf16 = bf16;
     fd.we_cls = base + o_we_cls;
     for (int s = 0; s < S; ++s) fd.we_em.push_back(base + o_we_em[s]);
     fd.enc_stream = base + o_enc_stream;
@@ -998,11 +1056,11 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
     if (split) {
       fd.w2_ee = base + o_w2_ee;
       for (int s = 0; s < S; ++s) fd.w2_em.push_back(base + o_w2_em[s]);
-      fd.enc_chunks = node_split_chunks(true, H, 2);
-      fd.upd_chunks = node_split_chunks(false, H, 1);
-      fd.grid_enc = edge_split_grid(EdgeMode::Enc, H, n_cu);
-      fd.grid_upd = edge_split_grid(EdgeMode::Upd, H, n_cu);
-      fd.grid_cls = edge_split_grid(EdgeMode::Cls, H, n_cu);
+      fd.enc_chunks = node_split_chunks(true, H, 2, bf16);
+      fd.upd_chunks = node_split_chunks(false, H, 1, bf16);
+      fd.grid_enc = edge_split_grid(EdgeMode::Enc, H, bf16, n_cu);
+      fd.grid_upd = edge_split_grid(EdgeMode::Upd, H, bf16, n_cu);
+      fd.grid_cls = edge_split_grid(EdgeMode::Cls, H, bf16, n_cu);
     } else {
       const int kg = H / 8;  // k-groups of one H-wide operand; 8 per chunk
       fd.enc_chunks = (kg + 4 * kg) / 8;

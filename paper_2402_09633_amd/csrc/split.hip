@@ -24,11 +24,19 @@
 //          layer, whose input includes the aggregates (sums over up to a
 //          node's whole degree, not bounded by any LayerNorm).
 //
+// The same kernels serve the bf16 model (PREC = BF16): h, e and the
+// aggregates are stored in bf16 and fed to the bf16 matrix cores as they are,
+// every weight is a pair hi = bf16(W), lo = bf16(W - hi) (two products), the
+// LayerNorm outputs are rounded to bf16 where they feed a product, and all
+// sums are fp32; the projections P stay fp32.  No scaling is needed there.
+//
 // An accumulator that holds s * y is never rescaled: the bias is added as
 // s * b and LayerNorm runs with eps * s^2, which gives the LayerNorm of y + b
 // exactly (s is a power of two).  The node kernel stores the projections
 // P = [W_s h; W_d h] already multiplied by the scale of the consuming edge
 // MLP's first layer, which is the scale its W_e part uses too.
+#include <type_traits>
+
 #include "device_common.h"
 
 namespace gnn {
@@ -133,6 +141,27 @@ __device__ __forceinline__ void step_b(f16v (&acc)[MB], const bf8 *rec, const f8
   }
 }
 
+// acc[mb] += (w_hi + w_lo) x over one k-step, x exact in bf16.
+template <int MB>
+__device__ __forceinline__ void step_hl(f16v (&acc)[MB], const bf8 *rec, const bf8 &x) {
+  bf8 w1[MB], w2[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    w1[mb] = rec[(2 * mb) * 64];
+    w2[mb] = rec[(2 * mb + 1) * 64];
+  }
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = mma_b(w1[mb], x, acc[mb]);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = mma_b(w2[mb], x, acc[mb]);
+}
+
+__device__ __forceinline__ bf8 to_bf16(const f8 &x) { return __builtin_convertvector(x, bf8); }
+
+// Operand precision of the kernels below.
+constexpr int SPLIT = 0;  // fp32 activations, split products
+constexpr int BF16 = 1;   // bf16 activations, hi/lo bf16 weights
+
 // The eight accumulator values a lane supplies as the B operand of k-step
 // g = 2 mb + p when the operand is the previous layer's accumulators: the
 // features 16 g + 8 (j / 4) + 4 hh + j % 4, j = 0..7.
@@ -159,6 +188,18 @@ __device__ __forceinline__ void store_rows(float *__restrict__ o, const f16v (&a
     for (int q = 0; q < 4; ++q) {
       const f4 val = {acc[mb][4 * q], acc[mb][4 * q + 1], acc[mb][4 * q + 2], acc[mb][4 * q + 3]};
       *(f4 *)(o + mb * 32 + 8 * q) = val;
+    }
+}
+
+template <int MB>
+__device__ __forceinline__ void store_rows_bf16(__bf16 *__restrict__ o, const f16v (&acc)[MB]) {
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const bf4 val = {(__bf16)acc[mb][4 * q], (__bf16)acc[mb][4 * q + 1],
+                       (__bf16)acc[mb][4 * q + 2], (__bf16)acc[mb][4 * q + 3]};
+      *(bf4 *)(o + mb * 32 + 8 * q) = val;
     }
 }
 
@@ -196,25 +237,31 @@ struct Stream {
   }
 };
 
-// Records per chunk: bf16x3 records (3 parts) in the first layer of the
-// node update, f16x2 records (2 parts) after it.  A chunk is 48 KB (MB = 4)
-// in the update and 32 KB in the encoder.
-constexpr int RPC_B = 4;
+// Records per chunk.  Split: bf16x3 records (3 parts) in the first layer of
+// the node update, f16x2 records (2 parts) after it; bf16: hi/lo records (2
+// parts) throughout.  A chunk is 48 KB (MB = 4) in the update and 32 KB in
+// the encoder.
+template <int PREC>
+constexpr int rpc_l1() { return PREC == SPLIT ? 4 : 6; }
+template <int PREC>
+constexpr int parts_l1() { return PREC == SPLIT ? 3 : 2; }
 template <bool ENC>
 constexpr int rpc_h() { return ENC ? 4 : 6; }
 template <int MB, bool ENC>
 constexpr int node_nf4() { return (ENC ? 4 * 2 : 4 * 3) * MB * 64 / 512; }
 
-template <int MB, bool ENC, int NPROJ>
+template <int MB, bool ENC, int NPROJ, int PREC>
 __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
   constexpr int H = 32 * MB;
   constexpr int G = H / 16;  // k-steps per H-wide operand
   constexpr int NF4 = node_nf4<MB, ENC>();
   constexpr int RPC_H = rpc_h<ENC>();
-  constexpr int REC_H = 2 * MB * 64;  // h8 slots per f16x2 record
-  constexpr int REC_B = 3 * MB * 64;  // bf8 slots per bf16x3 record
-  static_assert(RPC_H * REC_H == NF4 * 512, "f16x2 chunk size");
-  static_assert(ENC || RPC_B * REC_B == NF4 * 512, "bf16x3 chunk size");
+  constexpr int RPC_1 = rpc_l1<PREC>();
+  constexpr int REC_H = 2 * MB * 64;                 // 16-byte slots per 2-part record
+  constexpr int REC_1 = parts_l1<PREC>() * MB * 64;  // slots per layer-1 record
+  static_assert(RPC_H * REC_H == NF4 * 512, "2-part chunk size");
+  static_assert(ENC || RPC_1 * REC_1 == NF4 * 512, "layer-1 chunk size");
+  using act_t = typename std::conditional<PREC == SPLIT, float, __bf16>::type;
   __shared__ f4 wbuf[2 * NF4 * 512];
   const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, n = lane & 31;
   const int wave = tid >> 6;
@@ -238,7 +285,7 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
       small_k_layer<MB>(acc, a.x, a.F, (int)r, (const float *)a.mlp.l0.w, a.mlp.l0.b, hh);
       bias_ln_relu<MB>(acc, nullptr, a.mlp.l0.g, a.mlp.l0.beta, a.eps, hh, false);
     } else {
-      // Layer 1 over [h; agg_in; agg_out]: 3G bf16x3 records.  The node row
+      // Layer 1 over [h; agg_in; agg_out]: 3G records.  The node row
       // slices are loaded LA records ahead into a ring of LA + 1 slots.
       zero<MB>(acc);
       constexpr int NREC = 3 * G, LA = 3;
@@ -247,30 +294,39 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
       // registers that the look-ahead needs (a spill reload would wait for
       // every load in flight).
       const int64_t t0 = tile * 32 * SW;
-      const uint32_t roff = (uint32_t)((r - t0) * H + 8 * hh) * 4u;
+      const uint32_t roff = (uint32_t)((r - t0) * H + 8 * hh) * (uint32_t)sizeof(act_t);
+      const act_t *const *srcs = (const act_t *const *)a.src;
+      using xrec_t = typename std::conditional<PREC == SPLIT, f8, bf8>::type;
       auto load_rec = [&](int rec) {
-        const char *p = (const char *)(a.src[rec / G] + t0 * H) + roff + 64 * (rec % G);
-        return cat8(*(const f4 *)p, *(const f4 *)(p + 16));
+        const char *p = (const char *)(srcs[rec / G] + t0 * H) + roff +
+                        16 * (int)sizeof(act_t) * (rec % G);
+        if constexpr (PREC == SPLIT)
+          return cat8(*(const f4 *)p, *(const f4 *)(p + 16));
+        else
+          return *(const bf8 *)p;
       };
-      f8 xr[LA + 1];
+      xrec_t xr[LA + 1];
 #pragma unroll
       for (int i = 0; i < LA; ++i) xr[i] = load_rec(i);
       const bf8 *w = nullptr;
 #pragma unroll
       for (int i = 0; i < NREC; ++i) {
         if (i + LA < NREC) xr[(i + LA) % (LA + 1)] = load_rec(i + LA);
-        if (i % RPC_B == 0) w = (const bf8 *)ws.begin(tid) + lane;
-        step_b<MB>(acc, w + (i % RPC_B) * REC_B, xr[i % (LA + 1)]);
-        if (i % RPC_B == RPC_B - 1) ws.end(tid);
+        if (i % RPC_1 == 0) w = (const bf8 *)ws.begin(tid) + lane;
+        if constexpr (PREC == SPLIT)
+          step_b<MB>(acc, w + (i % RPC_1) * REC_1, xr[i % (LA + 1)]);
+        else
+          step_hl<MB>(acc, w + (i % RPC_1) * REC_1, xr[i % (LA + 1)]);
+        if (i % RPC_1 == RPC_1 - 1) ws.end(tid);
       }
       bias_ln_relu<MB>(acc, a.mlp.l0.b, a.mlp.l0.g, a.mlp.l0.beta, a.eps, hh, true);
     }
 
-    // The f16x2 records: layer 2, then the projection halves.  Record i of
+    // The 2-part records: layer 2, then the projection halves.  Record i of
     // this part sits in chunk i / RPC_H at slot i % RPC_H.
-    const h8 *wcur = nullptr;
+    const f4 *wcur = nullptr;
     auto rec_h = [&](int i) {
-      if (i % RPC_H == 0) wcur = (const h8 *)ws.begin(tid) + lane;
+      if (i % RPC_H == 0) wcur = ws.begin(tid) + lane;
       return wcur + (i % RPC_H) * REC_H;
     };
     auto rec_done = [&](int i) {
@@ -280,14 +336,29 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
     zero<MB>(hv);
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      step_h<MB>(hv, rec_h(g), acc_x<MB>(acc, g));
+      if constexpr (PREC == SPLIT)
+        step_h<MB>(hv, (const h8 *)rec_h(g), acc_x<MB>(acc, g));
+      else
+        step_hl<MB>(hv, (const bf8 *)rec_h(g), to_bf16(acc_x<MB>(acc, g)));
       rec_done(g);
     }
     bias_ln_relu<MB>(hv, a.mlp.l1.b, a.mlp.l1.g, a.mlp.l1.beta, eps2, hh, true, a.s2);
-    if (valid && a.h_out) store_rows<MB>(a.h_out + row * H + 4 * hh, hv);
-    h8 x1[G], x2[G];
+    if (valid && a.h_out) {
+      if constexpr (PREC == SPLIT)
+        store_rows<MB>(a.h_out + row * H + 4 * hh, hv);
+      else
+        store_rows_bf16<MB>((__bf16 *)a.h_out + row * H + 4 * hh, hv);
+    }
+    // the projections read h as it is stored
+    using xp_t = typename std::conditional<PREC == SPLIT, h8, bf8>::type;
+    xp_t x1[G], x2[PREC == SPLIT ? G : 1];
 #pragma unroll
-    for (int g = 0; g < G; ++g) split2(acc_x<MB>(hv, g), x1[g], x2[g]);
+    for (int g = 0; g < G; ++g) {
+      if constexpr (PREC == SPLIT)
+        split2(acc_x<MB>(hv, g), x1[g], x2[g]);
+      else
+        x1[g] = to_bf16(acc_x<MB>(hv, g));
+    }
 #pragma unroll
     for (int p = 0; p < NPROJ; ++p)
 #pragma unroll
@@ -297,7 +368,10 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
 #pragma unroll
         for (int g = 0; g < G; ++g) {
           const int i = G * (1 + 2 * p + half) + g;
-          step_h<MB>(pv, rec_h(i), x1[g], x2[g]);
+          if constexpr (PREC == SPLIT)
+            step_h<MB>(pv, (const h8 *)rec_h(i), x1[g], x2[g]);
+          else
+            step_hl<MB>(pv, (const bf8 *)rec_h(i), x1[g]);
           rec_done(i);
         }
         if (valid) store_rows<MB>(a.p_out[p] + row * 2 * H + half * H + 4 * hh, pv);
@@ -305,11 +379,12 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
   }
 }
 
-template <int MB, int MODE>
+template <int MB, int MODE, int PREC>
 __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
   constexpr int H = 32 * MB;
   constexpr int G = H / 16;
-  constexpr int NR = G * MB * 2 * 64;  // h8 slots of one H x H matrix
+  constexpr int NR = G * MB * 2 * 64;  // 16-byte slots of one H x H matrix (2-part records)
+  using act_t = typename std::conditional<PREC == SPLIT, float, __bf16>::type;
   constexpr bool HAS_E = MODE != (int)EdgeMode::Enc;
   constexpr bool HAS_L2 = MODE != (int)EdgeMode::Cls;
   __shared__ h8 lds[(HAS_E ? NR : 0) + (HAS_L2 ? NR : 0)];
@@ -348,11 +423,17 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
   // The next unit's edge indices and e row are requested before the
   // current unit's stores (vector-memory completions are counted in issue
   // order, so a load issued after a store is waited for with that store).
-  f8 ev[HAS_E ? G : 1];
+  using xrec_t = typename std::conditional<PREC == SPLIT, f8, bf8>::type;
+  xrec_t ev[HAS_E ? G : 1];
   auto load_e = [&](int64_t rr) {
-    const float *ep = a.e_in + rr * H + 8 * hh;
+    const act_t *ep = (const act_t *)a.e_in + rr * H + 8 * hh;
 #pragma unroll
-    for (int g = 0; g < G; ++g) ev[g] = cat8(*(const f4 *)(ep + 16 * g), *(const f4 *)(ep + 16 * g + 4));
+    for (int g = 0; g < G; ++g) {
+      if constexpr (PREC == SPLIT)
+        ev[g] = cat8(*(const f4 *)(ep + 16 * g), *(const f4 *)(ep + 16 * g + 4));
+      else
+        ev[g] = *(const bf8 *)(ep + 16 * g);
+    }
   };
   int32_t nsrc = 0, ndst = 0;
   if (gw < units) {
@@ -387,7 +468,12 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
     }
     if constexpr (HAS_E) {
 #pragma unroll
-      for (int g = 0; g < G; ++g) step_h<MB>(acc, lw_e + g * 2 * MB * 64 + lane, ev[g]);
+      for (int g = 0; g < G; ++g) {
+        if constexpr (PREC == SPLIT)
+          step_h<MB>(acc, lw_e + g * 2 * MB * 64 + lane, ev[g]);
+        else
+          step_hl<MB>(acc, (const bf8 *)(lw_e + g * 2 * MB * 64 + lane), ev[g]);
+      }
     }
     {
       const int64_t un = u + nw;
@@ -420,78 +506,89 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
       f16v acc2[MB];
       zero<MB>(acc2);
 #pragma unroll
-      for (int g = 0; g < G; ++g) step_h<MB>(acc2, lw_2 + g * 2 * MB * 64 + lane, acc_x<MB>(acc, g));
+      for (int g = 0; g < G; ++g) {
+        if constexpr (PREC == SPLIT)
+          step_h<MB>(acc2, lw_2 + g * 2 * MB * 64 + lane, acc_x<MB>(acc, g));
+        else
+          step_hl<MB>(acc2, (const bf8 *)(lw_2 + g * 2 * MB * 64 + lane), to_bf16(acc_x<MB>(acc, g)));
+      }
       ln_relu_lds<MB>(acc2, prm + 3 * H, eps2, hh);
-      if (valid) store_rows<MB>(a.e_out + row * H + 4 * hh, acc2);
+      if (valid) {
+        if constexpr (PREC == SPLIT)
+          store_rows<MB>(a.e_out + row * H + 4 * hh, acc2);
+        else
+          store_rows_bf16<MB>((__bf16 *)a.e_out + row * H + 4 * hh, acc2);
+      }
     }
   }
 }
 
-template <int MB>
+template <int MB, int PREC>
 hipError_t node_h(bool enc, const NodeArgs &a, int grid, hipStream_t stream) {
   const int64_t tiles = (a.n_rows + 32 * SW - 1) / (32 * SW);
   if (tiles <= 0) return hipSuccess;
   const unsigned nb = (unsigned)(tiles < grid ? tiles : grid);
   if (enc) {
     if (a.nproj == 2)
-      node_split<MB, true, 2><<<nb, 64 * SW, 0, stream>>>(a);
+      node_split<MB, true, 2, PREC><<<nb, 64 * SW, 0, stream>>>(a);
     else
-      node_split<MB, true, 1><<<nb, 64 * SW, 0, stream>>>(a);
+      node_split<MB, true, 1, PREC><<<nb, 64 * SW, 0, stream>>>(a);
   } else {
-    node_split<MB, false, 1><<<nb, 64 * SW, 0, stream>>>(a);
+    node_split<MB, false, 1, PREC><<<nb, 64 * SW, 0, stream>>>(a);
   }
   return hipGetLastError();
 }
 
-template <int MB>
+template <int MB, int PREC>
 hipError_t edge_h(EdgeMode mode, const EdgeArgs &a, int grid, hipStream_t stream) {
   const int64_t units = (a.n_rows + 31) / 32;
   const int64_t need = (units + SW - 1) / SW;
   if (need <= 0) return hipSuccess;
   const unsigned nb = (unsigned)(need < grid ? need : grid);
   switch (mode) {
-    case EdgeMode::Enc: edge_split<MB, 0><<<nb, 64 * SW, 0, stream>>>(a); break;
-    case EdgeMode::Upd: edge_split<MB, 1><<<nb, 64 * SW, 0, stream>>>(a); break;
-    case EdgeMode::Cls: edge_split<MB, 2><<<nb, 64 * SW, 0, stream>>>(a); break;
+    case EdgeMode::Enc: edge_split<MB, 0, PREC><<<nb, 64 * SW, 0, stream>>>(a); break;
+    case EdgeMode::Upd: edge_split<MB, 1, PREC><<<nb, 64 * SW, 0, stream>>>(a); break;
+    case EdgeMode::Cls: edge_split<MB, 2, PREC><<<nb, 64 * SW, 0, stream>>>(a); break;
   }
   return hipGetLastError();
 }
 
+template <int PREC>
+const void *edge_fn(EdgeMode mode, int hidden) {
+  if (hidden == 64)
+    return mode == EdgeMode::Enc   ? (const void *)edge_split<2, 0, PREC>
+           : mode == EdgeMode::Upd ? (const void *)edge_split<2, 1, PREC>
+                                   : (const void *)edge_split<2, 2, PREC>;
+  return mode == EdgeMode::Enc   ? (const void *)edge_split<4, 0, PREC>
+         : mode == EdgeMode::Upd ? (const void *)edge_split<4, 1, PREC>
+                                 : (const void *)edge_split<4, 2, PREC>;
+}
+
 }  // namespace
 
-// Chunks of a node stream: the encoder holds (1 + 2 nproj) f16x2 matrices,
-// the update 3H/16 bf16x3 records and three f16x2 matrices.
-int node_split_chunks(bool enc, int hidden, int nproj) {
+// Chunks of a node stream: the encoder holds (1 + 2 nproj) H x H matrices
+// of 2-part records; the update 3H/16 layer-1 records (3 parts when split, 2
+// in bf16) and three H x H matrices.
+int node_split_chunks(bool enc, int hidden, int nproj, bool bf16) {
   const int G = hidden / 16;
-  return enc ? (G * (1 + 2 * nproj)) / 4 : (3 * G) / RPC_B + (3 * G) / 6;
+  if (enc) return (G * (1 + 2 * nproj)) / 4;
+  return (3 * G) / (bf16 ? rpc_l1<BF16>() : rpc_l1<SPLIT>()) + (3 * G) / 6;
 }
 
-size_t node_split_chunk_bytes(bool enc, int hidden) {
-  return (size_t)(enc ? 4 * 2 : 4 * 3) * (hidden / 32) * 64 * 16;
-}
-
-hipError_t launch_node_split(bool enc, int hidden, const NodeArgs &a, int grid,
+hipError_t launch_node_split(bool enc, int hidden, const NodeArgs &a, int grid, bool bf16,
                              hipStream_t stream) {
   if (a.F > MAX_F || a.nproj < 1 || a.nproj > 2 || (!enc && a.nproj != 1) || grid <= 0)
     return hipErrorInvalidValue;
-  if (a.nchunks != node_split_chunks(enc, hidden, a.nproj)) return hipErrorInvalidValue;
+  if (a.nchunks != node_split_chunks(enc, hidden, a.nproj, bf16)) return hipErrorInvalidValue;
   switch (hidden) {
-    case 64: return node_h<2>(enc, a, grid, stream);
-    case 128: return node_h<4>(enc, a, grid, stream);
+    case 64: return bf16 ? node_h<2, BF16>(enc, a, grid, stream) : node_h<2, SPLIT>(enc, a, grid, stream);
+    case 128: return bf16 ? node_h<4, BF16>(enc, a, grid, stream) : node_h<4, SPLIT>(enc, a, grid, stream);
   }
   return hipErrorInvalidValue;
 }
 
-int edge_split_grid(EdgeMode mode, int hidden, int n_cu) {
-  const void *fn = nullptr;
-  if (hidden == 64)
-    fn = mode == EdgeMode::Enc   ? (const void *)edge_split<2, 0>
-         : mode == EdgeMode::Upd ? (const void *)edge_split<2, 1>
-                                 : (const void *)edge_split<2, 2>;
-  else
-    fn = mode == EdgeMode::Enc   ? (const void *)edge_split<4, 0>
-         : mode == EdgeMode::Upd ? (const void *)edge_split<4, 1>
-                                 : (const void *)edge_split<4, 2>;
+int edge_split_grid(EdgeMode mode, int hidden, bool bf16, int n_cu) {
+  const void *fn = bf16 ? edge_fn<BF16>(mode, hidden) : edge_fn<SPLIT>(mode, hidden);
   int per_cu = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 64 * SW, 0) != hipSuccess ||
       per_cu < 1)
@@ -499,12 +596,12 @@ int edge_split_grid(EdgeMode mode, int hidden, int n_cu) {
   return per_cu * (n_cu > 0 ? n_cu : 1);
 }
 
-hipError_t launch_edge_split(EdgeMode mode, int hidden, const EdgeArgs &a, int grid,
+hipError_t launch_edge_split(EdgeMode mode, int hidden, const EdgeArgs &a, int grid, bool bf16,
                              hipStream_t stream) {
   if (grid <= 0) return hipErrorInvalidValue;
   switch (hidden) {
-    case 64: return edge_h<2>(mode, a, grid, stream);
-    case 128: return edge_h<4>(mode, a, grid, stream);
+    case 64: return bf16 ? edge_h<2, BF16>(mode, a, grid, stream) : edge_h<2, SPLIT>(mode, a, grid, stream);
+    case 128: return bf16 ? edge_h<4, BF16>(mode, a, grid, stream) : edge_h<4, SPLIT>(mode, a, grid, stream);
   }
   return hipErrorInvalidValue;
 }

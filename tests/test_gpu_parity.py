@@ -39,6 +39,8 @@ def _tiny_random(seed, n, e, loops=False):
 # matrix cores (flags 0), the same regrouping on the fp32 matrix cores
 # (GNN_FP32_MFMA = 4), and the per-edge gather (GNN_LITERAL_GATHER = 2).
 PATHS = [0, 4, 2]
+# bf16 runs the regrouped kernels (flags 0) and the per-edge gather (2).
+BF16_PATHS = [0, 2]
 
 
 @pytest.mark.parametrize("flags", PATHS)
@@ -104,11 +106,12 @@ def test_mid_fp32_full_compare(G, oracle_mod):
                         g.edge_index)
         err = assert_logits_close(got, ref["logits"])
         print(f"mid flags={flags} max scaled logit error {err:.2e}", flush=True)
-    sc = run_model(G, w, G.make_dims(3, c.hidden, c.n_iters, dtype=G.GNN_BF16), g.x,
-                   g.edge_index, logits=False)
-    err = np.abs(sc - ref["scores"])
-    print(f"mid bf16 max score error {err.max():.3e}", flush=True)
-    assert err.max() <= BF16_SCORE_ATOL
+    for flags in BF16_PATHS:
+        sc = run_model(G, w, G.make_dims(3, c.hidden, c.n_iters, dtype=G.GNN_BF16, flags=flags),
+                       g.x, g.edge_index, logits=False)
+        err = np.abs(sc - ref["scores"])
+        print(f"mid bf16 flags={flags} max score error {err.max():.3e}", flush=True)
+        assert err.max() <= BF16_SCORE_ATOL
 
 
 def _golden(name):
@@ -132,30 +135,35 @@ def test_full_fp32_vs_stored_oracle(G, flags):
     np.testing.assert_allclose(sc[ids], gold["scores"], rtol=0, atol=2e-5)
 
 
-def test_full_bf16_scores_vs_stored_oracle(G):
+@pytest.mark.parametrize("flags", BF16_PATHS)
+def test_full_bf16_scores_vs_stored_oracle(G, flags):
     gold = _golden("full")
     c = I.CONFIGS["full_bf16"]
     g = I.make_graph(c)
     assert g.digest() == gold["graph_digest"] and c.weight_seed == gold["weight_seed"]
     w = I.make_weights(3, c.hidden, 1, c.weight_seed)
     ids = np.array(gold["edge_ids"])
-    sc = run_model(G, w, G.make_dims(3, c.hidden, c.n_iters, dtype=G.GNN_BF16), g.x,
-                   g.edge_index, logits=False)
+    sc = run_model(G, w, G.make_dims(3, c.hidden, c.n_iters, dtype=G.GNN_BF16, flags=flags),
+                   g.x, g.edge_index, logits=False)
     err = np.abs(sc[ids] - np.array(gold["scores"]))
-    print(f"full bf16 max score error {err.max():.3e} p99 {np.percentile(err, 99):.3e}",
-          flush=True)
+    print(f"full bf16 flags={flags} max score error {err.max():.3e} "
+          f"p99 {np.percentile(err, 99):.3e}", flush=True)
     assert err.max() <= BF16_SCORE_ATOL
 
 
-@pytest.mark.parametrize("noise", [0.0, 0.3])
-def test_tiny_bf16_scores(G, oracle_mod, noise):
+@pytest.mark.parametrize("flags", BF16_PATHS)
+@pytest.mark.parametrize("H,T,S,noise", [(64, 2, 1, 0.0), (64, 2, 1, 0.3), (128, 3, 1, 0.3),
+                                         (64, 3, 3, 0.3), (128, 0, 1, 0.3)])
+def test_tiny_bf16_scores(G, oracle_mod, H, T, S, noise, flags):
     c = I.CONFIGS["tiny"]
     g = I.make_graph(c)
-    w = I.make_weights(3, c.hidden, 1, c.weight_seed, affine_noise=noise)
-    ref = oracle_mod.forward(w, g.x, g.edge_index, c.hidden, c.n_iters)
-    sc = run_model(G, w, G.make_dims(3, c.hidden, c.n_iters, dtype=G.GNN_BF16), g.x,
+    w = I.make_weights(3, H, S, c.weight_seed, affine_noise=noise)
+    ref = oracle_mod.forward(w, g.x, g.edge_index, H, T, S)
+    sc = run_model(G, w, G.make_dims(3, H, T, S, dtype=G.GNN_BF16, flags=flags), g.x,
                    g.edge_index, logits=False)
-    assert np.abs(sc - ref["scores"]).max() <= BF16_SCORE_ATOL
+    err = np.abs(sc - ref["scores"]).max()
+    print(f"tiny bf16 H={H} T={T} S={S} flags={flags} max score error {err:.3e}", flush=True)
+    assert err <= BF16_SCORE_ATOL
 
 
 @pytest.mark.parametrize("dtype", [0, 1])
