@@ -58,10 +58,10 @@ def edge_update_flops(E, H, factored):
 
 
 def edge_update_bytes(N, E, H, s=4):
-    """Algorithmic HBM bytes of one regrouped edge-update launch: e read and
-    written (s bytes per element), both indices per edge, and every node's
-    projection row [W_s h; W_d h] (2H fp32) read once."""
-    return E * (2 * H * s + 8) + N * 2 * H * 4
+    """Algorithmic HBM bytes of one regrouped edge-update launch, gathered
+    rows counted per edge: e read and written (s bytes per element), the
+    P[src][0:H] and P[dst][H:2H] half-rows (fp32) and both indices."""
+    return E * (2 * H * s + 2 * H * 4 + 8)
 
 
 def node_update_bytes(N, H, s=4):
