@@ -72,14 +72,12 @@ def node_update_bytes(N, H, s=4):
 
 def split_mfma_flops(N, E, H, bf16=False):
     """Matrix-core work the regrouped kernels execute per launch (each
-    partial product counted).  fp32 split: the edge update runs 3 fp16
-    products per fp32 product over W_e e and W2; the node update 6 bf16
-    products over layer 1 (3H -> H) and 3 fp16 products over layer 2 and the
-    2H x H projection.  bf16 model: 2 products (hi/lo weights) throughout."""
-    if bf16:
-        return {"edge_update": 2 * 2.0 * E * 2 * H * H, "node_update": 2 * 2.0 * N * 6 * H * H}
-    return {"edge_update": 3 * 2.0 * E * 2 * H * H,
-            "node_update": 6 * 2.0 * N * 3 * H * H + 3 * 2.0 * N * 3 * H * H}
+    partial product counted).  fp32 split: 3 fp16 products per fp32 product
+    (W_e e and W2 in the edge update; layer 1 (3H -> H), layer 2 and the
+    2H x H projection in the node update).  bf16 model: 2 products (hi/lo
+    weights) throughout."""
+    k = 2 if bf16 else 3
+    return {"edge_update": k * 2.0 * E * 2 * H * H, "node_update": k * 2.0 * N * 6 * H * H}
 
 
 def aggregate_bytes(N, E, H, act_bytes):
@@ -251,12 +249,12 @@ def main():
         nu_mfma = mf["node_update"] / (nu_ms / 1000.0) / 1e12
         roof_node = {"kernel": ("node_split<4,false,1,bf16> (hi/lo bf16 weights streamed "
                                 "through LDS)") if bf16 else
-                               ("node_split<4,false,1> (layer 1 bf16x3, layer 2 and the "
-                                "next projection f16x2; weights streamed through LDS)"),
+                               ("node_split<4,false,1> (f16x2 products, per-node row scale in "
+                                "layer 1; weights streamed through LDS)"),
                      "bound": "hbm", "achieved": round(nu_gbs, 1), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(nu_gbs / PEAK_HBM_GBS, 4),
                      "bytes_per_launch": nb, "avg_launch_ms": round(nu_ms, 4),
-                     "mfma": {"dtype": "bf16" if bf16 else "bf16/fp16",
+                     "mfma": {"dtype": "bf16" if bf16 else "fp16",
                               "executed_tflop_per_launch": mf["node_update"] / 1e12,
                               "achieved": round(nu_mfma, 1), "peak": PEAK_TFLOPS["fp16"],
                               "unit": "TFLOP/s", "frac": round(nu_mfma / PEAK_TFLOPS["fp16"], 4)}}
@@ -286,8 +284,7 @@ def main():
         "config": {"workload": f"{cfg.name}: {N}-hit / {E}-edge layered event, H={H}, T={T}, "
                                f"{cfg.dtype}", "n_nodes": N, "n_edges": E, "hidden": H,
                    "n_iters": T, "parallelism": "single GPU",
-                   "products": {"split": "fp32 operands split into fp16 pairs (bf16 triples "
-                                         "for the node MLP's first layer) on the fp16/bf16 "
+                   "products": {"split": "fp32 operands split into fp16 pairs on the fp16 "
                                          "matrix cores, fp32 accumulation",
                                 "fp32_mfma": "fp32 matrix cores",
                                 "literal": "per-edge first layer",

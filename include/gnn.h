@@ -63,14 +63,14 @@ extern "C" {
                                    default multiplies fp32 operands split into
                                    fp16 pairs (x = x1 + x2, per-operand error
                                    <= 2^-22 |x|; weights pre-scaled by a power
-                                   of two) on the fp16 matrix cores, and the node
-                                   MLP's first layer, whose input holds the
-                                   unbounded aggregates, with operands split
-                                   exactly into bf16 triples; fp32 accumulation
-                                   throughout.  The default needs every
-                                   LayerNorm output bound max|gamma| sqrt(H-1) +
-                                   max|beta| <= 2^15 (fp16 range); weights that
-                                   break it select this path by themselves. */
+                                   of two; each node's aggregate row scaled by
+                                   a power of two when its degree would leave
+                                   the fp16 range) on the fp16 matrix cores,
+                                   with fp32 accumulation throughout.  The
+                                   default needs every LayerNorm output bound
+                                   max|gamma| sqrt(H-1) + max|beta| <= 2^15;
+                                   weights that break it select this path by
+                                   themselves. */
 
 typedef struct gnn_dims {
   uint32_t struct_size;     /* = sizeof(gnn_dims) (ABI versioning)              */

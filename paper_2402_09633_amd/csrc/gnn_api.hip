@@ -209,28 +209,6 @@ std::vector<uint16_t> rec_bf16x2(const BlobLayer &L, int c0, int K, bool from_ac
   return out;
 }
 
-// bf16x3 records of W[:, 0:K] with B from HBM: W = w1 + w2 + w3 exactly.
-std::vector<uint16_t> rec_bf16x3(const BlobLayer &L, int K) {
-  const int MB = L.fout / 32, G = K / 16;
-  std::vector<uint16_t> out((size_t)G * MB * 3 * 64 * 8);
-  for (int g = 0; g < G; ++g)
-    for (int mb = 0; mb < MB; ++mb)
-      for (int lane = 0; lane < 64; ++lane)
-        for (int j = 0; j < 8; ++j) {
-          const int k = 16 * g + 8 * (lane / 32) + j;
-          const float wv = L.W[(size_t)(mb * 32 + lane % 32) * L.fin + k];
-          const uint16_t p1 = f32_to_bf16(wv);
-          const float r = wv - bf16_to_f32(p1);
-          const uint16_t p2 = f32_to_bf16(r);
-          const uint16_t p3 = f32_to_bf16(r - bf16_to_f32(p2));
-          const size_t o = ((((size_t)g * MB + mb) * 3) * 64 + lane) * 8 + j;
-          out[o] = p1;
-          out[o + 64 * 8] = p2;
-          out[o + 2 * 64 * 8] = p3;
-        }
-  return out;
-}
-
 // Builds one host staging image of all device weights, section by section,
 // each 256-byte aligned; device pointers are fixed up after the upload.
 struct Staging {
@@ -255,7 +233,7 @@ struct MlpOff {
 
 // Extra weights of the regrouped first layers: W_e column blocks (H x H) and
 // the node-kernel streams with the stacked projections [W_s; W_d].  In the
-// split path every matrix is in f16x2 / bf16x3 records and the edge kernels
+// split path every matrix is in 16-bit records and the edge kernels
 // read W2 from records too; in the fp32 path they are fp32 MFMA fragments.
 struct FactDev {
   bool split = false;  // split.hip kernels (fp32 split products, or the bf16 model)
@@ -272,7 +250,8 @@ struct FactDev {
   const void *w2_ee = nullptr;
   std::vector<const void *> w2_em;
   float s1_ee = 1.f, s2_ee = 1.f, s1_cls = 1.f, s2_ne = 1.f;
-  std::vector<float> s1_em, s2_em, s2_nm;
+  std::vector<float> s1_em, s2_em, s1_nm, s2_nm;
+  float row_bound = 0.f;  // bound of any h or e entry (LayerNorm/ReLU outputs)
   int grid_enc = 0, grid_upd = 0, grid_cls = 0, grid_node = 0;  // persistent grids
 };
 
@@ -655,7 +634,13 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       nu.mlp = hd->node_mlp[k];
       nu.wstream = (const float *)fd.upd_stream[t];
       nu.nchunks = fd.upd_chunks;
-      nu.s2 = fd.split ? fd.s2_nm[k] : 1.f;
+      if (fd.split) {
+        nu.s1 = fd.s1_nm[k];
+        nu.s2 = fd.s2_nm[k];
+        nu.rp_in = w.rp_in;
+        nu.rp_out = w.rp_out;
+        nu.row_bound = fd.row_bound;
+      }
       nu.nproj = 1;
       nu.h_out = (float *)w.h;  // in place: a wave reads its rows before writing them
       nu.p_out[0] = w.pb;
@@ -916,6 +901,7 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
         for (const BlobLayer *L : {&e0s[s], &e1s[s], &n0s[s], &n1s[s]})
           bound = fmax(bound, ln_out_bound(*L));
       split = !(d.flags & GNN_FP32_MFMA) && bound <= 32768.0;
+      fdh.row_bound = (float)bound;
     }
     if (factored && bf16) {
       // The bf16 model on the same kernels: hi/lo bf16 records, no scales.
@@ -929,6 +915,7 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
       for (int s = 0; s < S; ++s) {
         fdh.s1_em.push_back(1.f);
         fdh.s2_em.push_back(1.f);
+        fdh.s1_nm.push_back(1.f);
         fdh.s2_nm.push_back(1.f);
         o_we_em[s] = add16(rec_bf16x2(e0s[s], 2 * H, H, false));
         o_w2_em[s] = add16(rec_bf16x2(e1s[s], 0, H, true));
@@ -964,6 +951,7 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
       for (int s = 0; s < S; ++s) {
         fdh.s1_em.push_back(pow2_scale(e0s[s]));
         fdh.s2_em.push_back(pow2_scale(e1s[s]));
+        fdh.s1_nm.push_back(pow2_scale(n0s[s]));
         fdh.s2_nm.push_back(pow2_scale(n1s[s]));
         o_we_em[s] = add16(rec_f16x2(e0s[s], 2 * H, H, fdh.s1_em[s], false));
         o_w2_em[s] = add16(rec_f16x2(e1s[s], 0, H, fdh.s2_em[s], true));
@@ -989,7 +977,7 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
       o_enc_stream = add16(es);
       for (int t = 0; t < T; ++t) {
         const int k = S == 1 ? 0 : t;
-        std::vector<uint16_t> us = rec_bf16x3(n0s[k], 3 * H);
+        std::vector<uint16_t> us = rec_f16x2(n0s[k], 0, 3 * H, fdh.s1_nm[k], false);
         cat(us, rec_f16x2(n1s[k], 0, H, fdh.s2_nm[k], true));
         proj(us, next_edge_l1(t));
         o_upd_stream[t] = add16(us);

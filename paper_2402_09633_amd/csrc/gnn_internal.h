@@ -66,7 +66,12 @@ struct NodeArgs {
   float *h_out = nullptr;                     // [n_rows][H] or nullptr
   float *p_out[2] = {nullptr, nullptr};       // [n_rows][2H]
   float eps = 1e-5f;
-  float s2 = 1.f;  // split kernels: power-of-two scale of the layer-2 weights
+  // split kernels: power-of-two scales of the layer-1 (update) and layer-2
+  // weights; the CSR row pointers and the bound of an h or message row
+  // entry, which give each node's aggregate bound (update only)
+  float s1 = 1.f, s2 = 1.f;
+  const int32_t *rp_in = nullptr, *rp_out = nullptr;
+  float row_bound = 0.f;
 };
 
 enum class EdgeMode : int { Enc = 0, Upd = 1, Cls = 2 };

@@ -18,11 +18,11 @@
 //          max_f |gamma_f| sqrt(H-1) + |beta_f|; the handle checks that bound
 //          against the fp16 range when it is created.  The edge kernels keep
 //          both of their H x H matrices in LDS in this form (2 x 64 KB).
-//  bf16x3  x = x1 + x2 + x3 exactly (bf16 has the fp32 exponent range), and
-//          the six partial products w_i x_j with i + j <= 4 are kept; the
-//          dropped ones are below 2^-25 |W||x|.  Used for the node MLP's first
-//          layer, whose input includes the aggregates (sums over up to a
-//          node's whole degree, not bounded by any LayerNorm).
+//          The node MLP's first layer also takes the aggregates, sums over a
+//          node's whole degree: there each node's input row is first
+//          multiplied by a power of two (1 unless the degree times the
+//          message bound leaves the fp16 range) and its product column
+//          divided by it again.
 //
 // The same kernels serve the bf16 model (PREC = BF16): h, e and the
 // aggregates are stored in bf16 and fed to the bf16 matrix cores as they are,
@@ -55,25 +55,6 @@ __device__ __forceinline__ f8 cat8(const f4 &a, const f4 &b) {
 __device__ __forceinline__ void split2(const f8 &x, h8 &x1, h8 &x2) {
   x1 = __builtin_convertvector(x, h8);
   x2 = __builtin_convertvector(x - __builtin_convertvector(x1, f8), h8);
-}
-
-// bf16 -> fp32 by placing the 16 bits on top (exact).
-__device__ __forceinline__ f8 widen_bf16(const bf8 &a) {
-  const u4 u = __builtin_bit_cast(u4, a);
-  f8 r;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    r[2 * i] = __builtin_bit_cast(float, u[i] << 16);
-    r[2 * i + 1] = __builtin_bit_cast(float, u[i] & 0xffff0000u);
-  }
-  return r;
-}
-
-__device__ __forceinline__ void split3(const f8 &x, bf8 &x1, bf8 &x2, bf8 &x3) {
-  x1 = __builtin_convertvector(x, bf8);
-  const f8 r1 = x - widen_bf16(x1);
-  x2 = __builtin_convertvector(r1, bf8);
-  x3 = __builtin_convertvector(r1 - widen_bf16(x2), bf8);
 }
 
 __device__ __forceinline__ f16v mma_h(const h8 &a, const h8 &b, const f16v &c) {
@@ -110,35 +91,6 @@ __device__ __forceinline__ void step_h(f16v (&acc)[MB], const h8 *rec, const f8 
   h8 x1, x2;
   split2(x, x1, x2);
   step_h<MB>(acc, rec, x1, x2);
-}
-
-// acc[mb] += (w1 + w2 + w3) (x1 + x2 + x3) over one k-step, six products,
-// two output blocks at a time (their weights, 24 registers, are the only
-// ones live).
-template <int MB>
-__device__ __forceinline__ void step_b(f16v (&acc)[MB], const bf8 *rec, const f8 &x) {
-  bf8 x1, x2, x3;
-  split3(x, x1, x2, x3);
-#pragma unroll
-  for (int m0 = 0; m0 < MB; m0 += 2) {
-    bf8 w[3][2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int p = 0; p < 3; ++p) w[p][i] = rec[(3 * (m0 + i) + p) * 64];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) acc[m0 + i] = mma_b(w[0][i], x1, acc[m0 + i]);
-#pragma unroll
-    for (int i = 0; i < 2; ++i) acc[m0 + i] = mma_b(w[1][i], x1, acc[m0 + i]);
-#pragma unroll
-    for (int i = 0; i < 2; ++i) acc[m0 + i] = mma_b(w[0][i], x2, acc[m0 + i]);
-#pragma unroll
-    for (int i = 0; i < 2; ++i) acc[m0 + i] = mma_b(w[2][i], x1, acc[m0 + i]);
-#pragma unroll
-    for (int i = 0; i < 2; ++i) acc[m0 + i] = mma_b(w[1][i], x2, acc[m0 + i]);
-#pragma unroll
-    for (int i = 0; i < 2; ++i) acc[m0 + i] = mma_b(w[0][i], x3, acc[m0 + i]);
-  }
 }
 
 // acc[mb] += (w_hi + w_lo) x over one k-step, x exact in bf16.
@@ -237,14 +189,12 @@ struct Stream {
   }
 };
 
-// Records per chunk.  Split: bf16x3 records (3 parts) in the first layer of
-// the node update, f16x2 records (2 parts) after it; bf16: hi/lo records (2
-// parts) throughout.  A chunk is 48 KB (MB = 4) in the update and 32 KB in
-// the encoder.
+// Records per chunk: every record has 2 parts (f16x2, or bf16 hi/lo).  A
+// chunk is 48 KB (MB = 4) in the update and 32 KB in the encoder.
 template <int PREC>
-constexpr int rpc_l1() { return PREC == SPLIT ? 4 : 6; }
+constexpr int rpc_l1() { return 6; }
 template <int PREC>
-constexpr int parts_l1() { return PREC == SPLIT ? 3 : 2; }
+constexpr int parts_l1() { return 2; }
 template <bool ENC>
 constexpr int rpc_h() { return ENC ? 4 : 6; }
 template <int MB, bool ENC>
@@ -308,18 +258,41 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
       xrec_t xr[LA + 1];
 #pragma unroll
       for (int i = 0; i < LA; ++i) xr[i] = load_rec(i);
-      const bf8 *w = nullptr;
+      // Split: the node's whole input row is multiplied by a power of two
+      // sv <= 1 that keeps it inside the fp16 range of the split parts: the
+      // aggregates are bounded by max(deg_in, deg_out) times the bound of a
+      // message row.  Column n of the product is then sv times the node's,
+      // and is divided by sv again after the last record (exact).
+      float sv = 1.f, inv_sv = 1.f;
+      if constexpr (PREC == SPLIT) {
+        const int32_t din = a.rp_in[r + 1] - a.rp_in[r];
+        const int32_t dout = a.rp_out[r + 1] - a.rp_out[r];
+        const float m = (float)(din > dout ? (din > 1 ? din : 1) : (dout > 1 ? dout : 1)) *
+                        a.row_bound;
+        if (m > 32768.f) {
+          int e = 0;
+          (void)frexpf(m * (1.f / 32768.f), &e);  // m / 2^15 <= 2^e
+          sv = ldexpf(1.f, -e);
+          inv_sv = ldexpf(1.f, e);
+        }
+      }
+      const f4 *w = nullptr;
 #pragma unroll
       for (int i = 0; i < NREC; ++i) {
         if (i + LA < NREC) xr[(i + LA) % (LA + 1)] = load_rec(i + LA);
-        if (i % RPC_1 == 0) w = (const bf8 *)ws.begin(tid) + lane;
+        if (i % RPC_1 == 0) w = ws.begin(tid) + lane;
         if constexpr (PREC == SPLIT)
-          step_b<MB>(acc, w + (i % RPC_1) * REC_1, xr[i % (LA + 1)]);
+          step_h<MB>(acc, (const h8 *)(w + (i % RPC_1) * REC_1), xr[i % (LA + 1)] * sv);
         else
-          step_hl<MB>(acc, w + (i % RPC_1) * REC_1, xr[i % (LA + 1)]);
+          step_hl<MB>(acc, (const bf8 *)(w + (i % RPC_1) * REC_1), xr[i % (LA + 1)]);
         if (i % RPC_1 == RPC_1 - 1) ws.end(tid);
       }
-      bias_ln_relu<MB>(acc, a.mlp.l0.b, a.mlp.l0.g, a.mlp.l0.beta, a.eps, hh, true);
+      if constexpr (PREC == SPLIT) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) acc[mb] *= inv_sv;
+      }
+      bias_ln_relu<MB>(acc, a.mlp.l0.b, a.mlp.l0.g, a.mlp.l0.beta, a.eps * a.s1 * a.s1, hh, true,
+                       a.s1);
     }
 
     // The 2-part records: layer 2, then the projection halves.  Record i of
@@ -571,8 +544,9 @@ const void *edge_fn(EdgeMode mode, int hidden) {
 // in bf16) and three H x H matrices.
 int node_split_chunks(bool enc, int hidden, int nproj, bool bf16) {
   const int G = hidden / 16;
+  (void)bf16;
   if (enc) return (G * (1 + 2 * nproj)) / 4;
-  return (3 * G) / (bf16 ? rpc_l1<BF16>() : rpc_l1<SPLIT>()) + (3 * G) / 6;
+  return (3 * G) / rpc_l1<SPLIT>() + (3 * G) / 6;
 }
 
 hipError_t launch_node_split(bool enc, int hidden, const NodeArgs &a, int grid, bool bf16,

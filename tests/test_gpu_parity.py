@@ -377,3 +377,24 @@ def test_split_products_error_matches_fp32_mfma(G, oracle_mod, H):
     e_split, e_f32 = err(0), err(G.GNN_FP32_MFMA)
     print(f"H={H} split {e_split:.2e} fp32 mfma {e_f32:.2e}", flush=True)
     assert e_split <= 2 * e_f32 + 1e-6
+
+
+def test_split_products_hub_rows_match_fp32_mfma(G, oracle_mod):
+    # A node with ~60k incoming messages: its aggregate (up to ~60k times the
+    # message bound) is far outside the fp16 range, so the node MLP's first
+    # layer scales that node's input row by a power of two before splitting
+    # it.  The result must stay as accurate as the fp32 matrix-core path.
+    rng = np.random.default_rng(61)
+    n, e = 4000, 120_000
+    x = rng.normal(size=(n, 3)).astype(np.float32)
+    ei = rng.integers(0, n, size=(2, e)).astype(np.int32)
+    ei[1, rng.random(e) < 0.5] = 123
+    w = I.make_weights(3, 64, 1, 61, affine_noise=0.2)
+    ref = oracle_mod.forward(w, x, ei, 64, 2)["logits"]
+    scale = np.maximum(1.0, np.abs(ref))
+    errs = {}
+    for flags in (0, G.GNN_FP32_MFMA):
+        z = run_model(G, w, G.make_dims(3, 64, 2, flags=flags), x, ei)
+        errs[flags] = float(np.max(np.abs(z - ref) / scale))
+    print(f"hub rows: split {errs[0]:.2e} fp32 mfma {errs[G.GNN_FP32_MFMA]:.2e}", flush=True)
+    assert errs[0] <= 2 * errs[G.GNN_FP32_MFMA] + 1e-6
