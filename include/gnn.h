@@ -178,6 +178,39 @@ void gnn_destroy(gnn_handle *h);
 /* Message of the last failed call on this thread ("" if none). */
 const char *gnn_last_error(void);
 
+/* ---- serving: a request queue in front of several model instances --------
+ * Paper sections 2.3 and 3.2: the GNN runs as a service, one GPU holding
+ * several instances of the model (Fig. 4b) behind a queue of requests from
+ * many clients.  A gnn_server runs n_instances worker threads, each with its
+ * own HIP stream (default priority), that take requests from one FIFO queue
+ * and run each as gnn_infer on the shared handle, then synchronise their
+ * stream.  The handle must outlive the server and may not be destroyed while
+ * requests are pending. */
+typedef struct gnn_server gnn_server;
+
+/* n_instances in 1..64; binds to the current HIP device.  NULL on error
+ * (gnn_last_error): GNN_E_INVALID_ARG, GNN_E_NO_DEVICE. */
+gnn_server *gnn_server_create(gnn_handle *h, int n_instances);
+
+/* Queue one event, with the arguments and device-pointer layouts of
+ * gnn_infer.  The buffers must stay valid and the outputs untouched until
+ * the request is waited for.  Returns the request id (>= 0), or a negative
+ * status: GNN_E_INVALID_ARG for NULL pointers, counts outside
+ * 0..INT32_MAX or a server that is shutting down. */
+int64_t gnn_server_submit(gnn_server *s, const float *node_feat, const int32_t *edge_index,
+                          int64_t n_nodes, int64_t n_edges, float *edge_scores);
+
+/* Block until request `id` has completed and release it; returns the status
+ * of its gnn_infer (its message becomes this thread's gnn_last_error).  With
+ * latency_ms non-NULL, stores the time from submission to completion
+ * (queueing included) in milliseconds.  An id that is unknown or already
+ * waited for gives GNN_E_INVALID_ARG. */
+int gnn_server_wait(gnn_server *s, int64_t id, double *latency_ms);
+
+/* Finish every queued request, stop the workers, free the server.  Results
+ * of requests not waited for are discarded.  NULL-safe. */
+void gnn_server_destroy(gnn_server *s);
+
 /* ---- profiling -----------------------------------------------------------
  * While profiling is enabled on a handle, every call brackets each stage's
  * kernel launches with HIP events on the call's stream (a few microseconds

@@ -35,6 +35,12 @@ int fail(int code, const char *fmt, ...) {
   return code;
 }
 
+}  // namespace
+
+int gnn::set_error(int code, const char *msg) { return fail(code, "%s", msg ? msg : ""); }
+
+namespace {
+
 // ---------------------------------------------------------------- dims ---
 
 int check_dims(const gnn_dims *d) {

@@ -170,4 +170,7 @@ hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t stream)
 // bf16 rows -> fp32 rows (debug export).
 hipError_t launch_bf16_to_f32(const void *in, float *out, int64_t n, hipStream_t stream);
 
+// Sets the calling thread's gnn_last_error() text; returns code (host).
+int set_error(int code, const char *msg);
+
 }  // namespace gnn

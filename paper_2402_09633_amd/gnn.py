@@ -33,7 +33,8 @@ GNN_FP32_MFMA = 4
 EXPORTS = ("gnn_weight_count", "gnn_create", "gnn_infer", "gnn_infer_logits",
            "gnn_filter_weight_count", "gnn_filter_create", "gnn_filter_apply",
            "gnn_filter_destroy", "gnn_wcc", "gnn_infer_labels", "gnn_destroy", "gnn_last_error",
-           "gnn_profile_enable", "gnn_profile_read", "gnn_debug_csr", "gnn_debug_stages")
+           "gnn_profile_enable", "gnn_profile_read", "gnn_debug_csr", "gnn_debug_stages",
+           "gnn_server_create", "gnn_server_submit", "gnn_server_wait", "gnn_server_destroy")
 STAGES = ("csr", "node_enc", "edge_enc", "edge_update", "aggregate", "node_update",
           "classifier", "total")
 
@@ -111,6 +112,14 @@ def _load():
     L.gnn_debug_csr.argtypes = [vp, vp, i64, i64, vp, vp, vp, vp, vp]
     L.gnn_debug_stages.restype = ctypes.c_int
     L.gnn_debug_stages.argtypes = [vp, vp, vp, i64, i64, i32, vp, vp, vp, vp, vp]
+    L.gnn_server_create.restype = vp
+    L.gnn_server_create.argtypes = [vp, ctypes.c_int]
+    L.gnn_server_submit.restype = i64
+    L.gnn_server_submit.argtypes = [vp, vp, vp, i64, i64, vp]
+    L.gnn_server_wait.restype = ctypes.c_int
+    L.gnn_server_wait.argtypes = [vp, i64, ctypes.POINTER(ctypes.c_double)]
+    L.gnn_server_destroy.restype = None
+    L.gnn_server_destroy.argtypes = [vp]
     return L
 
 
@@ -270,6 +279,60 @@ def gnn_debug_stages(handle, node_feat, edge_index, n_nodes: int, n_edges: int, 
     return _check(lib.gnn_debug_stages(handle, _addr(node_feat), _addr(edge_index), n_nodes,
                                        n_edges, stop_iter, _addr(h_out), _addr(e_out),
                                        _addr(agg_in_out), _addr(agg_out_out), _stream(stream)))
+
+
+def gnn_server_create(handle, n_instances: int):
+    s = lib.gnn_server_create(handle, int(n_instances))
+    if not s:
+        raise GnnError(GNN_E_INVALID_ARG, gnn_last_error())
+    return s
+
+
+def gnn_server_submit(server, node_feat, edge_index, n_nodes: int, n_edges: int,
+                      edge_scores) -> int:
+    """Queue one event; returns the request id."""
+    _check_io(node_feat, edge_index, edge_scores)
+    rid = lib.gnn_server_submit(server, _addr(node_feat), _addr(edge_index), n_nodes, n_edges,
+                                _addr(edge_scores))
+    if rid < 0:
+        raise GnnError(int(rid), gnn_last_error())
+    return int(rid)
+
+
+def gnn_server_wait(server, request_id: int) -> float:
+    """Wait for one request; returns its latency (ms, queueing included)."""
+    lat = ctypes.c_double(0.0)
+    _check(lib.gnn_server_wait(server, int(request_id), ctypes.byref(lat)))
+    return lat.value
+
+
+def gnn_server_destroy(server) -> None:
+    lib.gnn_server_destroy(server)
+
+
+class Server:
+    """A request queue served by ``n_instances`` streams of one model."""
+
+    def __init__(self, model: "Model", n_instances: int):
+        self.model = model
+        self.server = gnn_server_create(model.handle, n_instances)
+
+    def submit(self, x: torch.Tensor, edge_index: torch.Tensor, out: torch.Tensor) -> int:
+        return gnn_server_submit(self.server, x, edge_index, x.shape[0], edge_index.shape[1], out)
+
+    def wait(self, request_id: int) -> float:
+        return gnn_server_wait(self.server, request_id)
+
+    def close(self):
+        if self.server:
+            gnn_server_destroy(self.server)
+            self.server = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 class Model:

@@ -1,0 +1,98 @@
+"""The request queue in front of several model instances (gnn_server_*),
+called through the C ABI: every request must give exactly what a direct
+gnn_infer call gives (the kernels are deterministic), whatever the number of
+instances and the order in which the workers take the requests."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2402_09633_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def G():
+    from paper_2402_09633_amd import gnn
+    return gnn
+
+
+def _events(k):
+    evs = []
+    for i in range(k):
+        rng = np.random.default_rng(700 + i)
+        n = int(rng.integers(50, 3000))
+        e = int(rng.integers(1, 9000))
+        x = rng.normal(size=(n, 3)).astype(np.float32)
+        ei = rng.integers(0, n, size=(2, e)).astype(np.int32)
+        evs.append((torch.as_tensor(x).cuda(), torch.as_tensor(ei).cuda()))
+    return evs
+
+
+@pytest.mark.parametrize("n_inst", [1, 3, 8])
+def test_server_results_equal_direct_calls(G, n_inst):
+    w = I.make_weights(3, 64, 1, 71, affine_noise=0.2)
+    m = G.Model(w, G.make_dims(3, 64, 2))
+    evs = _events(12)
+    ref = [m(x, ei).cpu().numpy() for x, ei in evs]
+    torch.cuda.synchronize()
+    srv = G.Server(m, n_inst)
+    try:
+        outs = [torch.full((ei.shape[1],), -1.0, device="cuda") for _, ei in evs]
+        torch.cuda.synchronize()  # the workers' streams do not wait for torch's
+        ids = [srv.submit(x, ei, o) for (x, ei), o in zip(evs, outs)]
+        lats = [srv.wait(i) for i in reversed(ids)]
+        assert all(l > 0 for l in lats)
+        for o, r in zip(outs, ref):
+            assert np.array_equal(o.cpu().numpy(), r)
+    finally:
+        srv.close()
+        m.close()
+
+
+def test_server_errors_and_empty_requests(G):
+    w = I.make_weights(3, 64, 1, 72)
+    m = G.Model(w, G.make_dims(3, 64, 2))
+    srv = G.Server(m, 2)
+    try:
+        with pytest.raises(G.GnnError) as e:
+            srv.wait(12345)
+        assert e.value.code == G.GNN_E_INVALID_ARG
+        x = torch.zeros(4, 3, device="cuda")
+        ei = torch.zeros(2, 5, dtype=torch.int32, device="cuda")
+        out = torch.full((5,), 7.0, device="cuda")
+        torch.cuda.synchronize()
+        with pytest.raises(G.GnnError):
+            G.gnn_server_submit(srv.server, x, ei, -1, 5, out)
+        # n_nodes == 0 < n_edges is caught by the inference call itself and
+        # reported by wait
+        rid = G.gnn_server_submit(srv.server, x, ei, 0, 5, out)
+        with pytest.raises(G.GnnError) as e:
+            srv.wait(rid)
+        assert e.value.code == G.GNN_E_INVALID_ARG
+        # no edges: success, nothing written
+        rid = G.gnn_server_submit(srv.server, x, ei, 4, 0, out)
+        srv.wait(rid)
+        assert torch.all(out == 7.0)
+        with pytest.raises(G.GnnError):
+            srv.wait(rid)  # already released
+    finally:
+        srv.close()
+        m.close()
+
+
+def test_server_destroy_finishes_queued_requests(G):
+    w = I.make_weights(3, 64, 1, 73, affine_noise=0.2)
+    m = G.Model(w, G.make_dims(3, 64, 2))
+    evs = _events(6)
+    ref = [m(x, ei).cpu().numpy() for x, ei in evs]
+    srv = G.Server(m, 2)
+    outs = [torch.zeros(ei.shape[1], device="cuda") for _, ei in evs]
+    torch.cuda.synchronize()
+    for (x, ei), o in zip(evs, outs):
+        srv.submit(x, ei, o)
+    srv.close()  # drains the queue without waiting for any request
+    torch.cuda.synchronize()
+    for o, r in zip(outs, ref):
+        assert np.array_equal(o.cpu().numpy(), r)
+    m.close()
