@@ -34,7 +34,7 @@ TRAFFIC_SOURCES = {
     "fp32_mfma": ["paper_2402_09633_amd/csrc/factored.hip",
                   "paper_2402_09633_amd/csrc/device_common.h"],
 }
-MEASURED_TRAFFIC = {"1e41d2d9601c09d1": {"edge_update_bytes": 1.666e9},   # edge_split<4,1>
+MEASURED_TRAFFIC = {"b0131a8d543c8b86": {"edge_update_bytes": 1.941e9},   # edge_split<4,1>
                     "01db9dfa269e4bf7": {"edge_update_bytes": 1.652e9}}   # edge_f32<4,1>
 
 
