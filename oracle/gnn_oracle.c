@@ -48,6 +48,17 @@
  * + b2) + c) per candidate edge and keeps, in input order, the edges with
  * s_j > threshold.
  *
+ * Graph construction (paper section 2.1: an embedding network maps every
+ * space point into a latent space and a fixed-radius nearest-neighbour
+ * search there builds the candidate edges): oracle_embed evaluates
+ * z_v = W3 phi(W2 phi(W1 x_v + b1) + b2) + b3 (F -> H -> H -> D; the output
+ * layer has no LayerNorm or activation), and oracle_frnn lists every pair
+ * i < j of rows of a given fp32 matrix z with d2(i, j) < r2, where d2 is the
+ * squared Euclidean distance evaluated in fp32 as d = 0; d = fmaf(t, t, d)
+ * with t = z_i[k] - z_j[k] for k = 0 .. D-1 (one rounding per step, the
+ * same decision a GPU makes with the same operations), by brute force over
+ * all pairs, in ascending (i, j) order.
+ *
  * Every function here is pinned by the CPU tests against something other
  * than itself: a torch-CPU library evaluation of one hidden layer, an
  * incidence-matrix brute force on tiny graphs, closed forms (all-zero
@@ -504,5 +515,94 @@ int oracle_filter(const float *weights, int F, int H, double eps, const float *x
   if (n_kept) *n_kept = cnt;
   free(sc);
   free(store);
+  return 0;
+}
+
+/* ---- graph construction ---------------------------------------------- */
+
+long oracle_embed_weight_count(int F, int H, int D) {
+  return layer_floats(F, H, 1) + layer_floats(H, H, 1) + layer_floats(H, D, 0);
+}
+
+/* z[n_nodes][D] = embedding of every row of x[n_nodes][F].  Returns 0, or -1
+ * for bad arguments. */
+int oracle_embed(const float *weights, int F, int H, int D, double eps, const float *x,
+                 long n_nodes, double *z) {
+  if (F <= 0 || H <= 0 || D <= 0 || n_nodes < 0) return -1;
+  double *store = (double *)malloc(sizeof(double) * (size_t)oracle_embed_weight_count(F, H, D));
+  double *d = store;
+  const float *p = weights;
+  omlp m;
+  olayer out;
+  p = take_layer(&m.l0, p, F, H, 1, &d);
+  p = take_layer(&m.l1, p, H, H, 1, &d);
+  p = take_layer(&out, p, H, D, 0, &d);
+#pragma omp parallel
+  {
+    double *a = (double *)malloc(sizeof(double) * (size_t)F);
+    double *tmp = (double *)malloc(sizeof(double) * (size_t)H);
+    double *hid = (double *)malloc(sizeof(double) * (size_t)H);
+#pragma omp for schedule(static)
+    for (long v = 0; v < n_nodes; ++v) {
+      for (int k = 0; k < F; ++k) a[k] = x[v * F + k];
+      mlp_hidden(&m, eps, a, tmp, hid);
+      linear(&out, hid, z + v * D);
+    }
+    free(a);
+    free(tmp);
+    free(hid);
+  }
+  free(store);
+  return 0;
+}
+
+/* fp32 squared distance of rows i and j of z[.][D], one fused multiply-add
+ * per coordinate in ascending order. */
+static float frnn_d2(const float *zi, const float *zj, int D) {
+  float acc = 0.0f;
+  for (int k = 0; k < D; ++k) {
+    const float t = zi[k] - zj[k];
+    acc = fmaf(t, t, acc);
+  }
+  return acc;
+}
+
+/* Every pair i < j with d2 < r2, in ascending (i, j) order.  With pairs
+ * non-NULL, writes up to max_pairs of them as (i, j) at pairs[2k],
+ * pairs[2k+1]; the total count is returned through *n_pairs either way.
+ * Returns 0, or -1 for bad arguments. */
+int oracle_frnn(const float *z, long n_nodes, int D, float r2, int64_t *pairs, long max_pairs,
+                int64_t *n_pairs) {
+  if (n_nodes < 0 || D <= 0) return -1;
+  long *cnt = (long *)calloc((size_t)(n_nodes > 0 ? n_nodes : 1), sizeof(long));
+#pragma omp parallel for schedule(dynamic, 64)
+  for (long i = 0; i < n_nodes; ++i) {
+    long c = 0;
+    for (long j = i + 1; j < n_nodes; ++j)
+      if (frnn_d2(z + i * D, z + j * D, D) < r2) ++c;
+    cnt[i] = c;
+  }
+  long total = 0;
+  for (long i = 0; i < n_nodes; ++i) {
+    const long c = cnt[i];
+    cnt[i] = total;
+    total += c;
+  }
+  if (pairs) {
+#pragma omp parallel for schedule(dynamic, 64)
+    for (long i = 0; i < n_nodes; ++i) {
+      long o = cnt[i];
+      for (long j = i + 1; j < n_nodes; ++j)
+        if (frnn_d2(z + i * D, z + j * D, D) < r2) {
+          if (o < max_pairs) {
+            pairs[2 * o] = i;
+            pairs[2 * o + 1] = j;
+          }
+          ++o;
+        }
+    }
+  }
+  if (n_pairs) *n_pairs = total;
+  free(cnt);
   return 0;
 }

@@ -62,6 +62,15 @@ def lib():
         L.oracle_filter.argtypes = [_fp, ctypes.c_int, ctypes.c_int, ctypes.c_double, _fp, _ip,
                                     ctypes.c_long, ctypes.c_long, ctypes.c_double, _dp,
                                     ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64)]
+        L.oracle_embed_weight_count.restype = ctypes.c_long
+        L.oracle_embed_weight_count.argtypes = [ctypes.c_int] * 3
+        L.oracle_embed.restype = ctypes.c_int
+        L.oracle_embed.argtypes = [_fp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_double,
+                                   _fp, ctypes.c_long, _dp]
+        L.oracle_frnn.restype = ctypes.c_int
+        L.oracle_frnn.argtypes = [_fp, ctypes.c_long, ctypes.c_int, ctypes.c_float,
+                                  ctypes.POINTER(ctypes.c_int64), ctypes.c_long,
+                                  ctypes.POINTER(ctypes.c_int64)]
         L.oracle_max_threads.restype = ctypes.c_int
         L.oracle_set_threads.argtypes = [ctypes.c_int]
         _lib = L
@@ -175,3 +184,40 @@ def filter_edges(weights, x, edge_index, hidden, threshold=0.5, eps=1e-5):
     if rc:
         raise ValueError(f"oracle_filter failed ({rc})")
     return sc[:E], kept[:nk.value]
+
+
+def embed_weight_count(F: int, H: int, D: int) -> int:
+    return int(lib().oracle_embed_weight_count(F, H, D))
+
+
+def embed(weights, x, hidden, out_dim, eps=1e-5):
+    """Embedding z [N][D] (fp64) of every row of x."""
+    x = np.ascontiguousarray(x, np.float32)
+    n, F = x.shape
+    w = np.ascontiguousarray(weights, np.float32)
+    if w.size != embed_weight_count(F, hidden, out_dim):
+        raise ValueError("embedding weight blob has the wrong size")
+    z = np.zeros((max(n, 1), out_dim))
+    rc = lib().oracle_embed(_ptr(w, _fp), F, hidden, out_dim, float(eps), _ptr(x, _fp), n,
+                            _ptr(z, _dp))
+    if rc:
+        raise ValueError(f"oracle_embed failed ({rc})")
+    return z[:n]
+
+
+def frnn(z, r2):
+    """All pairs i < j of rows of the fp32 matrix z with fp32 squared
+    distance < r2, as an int64 [n_pairs][2] array in ascending (i, j) order."""
+    z = np.ascontiguousarray(z, np.float32)
+    n, D = z.shape
+    cnt = ctypes.c_int64(0)
+    P = ctypes.POINTER(ctypes.c_int64)
+    rc = lib().oracle_frnn(_ptr(z, _fp), n, D, float(np.float32(r2)), None, 0, ctypes.byref(cnt))
+    if rc:
+        raise ValueError(f"oracle_frnn failed ({rc})")
+    pairs = np.zeros((max(cnt.value, 1), 2), np.int64)
+    rc = lib().oracle_frnn(_ptr(z, _fp), n, D, float(np.float32(r2)), pairs.ctypes.data_as(P),
+                           cnt.value, ctypes.byref(cnt))
+    if rc:
+        raise ValueError(f"oracle_frnn failed ({rc})")
+    return pairs[:cnt.value]

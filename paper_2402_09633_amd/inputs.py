@@ -360,3 +360,66 @@ def filter_blob_views(blob: np.ndarray, in_features: int, hidden: int) -> dict:
             views[name + ".beta"] = blob[off:off + fout]; off += fout
     assert off == blob.size
     return views
+
+
+# ------------------------------------------------- graph construction ---
+
+def embed_layer_shapes(in_features: int, hidden: int, out_dim: int):
+    """(name, fan_in, fan_out, hidden_layer) of the embedding MLP, in blob
+    order: x (F) -> H -> H -> D; the output layer has no LayerNorm."""
+    return [("embed.0", in_features, hidden, True), ("embed.1", hidden, hidden, True),
+            ("embed.2", hidden, out_dim, False)]
+
+
+def embed_weight_count(in_features: int, hidden: int, out_dim: int) -> int:
+    return sum(fin * fout + fout + (2 * fout if hid else 0)
+               for _, fin, fout, hid in embed_layer_shapes(in_features, hidden, out_dim))
+
+
+def make_embed_weights(in_features: int, hidden: int, out_dim: int, seed: int,
+                       affine_noise: float = 0.0) -> np.ndarray:
+    """Packed fp32 embedding blob, drawn like make_weights (Xavier W, zero b,
+    gamma 1, beta 0; perturbed b/gamma/beta with affine_noise > 0)."""
+    rng = np.random.default_rng(seed)
+    parts = []
+    for _, fin, fout, hid in embed_layer_shapes(in_features, hidden, out_dim):
+        a = math.sqrt(6.0 / (fin + fout))
+        parts.append(rng.uniform(-a, a, fin * fout))
+        parts.append(rng.uniform(-affine_noise, affine_noise, fout) if affine_noise > 0
+                     else np.zeros(fout))
+        if hid:
+            if affine_noise > 0:
+                parts.append(rng.uniform(1 - affine_noise, 1 + affine_noise, fout))
+                parts.append(rng.uniform(-affine_noise, affine_noise, fout))
+            else:
+                parts.append(np.ones(fout))
+                parts.append(np.zeros(fout))
+    return np.concatenate(parts).astype(np.float32)
+
+
+def embed_blob_views(blob: np.ndarray, in_features: int, hidden: int, out_dim: int) -> dict:
+    views, off = {}, 0
+    for name, fin, fout, hid in embed_layer_shapes(in_features, hidden, out_dim):
+        views[name + ".W"] = blob[off:off + fin * fout].reshape(fout, fin); off += fin * fout
+        views[name + ".b"] = blob[off:off + fout]; off += fout
+        if hid:
+            views[name + ".g"] = blob[off:off + fout]; off += fout
+            views[name + ".beta"] = blob[off:off + fout]; off += fout
+    assert off == blob.size
+    return views
+
+
+def clustered_points(n: int, dim: int, seed: int, n_clusters: int = 0, sigma: float = 0.02,
+                     background: float = 0.2) -> np.ndarray:
+    """Synthetic embedded space points (fp32 [n][dim]): a fraction
+    `background` uniform in [0, 1]^dim, the rest in isotropic Gaussian
+    clusters of width sigma around uniform centres (track-like groups in an
+    embedding space).  n_clusters = 0 picks n / 10."""
+    rng = np.random.default_rng(seed)
+    k = n_clusters if n_clusters > 0 else max(1, n // 10)
+    centres = rng.uniform(0.0, 1.0, (k, dim))
+    nb = int(round(background * n))
+    which = rng.integers(0, k, n - nb)
+    pts = np.concatenate([rng.uniform(0.0, 1.0, (nb, dim)),
+                          centres[which] + rng.normal(0.0, sigma, (n - nb, dim))])
+    return pts[rng.permutation(n)].astype(np.float32)

@@ -279,3 +279,74 @@ def test_filter_closed_forms(oracle_mod):
     sc, kept = oracle_mod.filter_edges(w, x, ei, 8, 0.9)  # sigmoid(1.5) = 0.818 < 0.9
     assert kept.size == 0
     assert oracle_mod.filter_edges(w, x, np.zeros((2, 0), np.int32), 8)[1].size == 0
+
+
+# ---- graph construction: embedding MLP and fixed-radius neighbours ----
+
+def _embed_torch(w, x, F, H, D, eps=1e-5):
+    V = {k: torch.as_tensor(np.array(v, np.float64))
+         for k, v in I.embed_blob_views(w, F, H, D).items()}
+    a = torch.as_tensor(x.astype(np.float64))
+    for name in ("embed.0", "embed.1"):
+        y = Fn.linear(a, V[name + ".W"], V[name + ".b"])
+        a = torch.relu(Fn.layer_norm(y, (H,), V[name + ".g"], V[name + ".beta"], eps))
+    return Fn.linear(a, V["embed.2.W"], V["embed.2.b"]).numpy()
+
+
+@pytest.mark.parametrize("H,D,seed", [(8, 4, 0), (16, 8, 1), (32, 3, 2)])
+def test_embed_matches_torch(oracle_mod, H, D, seed):
+    x = np.random.default_rng(seed).normal(size=(50, 3)).astype(np.float32)
+    w = I.make_embed_weights(3, H, D, seed, affine_noise=0.3)
+    np.testing.assert_allclose(oracle_mod.embed(w, x, H, D), _embed_torch(w, x, 3, H, D),
+                               rtol=0, atol=1e-13)
+
+
+def test_embed_closed_form(oracle_mod):
+    # zero weights except the output bias: every point maps to that bias
+    w = np.zeros(I.embed_weight_count(3, 8, 5), np.float32)
+    v = I.embed_blob_views(w, 3, 8, 5)
+    v["embed.2.b"][:] = np.arange(5, dtype=np.float32) - 1.5
+    z = oracle_mod.embed(w, np.random.default_rng(0).normal(size=(7, 3)).astype(np.float32), 8, 5)
+    assert (z == np.arange(5) - 1.5).all()
+
+
+def _pair_set(p):
+    return set(map(tuple, np.asarray(p).reshape(-1, 2).tolist()))
+
+
+@pytest.mark.parametrize("seed,n,D,r", [(0, 300, 8, 0.05), (1, 800, 3, 0.03), (2, 500, 5, 0.1)])
+def test_frnn_matches_kdtree(oracle_mod, seed, n, D, r):
+    # scipy's k-d tree in float64 brackets the fp32 decision: every pair
+    # closer than r(1 - 1e-5) must be found, none farther than r(1 + 1e-5)
+    from scipy.spatial import cKDTree
+    z = I.clustered_points(n, D, seed)
+    got = _pair_set(oracle_mod.frnn(z, np.float32(r * r)))
+    t = cKDTree(z.astype(np.float64))
+    inner = t.query_pairs(r * (1 - 1e-5))
+    outer = t.query_pairs(r * (1 + 1e-5))
+    assert inner <= got <= outer
+    assert len(got) > 0
+
+
+def test_frnn_exact_on_integer_lattice(oracle_mod):
+    # integer coordinates: every fp32 squared distance is exact, so the pairs
+    # are exactly those a float64 k-d tree finds for r2 = 2.5 (distances^2 of
+    # 1 and 2 pass, 3 fails)
+    from scipy.spatial import cKDTree
+    g = np.stack(np.meshgrid(np.arange(6), np.arange(5), np.arange(4), indexing="ij"), -1)
+    z = g.reshape(-1, 3).astype(np.float32)
+    got = oracle_mod.frnn(z, 2.5)
+    assert _pair_set(got) == cKDTree(z.astype(np.float64)).query_pairs(np.sqrt(2.5))
+    assert (np.diff(got[:, 0]) >= 0).all() and (got[:, 0] < got[:, 1]).all()
+
+
+def test_frnn_permutation_and_edge_cases(oracle_mod):
+    z = I.clustered_points(400, 6, 9)
+    p = np.random.default_rng(3).permutation(400)
+    a = _pair_set(oracle_mod.frnn(z, 0.003))
+    # row k of z[p] is row p[k] of z
+    b = {tuple(sorted((int(p[i]), int(p[j])))) for i, j in _pair_set(oracle_mod.frnn(z[p], 0.003))}
+    assert a == b and len(a) > 0
+    assert oracle_mod.frnn(z, 0.0).shape == (0, 2)
+    assert oracle_mod.frnn(z[:1], 1e9).shape == (0, 2)
+    assert len(oracle_mod.frnn(z[:20], 1e9)) == 20 * 19 // 2
