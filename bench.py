@@ -208,6 +208,7 @@ def main():
                 "note": "same event with GNN_FP32_MFMA (products on the fp32 matrix cores), "
                         "5 events after the timed region; not part of value"}
     filt = bench_filter(G, I, cfg) if cfg.name == "full" else None
+    gc = bench_graph_construction(G, I, g) if cfg.name == "full" else None
 
     ms_per_step = (t1 - t0) * 1000.0 / args.steps
     value = E / (ms_per_step / 1000.0)
@@ -317,6 +318,8 @@ def main():
         rec["fp32_mfma_path"] = side
     if filt:
         rec["filter"] = filt
+    if gc:
+        rec["graph_construction"] = gc
 
     if not args.no_cpu_baseline:
         from oracle import oracle as O
@@ -354,6 +357,40 @@ def bench_filter(G, I, cfg):
             "note": "filter MLP (2F->64->64->1) + stable compaction at 0.5 on the same hits "
                     "with the wide windows (wall time incl. the count read-back); not part "
                     "of value"}
+
+
+def bench_graph_construction(G, I, g):
+    """Embedding MLP (F -> 128 -> 128 -> 8) on the event's hits and the
+    fixed-radius pair search on 300k clustered points in 8 dimensions (a
+    stand-in for a trained embedding space: 80% of the points in tight
+    groups)."""
+    import torch
+    w = I.make_embed_weights(3, 128, 8, 3000)
+    m = G.Embedder(w, G.make_embed_dims(3, 128, 8))
+    x = torch.as_tensor(g.x).cuda()
+    z = m(x)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    for _ in range(10):
+        m(x, z)
+    torch.cuda.synchronize()
+    embed_ms = (time.perf_counter() - t) * 100.0
+    m.close()
+    pts = torch.as_tensor(I.clustered_points(300_000, 8, 977, sigma=0.005)).cuda()
+    r2 = 0.02 ** 2
+    ei = G.radius_graph(pts, r2)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    for _ in range(5):
+        ei = G.radius_graph(pts, r2)
+    torch.cuda.synchronize()
+    frnn_ms = (time.perf_counter() - t) * 200.0
+    return {"embed_ms": round(embed_ms, 4), "embed_points": int(g.n_nodes),
+            "frnn_ms": round(frnn_ms, 4), "frnn_points": 300_000, "frnn_dim": 8,
+            "frnn_pairs": int(ei.shape[1]),
+            "note": "embedding MLP 3->128->128->8 on the event's hits; fixed-radius pairs "
+                    "(r = 0.02) on 300k clustered 8-d points, count + fill passes with the "
+                    "count read-back (wall time); not part of value"}
 
 
 def bench_batch(args, cfg):

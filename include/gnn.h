@@ -178,6 +178,49 @@ void gnn_destroy(gnn_handle *h);
 /* Message of the last failed call on this thread ("" if none). */
 const char *gnn_last_error(void);
 
+/* ---- graph construction ---------------------------------------------------
+ * Paper section 2.1: an embedding network maps every space point into a
+ * latent space, and a fixed-radius nearest-neighbour search there proposes
+ * the candidate edges.  The paper gives no architecture; the embedding here
+ * is z = W3 phi(W2 phi(W1 x + b1) + b2) + b3 (F -> H -> H -> D, phi =
+ * LayerNorm then ReLU as in the GNN's MLPs, no activation on the output). */
+typedef struct gnn_embed_dims {
+  uint32_t struct_size; /* = sizeof(gnn_embed_dims)                        */
+  int32_t in_features;  /* F, 1..16                                         */
+  int32_t hidden;       /* H, 64 or 128                                     */
+  int32_t out_dim;      /* D, 1..16                                         */
+  float ln_eps;         /* LayerNorm epsilon                                */
+} gnn_embed_dims;
+typedef struct gnn_embedder gnn_embedder;
+
+/* Floats in the embedding blob: W1 [H][F], b1, gamma1, beta1, W2 [H][H], b2,
+ * gamma2, beta2, W3 [D][H], b3 (host fp32, [out][in] row-major); 0 if dims
+ * are invalid. */
+size_t gnn_embed_weight_count(const gnn_embed_dims *dims);
+/* Copies and uploads the HOST blob; NULL on error (gnn_last_error). */
+gnn_embedder *gnn_embed_create(const float *weights, const gnn_embed_dims *dims);
+/* z [n_nodes][D] fp32 (device) from node_feat [n_nodes][F] (device),
+ * asynchronous on `stream`; fp32 throughout (fp32 matrix cores). */
+int gnn_embed_apply(gnn_embedder *m, const float *node_feat, int64_t n_nodes, float *z,
+                    hipStream_t stream);
+void gnn_embed_destroy(gnn_embedder *m);
+
+/* Every pair i < j of rows of z [n_nodes][dim] (device fp32, dim 1..16)
+ * whose squared distance, evaluated in fp32 as d = 0, d = fmaf(t, t, d) with
+ * t = z[i][k] - z[j][k] for k = 0 .. dim-1, is below r2.  The count goes to
+ * *n_pairs (host).  With edge_index non-NULL and room for max_pairs pairs,
+ * the pairs are written as a contiguous [2][n_pairs] int32 edge list (row 0
+ * = i, row 1 = j), grouped by ascending i, deterministic order within one i;
+ * that write is asynchronous on `stream`, the count is not (the call waits
+ * for it).  Returns GNN_OK; GNN_E_INVALID_ARG for bad arguments or when
+ * more than max_pairs pairs exist (nothing written, *n_pairs holds the
+ * count); GNN_E_UNSUPPORTED above INT32_MAX pairs.  r2 <= 0 or fewer than
+ * two rows give no pairs.  The search bins the rows on a grid over their
+ * first min(3, dim) coordinates with cells as wide as the radius: its cost
+ * grows with the number of rows per cell. */
+int gnn_frnn(const float *z, int64_t n_nodes, int32_t dim, float r2, int32_t *edge_index,
+             int64_t max_pairs, int64_t *n_pairs, hipStream_t stream);
+
 /* ---- serving: a request queue in front of several model instances --------
  * Paper sections 2.3 and 3.2: the GNN runs as a service, one GPU holding
  * several instances of the model (Fig. 4b) behind a queue of requests from

@@ -606,3 +606,17 @@ int oracle_frnn(const float *z, long n_nodes, int D, float r2, int64_t *pairs, l
   free(cnt);
   return 0;
 }
+
+/* The partners j > i of one row i, ascending (the pairs of oracle_frnn
+ * whose first element is i); returns their count, writing at most max_out
+ * of them to out. */
+long oracle_frnn_row(const float *z, long n_nodes, int D, float r2, long i, int64_t *out,
+                     long max_out) {
+  long c = 0;
+  for (long j = i + 1; j < n_nodes; ++j)
+    if (frnn_d2(z + i * D, z + j * D, D) < r2) {
+      if (out && c < max_out) out[c] = j;
+      ++c;
+    }
+  return c;
+}

@@ -71,6 +71,9 @@ def lib():
         L.oracle_frnn.argtypes = [_fp, ctypes.c_long, ctypes.c_int, ctypes.c_float,
                                   ctypes.POINTER(ctypes.c_int64), ctypes.c_long,
                                   ctypes.POINTER(ctypes.c_int64)]
+        L.oracle_frnn_row.restype = ctypes.c_long
+        L.oracle_frnn_row.argtypes = [_fp, ctypes.c_long, ctypes.c_int, ctypes.c_float,
+                                      ctypes.c_long, ctypes.POINTER(ctypes.c_int64), ctypes.c_long]
         L.oracle_max_threads.restype = ctypes.c_int
         L.oracle_set_threads.argtypes = [ctypes.c_int]
         _lib = L
@@ -221,3 +224,15 @@ def frnn(z, r2):
     if rc:
         raise ValueError(f"oracle_frnn failed ({rc})")
     return pairs[:cnt.value]
+
+
+def frnn_row(z, r2, i):
+    """The partners j > i of row i (ascending) under the same test as frnn."""
+    z = np.ascontiguousarray(z, np.float32)
+    n, D = z.shape
+    P = ctypes.POINTER(ctypes.c_int64)
+    c = lib().oracle_frnn_row(_ptr(z, _fp), n, D, float(np.float32(r2)), int(i), None, 0)
+    out = np.zeros(max(c, 1), np.int64)
+    lib().oracle_frnn_row(_ptr(z, _fp), n, D, float(np.float32(r2)), int(i),
+                          out.ctypes.data_as(P), c)
+    return out[:c]

@@ -1254,6 +1254,127 @@ void gnn_filter_destroy(gnn_filter *f) {
   delete f;
 }
 
+// ------------------------------------------------------ embedding MLP ---
+
+struct gnn_embedder {
+  gnn_embed_dims dims;
+  int device = 0;
+  void *dev = nullptr;
+  EmbedArgs tmpl;  // weight pointers
+};
+
+namespace {
+int check_embed_dims(const gnn_embed_dims *d) {
+  if (!d) return fail(GNN_E_INVALID_ARG, "dims is NULL");
+  if (d->struct_size != sizeof(gnn_embed_dims))
+    return fail(GNN_E_INVALID_ARG, "gnn_embed_dims.struct_size mismatch");
+  if (d->in_features < 1 || d->in_features > 16)
+    return fail(GNN_E_INVALID_ARG, "in_features %d outside 1..16", d->in_features);
+  if (d->hidden != 64 && d->hidden != 128)
+    return fail(d->hidden > 0 && d->hidden % 32 == 0 ? GNN_E_UNSUPPORTED : GNN_E_INVALID_ARG,
+                "hidden %d not supported (64 or 128)", d->hidden);
+  if (d->out_dim < 1 || d->out_dim > 16)
+    return fail(GNN_E_INVALID_ARG, "out_dim %d outside 1..16", d->out_dim);
+  if (!(d->ln_eps > 0.f) || !(d->ln_eps < 1.f))
+    return fail(GNN_E_INVALID_ARG, "ln_eps outside (0, 1)");
+  return GNN_OK;
+}
+}  // namespace
+
+size_t gnn_embed_weight_count(const gnn_embed_dims *d) {
+  if (check_embed_dims(d)) return 0;
+  const size_t F = d->in_features, H = d->hidden, D = d->out_dim;
+  return layer_floats(F, H, true) + layer_floats(H, H, true) + layer_floats(H, D, false);
+}
+
+gnn_embedder *gnn_embed_create(const float *weights, const gnn_embed_dims *dims) {
+  if (check_embed_dims(dims)) return nullptr;
+  if (!weights) {
+    fail(GNN_E_INVALID_ARG, "weights is NULL");
+    return nullptr;
+  }
+  int ndev = 0, dev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0 || hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    fail(GNN_E_NO_DEVICE, "no HIP device visible");
+    return nullptr;
+  }
+  const int F = dims->in_features, H = dims->hidden, D = dims->out_dim;
+  const float *p = weights;
+  auto next = [&](int fin, int fout, bool ln) {
+    BlobLayer L{p, nullptr, nullptr, nullptr, fin, fout};
+    p += (size_t)fin * fout;
+    L.b = p;
+    p += fout;
+    if (ln) {
+      L.g = p;
+      p += fout;
+      L.beta = p;
+      p += fout;
+    }
+    return L;
+  };
+  BlobLayer l0 = next(F, H, true), l1 = next(H, H, true), l2 = next(H, D, false);
+  Staging st;
+  LayerOff o0 = stage_layer(st, l0, WKind::PlainT, false, true);
+  LayerOff o1 = stage_layer(st, l1, WKind::FragAcc, false, true);
+  LayerOff o2 = stage_layer(st, l2, WKind::Plain, false, false);
+  gnn_embedder *m = new gnn_embedder();
+  m->dims = *dims;
+  m->device = dev;
+  if (hipMalloc(&m->dev, st.bytes.size()) != hipSuccess ||
+      hipMemcpy(m->dev, st.bytes.data(), st.bytes.size(), hipMemcpyHostToDevice) != hipSuccess) {
+    (void)hipGetLastError();
+    if (m->dev) (void)hipFree(m->dev);
+    delete m;
+    fail(GNN_E_OOM, "embedding weight upload failed");
+    return nullptr;
+  }
+  const unsigned char *base = (const unsigned char *)m->dev;
+  LayerDev d0 = fix_layer(o0, base), d1 = fix_layer(o1, base), d2 = fix_layer(o2, base);
+  m->tmpl.F = F;
+  m->tmpl.D = D;
+  m->tmpl.eps = dims->ln_eps;
+  m->tmpl.w0t = (const float *)d0.w;
+  m->tmpl.b0 = d0.b;
+  m->tmpl.g0 = d0.g;
+  m->tmpl.beta0 = d0.beta;
+  m->tmpl.w1 = (const float *)d1.w;
+  m->tmpl.b1 = d1.b;
+  m->tmpl.g1 = d1.g;
+  m->tmpl.beta1 = d1.beta;
+  m->tmpl.w2 = (const float *)d2.w;
+  m->tmpl.b2 = d2.b;
+  return m;
+}
+
+int gnn_embed_apply(gnn_embedder *m, const float *node_feat, int64_t n_nodes, float *z,
+                    hipStream_t stream) {
+  if (!m) return fail(GNN_E_INVALID_ARG, "embedder is NULL");
+  if (n_nodes < 0 || n_nodes > INT32_MAX)
+    return fail(GNN_E_INVALID_ARG, "n_nodes outside 0..INT32_MAX");
+  if (n_nodes == 0) return GNN_OK;
+  if (!node_feat || !z) return fail(GNN_E_INVALID_ARG, "NULL input or output pointer");
+  DeviceGuard guard(m->device);
+  EmbedArgs a = m->tmpl;
+  a.n = n_nodes;
+  a.x = node_feat;
+  a.z = z;
+  const hipError_t e = launch_embed(m->dims.hidden, a, stream);
+  if (e != hipSuccess) return fail(GNN_E_HIP, "embedding launch failed: %s", hipGetErrorString(e));
+  return GNN_OK;
+}
+
+void gnn_embed_destroy(gnn_embedder *m) {
+  if (!m) return;
+  {
+    DeviceGuard guard(m->device);
+    (void)hipDeviceSynchronize();
+    (void)hipFree(m->dev);
+  }
+  delete m;
+}
+
 int gnn_filter_apply(gnn_filter *f, const float *node_feat, const int32_t *edge_index,
                      int64_t n_nodes, int64_t n_edges, float threshold, float *edge_scores,
                      int32_t *edge_index_out, int64_t *n_kept, hipStream_t stream) {

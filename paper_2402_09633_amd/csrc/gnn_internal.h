@@ -155,6 +155,38 @@ hipError_t launch_compact(const float *scores, const int32_t *edge_index, int64_
                           float threshold, int32_t *counts, int32_t *total, int32_t *out,
                           hipStream_t stream);
 
+// Graph construction (graph.hip).  Embedding MLP F -> H -> H -> D.
+struct EmbedArgs {
+  int64_t n = 0;
+  const float *x = nullptr;  // [n][F]
+  int32_t F = 0, D = 0;
+  const float *w0t = nullptr, *b0 = nullptr, *g0 = nullptr, *beta0 = nullptr;  // W0 as [F][H]
+  const float *w1 = nullptr, *b1 = nullptr, *g1 = nullptr, *beta1 = nullptr;   // fragments
+  const float *w2 = nullptr, *b2 = nullptr;                                   // [D][H], [D]
+  float *z = nullptr;                                                         // [n][D]
+  float eps = 1e-5f;
+};
+hipError_t launch_embed(int hidden, const EmbedArgs &a, hipStream_t stream);
+
+// Fixed-radius pairs over the rows of z [n][D].
+struct FrnnArgs {
+  const float *z = nullptr;
+  int64_t n = 0;
+  int32_t D = 0, g = 0;       // dimensions, grid dimensions (min(3, D))
+  float r2 = 0.f, inv_cell = 0.f;
+  uint32_t mask = 0;          // bucket table size - 1 (power of two)
+  const int32_t *rp = nullptr, *perm = nullptr;  // buckets: CSR of the points by key
+  int32_t *count = nullptr;   // [n] pairs per point
+  int64_t *offs = nullptr;    // [n] exclusive offsets
+  int64_t *total_dev = nullptr;
+  int64_t total = 0;          // fill pass: number of pairs (row stride of out)
+  int32_t *out = nullptr;     // [2][total]
+};
+hipError_t launch_frnn_keys(const FrnnArgs &a, int32_t *keys, hipStream_t stream);
+// zs: [n][D] scratch for the coordinates in bucket order
+hipError_t launch_frnn_count(const FrnnArgs &a, float *zs, hipStream_t stream);
+hipError_t launch_frnn_fill(const FrnnArgs &a, const float *zs, hipStream_t stream);
+
 // Weakly-connected components (wcc.hip): labels <- identity, then rounds of
 // hooking over the kept edges and pointer jumping; `changed` is set to 1 by
 // a round that joined two trees.

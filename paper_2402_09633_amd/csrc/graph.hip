@@ -1,0 +1,324 @@
+// Graph construction, the first stage of the pipeline (paper section 2.1: an
+// embedding network maps every space point into a latent space, and a
+// fixed-radius nearest-neighbour search there proposes the candidate edges
+// that the filter and the GNN then score).
+//
+// embed_f32   one wave per 32 points: layer 1 (F -> H) on VALU, LayerNorm/
+//             ReLU, layer 2 (H -> H) on the fp32 matrix cores through the
+//             accumulator chain, LayerNorm/ReLU, then the D outputs as VALU
+//             dot products (D <= 16).
+// frnn        every pair i < j with d2(i, j) < r2, where d2 is evaluated in
+//             fp32 as d = fmaf(t, t, d) over the coordinates in ascending
+//             order (t = z_i[k] - z_j[k]).  Points are binned on a grid over
+//             the first min(3, D) coordinates with cells no narrower than the
+//             radius, so a pair within the radius sits in the same or
+//             adjacent cells; cells are hashed into a power-of-two table that
+//             is turned into buckets by the CSR builder (a stable sort of the
+//             points by bucket).  A point scans the 3^g neighbouring cells
+//             and keeps a candidate only if the candidate's own cell is the
+//             one being scanned, so hash collisions never produce a pair
+//             twice.  A count pass, an exclusive scan and a fill pass write
+//             the pairs grouped by i (within one i in cell-scan order), which
+//             is deterministic.
+#include "device_common.h"
+
+namespace gnn {
+namespace {
+
+constexpr int EWAVES = 4;
+constexpr int FTHREADS = 256;
+
+template <int MB>
+__global__ __launch_bounds__(64 * EWAVES) void embed_f32(EmbedArgs a) {
+  constexpr int H = 32 * MB;
+  const int lane = threadIdx.x & 63, hh = lane >> 5, n = lane & 31;
+  const int blk = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t row0 = ((int64_t)blk * EWAVES + (threadIdx.x >> 6)) * 32;
+  if (row0 >= a.n) return;
+  const int64_t row = row0 + n;
+  const bool valid = row < a.n;
+  const int64_t r = valid ? row : a.n - 1;
+
+  f16v acc[MB];
+  small_k_layer<MB>(acc, a.x, a.F, (int)r, a.w0t, a.b0, hh);
+  bias_ln_relu<MB>(acc, nullptr, a.g0, a.beta0, a.eps, hh, false);
+  f16v acc2[MB];
+  gemm_acc_f32<MB, MB>(acc2, acc, (const f4 *)a.w1 + lane, 0);
+  bias_ln_relu<MB>(acc2, a.b1, a.g1, a.beta1, a.eps, hh, true);
+  for (int d = 0; d < a.D; ++d) {
+    const float *wd = a.w2 + (int64_t)d * H + 4 * hh;
+    float part = 0.f;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f4 ww = *(const f4 *)(wd + mb * 32 + 8 * q);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) part += acc2[mb][4 * q + t] * ww[t];
+      }
+    part += __shfl_xor(part, 32);
+    if (valid && hh == 0) a.z[row * a.D + d] = part + a.b2[d];
+  }
+}
+
+// Grid cell of a point along the first g coordinates (coordinates clamped so
+// that the cell index fits comfortably in an int).
+__device__ __forceinline__ void cell_of(const float *zp, int g, float inv_cell, int (&c)[3]) {
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    float v = k < g ? floorf(zp[k] * inv_cell) : 0.f;
+    v = fminf(fmaxf(v, -1.0e9f), 1.0e9f);
+    c[k] = (int)v;
+  }
+}
+
+__device__ __forceinline__ uint32_t cell_hash(const int (&c)[3], uint32_t mask) {
+  return ((uint32_t)c[0] * 73856093u ^ (uint32_t)c[1] * 19349663u ^ (uint32_t)c[2] * 83492791u) &
+         mask;
+}
+
+// Bucket keys, written twice ([2][n]) as the CSR builder's edge list.
+__global__ __launch_bounds__(FTHREADS) void frnn_keys(FrnnArgs a, int32_t *__restrict__ keys) {
+  const int64_t i = (int64_t)blockIdx.x * FTHREADS + threadIdx.x;
+  if (i >= a.n) return;
+  int c[3];
+  cell_of(a.z + i * a.D, a.g, a.inv_cell, c);
+  const int32_t k = (int32_t)cell_hash(c, a.mask);
+  keys[i] = k;
+  keys[a.n + i] = k;
+}
+
+// The points' coordinates in bucket order: zs[p] = z[perm[p]].
+__global__ __launch_bounds__(FTHREADS) void frnn_gather(FrnnArgs a, float *__restrict__ zs) {
+  const int64_t t = (int64_t)blockIdx.x * FTHREADS + threadIdx.x;
+  if (t >= a.n * a.D) return;
+  const int64_t p = t / a.D;
+  zs[t] = a.z[(int64_t)a.perm[p] * a.D + (t - p * a.D)];
+}
+
+// FILL = false: count the pairs of every point; true: write them.  Thread
+// p handles the point at bucket position p (neighbouring threads handle
+// neighbouring points, whose candidates they share in the caches).  The
+// neighbouring cells' buckets are scanned once each (a bucket that two
+// cells share through the hash is skipped the second time), so every other
+// point is tested at most once; a point of a colliding far cell simply fails
+// the distance test.
+template <bool FILL>
+__global__ __launch_bounds__(FTHREADS) void frnn_pairs(FrnnArgs a, const float *__restrict__ zs) {
+  const int64_t p = (int64_t)blockIdx.x * FTHREADS + threadIdx.x;
+  if (p >= a.n) return;
+  const int32_t i = a.perm[p];
+  float zi[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) zi[k] = k < a.D ? zs[p * a.D + k] : 0.f;
+  int ci[3];
+  cell_of(zi, a.g, a.inv_cell, ci);
+  int64_t o = FILL ? a.offs[i] : 0;
+  int32_t cnt = 0;
+  uint32_t seen[27];
+  int ns = 0;
+  const int r2d = a.g > 1 ? 1 : 0, r3d = a.g > 2 ? 1 : 0;
+  for (int dz = -r3d; dz <= r3d; ++dz)
+    for (int dy = -r2d; dy <= r2d; ++dy)
+      for (int dx = -1; dx <= 1; ++dx) {
+        const int nc[3] = {ci[0] + dx, ci[1] + dy, ci[2] + dz};
+        const uint32_t key = cell_hash(nc, a.mask);
+        bool dup = false;
+        for (int u = 0; u < ns; ++u) dup |= seen[u] == key;
+        if (dup) continue;
+        seen[ns++] = key;
+        const int32_t qe = a.rp[key + 1];
+        for (int32_t q = a.rp[key]; q < qe; ++q) {
+          const int32_t j = a.perm[q];
+          if (j <= i) continue;
+          const float *zj = zs + (int64_t)q * a.D;
+          float acc = 0.f;
+          for (int k = 0; k < a.D; ++k) {
+            const float t = zi[k] - zj[k];
+            acc = __builtin_fmaf(t, t, acc);
+          }
+          if (acc < a.r2) {
+            if constexpr (FILL) {
+              a.out[o] = i;
+              a.out[a.total + o] = j;
+              ++o;
+            } else {
+              ++cnt;
+            }
+          }
+        }
+      }
+  if constexpr (!FILL) a.count[i] = cnt;
+}
+
+// Exclusive scan of the per-point counts into offs (int64), total -> *total.
+// One block of 1024 threads, each scanning a contiguous chunk.
+__global__ __launch_bounds__(1024) void frnn_scan(const int32_t *__restrict__ count, int64_t n,
+                                                  int64_t *__restrict__ offs,
+                                                  int64_t *__restrict__ total) {
+  __shared__ int64_t part[1024];
+  const int t = threadIdx.x;
+  const int64_t chunk = (n + 1023) / 1024;
+  const int64_t beg = min((int64_t)t * chunk, n), end = min(beg + chunk, n);
+  int64_t s = 0;
+  for (int64_t i = beg; i < end; ++i) s += count[i];
+  part[t] = s;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int64_t v = t >= off ? part[t - off] : 0;
+    __syncthreads();
+    part[t] += v;
+    __syncthreads();
+  }
+  int64_t run = part[t] - s;
+  for (int64_t i = beg; i < end; ++i) {
+    offs[i] = run;
+    run += count[i];
+  }
+  if (t == 1023) *total = part[1023];
+}
+
+}  // namespace
+
+hipError_t launch_embed(int hidden, const EmbedArgs &a, hipStream_t stream) {
+  if (a.n <= 0) return hipSuccess;
+  if (a.D < 1 || a.D > 16 || a.F < 1 || a.F > MAX_F) return hipErrorInvalidValue;
+  const int64_t waves = (a.n + 31) / 32;
+  const unsigned blocks = (unsigned)((waves + EWAVES - 1) / EWAVES);
+  switch (hidden) {
+    case 64: embed_f32<2><<<blocks, 64 * EWAVES, 0, stream>>>(a); break;
+    case 128: embed_f32<4><<<blocks, 64 * EWAVES, 0, stream>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_frnn_keys(const FrnnArgs &a, int32_t *keys, hipStream_t stream) {
+  if (a.n <= 0) return hipSuccess;
+  frnn_keys<<<(unsigned)((a.n + FTHREADS - 1) / FTHREADS), FTHREADS, 0, stream>>>(a, keys);
+  return hipGetLastError();
+}
+
+hipError_t launch_frnn_count(const FrnnArgs &a, float *zs, hipStream_t stream) {
+  if (a.n <= 0) return hipSuccess;
+  const int64_t nz = a.n * a.D;
+  frnn_gather<<<(unsigned)((nz + FTHREADS - 1) / FTHREADS), FTHREADS, 0, stream>>>(a, zs);
+  const unsigned blocks = (unsigned)((a.n + FTHREADS - 1) / FTHREADS);
+  frnn_pairs<false><<<blocks, FTHREADS, 0, stream>>>(a, zs);
+  frnn_scan<<<1, 1024, 0, stream>>>(a.count, a.n, a.offs, a.total_dev);
+  return hipGetLastError();
+}
+
+hipError_t launch_frnn_fill(const FrnnArgs &a, const float *zs, hipStream_t stream) {
+  if (a.n <= 0) return hipSuccess;
+  frnn_pairs<true><<<(unsigned)((a.n + FTHREADS - 1) / FTHREADS), FTHREADS, 0, stream>>>(a, zs);
+  return hipGetLastError();
+}
+
+}  // namespace gnn
+
+// ---------------------------------------------------------------- host ---
+
+#include <cmath>
+
+#include "../../include/gnn.h"
+
+namespace {
+
+size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+}  // namespace
+
+extern "C" int gnn_frnn(const float *z, int64_t n_nodes, int32_t dim, float r2,
+                        int32_t *edge_index, int64_t max_pairs, int64_t *n_pairs,
+                        hipStream_t stream) {
+  using namespace gnn;
+  if (!n_pairs) return set_error(GNN_E_INVALID_ARG, "n_pairs is NULL");
+  *n_pairs = 0;
+  if (n_nodes < 0 || n_nodes > INT32_MAX)
+    return set_error(GNN_E_INVALID_ARG, "n_nodes outside 0..INT32_MAX");
+  if (dim < 1 || dim > 16) return set_error(GNN_E_INVALID_ARG, "dim outside 1..16");
+  if (max_pairs < 0) return set_error(GNN_E_INVALID_ARG, "max_pairs is negative");
+  if (n_nodes > 0 && !z) return set_error(GNN_E_INVALID_ARG, "z is NULL");
+  if (std::isnan(r2)) return set_error(GNN_E_INVALID_ARG, "r2 is NaN");
+  if (n_nodes < 2 || !(r2 > 0.f)) return GNN_OK;
+
+  FrnnArgs a;
+  a.z = z;
+  a.n = n_nodes;
+  a.D = dim;
+  a.g = dim < 3 ? dim : 3;
+  a.r2 = r2;
+  // Cells a little wider than the radius: a pair that passes the fp32 test
+  // differs by less than that along every coordinate.
+  const double cell = 1.001 * std::sqrt((double)r2);
+  a.inv_cell = std::isfinite(cell) && cell > 0.0 ? (float)(1.0 / cell) : 0.f;
+  uint32_t m = 64;
+  while ((int64_t)m < 2 * n_nodes && m < (1u << 30)) m <<= 1;
+  a.mask = m - 1;
+
+  const int64_t n = n_nodes;
+  size_t off = 0;
+  auto take = [&](size_t b) {
+    const size_t o = off;
+    off += align256(b > 0 ? b : 1);
+    return o;
+  };
+  const size_t o_keys = take((size_t)2 * n * 4);
+  const size_t o_rpi = take(((size_t)m + 1) * 4), o_pi = take((size_t)n * 4);
+  const size_t o_rpo = take(((size_t)m + 1) * 4), o_po = take((size_t)n * 4);
+  const size_t o_ka = take((size_t)2 * n * 4), o_kb = take((size_t)2 * n * 4);
+  const size_t o_va = take((size_t)2 * n * 4), o_vb = take((size_t)2 * n * 4);
+  const size_t o_hist = take(2 * csr_hist_len(n) * 4), o_tot = take(2 * 256 * 4 * 4);
+  const size_t o_cnt = take((size_t)n * 4), o_offs = take((size_t)n * 8), o_total = take(8);
+  const size_t o_zs = take((size_t)n * dim * 4);
+  void *base = nullptr;
+  if (hipMallocAsync(&base, off, stream) != hipSuccess) {
+    (void)hipGetLastError();
+    return set_error(GNN_E_OOM, "frnn workspace allocation failed");
+  }
+  unsigned char *b = (unsigned char *)base;
+  int32_t *keys = (int32_t *)(b + o_keys);
+  CsrScratch cs;
+  cs.keys_a = (uint32_t *)(b + o_ka);
+  cs.keys_b = (uint32_t *)(b + o_kb);
+  cs.vals_a = (uint32_t *)(b + o_va);
+  cs.vals_b = (uint32_t *)(b + o_vb);
+  cs.hist = (uint32_t *)(b + o_hist);
+  cs.totals = (uint32_t *)(b + o_tot);
+  a.rp = (const int32_t *)(b + o_rpi);
+  a.perm = (const int32_t *)(b + o_pi);
+  a.count = (int32_t *)(b + o_cnt);
+  a.offs = (int64_t *)(b + o_offs);
+  a.total_dev = (int64_t *)(b + o_total);
+
+  int rc = GNN_OK;
+  int64_t total = 0;
+  hipError_t e = launch_frnn_keys(a, keys, stream);
+  if (e == hipSuccess)
+    e = build_csr(keys, (int32_t)n, (int32_t)m, (int32_t *)(b + o_rpi), (int32_t *)(b + o_pi),
+                  (int32_t *)(b + o_rpo), (int32_t *)(b + o_po), cs, stream);
+  float *zs = (float *)(b + o_zs);
+  if (e == hipSuccess) e = launch_frnn_count(a, zs, stream);
+  if (e == hipSuccess) e = hipMemcpyAsync(&total, a.total_dev, 8, hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    rc = set_error(GNN_E_HIP, hipGetErrorString(e));
+  } else {
+    *n_pairs = total;
+    if (total > INT32_MAX) {
+      rc = set_error(GNN_E_UNSUPPORTED, "more than INT32_MAX pairs");
+    } else if (edge_index && total > max_pairs) {
+      rc = set_error(GNN_E_INVALID_ARG, "edge_index holds fewer pairs than found (see n_pairs)");
+    } else if (edge_index && total > 0) {
+      a.total = total;
+      a.out = edge_index;
+      e = launch_frnn_fill(a, zs, stream);
+      if (e != hipSuccess) rc = set_error(GNN_E_HIP, hipGetErrorString(e));
+    }
+  }
+  if (hipFreeAsync(base, stream) != hipSuccess && rc == GNN_OK)
+    rc = set_error(GNN_E_HIP, "frnn workspace release failed");
+  return rc;
+}

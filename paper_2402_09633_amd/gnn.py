@@ -34,9 +34,17 @@ EXPORTS = ("gnn_weight_count", "gnn_create", "gnn_infer", "gnn_infer_logits",
            "gnn_filter_weight_count", "gnn_filter_create", "gnn_filter_apply",
            "gnn_filter_destroy", "gnn_wcc", "gnn_infer_labels", "gnn_destroy", "gnn_last_error",
            "gnn_profile_enable", "gnn_profile_read", "gnn_debug_csr", "gnn_debug_stages",
-           "gnn_server_create", "gnn_server_submit", "gnn_server_wait", "gnn_server_destroy")
+           "gnn_server_create", "gnn_server_submit", "gnn_server_wait", "gnn_server_destroy",
+           "gnn_embed_weight_count", "gnn_embed_create", "gnn_embed_apply", "gnn_embed_destroy",
+           "gnn_frnn")
 STAGES = ("csr", "node_enc", "edge_enc", "edge_update", "aggregate", "node_update",
           "classifier", "total")
+
+
+class gnn_embed_dims(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("in_features", ctypes.c_int32),
+                ("hidden", ctypes.c_int32), ("out_dim", ctypes.c_int32),
+                ("ln_eps", ctypes.c_float)]
 
 
 class gnn_dims(ctypes.Structure):
@@ -112,6 +120,18 @@ def _load():
     L.gnn_debug_csr.argtypes = [vp, vp, i64, i64, vp, vp, vp, vp, vp]
     L.gnn_debug_stages.restype = ctypes.c_int
     L.gnn_debug_stages.argtypes = [vp, vp, vp, i64, i64, i32, vp, vp, vp, vp, vp]
+    edp = ctypes.POINTER(gnn_embed_dims)
+    L.gnn_embed_weight_count.restype = ctypes.c_size_t
+    L.gnn_embed_weight_count.argtypes = [edp]
+    L.gnn_embed_create.restype = vp
+    L.gnn_embed_create.argtypes = [vp, edp]
+    L.gnn_embed_apply.restype = ctypes.c_int
+    L.gnn_embed_apply.argtypes = [vp, vp, i64, vp, vp]
+    L.gnn_embed_destroy.restype = None
+    L.gnn_embed_destroy.argtypes = [vp]
+    L.gnn_frnn.restype = ctypes.c_int
+    L.gnn_frnn.argtypes = [vp, i64, i32, ctypes.c_float, vp, i64, ctypes.POINTER(ctypes.c_int64),
+                           vp]
     L.gnn_server_create.restype = vp
     L.gnn_server_create.argtypes = [vp, ctypes.c_int]
     L.gnn_server_submit.restype = i64
@@ -279,6 +299,87 @@ def gnn_debug_stages(handle, node_feat, edge_index, n_nodes: int, n_edges: int, 
     return _check(lib.gnn_debug_stages(handle, _addr(node_feat), _addr(edge_index), n_nodes,
                                        n_edges, stop_iter, _addr(h_out), _addr(e_out),
                                        _addr(agg_in_out), _addr(agg_out_out), _stream(stream)))
+
+
+def make_embed_dims(in_features=3, hidden=64, out_dim=8, ln_eps=1e-5) -> gnn_embed_dims:
+    return gnn_embed_dims(ctypes.sizeof(gnn_embed_dims), in_features, hidden, out_dim, ln_eps)
+
+
+def gnn_embed_weight_count(dims: gnn_embed_dims) -> int:
+    return int(lib.gnn_embed_weight_count(ctypes.byref(dims)))
+
+
+def gnn_embed_create(weights: np.ndarray, dims: gnn_embed_dims):
+    w = np.ascontiguousarray(weights, np.float32)
+    if w.size != gnn_embed_weight_count(dims):
+        raise ValueError("embedding weight blob has the wrong size")
+    m = lib.gnn_embed_create(w.ctypes.data, ctypes.byref(dims))
+    if not m:
+        raise GnnError(GNN_E_INVALID_ARG, gnn_last_error())
+    return m
+
+
+def gnn_embed_apply(embedder, node_feat, n_nodes: int, z, stream=None) -> int:
+    return _check(lib.gnn_embed_apply(embedder, _addr(node_feat), n_nodes, _addr(z),
+                                      _stream(stream)))
+
+
+def gnn_embed_destroy(embedder) -> None:
+    lib.gnn_embed_destroy(embedder)
+
+
+def gnn_frnn(z, n_nodes: int, dim: int, r2: float, edge_index=None, max_pairs: int = 0,
+             stream=None) -> int:
+    """Fixed-radius pairs of the rows of z; returns the pair count (and
+    fills edge_index [2][count] when given and large enough)."""
+    cnt = ctypes.c_int64(0)
+    rc = lib.gnn_frnn(_addr(z), n_nodes, dim, float(r2), _addr(edge_index), int(max_pairs),
+                      ctypes.byref(cnt), _stream(stream))
+    if rc != GNN_OK:
+        raise GnnError(rc, gnn_last_error())
+    return int(cnt.value)
+
+
+class Embedder:
+    """Owns one embedding model: ``Embedder(w, dims)(x) -> z``."""
+
+    def __init__(self, weights: np.ndarray, dims: gnn_embed_dims):
+        self.dims = dims
+        self.handle = gnn_embed_create(weights, dims)
+
+    def __call__(self, x: torch.Tensor, z=None, stream=None) -> torch.Tensor:
+        if z is None:
+            z = torch.empty(x.shape[0], self.dims.out_dim, dtype=torch.float32, device=x.device)
+        gnn_embed_apply(self.handle, x, x.shape[0], z, stream)
+        return z
+
+    def close(self):
+        if self.handle:
+            gnn_embed_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def radius_graph(z: torch.Tensor, r2: float, stream=None) -> torch.Tensor:
+    """[2][n_pairs] int32 edge list of the pairs i < j of rows of z with
+    fp32 squared distance < r2 (count first, then fill)."""
+    n, d = z.shape
+    cap = max(16 * n, 1)  # one call when the pairs fit, a second one otherwise
+    out = torch.empty(2 * cap, dtype=torch.int32, device=z.device)
+    try:
+        cnt = gnn_frnn(z, n, d, r2, out, cap, stream)
+    except GnnError as e:
+        if e.code != GNN_E_INVALID_ARG:
+            raise
+        cnt = gnn_frnn(z, n, d, r2, None, 0, stream)
+        out = torch.empty(2 * max(cnt, 1), dtype=torch.int32, device=z.device)
+        cnt = gnn_frnn(z, n, d, r2, out, cnt, stream)
+    return out[:2 * cnt].view(2, cnt)
 
 
 def gnn_server_create(handle, n_instances: int):

@@ -1,0 +1,129 @@
+"""Graph construction on the GPU (gnn_embed_*, gnn_frnn) against the oracle,
+through the C ABI.
+
+Embedding: fp32 GPU against the fp64 oracle, 1e-4 relative.  Fixed-radius
+pairs: the GPU and the oracle take the same fp32 decision (the same
+subtractions and fused multiply-adds in the same order), so the pair sets
+must be identical, bit for bit, on the same fp32 input points.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2402_09633_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def G():
+    from paper_2402_09633_amd import gnn
+    return gnn
+
+
+def _pairs_np(ei):
+    e = ei.cpu().numpy().astype(np.int64)
+    return e.T  # [n][2]
+
+
+def _check_layout(p):
+    assert (p[:, 0] < p[:, 1]).all()
+    assert (np.diff(p[:, 0]) >= 0).all()  # grouped by ascending i
+
+
+@pytest.mark.parametrize("H,D,seed", [(64, 8, 0), (128, 8, 1), (64, 3, 2), (128, 16, 3),
+                                      (64, 1, 4)])
+def test_embed_matches_oracle(G, oracle_mod, H, D, seed):
+    g = I.make_graph(I.CONFIGS["tiny"])
+    x = np.concatenate([g.x, np.random.default_rng(seed).normal(size=(77, 3)).astype(np.float32)])
+    w = I.make_embed_weights(3, H, D, 50 + seed, affine_noise=0.3)
+    ref = oracle_mod.embed(w, x, H, D)
+    m = G.Embedder(w, G.make_embed_dims(3, H, D))
+    try:
+        z = m(torch.as_tensor(x).cuda()).cpu().numpy()
+    finally:
+        m.close()
+    np.testing.assert_allclose(z, ref, rtol=1e-4, atol=1e-4)
+
+
+@pytest.mark.parametrize("n,D,r,seed", [(2000, 8, 0.05, 0), (3001, 3, 0.02, 1), (500, 1, 0.001, 2),
+                                        (1500, 2, 0.01, 3), (2500, 5, 0.04, 4), (800, 16, 0.15, 5),
+                                        (20000, 8, 0.08, 6), (2, 4, 10.0, 7)])
+def test_frnn_pairs_equal_oracle(G, oracle_mod, n, D, r, seed):
+    z = I.clustered_points(n, D, 900 + seed)
+    r2 = np.float32(r * r)
+    ref = oracle_mod.frnn(z, r2)
+    got = _pairs_np(G.radius_graph(torch.as_tensor(z).cuda(), float(r2)))
+    print(f"frnn n={n} D={D} r={r}: {len(ref)} pairs", flush=True)
+    _check_layout(got)
+    assert len(got) == len(ref)
+    np.testing.assert_array_equal(got[np.lexsort((got[:, 1], got[:, 0]))], ref)
+
+
+def test_frnn_exact_ties_on_lattice(G, oracle_mod):
+    # integer coordinates: squared distances are exact integers; r2 = 2 sits
+    # exactly on the distance of diagonal neighbours (strict test: excluded)
+    g = np.stack(np.meshgrid(np.arange(9), np.arange(7), np.arange(5), indexing="ij"), -1)
+    z = g.reshape(-1, 3).astype(np.float32)
+    for r2 in (1.0, 2.0, 2.5, 3.0):
+        ref = oracle_mod.frnn(z, r2)
+        got = _pairs_np(G.radius_graph(torch.as_tensor(z).cuda(), r2))
+        np.testing.assert_array_equal(got[np.lexsort((got[:, 1], got[:, 0]))], ref)
+
+
+def test_frnn_full_scale_sampled_rows(G, oracle_mod):
+    # 300k points in 8 dimensions: every sampled row's partner list must equal
+    # the oracle's (computed row by row)
+    n, D, r2 = 300_000, 8, np.float32(0.02 ** 2)
+    z = I.clustered_points(n, D, 977, sigma=0.005)  # ~544k pairs
+    zt = torch.as_tensor(z).cuda()
+    ei = G.radius_graph(zt, float(r2))
+    p = _pairs_np(ei)
+    print(f"frnn full: {len(p)} pairs", flush=True)
+    _check_layout(p)
+    assert len(p) > 100_000
+    starts = np.searchsorted(p[:, 0], np.arange(n + 1))
+    for i in np.random.default_rng(5).choice(n, 300, replace=False):
+        mine = np.sort(p[starts[i]:starts[i + 1], 1])
+        np.testing.assert_array_equal(mine, oracle_mod.frnn_row(z, r2, int(i)))
+    # deterministic: a second call gives the same list in the same order
+    assert torch.equal(G.radius_graph(zt, float(r2)), ei)
+
+
+def test_frnn_arguments(G):
+    z = torch.as_tensor(I.clustered_points(1000, 4, 3)).cuda()
+    n = G.gnn_frnn(z, 1000, 4, 0.01)
+    assert n > 0
+    small = torch.empty(2, 1, dtype=torch.int32, device="cuda")
+    with pytest.raises(G.GnnError) as e:
+        G.gnn_frnn(z, 1000, 4, 0.01, small, 1)
+    assert e.value.code == G.GNN_E_INVALID_ARG
+    assert G.gnn_frnn(z, 1000, 4, 0.0) == 0
+    assert G.gnn_frnn(z, 1000, 4, -1.0) == 0
+    assert G.gnn_frnn(z, 1, 4, 1.0) == 0
+    assert G.gnn_frnn(z, 0, 4, 1.0) == 0
+    with pytest.raises(G.GnnError):
+        G.gnn_frnn(z, 1000, 17, 0.01)
+    with pytest.raises(G.GnnError):
+        G.gnn_frnn(z, 1000, 0, 0.01)
+
+
+def test_embed_then_frnn_chain(G, oracle_mod):
+    # GPU embedding -> GPU pairs against the oracle's embedding -> oracle
+    # pairs: the two embeddings differ by fp32 rounding, so the pair sets may
+    # differ only on pairs whose distance is within 1e-3 of the radius
+    g = I.make_graph(I.CONFIGS["tiny"])
+    w = I.make_embed_weights(3, 64, 8, 61)
+    m = G.Embedder(w, G.make_embed_dims(3, 64, 8))
+    try:
+        z = m(torch.as_tensor(g.x).cuda())
+    finally:
+        m.close()
+    zr = oracle_mod.embed(w, g.x, 64, 8)
+    d2 = ((zr[:, None, :] - zr[None, :, :]) ** 2).sum(-1)
+    r2 = float(np.quantile(d2[np.triu_indices(len(zr), 1)], 0.002))
+    got = {tuple(x) for x in _pairs_np(G.radius_graph(z, r2)).tolist()}
+    ref = {tuple(x) for x in oracle_mod.frnn(zr.astype(np.float32), np.float32(r2)).tolist()}
+    diff = got ^ ref
+    assert len(ref) > 1000
+    assert all(abs(d2[i, j] - r2) <= 1e-3 * r2 for i, j in diff), len(diff)

@@ -350,3 +350,10 @@ def test_frnn_permutation_and_edge_cases(oracle_mod):
     assert oracle_mod.frnn(z, 0.0).shape == (0, 2)
     assert oracle_mod.frnn(z[:1], 1e9).shape == (0, 2)
     assert len(oracle_mod.frnn(z[:20], 1e9)) == 20 * 19 // 2
+
+
+def test_frnn_row_agrees_with_frnn(oracle_mod):
+    z = I.clustered_points(600, 8, 11)
+    pairs = oracle_mod.frnn(z, 0.004)
+    for i in (0, 5, 77, 599):
+        np.testing.assert_array_equal(oracle_mod.frnn_row(z, 0.004, i), pairs[pairs[:, 0] == i, 1])
