@@ -155,6 +155,37 @@ __device__ __forceinline__ void store_rows_bf16(__bf16 *__restrict__ o, const f1
     }
 }
 
+// Stores the wave's 32 rows x 32 MB floats (row r at out + r * stride,
+// rows >= nvalid skipped) through a 32 x 32-float LDS staging tile, one
+// 128-byte column block at a time: every store instruction then writes 8
+// full 128-byte lines instead of 32-byte pieces of 32 rows.
+constexpr int SST = 36;  // staging row stride in floats (16-byte aligned rows)
+template <int MB>
+__device__ __forceinline__ void store_block(float *__restrict__ out, int64_t stride, int nvalid,
+                                            const f16v (&acc)[MB], float *stg, int lane) {
+  const int n = lane & 31, hh = lane >> 5;
+  const int rr = lane >> 3, cc = 4 * (lane & 7);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      *(f4 *)(stg + n * SST + 8 * q + 4 * hh) =
+          f4{acc[mb][4 * q], acc[mb][4 * q + 1], acc[mb][4 * q + 2], acc[mb][4 * q + 3]};
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int row = 8 * k + rr;
+      const f4 v = *(const f4 *)(stg + row * SST + cc);
+      if (row < nvalid) *(f4 *)(out + row * stride + mb * 32 + cc) = v;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+}
+
 // Weight stream of the node kernel: all records of one tile, cut into chunks
 // of NF4 float4 per thread (NF4 * 8 KB), double-buffered through LDS.  While
 // the waves multiply out of one buffer, the next chunk is fetched from L2
@@ -213,8 +244,10 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
   static_assert(ENC || RPC_1 * REC_1 == NF4 * 512, "layer-1 chunk size");
   using act_t = typename std::conditional<PREC == SPLIT, float, __bf16>::type;
   __shared__ f4 wbuf[2 * NF4 * 512];
+  __shared__ float stage[SW][32 * SST];
   const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, n = lane & 31;
   const int wave = tid >> 6;
+  float *stg = stage[wave];
   Stream<NF4> ws{(const f4 *)a.wstream, a.nchunks, wbuf};
   ws.fetch(0, tid);
   ws.commit(0, tid);
@@ -316,10 +349,12 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
       rec_done(g);
     }
     bias_ln_relu<MB>(hv, a.mlp.l1.b, a.mlp.l1.g, a.mlp.l1.beta, eps2, hh, true, a.s2);
-    if (valid && a.h_out) {
+    const int64_t wrow0 = tile * 32 * SW + wave * 32;
+    const int nvalid = (int)(a.n_rows - wrow0 < 32 ? a.n_rows - wrow0 : 32);
+    if (a.h_out) {
       if constexpr (PREC == SPLIT)
-        store_rows<MB>(a.h_out + row * H + 4 * hh, hv);
-      else
+        store_block<MB>(a.h_out + wrow0 * H, H, nvalid, hv, stg, lane);
+      else if (valid)
         store_rows_bf16<MB>((__bf16 *)a.h_out + row * H + 4 * hh, hv);
     }
     // the projections read h as it is stored
@@ -347,7 +382,7 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
             step_hl<MB>(pv, (const bf8 *)rec_h(i), x1[g]);
           rec_done(i);
         }
-        if (valid) store_rows<MB>(a.p_out[p] + row * 2 * H + half * H + 4 * hh, pv);
+        store_block<MB>(a.p_out[p] + wrow0 * 2 * H + half * H, 2 * H, nvalid, pv, stg, lane);
       }
   }
 }
