@@ -245,12 +245,30 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
   using act_t = typename std::conditional<PREC == SPLIT, float, __bf16>::type;
   __shared__ f4 wbuf[2 * NF4 * 512];
   __shared__ float stage[SW][32 * SST];
+  // LayerNorm parameters of both layers, [b1 g1 beta1 b2 g2 beta2] with
+  // each bias multiplied by its accumulator scale; the encoder adds its
+  // first-layer bias and W^T ([F][H]).  Read from LDS, they stay off the
+  // vector-memory counter that the row loads and stores wait on.
+  constexpr int NPRM = 6 * H + (ENC ? H + MAX_F * H : 0);
+  __shared__ float prm[NPRM];
   const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, n = lane & 31;
   const int wave = tid >> 6;
   float *stg = stage[wave];
+  for (int i = tid; i < H; i += 64 * SW) {
+    prm[i] = ENC ? 0.f : a.mlp.l0.b[i] * a.s1;
+    prm[H + i] = a.mlp.l0.g[i];
+    prm[2 * H + i] = a.mlp.l0.beta[i];
+    prm[3 * H + i] = a.mlp.l1.b[i] * a.s2;
+    prm[4 * H + i] = a.mlp.l1.g[i];
+    prm[5 * H + i] = a.mlp.l1.beta[i];
+    if constexpr (ENC) prm[6 * H + i] = a.mlp.l0.b[i];
+  }
+  if constexpr (ENC)
+    for (int i = tid; i < a.F * H; i += 64 * SW) prm[7 * H + i] = ((const float *)a.mlp.l0.w)[i];
   Stream<NF4> ws{(const f4 *)a.wstream, a.nchunks, wbuf};
   ws.fetch(0, tid);
   ws.commit(0, tid);
+  __syncthreads();
 
   const float eps2 = a.eps * a.s2 * a.s2;
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
@@ -265,8 +283,9 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
 
     f16v acc[MB];
     if constexpr (ENC) {
-      small_k_layer<MB>(acc, a.x, a.F, (int)r, (const float *)a.mlp.l0.w, a.mlp.l0.b, hh);
-      bias_ln_relu<MB>(acc, nullptr, a.mlp.l0.g, a.mlp.l0.beta, a.eps, hh, false);
+      // the bias is in the accumulators already (the LayerNorm adds zeros)
+      small_k_layer<MB>(acc, a.x, a.F, (int)r, prm + 7 * H, prm + 6 * H, hh);
+      ln_relu_lds<MB>(acc, prm, a.eps, hh);
     } else {
       // Layer 1 over [h; agg_in; agg_out]: 3G records.  The node row
       // slices are loaded LA records ahead into a ring of LA + 1 slots.
@@ -313,6 +332,9 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
 #pragma unroll
       for (int i = 0; i < NREC; ++i) {
         if (i + LA < NREC) xr[(i + LA) % (LA + 1)] = load_rec(i + LA);
+        // keeps the load here: under register pressure the scheduler would
+        // sink it next to its use and the look-ahead would be lost
+        __builtin_amdgcn_sched_barrier(0);
         if (i % RPC_1 == 0) w = ws.begin(tid) + lane;
         if constexpr (PREC == SPLIT)
           step_h<MB>(acc, (const h8 *)(w + (i % RPC_1) * REC_1), xr[i % (LA + 1)] * sv);
@@ -324,8 +346,7 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) acc[mb] *= inv_sv;
       }
-      bias_ln_relu<MB>(acc, a.mlp.l0.b, a.mlp.l0.g, a.mlp.l0.beta, a.eps * a.s1 * a.s1, hh, true,
-                       a.s1);
+      ln_relu_lds<MB>(acc, prm, a.eps * a.s1 * a.s1, hh);
     }
 
     // The 2-part records: layer 2, then the projection halves.  Record i of
@@ -348,7 +369,7 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
         step_hl<MB>(hv, (const bf8 *)rec_h(g), to_bf16(acc_x<MB>(acc, g)));
       rec_done(g);
     }
-    bias_ln_relu<MB>(hv, a.mlp.l1.b, a.mlp.l1.g, a.mlp.l1.beta, eps2, hh, true, a.s2);
+    ln_relu_lds<MB>(hv, prm + 3 * H, eps2, hh);
     const int64_t wrow0 = tile * 32 * SW + wave * 32;
     const int nvalid = (int)(a.n_rows - wrow0 < 32 ? a.n_rows - wrow0 : 32);
     if (a.h_out) {
