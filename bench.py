@@ -57,11 +57,13 @@ def edge_update_flops(E, H, factored):
     return 2.0 * E * ((1 if factored else 3) * H * H + H * H)
 
 
-def edge_update_bytes(N, E, H, s=4):
+def edge_update_bytes(N, E, H, s=4, n_src=0):
     """Algorithmic HBM bytes of one regrouped edge-update launch, gathered
     rows counted per edge: e read and written (s bytes per element), the
-    P[src][0:H] and P[dst][H:2H] half-rows (fp32) and both indices."""
-    return E * (2 * H * s + 2 * H * 4 + 8)
+    P[src][0:H] and P[dst][H:2H] half-rows (fp32) and both indices; with the
+    fused out-sums (n_src > 0), one fp32 agg_out row per node that has
+    out-edges."""
+    return E * (2 * H * s + 2 * H * 4 + 8) + n_src * H * 4
 
 
 def node_update_bytes(N, H, s=4):
@@ -80,9 +82,14 @@ def split_mfma_flops(N, E, H, bf16=False):
     return {"edge_update": k * 2.0 * E * 2 * H * H, "node_update": k * 2.0 * N * 6 * H * H}
 
 
-def aggregate_bytes(N, E, H, act_bytes):
-    # every message row read once per direction, both aggregates written,
-    # perm read per direction, row pointers read per direction
+def aggregate_bytes(N, E, H, act_bytes, n_src=0):
+    """Both directions: every message row read once per direction, both
+    aggregates written, perm and row pointers read per direction.  After the
+    fused edge update (n_src > 0): the in-direction only, both row-pointer
+    arrays, and a zero agg_out row per node without out-edges."""
+    if n_src:
+        return (E * H * act_bytes + N * H * act_bytes + E * 4 + 2.0 * (N + 1) * 4
+                + (N - n_src) * H * 4)
     return 2.0 * E * H * act_bytes + 2.0 * N * H * act_bytes + 2.0 * E * 4 + 2.0 * (N + 1) * 4
 
 
@@ -217,9 +224,13 @@ def main():
     eu = prof["edge_update"]
     eu_ms = eu["ms"] / max(eu["launches"], 1)
     eu_flops = edge_update_flops(E, H, factored)
+    # the split fp32 kernels sum the edge rows per source inside the edge
+    # update (rows kept in source order)
+    fused = split and not bf16
+    n_src = int(np.unique(g.edge_index[0]).size) if fused else 0
     ag = prof["aggregate"]
     ag_ms = ag["ms"] / max(ag["launches"], 1)
-    ag_bytes = aggregate_bytes(N, E, H, act_bytes)
+    ag_bytes = aggregate_bytes(N, E, H, act_bytes, n_src)
     ag_gbs = ag_bytes / (ag_ms / 1000.0) / 1e9
     nu = prof["node_update"]
     nu_ms = nu["ms"] / max(nu["launches"], 1)
@@ -229,15 +240,15 @@ def main():
         m_t = MEASURED_TRAFFIC.get(kernel_source_hash(path))
         traffic = m_t["edge_update_bytes"] if m_t else None
     if split:
-        eb = edge_update_bytes(N, E, H, act_bytes)
+        eb = edge_update_bytes(N, E, H, act_bytes, n_src)
         gbs = eb / (eu_ms / 1000.0) / 1e9
         mf = split_mfma_flops(N, E, H, bf16)
         eu_mfma = mf["edge_update"] / (eu_ms / 1000.0) / 1e12
         mdt = "bf16" if bf16 else "fp16"
         roof = {"kernel": ("edge_split<4,1,bf16> (gathers node projections, W_e e, layer 2; "
                            "hi/lo bf16 weights in LDS)") if bf16 else
-                          ("edge_split<4,1> (gathers node projections, W_e e, layer 2; "
-                           "f16x2 weights in LDS)"),
+                          ("edge_split<4,3> (gathers node projections, W_e e, layer 2 "
+                           "transposed, per-source sums of its rows; f16x2 weights in LDS)"),
                 "bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "bytes_per_launch": eb, "avg_launch_ms": round(eu_ms, 4),
@@ -295,7 +306,10 @@ def main():
         "ms_per_event_p99": round(float(np.percentile(per, 99)), 4),
         "ms_per_event_min": round(float(per.min()), 4),
         "roofline": roof,
-        "roofline_aggregate": {"kernel": "aggregate (CSR segmented sums, in and out)",
+        "roofline_aggregate": {"kernel": ("aggregate (in-direction CSR sums; out-direction "
+                                          "rows the edge update left in pieces completed, "
+                                          "empty rows zeroed)") if fused else
+                                         "aggregate (CSR segmented sums, in and out)",
                                "bound": "hbm", "achieved": round(ag_gbs, 1),
                                "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                "frac": round(ag_gbs / PEAK_HBM_GBS, 4),

@@ -205,6 +205,34 @@ __global__ void bf16_to_f32(const __bf16 *__restrict__ in, float *__restrict__ o
   if (i < n) out[i] = (float)in[i];
 }
 
+// The edge list in source order (positions p of the source CSR) and the
+// inverse of that order.
+__global__ void edge_order_k(const int32_t *__restrict__ ei, const int32_t *__restrict__ perm_out,
+                             int32_t n, int32_t n_nodes, int32_t *__restrict__ eis,
+                             int32_t *__restrict__ inv) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= n) return;
+  const int32_t j = perm_out[p];
+  eis[p] = (int32_t)clamp_key(ei[j], n_nodes);
+  eis[n + p] = (int32_t)clamp_key(ei[n + j], n_nodes);
+  inv[j] = (int32_t)p;
+}
+
+__global__ void compose_k(const int32_t *__restrict__ perm_in, const int32_t *__restrict__ inv,
+                          int32_t n, int32_t *__restrict__ q_in) {
+  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (k < n) q_in[k] = inv[perm_in[k]];
+}
+
+template <typename T>
+__global__ void scatter_rows_k(const T *__restrict__ src, const int32_t *__restrict__ idx,
+                               float *__restrict__ dst, int64_t rows, int H) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= rows * H) return;
+  const int64_t r = i / H, c = i % H;
+  dst[(int64_t)idx[r] * H + c] = (float)src[i];
+}
+
 inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
 
 }  // namespace
@@ -275,6 +303,29 @@ hipError_t launch_validate(const int32_t *edge_index, int64_t n_edges, int32_t n
 
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t stream) {
   if (n > 0) fill_i32<<<blocks_for(n, 256), 256, 0, stream>>>(p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_edge_order(const int32_t *edge_index, const int32_t *perm_out,
+                             const int32_t *perm_in, int32_t n_edges, int32_t n_nodes,
+                             int32_t *eis, int32_t *inv, int32_t *q_in, hipStream_t stream) {
+  if (n_edges <= 0) return hipSuccess;
+  edge_order_k<<<blocks_for(n_edges, 256), 256, 0, stream>>>(edge_index, perm_out, n_edges,
+                                                            n_nodes, eis, inv);
+  compose_k<<<blocks_for(n_edges, 256), 256, 0, stream>>>(perm_in, inv, n_edges, q_in);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_rows(Act act, const void *src, const int32_t *idx, float *dst,
+                               int64_t rows, int H, hipStream_t stream) {
+  const int64_t n = rows * H;
+  if (n <= 0) return hipSuccess;
+  if (act == Act::F32)
+    scatter_rows_k<float><<<blocks_for(n, 256), 256, 0, stream>>>((const float *)src, idx, dst,
+                                                                  rows, H);
+  else
+    scatter_rows_k<__bf16><<<blocks_for(n, 256), 256, 0, stream>>>((const __bf16 *)src, idx,
+                                                                   dst, rows, H);
   return hipGetLastError();
 }
 

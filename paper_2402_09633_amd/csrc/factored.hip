@@ -350,8 +350,9 @@ __global__ __launch_bounds__(64 * EDGE_WAVES) void edge_f32(EdgeArgs a) {
       part += __shfl_xor(part, 32);
       if (valid && hh == 0) {
         const float z = part + a.b2[0];
-        if (a.out_logit) a.out_logit[row] = z;
-        if (a.out_score) a.out_score[row] = sigmoidf_stable(z);
+        const int64_t o = a.out_idx ? a.out_idx[row] : row;
+        if (a.out_logit) a.out_logit[o] = z;
+        if (a.out_score) a.out_score[o] = sigmoidf_stable(z);
       }
     } else {
       f16v acc2[MB];
@@ -406,6 +407,7 @@ hipError_t edge_h(EdgeMode mode, const EdgeArgs &a, int grid, hipStream_t stream
     case EdgeMode::Enc: edge_f32<MB, 0><<<nb, 64 * EDGE_WAVES, 0, stream>>>(a); break;
     case EdgeMode::Upd: edge_f32<MB, 1><<<nb, 64 * EDGE_WAVES, 0, stream>>>(a); break;
     case EdgeMode::Cls: edge_f32<MB, 2><<<nb, 64 * EDGE_WAVES, 0, stream>>>(a); break;
+    default: return hipErrorInvalidValue;  // no fused sums on the fp32 matrix cores
   }
   return hipGetLastError();
 }

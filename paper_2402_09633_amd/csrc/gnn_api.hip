@@ -391,10 +391,15 @@ struct Workspace {
   int32_t *rp_in = nullptr, *rp_out = nullptr, *perm_in = nullptr, *perm_out = nullptr;
   CsrScratch csr{};
   int32_t *flag = nullptr;
+  // regrouped path: edges in source order ([2][E], in the sort scratch once
+  // the CSR is built), the in-CSR over that order, and the unit pieces of
+  // the fused out-sums ([units][2][H] fp32)
+  int32_t *eis = nullptr, *inv = nullptr, *q_in = nullptr;
+  float *part = nullptr;
 };
 
 size_t plan_workspace(Workspace &w, int64_t N, int64_t E, int H, size_t act_bytes,
-                      bool factored) {
+                      bool factored, bool fused) {
   size_t off = 0;
   auto take = [&](size_t n) {
     const size_t o = off;
@@ -414,11 +419,13 @@ size_t plan_workspace(Workspace &w, int64_t N, int64_t E, int H, size_t act_byte
   const size_t o_flag = take(4);
   const size_t o_pa = factored ? take((size_t)N * 2 * H * 4) : 0;
   const size_t o_pb = factored ? take((size_t)N * 2 * H * 4) : 0;
+  const size_t o_part = fused ? take((size_t)((E + 31) / 32) * 2 * H * 4) : 0;
   if (w.base) {
     if (factored) {
       w.pa = (float *)((unsigned char *)w.base + o_pa);
       w.pb = (float *)((unsigned char *)w.base + o_pb);
     }
+    if (fused) w.part = (float *)((unsigned char *)w.base + o_part);
     unsigned char *b = (unsigned char *)w.base;
     w.h = b + o_h;
     w.e = b + o_e;
@@ -435,6 +442,9 @@ size_t plan_workspace(Workspace &w, int64_t N, int64_t E, int H, size_t act_byte
     w.csr.hist = (uint32_t *)(b + o_hist);
     w.csr.totals = (uint32_t *)(b + o_tot);
     w.flag = (int32_t *)(b + o_flag);
+    w.eis = (int32_t *)w.csr.keys_a;
+    w.inv = (int32_t *)w.csr.keys_b;
+    w.q_in = w.inv + E;
   }
   return off;
 }
@@ -520,7 +530,9 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
   total.begin();
 
   const bool fac = hd->factored;
-  w.bytes = plan_workspace(w, N, E, H, ab, fac);
+  // the edge update sums its rows per source itself (split fp32 kernels)
+  const bool fused = fac && hd->fd.split && !hd->fd.bf16;
+  w.bytes = plan_workspace(w, N, E, H, ab, fac, fused);
   {
     hipError_t ae = hipMallocAsync(&w.base, w.bytes, stream);
     if (ae != hipSuccess) {
@@ -529,7 +541,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
                   "hipMallocAsync(%zu bytes) failed: %s", w.bytes, hipGetErrorString(ae));
     }
   }
-  plan_workspace(w, N, E, H, ab, fac);
+  plan_workspace(w, N, E, H, ab, fac, fused);
 
   if (d.flags & GNN_VALIDATE_INDICES) {
     int32_t bad = 0;
@@ -554,6 +566,9 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
     w.perm_in = pi;
     w.rp_out = rpo;
     w.perm_out = po;
+    // The regrouped kernels keep the edge rows in source order (a node's
+    // out-edges are consecutive); outputs go back to input order.
+    if (fac) HIP_TRY(launch_edge_order(ei, po, pi, m, n, w.eis, w.inv, w.q_in, stream));
   }
 
   if (fac) {
@@ -585,8 +600,8 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       EdgeArgs ea;
       ea.n_rows = E;
       ea.n_nodes = n;
-      ea.src_idx = ei;
-      ea.dst_idx = ei + E;
+      ea.src_idx = w.eis;
+      ea.dst_idx = w.eis + E;
       ea.P = P;
       ea.b1 = m.l0.b;
       ea.g1 = m.l0.g;
@@ -625,12 +640,20 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
         ea.s1 = fd.s1_em[k];
         ea.s2 = fd.s2_em[k];
       }
+      if (fused) {
+        ea.agg_out = (float *)w.aout;
+        ea.agg_part = w.part;
+      }
       st.begin();
-      HIP_TRY(launch_edge(EdgeMode::Upd, ea, fd.grid_upd));
+      HIP_TRY(launch_edge(fused ? EdgeMode::UpdAgg : EdgeMode::Upd, ea, fd.grid_upd));
       st.end(GNN_STAGE_EDGE_UPDATE);
       st.begin();
-      HIP_TRY(launch_segsum(act, H, w.e, w.rp_in, w.perm_in, w.rp_out, w.perm_out, w.ain,
-                            w.aout, n, stream));
+      if (fused)
+        HIP_TRY(launch_segsum_fused(H, (const float *)w.e, w.rp_in, w.q_in, w.rp_out, w.part,
+                                    (float *)w.ain, (float *)w.aout, n, stream));
+      else  // source-order rows: the out-CSR is the identity
+        HIP_TRY(launch_segsum(act, H, w.e, w.rp_in, w.q_in, w.rp_out, nullptr, w.ain, w.aout,
+                              n, stream));
       st.end(GNN_STAGE_AGGREGATE);
       NodeArgs nu;
       nu.n_rows = N;
@@ -663,7 +686,9 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
           {ro.ain, w.ain, nh, true}, {ro.aout, w.aout, nh, true}};
       for (auto &x2 : ex) {
         if (!x2.dst || x2.n == 0 || (x2.agg && T == 0)) continue;
-        if (act == Act::F32)
+        if (x2.src == w.e)  // back to input order
+          HIP_TRY(launch_scatter_rows(act, w.e, w.perm_out, x2.dst, E, H, stream));
+        else if (act == Act::F32)
           HIP_TRY(hipMemcpyAsync(x2.dst, x2.src, x2.n * 4, hipMemcpyDeviceToDevice, stream));
         else
           HIP_TRY(launch_bf16_to_f32(x2.src, x2.dst, x2.n, stream));
@@ -672,6 +697,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
     }
     {
       EdgeArgs ea = edge_args(w.pb, hd->cls);
+      ea.out_idx = w.perm_out;
       ea.e_in = (const float *)w.e;
       ea.we = (const float *)fd.we_cls;
       ea.g2 = ea.beta2 = nullptr;
@@ -1053,7 +1079,7 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
       fd.enc_chunks = node_split_chunks(true, H, 2, bf16);
       fd.upd_chunks = node_split_chunks(false, H, 1, bf16);
       fd.grid_enc = edge_split_grid(EdgeMode::Enc, H, bf16, n_cu);
-      fd.grid_upd = edge_split_grid(EdgeMode::Upd, H, bf16, n_cu);
+      fd.grid_upd = edge_split_grid(bf16 ? EdgeMode::Upd : EdgeMode::UpdAgg, H, bf16, n_cu);
       fd.grid_cls = edge_split_grid(EdgeMode::Cls, H, bf16, n_cu);
     } else {
       const int kg = H / 8;  // k-groups of one H-wide operand; 8 per chunk

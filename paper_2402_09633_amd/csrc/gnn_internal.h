@@ -74,7 +74,10 @@ struct NodeArgs {
   float row_bound = 0.f;
 };
 
-enum class EdgeMode : int { Enc = 0, Upd = 1, Cls = 2 };
+// UpdAgg: the edge update that also sums its output rows per source node
+// (split fp32 kernels only).  It needs the rows in source order: every run
+// of equal src_idx is one node's complete out-edge list.
+enum class EdgeMode : int { Enc = 0, Upd = 1, Cls = 2, UpdAgg = 3 };
 
 struct EdgeArgs {
   int64_t n_rows = 0;
@@ -87,10 +90,18 @@ struct EdgeArgs {
   const float *w2 = nullptr;     // fragments of W2 (H x H), or the classifier head [H]
   const float *b2 = nullptr, *g2 = nullptr, *beta2 = nullptr;
   float *e_out = nullptr, *out_logit = nullptr, *out_score = nullptr;
+  // classifier: row r's outputs go to position out_idx[r] (nullptr: r)
+  const int32_t *out_idx = nullptr;
   float eps = 1e-5f;
   // split kernels: power-of-two scales of the first layer (W_e and the
   // stored P rows) and of W2
   float s1 = 1.f, s2 = 1.f;
+  // UpdAgg: the sum of every run of rows with one source node that lies
+  // inside one 32-row unit goes to agg_out[src]; a run cut by a unit
+  // boundary leaves its piece in agg_part[unit][0] (the unit's first run,
+  // continued from the previous unit) or agg_part[unit][1] (its last run,
+  // continued in the next), H floats each, for launch_segsum_fused.
+  float *agg_out = nullptr, *agg_part = nullptr;
 };
 
 hipError_t launch_node_f32(bool enc, int hidden, const NodeArgs &a, int grid,
@@ -115,10 +126,20 @@ int edge_split_grid(EdgeMode mode, int hidden, bool bf16, int n_cu);
 
 // Deterministic CSR segmented sums of the edge rows `e` ([n_edges][H]):
 // agg_in[v] = sum over p in [rp_in[v], rp_in[v+1]) of e[perm_in[p]], in
-// ascending p, and the same for agg_out.  fp32 accumulation in both modes.
+// ascending p, and the same for agg_out; a null perm is the identity.  fp32
+// accumulation in both modes.
 hipError_t launch_segsum(Act act, int hidden, const void *e, const int32_t *rp_in,
                          const int32_t *perm_in, const int32_t *rp_out, const int32_t *perm_out,
                          void *agg_in, void *agg_out, int32_t n_nodes, hipStream_t stream);
+// fp32 rows in source order after an UpdAgg edge update: agg_in as above;
+// agg_out[v] is completed for the nodes whose out-edge positions
+// [rp_out[v], rp_out[v+1]) span several 32-row units (sum of the unit
+// pieces in agg_part, in unit order) and zeroed for nodes without out-edges;
+// the edge update wrote every other row.
+hipError_t launch_segsum_fused(int hidden, const float *e, const int32_t *rp_in,
+                               const int32_t *perm_in, const int32_t *rp_out,
+                               const float *agg_part, float *agg_in, float *agg_out,
+                               int32_t n_nodes, hipStream_t stream);
 
 // Stable CSRs of edge_index ([2][n_edges] int32, indices clamped into
 // [0, n_nodes)): by destination (row_ptr_in, perm_in) and by source
@@ -133,6 +154,15 @@ size_t csr_hist_len(int64_t n_edges);
 hipError_t build_csr(const int32_t *edge_index, int32_t n_edges, int32_t n_nodes,
                      int32_t *row_ptr_in, int32_t *perm_in, int32_t *row_ptr_out,
                      int32_t *perm_out, const CsrScratch &s, hipStream_t stream);
+// The edges in source order: eis[0][p] = src[perm_out[p]], eis[1][p] =
+// dst[perm_out[p]] (clamped into [0, n_nodes)), and q_in[k] = the source-order
+// position of edge perm_in[k]; inv ([n_edges]) is scratch.
+hipError_t launch_edge_order(const int32_t *edge_index, const int32_t *perm_out,
+                             const int32_t *perm_in, int32_t n_edges, int32_t n_nodes,
+                             int32_t *eis, int32_t *inv, int32_t *q_in, hipStream_t stream);
+// dst[idx[r]][:] = src[r][:] (fp32 or bf16 rows of width H, written as fp32).
+hipError_t launch_scatter_rows(Act act, const void *src, const int32_t *idx, float *dst,
+                               int64_t rows, int H, hipStream_t stream);
 
 // Edge filter (filter.hip): scores[j] = sigmoid(MLP([x_src; x_dst])).
 struct FilterArgs {

@@ -93,6 +93,91 @@ __device__ __forceinline__ void step_h(f16v (&acc)[MB], const h8 *rec, const f8 
   step_h<MB>(acc, rec, x1, x2);
 }
 
+// The same k-step with the operands exchanged: the graph rows are the A
+// operand and the weights the B operand (a record's lane slots hold W[f][k]
+// for f = lane % 32, which is also the B-operand layout of W^T), so the
+// accumulators hold the product transposed: lane l has feature 32 mb + l % 32
+// of the rows 8 (v / 4) + 4 (l / 32) + v % 4, v = 0..15.
+template <int MB>
+__device__ __forceinline__ void step_ht(f16v (&acc)[MB], const h8 *rec, const f8 &x) {
+  h8 x1, x2, w1[MB], w2[MB];
+  split2(x, x1, x2);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    w1[mb] = rec[(2 * mb) * 64];
+    w2[mb] = rec[(2 * mb + 1) * 64];
+  }
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = mma_h(x1, w1[mb], acc[mb]);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = mma_h(x1, w2[mb], acc[mb]);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = mma_h(x2, w1[mb], acc[mb]);
+}
+
+// Sum over the 32 lanes of this lane's half of the wave; every lane of the
+// half receives the same value (each step adds two partial sums, and fp32
+// addition is commutative).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                               CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float sum32(float v) {
+  v += dpp_f<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_f<0x141>(v);  // row_half_mirror
+  v += dpp_f<0x140>(v);  // row_mirror
+  // swap the two 16-lane rows of each 32-lane group
+  return v + __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v),
+                                                                   0x401F));
+}
+
+// Bias + LayerNorm + ReLU on transposed accumulators (step_ht): lane l holds
+// feature 32 mb + n, n = l % 32, of 16 rows; a row's statistics are sums
+// over the 32 lanes of its half of the wave.  prm as for ln_relu_lds.
+template <int MB>
+__device__ __forceinline__ void ln_relu_t(f16v (&t)[MB], const float *prm, float eps, int n) {
+  constexpr int H = 32 * MB;
+  constexpr float inv_h = 1.0f / H;
+  float gg[MB], bt[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    const float bb = prm[32 * mb + n];
+    gg[mb] = prm[H + 32 * mb + n];
+    bt[mb] = prm[2 * H + 32 * mb + n];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) t[mb][v] += bb;
+  }
+  // four rows at a time: their reductions overlap, with few live registers
+#pragma unroll
+  for (int v0 = 0; v0 < 16; v0 += 4) {
+    float mean[4], rstd[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float sv = 0.f;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) sv += t[mb][v0 + j];
+      mean[j] = sum32(sv) * inv_h;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float q = 0.f;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const float d = t[mb][v0 + j] - mean[j];
+        q += d * d;
+      }
+      rstd[j] = 1.0f / sqrtf(sum32(q) * inv_h + eps);
+    }
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        t[mb][v0 + j] = fmaxf((t[mb][v0 + j] - mean[j]) * rstd[j] * gg[mb] + bt[mb], 0.f);
+  }
+}
+
 // acc[mb] += (w_hi + w_lo) x over one k-step, x exact in bf16.
 template <int MB>
 __device__ __forceinline__ void step_hl(f16v (&acc)[MB], const bf8 *rec, const bf8 &x) {
@@ -416,6 +501,8 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
   using act_t = typename std::conditional<PREC == SPLIT, float, __bf16>::type;
   constexpr bool HAS_E = MODE != (int)EdgeMode::Enc;
   constexpr bool HAS_L2 = MODE != (int)EdgeMode::Cls;
+  constexpr bool FUSE = MODE == (int)EdgeMode::UpdAgg;
+  static_assert(!FUSE || PREC == SPLIT, "fused sums: fp32 rows only");
   __shared__ h8 lds[(HAS_E ? NR : 0) + (HAS_L2 ? NR : 0)];
   __shared__ float prm[6 * H];  // s1 b1, gamma1, beta1, s2 b2, gamma2, beta2
   h8 *lw_e = lds;
@@ -464,12 +551,26 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
         ev[g] = *(const bf8 *)(ep + 16 * g);
     }
   };
-  int32_t nsrc = 0, ndst = 0;
-  if (gw < units) {
-    const int64_t r0 = row_of(gw);
+  // FUSE: the source of the rows just before and after this lane's row
+  // (-1 / -2 outside the edge list) find the runs of equal sources.
+  int32_t nsrc = 0, ndst = 0, nprev = -1, nnext = -2;
+  auto load_idx = [&](int64_t uu) {
+    const int64_t r0 = row_of(uu);
     nsrc = a.src_idx[r0];
     ndst = a.dst_idx[r0];
-    if constexpr (HAS_E) load_e(r0);
+    if constexpr (FUSE) {
+      const int64_t rr = uu * 32 + n;
+      nprev = rr >= 1 && rr - 1 < a.n_rows ? a.src_idx[rr - 1] : -1;
+      nnext = rr + 1 < a.n_rows ? a.src_idx[rr + 1] : -2;
+    }
+    // FUSE requests the e row at the end of the unit instead: the next
+    // unit's first products wait for its P gathers, issued after this
+    // unit's stores anyway, and the registers are needed until then.
+    if constexpr (HAS_E && !FUSE) load_e(r0);
+  };
+  if (gw < units) {
+    load_idx(gw);
+    if constexpr (FUSE) load_e(row_of(gw));
   }
   for (int64_t u = gw; u < units; u += nw) {
     // Keeps the LDS record reads inside the loop (they are loop-invariant;
@@ -504,15 +605,9 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
           step_hl<MB>(acc, (const bf8 *)(lw_e + g * 2 * MB * 64 + lane), ev[g]);
       }
     }
-    {
-      const int64_t un = u + nw;
-      if (un < units) {
-        const int64_t rn = row_of(un);
-        nsrc = a.src_idx[rn];
-        ndst = a.dst_idx[rn];
-        if constexpr (HAS_E) load_e(rn);
-      }
-    }
+    // (FUSE: after layer 2's LayerNorm, which needs the registers)
+    if constexpr (!FUSE)
+      if (u + nw < units) load_idx(u + nw);
     ln_relu_lds<MB>(acc, prm, eps1, hh);
 
     if constexpr (!HAS_L2) {
@@ -528,9 +623,86 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
       part += __shfl_xor(part, 32);
       if (valid && hh == 0) {
         const float z = part + a.b2[0];
-        if (a.out_logit) a.out_logit[row] = z;
-        if (a.out_score) a.out_score[row] = sigmoidf_stable(z);
+        const int64_t o = a.out_idx ? a.out_idx[row] : row;
+        if (a.out_logit) a.out_logit[o] = z;
+        if (a.out_score) a.out_score[o] = sigmoidf_stable(z);
       }
+    } else if constexpr (FUSE) {
+      // Layer 2 transposed: lane l holds feature 32 mb + n of the unit's
+      // rows 8 (v / 4) + 4 hh + v % 4.
+      f16v t2[MB];
+      zero<MB>(t2);
+#pragma unroll
+      for (int g = 0; g < G; ++g) step_ht<MB>(t2, lw_2 + g * 2 * MB * 64 + lane, acc_x<MB>(acc, g));
+      ln_relu_t<MB>(t2, prm + 3 * H, eps2, n);
+      // Bit e of `ends` marks the last row of a run of equal sources
+      // (within the unit's valid rows); hc: the unit's first run began in
+      // the previous unit; tc: its last run continues in the next one.  All
+      // three are wave-uniform; taken before the next unit's indices replace
+      // this unit's.
+      const int nvalid = (int)(a.n_rows - u * 32 < 32 ? a.n_rows - u * 32 : 32);
+      const uint32_t ends = (uint32_t)__ballot(n < nvalid && (n == nvalid - 1 || nsrc != nnext));
+      const bool hc = __ballot(n == 0 && nprev == nsrc) != 0;
+      const bool tc = __ballot(n == 31 && nsrc == nnext) != 0;
+      const int32_t cur_src = nsrc;
+      if (u + nw < units) load_idx(u + nw);
+      // e rows: each store writes 128 contiguous bytes of a row per half-wave
+      float *eo = a.e_out + (u * 32 + 4 * hh) * H + n;
+      if (nvalid == 32) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) eo[(8 * (v / 4) + v % 4) * H + 32 * mb] = t2[mb][v];
+      } else {
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (8 * (v / 4) + 4 * hh + v % 4 < nvalid)
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) eo[(8 * (v / 4) + v % 4) * H + 32 * mb] = t2[mb][v];
+      }
+      // Exchange halves: afterwards lane l holds block b = p + hh MB/2 of
+      // all 32 rows, rows 8 (v / 4) + v % 4 in t2[p][v] and rows
+      // 8 (v / 4) + 4 + v % 4 in t2[p + MB/2][v].
+      // (Elements are copied to scalars first: this compiler's
+      // __builtin_bit_cast of a vector element reads element 0.)
+#pragma unroll
+      for (int p = 0; p < MB / 2; ++p)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const unsigned lo = __float_as_uint(t2[p][v]);
+          const unsigned hi = __float_as_uint(t2[p + MB / 2][v]);
+          const auto r = __builtin_amdgcn_permlane32_swap(lo, hi, false, false);
+          const unsigned r0 = r[0], r1 = r[1];
+          t2[p][v] = __uint_as_float(r0);
+          t2[p + MB / 2][v] = __uint_as_float(r1);
+        }
+      // Run sums in row order, one feature of MB/2 blocks per lane.
+      float sum[MB / 2];
+#pragma unroll
+      for (int p = 0; p < MB / 2; ++p) sum[p] = 0.f;
+#pragma unroll
+      for (int e = 0; e < 32; ++e) {
+        const int v = 4 * (e / 8) + e % 4;
+#pragma unroll
+        for (int p = 0; p < MB / 2; ++p) sum[p] += (e / 4) % 2 ? t2[p + MB / 2][v] : t2[p][v];
+        if (ends & (1u << e)) {
+          const bool first = (ends & ((1u << e) - 1u)) == 0u;
+          const bool last = (ends >> e) == 1u;
+          float *dst;
+          if (first && hc)
+            dst = a.agg_part + (u * 2) * H;
+          else if (last && tc)
+            dst = a.agg_part + (u * 2 + 1) * H;
+          else
+            dst = a.agg_out + (int64_t)__builtin_amdgcn_readlane(cur_src, e) * H;
+#pragma unroll
+          for (int p = 0; p < MB / 2; ++p) {
+            dst[32 * (p + hh * (MB / 2)) + n] = sum[p];
+            sum[p] = 0.f;
+          }
+        }
+      }
+      if (u + nw < units) load_e(row_of(u + nw));
     } else {
       f16v acc2[MB];
       zero<MB>(acc2);
@@ -578,19 +750,31 @@ hipError_t edge_h(EdgeMode mode, const EdgeArgs &a, int grid, hipStream_t stream
     case EdgeMode::Enc: edge_split<MB, 0, PREC><<<nb, 64 * SW, 0, stream>>>(a); break;
     case EdgeMode::Upd: edge_split<MB, 1, PREC><<<nb, 64 * SW, 0, stream>>>(a); break;
     case EdgeMode::Cls: edge_split<MB, 2, PREC><<<nb, 64 * SW, 0, stream>>>(a); break;
+    case EdgeMode::UpdAgg:
+      if constexpr (PREC != SPLIT) return hipErrorInvalidValue;
+      if (!a.agg_out || !a.agg_part) return hipErrorInvalidValue;
+      edge_split<MB, 3, SPLIT><<<nb, 64 * SW, 0, stream>>>(a);
+      break;
   }
   return hipGetLastError();
 }
 
+template <int MB, int PREC>
+const void *edge_fn_mb(EdgeMode mode) {
+  switch (mode) {
+    case EdgeMode::Enc: return (const void *)edge_split<MB, 0, PREC>;
+    case EdgeMode::Upd: return (const void *)edge_split<MB, 1, PREC>;
+    case EdgeMode::Cls: return (const void *)edge_split<MB, 2, PREC>;
+    case EdgeMode::UpdAgg:
+      if constexpr (PREC == SPLIT) return (const void *)edge_split<MB, 3, SPLIT>;
+      break;
+  }
+  return (const void *)edge_split<MB, 1, PREC>;
+}
+
 template <int PREC>
 const void *edge_fn(EdgeMode mode, int hidden) {
-  if (hidden == 64)
-    return mode == EdgeMode::Enc   ? (const void *)edge_split<2, 0, PREC>
-           : mode == EdgeMode::Upd ? (const void *)edge_split<2, 1, PREC>
-                                   : (const void *)edge_split<2, 2, PREC>;
-  return mode == EdgeMode::Enc   ? (const void *)edge_split<4, 0, PREC>
-         : mode == EdgeMode::Upd ? (const void *)edge_split<4, 1, PREC>
-                                 : (const void *)edge_split<4, 2, PREC>;
+  return hidden == 64 ? edge_fn_mb<2, PREC>(mode) : edge_fn_mb<4, PREC>(mode);
 }
 
 }  // namespace

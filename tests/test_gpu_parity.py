@@ -212,6 +212,42 @@ def test_constant_messages_aggregate_to_degrees_full_scale(G, dtype):
         G.gnn_destroy(h)
 
 
+@pytest.mark.parametrize("flags", PATHS)
+@pytest.mark.parametrize("H", [64, 128])
+def test_out_sums_every_run_offset_exact(G, flags, H):
+    # Out-degrees 0..129 and random ones, with nodes without out-edges in
+    # between and the edge list in a random order: in source order the runs
+    # of one node start and end at every offset of a 32-row unit and span up
+    # to five units.  With constant messages the sums are exact degrees.
+    rng = np.random.default_rng(77)
+    degs = np.concatenate([np.arange(130), rng.integers(0, 40, 400), np.zeros(50, np.int64)])
+    rng.shuffle(degs)
+    N = len(degs)
+    src = np.repeat(np.arange(N), degs)
+    E = len(src)
+    dst = rng.integers(0, N, E)
+    p = rng.permutation(E)
+    ei = np.stack([src[p], dst[p]]).astype(np.int32)
+    x = rng.normal(size=(N, 3)).astype(np.float32)
+    w = I.make_weights(3, H, 1, 77)
+    v = I.blob_views(w, 3, H, 1)
+    v["edge_mlp0.1.W"][:] = 0.0
+    v["edge_mlp0.1.beta"][:] = 1.0
+    h = G.gnn_create(w, G.make_dims(3, H, 2, flags=flags))
+    try:
+        ain = torch.zeros(N, H, device="cuda")
+        aout = torch.zeros(N, H, device="cuda")
+        e = torch.zeros(E, H, device="cuda")
+        G.gnn_debug_stages(h, dev(x), dev(ei), N, E, 1, None, e, ain, aout)
+        torch.cuda.synchronize()
+        assert (e == 1).all()
+        indeg = np.bincount(ei[1], minlength=N).astype(np.float32)
+        np.testing.assert_array_equal(aout.cpu().numpy(), np.repeat(degs[:, None], H, 1).astype(np.float32))
+        np.testing.assert_array_equal(ain.cpu().numpy(), np.repeat(indeg[:, None], H, 1))
+    finally:
+        G.gnn_destroy(h)
+
+
 def test_full_deterministic_and_permutation_equivariant(G):
     c = I.CONFIGS["full"]
     g = I.make_graph(c)
