@@ -502,6 +502,9 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
   constexpr bool HAS_E = MODE != (int)EdgeMode::Enc;
   constexpr bool HAS_L2 = MODE != (int)EdgeMode::Cls;
   constexpr bool FUSE = MODE == (int)EdgeMode::UpdAgg;
+  // Layer 2 transposed (step_ht) with full-line e stores: the fused update
+  // and the fp32 encoder
+  constexpr bool TRANS = FUSE || (MODE == (int)EdgeMode::Enc && PREC == SPLIT);
   static_assert(!FUSE || PREC == SPLIT, "fused sums: fp32 rows only");
   __shared__ h8 lds[(HAS_E ? NR : 0) + (HAS_L2 ? NR : 0)];
   __shared__ float prm[6 * H];  // s1 b1, gamma1, beta1, s2 b2, gamma2, beta2
@@ -627,7 +630,7 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
         if (a.out_logit) a.out_logit[o] = z;
         if (a.out_score) a.out_score[o] = sigmoidf_stable(z);
       }
-    } else if constexpr (FUSE) {
+    } else if constexpr (TRANS) {
       // Layer 2 transposed: lane l holds feature 32 mb + n of the unit's
       // rows 8 (v / 4) + 4 hh + v % 4.
       f16v t2[MB];
@@ -641,11 +644,16 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
       // three are wave-uniform; taken before the next unit's indices replace
       // this unit's.
       const int nvalid = (int)(a.n_rows - u * 32 < 32 ? a.n_rows - u * 32 : 32);
-      const uint32_t ends = (uint32_t)__ballot(n < nvalid && (n == nvalid - 1 || nsrc != nnext));
-      const bool hc = __ballot(n == 0 && nprev == nsrc) != 0;
-      const bool tc = __ballot(n == 31 && nsrc == nnext) != 0;
-      const int32_t cur_src = nsrc;
-      if (u + nw < units) load_idx(u + nw);
+      uint32_t ends = 0;
+      bool hc = false, tc = false;
+      int32_t cur_src = 0;
+      if constexpr (FUSE) {
+        ends = (uint32_t)__ballot(n < nvalid && (n == nvalid - 1 || nsrc != nnext));
+        hc = __ballot(n == 0 && nprev == nsrc) != 0;
+        tc = __ballot(n == 31 && nsrc == nnext) != 0;
+        cur_src = nsrc;
+        if (u + nw < units) load_idx(u + nw);
+      }
       // e rows: each store writes 128 contiguous bytes of a row per half-wave
       float *eo = a.e_out + (u * 32 + 4 * hh) * H + n;
       if (nvalid == 32) {
@@ -660,6 +668,7 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb) eo[(8 * (v / 4) + v % 4) * H + 32 * mb] = t2[mb][v];
       }
+      if constexpr (FUSE) {
       // Exchange halves: afterwards lane l holds block b = p + hh MB/2 of
       // all 32 rows, rows 8 (v / 4) + v % 4 in t2[p][v] and rows
       // 8 (v / 4) + 4 + v % 4 in t2[p + MB/2][v].
@@ -703,6 +712,7 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
         }
       }
       if (u + nw < units) load_e(row_of(u + nw));
+      }
     } else {
       f16v acc2[MB];
       zero<MB>(acc2);
