@@ -34,8 +34,8 @@ TRAFFIC_SOURCES = {
     "fp32_mfma": ["paper_2402_09633_amd/csrc/factored.hip",
                   "paper_2402_09633_amd/csrc/device_common.h"],
 }
-MEASURED_TRAFFIC = {"b0131a8d543c8b86": {"edge_update_bytes": 1.941e9},   # edge_split<4,1>
-                    "01db9dfa269e4bf7": {"edge_update_bytes": 1.652e9}}   # edge_f32<4,1>
+MEASURED_TRAFFIC = {"f4c4c9c468e2ba92": {"edge_update_bytes": 1.802e9},   # edge_split<4,3>
+                    "d13e7c0d9ceb8c2f": {"edge_update_bytes": 1.652e9}}   # edge_f32<4,1>
 
 
 def kernel_source_hash(path):
