@@ -208,10 +208,12 @@ struct FrnnArgs {
   const int32_t *rp = nullptr, *perm = nullptr;  // buckets: CSR of the points by key
   int32_t *count = nullptr;   // [n] pairs per point
   int64_t *offs = nullptr;    // [n] exclusive offsets
+  int64_t *bsum = nullptr;    // [frnn_scan_blocks(n)] scan scratch
   int64_t *total_dev = nullptr;
   int64_t total = 0;          // fill pass: number of pairs (row stride of out)
   int32_t *out = nullptr;     // [2][total]
 };
+size_t frnn_scan_blocks(int64_t n);
 hipError_t launch_frnn_keys(const FrnnArgs &a, int32_t *keys, hipStream_t stream);
 // zs: [n][D] scratch for the coordinates in bucket order
 hipError_t launch_frnn_count(const FrnnArgs &a, float *zs, hipStream_t stream);

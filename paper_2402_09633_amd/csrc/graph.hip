@@ -151,31 +151,75 @@ __global__ __launch_bounds__(FTHREADS) void frnn_pairs(FrnnArgs a, const float *
   if constexpr (!FILL) a.count[i] = cnt;
 }
 
-// Exclusive scan of the per-point counts into offs (int64), total -> *total.
-// One block of 1024 threads, each scanning a contiguous chunk.
-__global__ __launch_bounds__(1024) void frnn_scan(const int32_t *__restrict__ count, int64_t n,
-                                                  int64_t *__restrict__ offs,
-                                                  int64_t *__restrict__ total) {
-  __shared__ int64_t part[1024];
+// Exclusive scan of the per-point counts into offs (int64), total -> *total:
+// per-tile sums (tiles of 2048 counts), a scan of the tile sums, then each
+// tile's own scan.  Thread t of a tile owns its 8 consecutive counts.
+constexpr int ST = 256, SI = 8, STILE = ST * SI;
+
+// Exclusive scan of v over the block; *sum gets the block total.
+__device__ __forceinline__ int64_t block_excl_scan(int64_t v, int64_t *sum) {
+  __shared__ int64_t part[ST];
   const int t = threadIdx.x;
-  const int64_t chunk = (n + 1023) / 1024;
-  const int64_t beg = min((int64_t)t * chunk, n), end = min(beg + chunk, n);
-  int64_t s = 0;
-  for (int64_t i = beg; i < end; ++i) s += count[i];
-  part[t] = s;
+  part[t] = v;
   __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
-    const int64_t v = t >= off ? part[t - off] : 0;
+  for (int off = 1; off < ST; off <<= 1) {
+    const int64_t u = t >= off ? part[t - off] : 0;
     __syncthreads();
-    part[t] += v;
+    part[t] += u;
     __syncthreads();
   }
-  int64_t run = part[t] - s;
-  for (int64_t i = beg; i < end; ++i) {
-    offs[i] = run;
-    run += count[i];
+  const int64_t incl = part[t];
+  *sum = part[ST - 1];
+  __syncthreads();
+  return incl - v;
+}
+
+__global__ __launch_bounds__(ST) void scan_tiles(const int32_t *__restrict__ count, int64_t n,
+                                                 int64_t *__restrict__ bsum) {
+  const int64_t base = (int64_t)blockIdx.x * STILE + (int64_t)threadIdx.x * SI;
+  int64_t s = 0;
+#pragma unroll
+  for (int k = 0; k < SI; ++k)
+    if (base + k < n) s += count[base + k];
+  int64_t tot;
+  (void)block_excl_scan(s, &tot);
+  if (threadIdx.x == 0) bsum[blockIdx.x] = tot;
+}
+
+// In place over the nb tile sums, ST at a time with a running carry.
+__global__ __launch_bounds__(ST) void scan_sums(int64_t *__restrict__ bsum, int64_t nb,
+                                                int64_t *__restrict__ total) {
+  int64_t carry = 0;
+  for (int64_t b0 = 0; b0 < nb; b0 += ST) {
+    const int64_t i = b0 + threadIdx.x;
+    const int64_t v = i < nb ? bsum[i] : 0;
+    int64_t tot;
+    const int64_t ex = block_excl_scan(v, &tot);
+    if (i < nb) bsum[i] = carry + ex;
+    carry += tot;
   }
-  if (t == 1023) *total = part[1023];
+  if (threadIdx.x == 0) *total = carry;
+}
+
+__global__ __launch_bounds__(ST) void scan_down(const int32_t *__restrict__ count, int64_t n,
+                                                const int64_t *__restrict__ bsum,
+                                                int64_t *__restrict__ offs) {
+  const int64_t base = (int64_t)blockIdx.x * STILE + (int64_t)threadIdx.x * SI;
+  int32_t c[SI];
+  int64_t s = 0;
+#pragma unroll
+  for (int k = 0; k < SI; ++k) {
+    c[k] = base + k < n ? count[base + k] : 0;
+    s += c[k];
+  }
+  int64_t tot;
+  int64_t run = bsum[blockIdx.x] + block_excl_scan(s, &tot);
+#pragma unroll
+  for (int k = 0; k < SI; ++k)
+    if (base + k < n) {
+      offs[base + k] = run;
+      run += c[k];
+    }
 }
 
 }  // namespace
@@ -193,6 +237,8 @@ hipError_t launch_embed(int hidden, const EmbedArgs &a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+size_t frnn_scan_blocks(int64_t n) { return (size_t)((n + STILE - 1) / STILE); }
+
 hipError_t launch_frnn_keys(const FrnnArgs &a, int32_t *keys, hipStream_t stream) {
   if (a.n <= 0) return hipSuccess;
   frnn_keys<<<(unsigned)((a.n + FTHREADS - 1) / FTHREADS), FTHREADS, 0, stream>>>(a, keys);
@@ -205,7 +251,10 @@ hipError_t launch_frnn_count(const FrnnArgs &a, float *zs, hipStream_t stream) {
   frnn_gather<<<(unsigned)((nz + FTHREADS - 1) / FTHREADS), FTHREADS, 0, stream>>>(a, zs);
   const unsigned blocks = (unsigned)((a.n + FTHREADS - 1) / FTHREADS);
   frnn_pairs<false><<<blocks, FTHREADS, 0, stream>>>(a, zs);
-  frnn_scan<<<1, 1024, 0, stream>>>(a.count, a.n, a.offs, a.total_dev);
+  const int64_t nb = (int64_t)frnn_scan_blocks(a.n);
+  scan_tiles<<<(unsigned)nb, ST, 0, stream>>>(a.count, a.n, a.bsum);
+  scan_sums<<<1, ST, 0, stream>>>(a.bsum, nb, a.total_dev);
+  scan_down<<<(unsigned)nb, ST, 0, stream>>>(a.count, a.n, a.bsum, a.offs);
   return hipGetLastError();
 }
 
@@ -271,6 +320,7 @@ extern "C" int gnn_frnn(const float *z, int64_t n_nodes, int32_t dim, float r2,
   const size_t o_va = take((size_t)2 * n * 4), o_vb = take((size_t)2 * n * 4);
   const size_t o_hist = take(2 * csr_hist_len(n) * 4), o_tot = take(2 * 256 * 4 * 4);
   const size_t o_cnt = take((size_t)n * 4), o_offs = take((size_t)n * 8), o_total = take(8);
+  const size_t o_bsum = take(frnn_scan_blocks(n) * 8);
   const size_t o_zs = take((size_t)n * dim * 4);
   void *base = nullptr;
   if (hipMallocAsync(&base, off, stream) != hipSuccess) {
@@ -291,6 +341,7 @@ extern "C" int gnn_frnn(const float *z, int64_t n_nodes, int32_t dim, float r2,
   a.count = (int32_t *)(b + o_cnt);
   a.offs = (int64_t *)(b + o_offs);
   a.total_dev = (int64_t *)(b + o_total);
+  a.bsum = (int64_t *)(b + o_bsum);
 
   int rc = GNN_OK;
   int64_t total = 0;

@@ -28,10 +28,17 @@ __device__ __forceinline__ int32_t load_parent(const int32_t *parent, int32_t v)
   return __hip_atomic_load(parent + v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ __forceinline__ int32_t find_root(const int32_t *parent, int32_t v) {
+// Path halving on the way: each visited node is pointed at its grandparent
+// with atomicMin, so links only ever decrease (a smaller link written by a
+// concurrent hook is never overwritten) and the chains that concurrent
+// hooks build in a large component stay short.
+__device__ __forceinline__ int32_t find_root(int32_t *parent, int32_t v) {
   int32_t p = load_parent(parent, v);
   while (p != v) {
-    v = p;
+    const int32_t gp = load_parent(parent, p);
+    if (gp == p) return p;
+    if (gp < load_parent(parent, v)) atomicMin(parent + v, gp);
+    v = gp;
     p = load_parent(parent, v);
   }
   return v;
@@ -42,19 +49,29 @@ __global__ void wcc_init(int32_t *__restrict__ parent, int32_t n) {
   if (v < n) parent[v] = (int32_t)v;
 }
 
+// `changed` is raised once per workgroup: one store per joining edge to a
+// single word would serialise on its L2 channel (milliseconds in the first
+// round, when most kept edges join two trees).
 __global__ void wcc_hook(const int32_t *__restrict__ ei, const float *__restrict__ scores,
                          float threshold, int64_t n_edges, int32_t n_nodes, int32_t *parent,
                          int32_t *__restrict__ changed) {
+  __shared__ int32_t joined;
+  if (threadIdx.x == 0) joined = 0;
+  __syncthreads();
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= n_edges) return;
-  if (scores && !(scores[j] > threshold)) return;
-  const int32_t ru = find_root(parent, clampi(ei[j], n_nodes));
-  const int32_t rv = find_root(parent, clampi(ei[n_edges + j], n_nodes));
-  if (ru != rv) {
-    const int32_t hi = ru > rv ? ru : rv, lo = ru > rv ? rv : ru;
-    atomicMin(&parent[hi], lo);
-    *changed = 1;  // every writer stores the same value
+  if (j < n_edges && (!scores || scores[j] > threshold)) {
+    const int32_t ru = find_root(parent, clampi(ei[j], n_nodes));
+    const int32_t rv = find_root(parent, clampi(ei[n_edges + j], n_nodes));
+    if (ru != rv) {
+      const int32_t hi = ru > rv ? ru : rv, lo = ru > rv ? rv : ru;
+      // Many edges join the same pair of large trees: the atomic is issued
+      // only when it would lower the link, so a root is not a hot spot.
+      if (lo < load_parent(parent, hi)) atomicMin(&parent[hi], lo);
+      joined = 1;  // every writer stores the same value
+    }
   }
+  __syncthreads();
+  if (threadIdx.x == 0 && joined) *changed = 1;
 }
 
 __global__ void wcc_compress(int32_t *parent, int32_t n) {
