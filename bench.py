@@ -61,9 +61,9 @@ def edge_update_bytes(N, E, H, s=4, n_src=0):
     """Algorithmic HBM bytes of one regrouped edge-update launch, gathered
     rows counted per edge: e read and written (s bytes per element), the
     P[src][0:H] and P[dst][H:2H] half-rows (fp32) and both indices; with the
-    fused out-sums (n_src > 0), one fp32 agg_out row per node that has
-    out-edges."""
-    return E * (2 * H * s + 2 * H * 4 + 8) + n_src * H * 4
+    fused out-sums (n_src > 0), one agg_out row (s bytes per element) per
+    node that has out-edges."""
+    return E * (2 * H * s + 2 * H * 4 + 8) + n_src * H * s
 
 
 def node_update_bytes(N, H, s=4):
@@ -89,7 +89,7 @@ def aggregate_bytes(N, E, H, act_bytes, n_src=0):
     arrays, and a zero agg_out row per node without out-edges."""
     if n_src:
         return (E * H * act_bytes + N * H * act_bytes + E * 4 + 2.0 * (N + 1) * 4
-                + (N - n_src) * H * 4)
+                + (N - n_src) * H * act_bytes)
     return 2.0 * E * H * act_bytes + 2.0 * N * H * act_bytes + 2.0 * E * 4 + 2.0 * (N + 1) * 4
 
 
@@ -224,9 +224,9 @@ def main():
     eu = prof["edge_update"]
     eu_ms = eu["ms"] / max(eu["launches"], 1)
     eu_flops = edge_update_flops(E, H, factored)
-    # the split fp32 kernels sum the edge rows per source inside the edge
-    # update (rows kept in source order)
-    fused = split and not bf16
+    # the split kernels (fp32 and bf16) sum the edge rows per source inside
+    # the edge update (rows kept in source order)
+    fused = split
     n_src = int(np.unique(g.edge_index[0]).size) if fused else 0
     ag = prof["aggregate"]
     ag_ms = ag["ms"] / max(ag["launches"], 1)
@@ -245,8 +245,9 @@ def main():
         mf = split_mfma_flops(N, E, H, bf16)
         eu_mfma = mf["edge_update"] / (eu_ms / 1000.0) / 1e12
         mdt = "bf16" if bf16 else "fp16"
-        roof = {"kernel": ("edge_split<4,1,bf16> (gathers node projections, W_e e, layer 2; "
-                           "hi/lo bf16 weights in LDS)") if bf16 else
+        roof = {"kernel": ("edge_split<4,3,bf16> (gathers node projections, W_e e, layer 2 "
+                           "transposed, per-source sums of its rows; hi/lo bf16 weights in "
+                           "LDS)") if bf16 else
                           ("edge_split<4,3> (gathers node projections, W_e e, layer 2 "
                            "transposed, per-source sums of its rows; f16x2 weights in LDS)"),
                 "bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",

@@ -186,6 +186,63 @@ __global__ __launch_bounds__(THREADS) void segsum_fused_f32(
   *(f4 *)(agg_out + v * H + 4 * sub) = f4{s[0] + c[0], s[1] + c[1], s[2] + c[2], s[3] + c[3]};
 }
 
+// The same for bf16 rows and aggregates (H/8 lanes per node, 8 features
+// each); the pieces are fp32, the sums fp32, the stored aggregates bf16.
+template <int H>
+__global__ __launch_bounds__(THREADS) void segsum_fused_bf16(
+    const __bf16 *__restrict__ e, const int32_t *__restrict__ rp_in,
+    const int32_t *__restrict__ perm_in, const int32_t *__restrict__ rp_out,
+    const float *__restrict__ part, __bf16 *__restrict__ agg_in, __bf16 *__restrict__ agg_out,
+    int32_t n_nodes) {
+  constexpr int LPR = H / 8;
+  constexpr int TPB = THREADS / LPR;
+  const int sub = threadIdx.x % LPR;
+  const int64_t v = (int64_t)blockIdx.x * TPB + threadIdx.x / LPR;
+  if (v >= n_nodes) return;
+  const int32_t a = rp_out[v], b = rp_out[v + 1];
+  {
+    float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    float c[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    row_sum_bf16<H>(e + 8 * sub, perm_in, rp_in[v], rp_in[v + 1], s, c);
+    bf8 o;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) o[k] = (__bf16)(s[k] + c[k]);
+    *(bf8 *)(agg_in + v * H + 8 * sub) = o;
+  }
+  const int32_t u0 = a >> 5, u1 = (b - 1) >> 5;
+  if (a < b && u0 == u1) return;  // written by the edge update
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float c[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (a < b) {
+    const float *pc = part + 8 * sub;
+    auto piece = [&](int64_t slot, float (&r)[8]) {
+      const f4 lo = *(const f4 *)(pc + slot * H), hi = *(const f4 *)(pc + slot * H + 4);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        r[k] = lo[k];
+        r[4 + k] = hi[k];
+      }
+    };
+    piece(2 * (int64_t)u0 + 1, s);
+    const bool comp = u1 - u0 > LONG_ROW;
+    for (int32_t u = u0 + 1; u <= u1; ++u) {
+      float r[8];
+      piece(2 * (int64_t)u, r);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        if (comp)
+          nsum<true>(s[k], c[k], r[k]);
+        else
+          s[k] += r[k];
+      }
+    }
+  }
+  bf8 o;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) o[k] = (__bf16)(s[k] + c[k]);
+  *(bf8 *)(agg_out + v * H + 8 * sub) = o;
+}
+
 template <int H>
 __global__ __launch_bounds__(THREADS) void segsum_bf16(
     const __bf16 *__restrict__ e, const int32_t *__restrict__ rp_in,
@@ -235,27 +292,33 @@ hipError_t launch_h(Act act, const void *e, const int32_t *rp_in, const int32_t 
 }
 
 template <int H>
-hipError_t launch_fused_h(const float *e, const int32_t *rp_in, const int32_t *perm_in,
-                          const int32_t *rp_out, const float *part, float *agg_in,
-                          float *agg_out, int32_t n_nodes, hipStream_t stream) {
-  constexpr int tpb = THREADS / (H / 4);
+hipError_t launch_fused_h(Act act, const void *e, const int32_t *rp_in, const int32_t *perm_in,
+                          const int32_t *rp_out, const float *part, void *agg_in, void *agg_out,
+                          int32_t n_nodes, hipStream_t stream) {
+  const int tpb = THREADS / (act == Act::F32 ? H / 4 : H / 8);
   const int64_t tasks = n_nodes;
   const unsigned blocks = (unsigned)((tasks + tpb - 1) / tpb);
   if (blocks == 0) return hipSuccess;
-  segsum_fused_f32<H><<<blocks, THREADS, 0, stream>>>(e, rp_in, perm_in, rp_out, part, agg_in,
-                                                      agg_out, n_nodes);
+  if (act == Act::F32)
+    segsum_fused_f32<H><<<blocks, THREADS, 0, stream>>>((const float *)e, rp_in, perm_in, rp_out,
+                                                        part, (float *)agg_in, (float *)agg_out,
+                                                        n_nodes);
+  else
+    segsum_fused_bf16<H><<<blocks, THREADS, 0, stream>>>((const __bf16 *)e, rp_in, perm_in,
+                                                         rp_out, part, (__bf16 *)agg_in,
+                                                         (__bf16 *)agg_out, n_nodes);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_segsum_fused(int hidden, const float *e, const int32_t *rp_in,
+hipError_t launch_segsum_fused(Act act, int hidden, const void *e, const int32_t *rp_in,
                                const int32_t *perm_in, const int32_t *rp_out,
-                               const float *agg_part, float *agg_in, float *agg_out,
+                               const float *agg_part, void *agg_in, void *agg_out,
                                int32_t n_nodes, hipStream_t stream) {
   switch (hidden) {
-    case 64: return launch_fused_h<64>(e, rp_in, perm_in, rp_out, agg_part, agg_in, agg_out, n_nodes, stream);
-    case 128: return launch_fused_h<128>(e, rp_in, perm_in, rp_out, agg_part, agg_in, agg_out, n_nodes, stream);
+    case 64: return launch_fused_h<64>(act, e, rp_in, perm_in, rp_out, agg_part, agg_in, agg_out, n_nodes, stream);
+    case 128: return launch_fused_h<128>(act, e, rp_in, perm_in, rp_out, agg_part, agg_in, agg_out, n_nodes, stream);
   }
   return hipErrorInvalidValue;
 }

@@ -530,8 +530,8 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
   total.begin();
 
   const bool fac = hd->factored;
-  // the edge update sums its rows per source itself (split fp32 kernels)
-  const bool fused = fac && hd->fd.split && !hd->fd.bf16;
+  // the edge update sums its rows per source itself (split kernels)
+  const bool fused = fac && hd->fd.split;
   w.bytes = plan_workspace(w, N, E, H, ab, fac, fused);
   {
     hipError_t ae = hipMallocAsync(&w.base, w.bytes, stream);
@@ -641,7 +641,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
         ea.s2 = fd.s2_em[k];
       }
       if (fused) {
-        ea.agg_out = (float *)w.aout;
+        ea.agg_out = w.aout;
         ea.agg_part = w.part;
       }
       st.begin();
@@ -649,8 +649,8 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       st.end(GNN_STAGE_EDGE_UPDATE);
       st.begin();
       if (fused)
-        HIP_TRY(launch_segsum_fused(H, (const float *)w.e, w.rp_in, w.q_in, w.rp_out, w.part,
-                                    (float *)w.ain, (float *)w.aout, n, stream));
+        HIP_TRY(launch_segsum_fused(act, H, w.e, w.rp_in, w.q_in, w.rp_out, w.part, w.ain,
+                                    w.aout, n, stream));
       else  // source-order rows: the out-CSR is the identity
         HIP_TRY(launch_segsum(act, H, w.e, w.rp_in, w.q_in, w.rp_out, nullptr, w.ain, w.aout,
                               n, stream));
@@ -1079,7 +1079,7 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
       fd.enc_chunks = node_split_chunks(true, H, 2, bf16);
       fd.upd_chunks = node_split_chunks(false, H, 1, bf16);
       fd.grid_enc = edge_split_grid(EdgeMode::Enc, H, bf16, n_cu);
-      fd.grid_upd = edge_split_grid(bf16 ? EdgeMode::Upd : EdgeMode::UpdAgg, H, bf16, n_cu);
+      fd.grid_upd = edge_split_grid(EdgeMode::UpdAgg, H, bf16, n_cu);
       fd.grid_cls = edge_split_grid(EdgeMode::Cls, H, bf16, n_cu);
     } else {
       const int kg = H / 8;  // k-groups of one H-wide operand; 8 per chunk

@@ -75,8 +75,8 @@ struct NodeArgs {
 };
 
 // UpdAgg: the edge update that also sums its output rows per source node
-// (split fp32 kernels only).  It needs the rows in source order: every run
-// of equal src_idx is one node's complete out-edge list.
+// (split kernels, fp32 or bf16 rows).  It needs the rows in source order:
+// every run of equal src_idx is one node's complete out-edge list.
 enum class EdgeMode : int { Enc = 0, Upd = 1, Cls = 2, UpdAgg = 3 };
 
 struct EdgeArgs {
@@ -97,11 +97,12 @@ struct EdgeArgs {
   // stored P rows) and of W2
   float s1 = 1.f, s2 = 1.f;
   // UpdAgg: the sum of every run of rows with one source node that lies
-  // inside one 32-row unit goes to agg_out[src]; a run cut by a unit
-  // boundary leaves its piece in agg_part[unit][0] (the unit's first run,
-  // continued from the previous unit) or agg_part[unit][1] (its last run,
-  // continued in the next), H floats each, for launch_segsum_fused.
-  float *agg_out = nullptr, *agg_part = nullptr;
+  // inside one 32-row unit goes to agg_out[src] (row type); a run cut by a
+  // unit boundary leaves its piece in agg_part[unit][0] (the unit's first
+  // run, continued from the previous unit) or agg_part[unit][1] (its last
+  // run, continued in the next), H fp32 each, for launch_segsum_fused.
+  void *agg_out = nullptr;
+  float *agg_part = nullptr;
 };
 
 hipError_t launch_node_f32(bool enc, int hidden, const NodeArgs &a, int grid,
@@ -131,14 +132,14 @@ int edge_split_grid(EdgeMode mode, int hidden, bool bf16, int n_cu);
 hipError_t launch_segsum(Act act, int hidden, const void *e, const int32_t *rp_in,
                          const int32_t *perm_in, const int32_t *rp_out, const int32_t *perm_out,
                          void *agg_in, void *agg_out, int32_t n_nodes, hipStream_t stream);
-// fp32 rows in source order after an UpdAgg edge update: agg_in as above;
+// Rows in source order after an UpdAgg edge update: agg_in as above;
 // agg_out[v] is completed for the nodes whose out-edge positions
-// [rp_out[v], rp_out[v+1]) span several 32-row units (sum of the unit
+// [rp_out[v], rp_out[v+1]) span several 32-row units (sum of the fp32 unit
 // pieces in agg_part, in unit order) and zeroed for nodes without out-edges;
 // the edge update wrote every other row.
-hipError_t launch_segsum_fused(int hidden, const float *e, const int32_t *rp_in,
+hipError_t launch_segsum_fused(Act act, int hidden, const void *e, const int32_t *rp_in,
                                const int32_t *perm_in, const int32_t *rp_out,
-                               const float *agg_part, float *agg_in, float *agg_out,
+                               const float *agg_part, void *agg_in, void *agg_out,
                                int32_t n_nodes, hipStream_t stream);
 
 // Stable CSRs of edge_index ([2][n_edges] int32, indices clamped into

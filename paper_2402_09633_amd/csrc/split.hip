@@ -193,6 +193,21 @@ __device__ __forceinline__ void step_hl(f16v (&acc)[MB], const bf8 *rec, const b
   for (int mb = 0; mb < MB; ++mb) acc[mb] = mma_b(w2[mb], x, acc[mb]);
 }
 
+// step_hl with the operands exchanged (transposed accumulators, as step_ht).
+template <int MB>
+__device__ __forceinline__ void step_hlt(f16v (&acc)[MB], const bf8 *rec, const bf8 &x) {
+  bf8 w1[MB], w2[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    w1[mb] = rec[(2 * mb) * 64];
+    w2[mb] = rec[(2 * mb + 1) * 64];
+  }
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = mma_b(x, w1[mb], acc[mb]);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = mma_b(x, w2[mb], acc[mb]);
+}
+
 __device__ __forceinline__ bf8 to_bf16(const f8 &x) { return __builtin_convertvector(x, bf8); }
 
 // Operand precision of the kernels below.
@@ -502,10 +517,9 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
   constexpr bool HAS_E = MODE != (int)EdgeMode::Enc;
   constexpr bool HAS_L2 = MODE != (int)EdgeMode::Cls;
   constexpr bool FUSE = MODE == (int)EdgeMode::UpdAgg;
-  // Layer 2 transposed (step_ht) with full-line e stores: the fused update
-  // and the fp32 encoder
-  constexpr bool TRANS = FUSE || (MODE == (int)EdgeMode::Enc && PREC == SPLIT);
-  static_assert(!FUSE || PREC == SPLIT, "fused sums: fp32 rows only");
+  // Layer 2 transposed (step_ht / step_hlt) with row-contiguous e stores:
+  // the fused update and the encoder
+  constexpr bool TRANS = FUSE || MODE == (int)EdgeMode::Enc;
   __shared__ h8 lds[(HAS_E ? NR : 0) + (HAS_L2 ? NR : 0)];
   __shared__ float prm[6 * H];  // s1 b1, gamma1, beta1, s2 b2, gamma2, beta2
   h8 *lw_e = lds;
@@ -636,8 +650,20 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
       f16v t2[MB];
       zero<MB>(t2);
 #pragma unroll
-      for (int g = 0; g < G; ++g) step_ht<MB>(t2, lw_2 + g * 2 * MB * 64 + lane, acc_x<MB>(acc, g));
+      for (int g = 0; g < G; ++g) {
+        if constexpr (PREC == SPLIT)
+          step_ht<MB>(t2, lw_2 + g * 2 * MB * 64 + lane, acc_x<MB>(acc, g));
+        else
+          step_hlt<MB>(t2, (const bf8 *)(lw_2 + g * 2 * MB * 64 + lane), to_bf16(acc_x<MB>(acc, g)));
+      }
       ln_relu_t<MB>(t2, prm + 3 * H, eps2, n);
+      if constexpr (PREC == BF16) {
+        // the stored rows are the bf16 values; the sums add exactly those
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) t2[mb][v] = (float)(__bf16)t2[mb][v];
+      }
       // Bit e of `ends` marks the last row of a run of equal sources
       // (within the unit's valid rows); hc: the unit's first run began in
       // the previous unit; tc: its last run continues in the next one.  All
@@ -654,19 +680,22 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
         cur_src = nsrc;
         if (u + nw < units) load_idx(u + nw);
       }
-      // e rows: each store writes 128 contiguous bytes of a row per half-wave
-      float *eo = a.e_out + (u * 32 + 4 * hh) * H + n;
+      // e rows: each store writes 32 contiguous elements of a row per
+      // half-wave (128 bytes fp32, 64 bytes bf16)
+      act_t *eo = (act_t *)a.e_out + (u * 32 + 4 * hh) * H + n;
       if (nvalid == 32) {
 #pragma unroll
         for (int v = 0; v < 16; ++v)
 #pragma unroll
-          for (int mb = 0; mb < MB; ++mb) eo[(8 * (v / 4) + v % 4) * H + 32 * mb] = t2[mb][v];
+          for (int mb = 0; mb < MB; ++mb)
+            eo[(8 * (v / 4) + v % 4) * H + 32 * mb] = (act_t)t2[mb][v];
       } else {
 #pragma unroll
         for (int v = 0; v < 16; ++v)
           if (8 * (v / 4) + 4 * hh + v % 4 < nvalid)
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb) eo[(8 * (v / 4) + v % 4) * H + 32 * mb] = t2[mb][v];
+            for (int mb = 0; mb < MB; ++mb)
+              eo[(8 * (v / 4) + v % 4) * H + 32 * mb] = (act_t)t2[mb][v];
       }
       if constexpr (FUSE) {
       // Exchange halves: afterwards lane l holds block b = p + hh MB/2 of
@@ -697,18 +726,18 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
         if (ends & (1u << e)) {
           const bool first = (ends & ((1u << e) - 1u)) == 0u;
           const bool last = (ends >> e) == 1u;
-          float *dst;
-          if (first && hc)
-            dst = a.agg_part + (u * 2) * H;
-          else if (last && tc)
-            dst = a.agg_part + (u * 2 + 1) * H;
-          else
-            dst = a.agg_out + (int64_t)__builtin_amdgcn_readlane(cur_src, e) * H;
+          // pieces stay fp32; a complete run is stored in the row type
+          if ((first && hc) || (last && tc)) {
+            float *dst = a.agg_part + (u * 2 + (first && hc ? 0 : 1)) * H;
 #pragma unroll
-          for (int p = 0; p < MB / 2; ++p) {
-            dst[32 * (p + hh * (MB / 2)) + n] = sum[p];
-            sum[p] = 0.f;
+            for (int p = 0; p < MB / 2; ++p) dst[32 * (p + hh * (MB / 2)) + n] = sum[p];
+          } else {
+            act_t *dst = (act_t *)a.agg_out + (int64_t)__builtin_amdgcn_readlane(cur_src, e) * H;
+#pragma unroll
+            for (int p = 0; p < MB / 2; ++p) dst[32 * (p + hh * (MB / 2)) + n] = (act_t)sum[p];
           }
+#pragma unroll
+          for (int p = 0; p < MB / 2; ++p) sum[p] = 0.f;
         }
       }
       if (u + nw < units) load_e(row_of(u + nw));
@@ -761,9 +790,8 @@ hipError_t edge_h(EdgeMode mode, const EdgeArgs &a, int grid, hipStream_t stream
     case EdgeMode::Upd: edge_split<MB, 1, PREC><<<nb, 64 * SW, 0, stream>>>(a); break;
     case EdgeMode::Cls: edge_split<MB, 2, PREC><<<nb, 64 * SW, 0, stream>>>(a); break;
     case EdgeMode::UpdAgg:
-      if constexpr (PREC != SPLIT) return hipErrorInvalidValue;
       if (!a.agg_out || !a.agg_part) return hipErrorInvalidValue;
-      edge_split<MB, 3, SPLIT><<<nb, 64 * SW, 0, stream>>>(a);
+      edge_split<MB, 3, PREC><<<nb, 64 * SW, 0, stream>>>(a);
       break;
   }
   return hipGetLastError();
@@ -775,9 +803,7 @@ const void *edge_fn_mb(EdgeMode mode) {
     case EdgeMode::Enc: return (const void *)edge_split<MB, 0, PREC>;
     case EdgeMode::Upd: return (const void *)edge_split<MB, 1, PREC>;
     case EdgeMode::Cls: return (const void *)edge_split<MB, 2, PREC>;
-    case EdgeMode::UpdAgg:
-      if constexpr (PREC == SPLIT) return (const void *)edge_split<MB, 3, SPLIT>;
-      break;
+    case EdgeMode::UpdAgg: return (const void *)edge_split<MB, 3, PREC>;
   }
   return (const void *)edge_split<MB, 1, PREC>;
 }

@@ -37,7 +37,7 @@ __device__ __forceinline__ int32_t find_root(int32_t *parent, int32_t v) {
   while (p != v) {
     const int32_t gp = load_parent(parent, p);
     if (gp == p) return p;
-    if (gp < load_parent(parent, v)) atomicMin(parent + v, gp);
+    if (gp < load_parent(parent, v)) atomicMin(&parent[v], gp);
     v = gp;
     p = load_parent(parent, v);
   }

@@ -212,13 +212,14 @@ def test_constant_messages_aggregate_to_degrees_full_scale(G, dtype):
         G.gnn_destroy(h)
 
 
-@pytest.mark.parametrize("flags", PATHS)
+@pytest.mark.parametrize("dtype,flags", [(0, f) for f in PATHS] + [(1, f) for f in BF16_PATHS])
 @pytest.mark.parametrize("H", [64, 128])
-def test_out_sums_every_run_offset_exact(G, flags, H):
+def test_out_sums_every_run_offset_exact(G, dtype, flags, H):
     # Out-degrees 0..129 and random ones, with nodes without out-edges in
     # between and the edge list in a random order: in source order the runs
     # of one node start and end at every offset of a 32-row unit and span up
-    # to five units.  With constant messages the sums are exact degrees.
+    # to five units.  With constant messages the sums are exact degrees
+    # (in bf16 too: every degree here is below 256).
     rng = np.random.default_rng(77)
     degs = np.concatenate([np.arange(130), rng.integers(0, 40, 400), np.zeros(50, np.int64)])
     rng.shuffle(degs)
@@ -233,7 +234,7 @@ def test_out_sums_every_run_offset_exact(G, flags, H):
     v = I.blob_views(w, 3, H, 1)
     v["edge_mlp0.1.W"][:] = 0.0
     v["edge_mlp0.1.beta"][:] = 1.0
-    h = G.gnn_create(w, G.make_dims(3, H, 2, flags=flags))
+    h = G.gnn_create(w, G.make_dims(3, H, 2, dtype=dtype, flags=flags))
     try:
         ain = torch.zeros(N, H, device="cuda")
         aout = torch.zeros(N, H, device="cuda")
