@@ -372,14 +372,37 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
 
   const float eps2 = a.eps * a.s2 * a.s2;
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
-  const int64_t tiles = (a.n_rows + 32 * SW - 1) / (32 * SW);
-  for (int64_t tile = blk; tile < tiles; tile += gridDim.x) {
+  // Rounds of one 32-row unit per wave: K full rounds of SW units per
+  // workgroup, then the remaining units spread over all workgroups (unit j
+  // to workgroup j % grid, wave j / grid), so that the last round is not
+  // carried by a few workgroups only.  A wave without a unit in the last
+  // round keeps streaming the weights (barriers) and does nothing else.
+  const int64_t G_ = gridDim.x;
+  const int64_t full = 32 * SW * G_;
+  const int64_t K = a.n_rows / full;
+  const int64_t rem_units = (a.n_rows - K * full + 31) / 32;
+  const int64_t rounds = K + (blk < rem_units ? 1 : 0);
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  for (int64_t rd = 0; rd < rounds; ++rd) {
     // Keeps loop-invariant loads inside the loop (hoisted, they would stay
     // in registers for the whole kernel).
     asm volatile("" ::: "memory");
-    const int64_t row = tile * 32 * SW + wave * 32 + n;
-    const bool valid = row < a.n_rows;
-    const int64_t r = valid ? row : a.n_rows - 1;
+    const int64_t unit = rd < K ? (rd * G_ + blk) * SW + wv : K * full / 32 + wv * G_ + blk;
+    const bool active = rd < K || wv * G_ + blk < rem_units;
+    const int64_t wrow0 = unit * 32;  // the wave's first row (wave-uniform)
+    const int nvalid = !active ? 0 : (int)(a.n_rows - wrow0 < 32 ? a.n_rows - wrow0 : 32);
+    const int64_t row = wrow0 + n;
+    const bool valid = n < nvalid;
+    const int64_t r = valid ? row : (nvalid > 0 ? wrow0 + nvalid - 1 : 0);
+    if (!active) {
+      // one tile's worth of the weight stream: same barriers, same share
+      // of every chunk fetch
+      for (int c = 0; c < a.nchunks; ++c) {
+        (void)ws.begin(tid);
+        ws.end(tid);
+      }
+      continue;
+    }
 
     f16v acc[MB];
     if constexpr (ENC) {
@@ -395,7 +418,7 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
       // shared by the three sources: 64-bit per-lane pointers cost the
       // registers that the look-ahead needs (a spill reload would wait for
       // every load in flight).
-      const int64_t t0 = tile * 32 * SW;
+      const int64_t t0 = wrow0;
       const uint32_t roff = (uint32_t)((r - t0) * H + 8 * hh) * (uint32_t)sizeof(act_t);
       const act_t *const *srcs = (const act_t *const *)a.src;
       using xrec_t = typename std::conditional<PREC == SPLIT, f8, bf8>::type;
@@ -470,8 +493,6 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
       rec_done(g);
     }
     ln_relu_lds<MB>(hv, prm + 3 * H, eps2, hh);
-    const int64_t wrow0 = tile * 32 * SW + wave * 32;
-    const int nvalid = (int)(a.n_rows - wrow0 < 32 ? a.n_rows - wrow0 : 32);
     if (a.h_out) {
       if constexpr (PREC == SPLIT)
         store_block<MB>(a.h_out + wrow0 * H, H, nvalid, hv, stg, lane);
