@@ -270,10 +270,13 @@ struct gnn_handle {
   std::vector<MlpDev> edge_mlp, node_mlp;
   FactDev fd;
   // profiling: recorded (stage, start, end) event pairs not yet read, the
-  // running totals and a pool of reusable events
+  // running totals and a pool of reusable events.  Consecutive stages share
+  // the event between them (the mark of the later stage does not own its
+  // start event).
   struct Mark {
     int stage;
     hipEvent_t a, b;
+    bool own_a;
   };
   std::mutex prof_mu;
   bool prof_on = false;
@@ -468,12 +471,17 @@ int check_counts(gnn_handle *h, int64_t N, int64_t E) {
     }                                                                                \
   } while (0)
 
-// Brackets stage launches with events when profiling is on.
+// Brackets stage launches with events when profiling is on.  A stage that
+// begins right where the previous one ended starts at that stage's end
+// event, so a call records one event per stage boundary (each record costs
+// the stream a few microseconds).
 struct StageTimer {
   gnn_handle *h;
   hipStream_t s;
   bool on;
-  hipEvent_t a = nullptr;
+  hipEvent_t a = nullptr;     // start of the open stage
+  bool own_a = false;
+  hipEvent_t last = nullptr;  // end of the previous stage
   StageTimer(gnn_handle *h_, hipStream_t s_, bool count_call) : h(h_), s(s_) {
     std::lock_guard<std::mutex> lk(h->prof_mu);
     on = h->prof_on;
@@ -490,18 +498,33 @@ struct StageTimer {
     }
     return e;
   }
+  void put(hipEvent_t e) {
+    std::lock_guard<std::mutex> lk(h->prof_mu);
+    h->prof_free.push_back(e);
+  }
   void begin() {
     if (!on) return;
+    if (last) {
+      a = last;
+      own_a = false;
+      return;
+    }
     a = get();
+    own_a = true;
     if (a) (void)hipEventRecord(a, s);
   }
   void end(int stage) {
     if (!on || !a) return;
     hipEvent_t b = get();
-    if (!b) return;
+    if (!b) {
+      if (own_a) put(a);
+      a = last = nullptr;
+      return;
+    }
     (void)hipEventRecord(b, s);
     std::lock_guard<std::mutex> lk(h->prof_mu);
-    h->prof_pending.push_back({stage, a, b});
+    h->prof_pending.push_back({stage, a, b, own_a});
+    last = b;
     a = nullptr;
   }
 };
@@ -1101,7 +1124,7 @@ void gnn_destroy(gnn_handle *h) {
     (void)hipDeviceSynchronize();
     (void)hipFree(h->dev_weights);
     for (auto &mk : h->prof_pending) {
-      (void)hipEventDestroy(mk.a);
+      if (mk.own_a) (void)hipEventDestroy(mk.a);
       (void)hipEventDestroy(mk.b);
     }
     for (auto e : h->prof_free) (void)hipEventDestroy(e);
@@ -1118,6 +1141,15 @@ int gnn_profile_enable(gnn_handle *h, int enable) {
   std::lock_guard<std::mutex> lk(h->prof_mu);
   h->prof_on = enable != 0;
   h->prof_calls = 0;
+  // events for about 64 calls, so that none is created while timing
+  if (h->prof_on) {
+    DeviceGuard guard(h->device);
+    while (h->prof_free.size() < 2048) {
+      hipEvent_t e = nullptr;
+      if (hipEventCreate(&e) != hipSuccess) break;
+      h->prof_free.push_back(e);
+    }
+  }
   for (int i = 0; i < GNN_N_STAGES; ++i) {
     h->prof_launches[i] = 0;
     h->prof_ms[i] = 0.0;
@@ -1150,7 +1182,7 @@ int gnn_profile_read(gnn_handle *h, gnn_profile_stats *out) {
   }
   std::lock_guard<std::mutex> lk(h->prof_mu);
   for (auto &mk : marks) {
-    h->prof_free.push_back(mk.a);
+    if (mk.own_a) h->prof_free.push_back(mk.a);
     h->prof_free.push_back(mk.b);
   }
   for (int i = 0; i < GNN_N_STAGES; ++i) {
