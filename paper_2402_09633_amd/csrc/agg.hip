@@ -7,8 +7,11 @@
 // slice of every message row: each message row is read as one contiguous,
 // fully coalesced 256/512-byte chunk, sums run in a fixed order (bitwise
 // reproducible, no float atomics), and empty rows are written as zeros.
-// Four rows are loaded before they are added to keep several HBM requests
-// in flight per lane.  Accumulation is fp32 in both storage modes.  Rows
+// The row ids of a task come in with one load and four rows are requested
+// before any is added, so a typical node (a few messages) costs three
+// dependent round trips: row bounds, row ids, rows.  The gather of 512-byte
+// rows at scattered positions is bound by HBM at a lower rate than a
+// streaming read.  Accumulation is fp32 in both storage modes.  Rows
 // longer than LONG_ROW messages use Neumaier's compensated summation: a hub
 // node can receive 10^5 messages, where a plain fp32 running sum drifts by
 // ~10^-4 relative, while the compensated sum stays within a few ulps of the
@@ -37,79 +40,105 @@ __device__ __forceinline__ void nsum(float &s, float &c, float x) {
   }
 }
 
-// Message row of CSR position p: perm[p], or p itself for a null perm
-// (rows already in CSR order).
-template <bool IDX>
-__device__ __forceinline__ int64_t msg_row(const int32_t *__restrict__ perm, int32_t p) {
-  if constexpr (IDX)
-    return perm[p];
-  else
-    return p;
+// Value of x held by lane j of the calling lane's G-lane group (G divides 64).
+template <int G>
+__device__ __forceinline__ int32_t group_lane(int32_t x, int j) {
+  const int src = ((int)threadIdx.x & 63 & ~(G - 1)) + j;
+  return __builtin_amdgcn_ds_bpermute(src << 2, x);
 }
 
-template <int H, bool COMP, bool IDX>
+// Sum of the message rows at CSR positions [p, pe) into (s, c), G lanes per
+// row, each lane one 16-byte slice.  The row ids of up to G positions are
+// fetched with one coalesced load (lane i holds position p + i) and handed
+// round the group, then B rows are requested before any of them is added,
+// so a node's whole row list is in flight after two round trips rather than
+// one pair of dependent loads per message.  Rows are added in ascending
+// position whatever B is.  A null perm means row id = position.
+template <int H, int B, bool COMP, bool IDX>
 __device__ __forceinline__ void row_sum_f32(const float *__restrict__ base,
                                             const int32_t *__restrict__ perm, int32_t p,
-                                            int32_t pe, float (&s)[4], float (&c)[4]) {
-  for (; p + 4 <= pe; p += 4) {
-    f4 r[4];
+                                            int32_t pe, int sub, float (&s)[4], float (&c)[4]) {
+  constexpr int G = H / 4;
+  static_assert(G % B == 0, "batch must divide the group");
+  for (; p < pe; p += G) {
+    const int n = min(G, pe - p);
+    int32_t my = 0;
+    if constexpr (IDX) my = perm[p + min(sub, n - 1)];
+    for (int j = 0; j < n; j += B) {
+      // Every load is issued (positions past the end repeat the last row, a
+      // cache hit), so the waits before the adds count loads exactly.
+      f4 r[B];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) r[u] = *(const f4 *)(base + msg_row<IDX>(perm, p + u) * H);
+      for (int u = 0; u < B; ++u) {
+        int64_t q;
+        if constexpr (IDX)
+          q = group_lane<G>(my, min(j + u, n - 1));
+        else
+          q = p + min(j + u, n - 1);
+        r[u] = *(const f4 *)(base + q * H);
+      }
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < B; ++u)
+        if (j + u < n)
 #pragma unroll
-      for (int k = 0; k < 4; ++k) nsum<COMP>(s[k], c[k], r[u][k]);
-  }
-  for (; p < pe; ++p) {
-    const f4 r = *(const f4 *)(base + msg_row<IDX>(perm, p) * H);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) nsum<COMP>(s[k], c[k], r[k]);
+          for (int k = 0; k < 4; ++k) nsum<COMP>(s[k], c[k], r[u][k]);
+    }
   }
 }
 
-template <int H, bool COMP, bool IDX>
+template <int H, int B, bool COMP, bool IDX>
 __device__ __forceinline__ void row_sum_bf16(const __bf16 *__restrict__ base,
                                              const int32_t *__restrict__ perm, int32_t p,
-                                             int32_t pe, float (&s)[8], float (&c)[8]) {
-  for (; p + 4 <= pe; p += 4) {
-    bf8 r[4];
+                                             int32_t pe, int sub, float (&s)[8], float (&c)[8]) {
+  constexpr int G = H / 8;
+  static_assert(G % B == 0, "batch must divide the group");
+  for (; p < pe; p += G) {
+    const int n = min(G, pe - p);
+    int32_t my = 0;
+    if constexpr (IDX) my = perm[p + min(sub, n - 1)];
+    for (int j = 0; j < n; j += B) {
+      bf8 r[B];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) r[u] = *(const bf8 *)(base + msg_row<IDX>(perm, p + u) * H);
+      for (int u = 0; u < B; ++u) {
+        int64_t q;
+        if constexpr (IDX)
+          q = group_lane<G>(my, min(j + u, n - 1));
+        else
+          q = p + min(j + u, n - 1);
+        r[u] = *(const bf8 *)(base + q * H);
+      }
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < B; ++u)
+        if (j + u < n)
 #pragma unroll
-      for (int k = 0; k < 8; ++k) nsum<COMP>(s[k], c[k], (float)r[u][k]);
-  }
-  for (; p < pe; ++p) {
-    const bf8 r = *(const bf8 *)(base + msg_row<IDX>(perm, p) * H);
-#pragma unroll
-    for (int k = 0; k < 8; ++k) nsum<COMP>(s[k], c[k], (float)r[k]);
+          for (int k = 0; k < 8; ++k) nsum<COMP>(s[k], c[k], (float)r[u][k]);
+    }
   }
 }
 
-template <int H>
+template <int H, int B = 4>
 __device__ __forceinline__ void row_sum_f32(const float *base, const int32_t *perm, int32_t p,
-                                            int32_t pe, float (&s)[4], float (&c)[4]) {
+                                            int32_t pe, int sub, float (&s)[4], float (&c)[4]) {
   const bool comp = pe - p > LONG_ROW;
   if (perm) {
-    if (comp) row_sum_f32<H, true, true>(base, perm, p, pe, s, c);
-    else row_sum_f32<H, false, true>(base, perm, p, pe, s, c);
+    if (comp) row_sum_f32<H, B, true, true>(base, perm, p, pe, sub, s, c);
+    else row_sum_f32<H, B, false, true>(base, perm, p, pe, sub, s, c);
   } else {
-    if (comp) row_sum_f32<H, true, false>(base, perm, p, pe, s, c);
-    else row_sum_f32<H, false, false>(base, perm, p, pe, s, c);
+    if (comp) row_sum_f32<H, B, true, false>(base, perm, p, pe, sub, s, c);
+    else row_sum_f32<H, B, false, false>(base, perm, p, pe, sub, s, c);
   }
 }
 
-template <int H>
+template <int H, int B = 4>
 __device__ __forceinline__ void row_sum_bf16(const __bf16 *base, const int32_t *perm, int32_t p,
-                                             int32_t pe, float (&s)[8], float (&c)[8]) {
+                                             int32_t pe, int sub, float (&s)[8], float (&c)[8]) {
   const bool comp = pe - p > LONG_ROW;
   if (perm) {
-    if (comp) row_sum_bf16<H, true, true>(base, perm, p, pe, s, c);
-    else row_sum_bf16<H, false, true>(base, perm, p, pe, s, c);
+    if (comp) row_sum_bf16<H, B, true, true>(base, perm, p, pe, sub, s, c);
+    else row_sum_bf16<H, B, false, true>(base, perm, p, pe, sub, s, c);
   } else {
-    if (comp) row_sum_bf16<H, true, false>(base, perm, p, pe, s, c);
-    else row_sum_bf16<H, false, false>(base, perm, p, pe, s, c);
+    if (comp) row_sum_bf16<H, B, true, false>(base, perm, p, pe, sub, s, c);
+    else row_sum_bf16<H, B, false, false>(base, perm, p, pe, sub, s, c);
   }
 }
 
@@ -133,7 +162,7 @@ __global__ __launch_bounds__(THREADS) void segsum_f32(
   const int32_t pe = rp[v + 1];
   const float *base = e + 4 * sub;
   float s[4] = {0.f, 0.f, 0.f, 0.f}, c[4] = {0.f, 0.f, 0.f, 0.f};
-  row_sum_f32<H>(base, perm, p, pe, s, c);
+  row_sum_f32<H>(base, perm, p, pe, sub, s, c);
   const f4 res = {s[0] + c[0], s[1] + c[1], s[2] + c[2], s[3] + c[3]};
   *(f4 *)(dst + v * H + 4 * sub) = res;
 }
@@ -149,34 +178,46 @@ __global__ __launch_bounds__(THREADS) void segsum_fused_f32(
     const float *__restrict__ e, const int32_t *__restrict__ rp_in,
     const int32_t *__restrict__ perm_in, const int32_t *__restrict__ rp_out,
     const float *__restrict__ part, float *__restrict__ agg_in, float *__restrict__ agg_out,
-    int32_t n_nodes) {
+    int32_t n_nodes, int32_t n_units) {
   constexpr int LPR = H / 4;
   constexpr int TPB = THREADS / LPR;
   const int sub = threadIdx.x % LPR;
   const int64_t v = (int64_t)blockIdx.x * TPB + threadIdx.x / LPR;
   if (v >= n_nodes) return;
   const int32_t a = rp_out[v], b = rp_out[v + 1];
+  const int32_t pi = rp_in[v], pie = rp_in[v + 1];
+  const int32_t u0 = a >> 5, u1 = (b - 1) >> 5;
+  const bool spans = a < b && u1 > u0;
+  // The first two pieces of a run that spans units are requested before the
+  // in-direction rows, so their latency overlaps.
+  const float *pc = part + 4 * sub;
+  // Nodes whose run does not span read a piece of a nearby unit instead
+  // (discarded), so that the loads need no branch.
+  const int32_t w0 = spans ? u0 : min(u0, n_units - 1), w1 = spans ? u0 + 1 : w0;
+  const f4 t0 = *(const f4 *)(pc + (int64_t)(2 * w0 + 1) * H);
+  const f4 t1 = *(const f4 *)(pc + (int64_t)(2 * w1) * H);
   {
     float s[4] = {0.f, 0.f, 0.f, 0.f}, c[4] = {0.f, 0.f, 0.f, 0.f};
-    row_sum_f32<H>(e + 4 * sub, perm_in, rp_in[v], rp_in[v + 1], s, c);
+    row_sum_f32<H>(e + 4 * sub, perm_in, pi, pie, sub, s, c);
     *(f4 *)(agg_in + v * H + 4 * sub) = f4{s[0] + c[0], s[1] + c[1], s[2] + c[2], s[3] + c[3]};
   }
-  const int32_t u0 = a >> 5, u1 = (b - 1) >> 5;
-  if (a < b && u0 == u1) return;  // written by the edge update
+  if (a < b && !spans) return;  // written by the edge update
   float s[4] = {0.f, 0.f, 0.f, 0.f}, c[4] = {0.f, 0.f, 0.f, 0.f};
-  if (a < b) {
-    const float *pc = part + 4 * sub;
-    const f4 t = *(const f4 *)(pc + (int64_t)(2 * u0 + 1) * H);
+  if (spans) {
 #pragma unroll
-    for (int k = 0; k < 4; ++k) s[k] = t[k];
+    for (int k = 0; k < 4; ++k) s[k] = t0[k];
     if (u1 - u0 > LONG_ROW) {
-      for (int32_t u = u0 + 1; u <= u1; ++u) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) nsum<true>(s[k], c[k], t1[k]);
+      for (int32_t u = u0 + 2; u <= u1; ++u) {
         const f4 r = *(const f4 *)(pc + (int64_t)(2 * u) * H);
 #pragma unroll
         for (int k = 0; k < 4; ++k) nsum<true>(s[k], c[k], r[k]);
       }
     } else {
-      for (int32_t u = u0 + 1; u <= u1; ++u) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) s[k] += t1[k];
+      for (int32_t u = u0 + 2; u <= u1; ++u) {
         const f4 r = *(const f4 *)(pc + (int64_t)(2 * u) * H);
 #pragma unroll
         for (int k = 0; k < 4; ++k) s[k] += r[k];
@@ -193,39 +234,54 @@ __global__ __launch_bounds__(THREADS) void segsum_fused_bf16(
     const __bf16 *__restrict__ e, const int32_t *__restrict__ rp_in,
     const int32_t *__restrict__ perm_in, const int32_t *__restrict__ rp_out,
     const float *__restrict__ part, __bf16 *__restrict__ agg_in, __bf16 *__restrict__ agg_out,
-    int32_t n_nodes) {
+    int32_t n_nodes, int32_t n_units) {
   constexpr int LPR = H / 8;
   constexpr int TPB = THREADS / LPR;
   const int sub = threadIdx.x % LPR;
   const int64_t v = (int64_t)blockIdx.x * TPB + threadIdx.x / LPR;
   if (v >= n_nodes) return;
   const int32_t a = rp_out[v], b = rp_out[v + 1];
+  const int32_t pi = rp_in[v], pie = rp_in[v + 1];
+  const int32_t u0 = a >> 5, u1 = (b - 1) >> 5;
+  const bool spans = a < b && u1 > u0;
+  const float *pc = part + 8 * sub;
+  auto piece = [&](int64_t slot, float (&r)[8]) {
+    const f4 lo = *(const f4 *)(pc + slot * H), hi = *(const f4 *)(pc + slot * H + 4);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      r[k] = lo[k];
+      r[4 + k] = hi[k];
+    }
+  };
+  // As in the fp32 kernel: the first two pieces are requested up front, from
+  // a nearby unit (discarded) when the run does not span.
+  const int32_t w0 = spans ? u0 : min(u0, n_units - 1), w1 = spans ? u0 + 1 : w0;
+  float t0[8], t1[8];
+  piece(2 * (int64_t)w0 + 1, t0);
+  piece(2 * (int64_t)w1, t1);
   {
     float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     float c[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    row_sum_bf16<H>(e + 8 * sub, perm_in, rp_in[v], rp_in[v + 1], s, c);
+    row_sum_bf16<H>(e + 8 * sub, perm_in, pi, pie, sub, s, c);
     bf8 o;
 #pragma unroll
     for (int k = 0; k < 8; ++k) o[k] = (__bf16)(s[k] + c[k]);
     *(bf8 *)(agg_in + v * H + 8 * sub) = o;
   }
-  const int32_t u0 = a >> 5, u1 = (b - 1) >> 5;
-  if (a < b && u0 == u1) return;  // written by the edge update
+  if (a < b && !spans) return;  // written by the edge update
   float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   float c[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  if (a < b) {
-    const float *pc = part + 8 * sub;
-    auto piece = [&](int64_t slot, float (&r)[8]) {
-      const f4 lo = *(const f4 *)(pc + slot * H), hi = *(const f4 *)(pc + slot * H + 4);
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        r[k] = lo[k];
-        r[4 + k] = hi[k];
-      }
-    };
-    piece(2 * (int64_t)u0 + 1, s);
+  if (spans) {
     const bool comp = u1 - u0 > LONG_ROW;
-    for (int32_t u = u0 + 1; u <= u1; ++u) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      s[k] = t0[k];
+      if (comp)
+        nsum<true>(s[k], c[k], t1[k]);
+      else
+        s[k] += t1[k];
+    }
+    for (int32_t u = u0 + 2; u <= u1; ++u) {
       float r[8];
       piece(2 * (int64_t)u, r);
 #pragma unroll
@@ -264,7 +320,7 @@ __global__ __launch_bounds__(THREADS) void segsum_bf16(
   const __bf16 *base = e + 8 * sub;
   float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   float c[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  row_sum_bf16<H>(base, perm, p, pe, s, c);
+  row_sum_bf16<H>(base, perm, p, pe, sub, s, c);
   bf8 o;
 #pragma unroll
   for (int k = 0; k < 8; ++k) o[k] = (__bf16)(s[k] + c[k]);
@@ -294,19 +350,22 @@ hipError_t launch_h(Act act, const void *e, const int32_t *rp_in, const int32_t 
 template <int H>
 hipError_t launch_fused_h(Act act, const void *e, const int32_t *rp_in, const int32_t *perm_in,
                           const int32_t *rp_out, const float *part, void *agg_in, void *agg_out,
-                          int32_t n_nodes, hipStream_t stream) {
+                          int32_t n_nodes, int64_t n_edges, hipStream_t stream) {
   const int tpb = THREADS / (act == Act::F32 ? H / 4 : H / 8);
   const int64_t tasks = n_nodes;
   const unsigned blocks = (unsigned)((tasks + tpb - 1) / tpb);
   if (blocks == 0) return hipSuccess;
+  // The kernels read pieces of unit min(u, n_units - 1): at least one unit.
+  const int64_t n_units = (n_edges + 31) / 32;
+  if (n_units < 1 || n_units > INT32_MAX) return hipErrorInvalidValue;
   if (act == Act::F32)
     segsum_fused_f32<H><<<blocks, THREADS, 0, stream>>>((const float *)e, rp_in, perm_in, rp_out,
                                                         part, (float *)agg_in, (float *)agg_out,
-                                                        n_nodes);
+                                                        n_nodes, (int32_t)n_units);
   else
     segsum_fused_bf16<H><<<blocks, THREADS, 0, stream>>>((const __bf16 *)e, rp_in, perm_in,
                                                          rp_out, part, (__bf16 *)agg_in,
-                                                         (__bf16 *)agg_out, n_nodes);
+                                                         (__bf16 *)agg_out, n_nodes, (int32_t)n_units);
   return hipGetLastError();
 }
 
@@ -315,10 +374,10 @@ hipError_t launch_fused_h(Act act, const void *e, const int32_t *rp_in, const in
 hipError_t launch_segsum_fused(Act act, int hidden, const void *e, const int32_t *rp_in,
                                const int32_t *perm_in, const int32_t *rp_out,
                                const float *agg_part, void *agg_in, void *agg_out,
-                               int32_t n_nodes, hipStream_t stream) {
+                               int32_t n_nodes, int64_t n_edges, hipStream_t stream) {
   switch (hidden) {
-    case 64: return launch_fused_h<64>(act, e, rp_in, perm_in, rp_out, agg_part, agg_in, agg_out, n_nodes, stream);
-    case 128: return launch_fused_h<128>(act, e, rp_in, perm_in, rp_out, agg_part, agg_in, agg_out, n_nodes, stream);
+    case 64: return launch_fused_h<64>(act, e, rp_in, perm_in, rp_out, agg_part, agg_in, agg_out, n_nodes, n_edges, stream);
+    case 128: return launch_fused_h<128>(act, e, rp_in, perm_in, rp_out, agg_part, agg_in, agg_out, n_nodes, n_edges, stream);
   }
   return hipErrorInvalidValue;
 }

@@ -673,7 +673,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       st.begin();
       if (fused)
         HIP_TRY(launch_segsum_fused(act, H, w.e, w.rp_in, w.q_in, w.rp_out, w.part, w.ain,
-                                    w.aout, n, stream));
+                                    w.aout, n, E, stream));
       else  // source-order rows: the out-CSR is the identity
         HIP_TRY(launch_segsum(act, H, w.e, w.rp_in, w.q_in, w.rp_out, nullptr, w.ain, w.aout,
                               n, stream));

@@ -140,7 +140,7 @@ hipError_t launch_segsum(Act act, int hidden, const void *e, const int32_t *rp_i
 hipError_t launch_segsum_fused(Act act, int hidden, const void *e, const int32_t *rp_in,
                                const int32_t *perm_in, const int32_t *rp_out,
                                const float *agg_part, void *agg_in, void *agg_out,
-                               int32_t n_nodes, hipStream_t stream);
+                               int32_t n_nodes, int64_t n_edges, hipStream_t stream);
 
 // Stable CSRs of edge_index ([2][n_edges] int32, indices clamped into
 // [0, n_nodes)): by destination (row_ptr_in, perm_in) and by source

@@ -249,6 +249,39 @@ def test_out_sums_every_run_offset_exact(G, dtype, flags, H):
         G.gnn_destroy(h)
 
 
+@pytest.mark.parametrize("flags", PATHS)
+@pytest.mark.parametrize("H", [64, 128])
+def test_in_sums_every_degree_stage_parity(G, oracle_mod, flags, H):
+    # In-degrees 0..70 (each once) and random small ones, edges in a random
+    # order, distinct messages: the in-direction sums take one, two and three
+    # loads of row ids (16 or 32 per load), every ragged tail of a batch of
+    # four row loads, and both sides of the compensated-summation threshold.
+    rng = np.random.default_rng(91)
+    indeg = np.concatenate([np.arange(71), rng.integers(0, 12, 300)])
+    rng.shuffle(indeg)
+    N = len(indeg)
+    dst = np.repeat(np.arange(N), indeg)
+    E = len(dst)
+    src = rng.integers(0, N, E)
+    p = rng.permutation(E)
+    ei = np.stack([src[p], dst[p]]).astype(np.int32)
+    x = rng.normal(size=(N, 3)).astype(np.float32)
+    w = I.make_weights(3, H, 1, 91, affine_noise=0.3)
+    print(f"in-degree sweep H={H} flags={flags} N={N} E={E}", flush=True)
+    ref = oracle_mod.forward(w, x, ei, H, 2, dump_iter=1)
+    h = G.gnn_create(w, G.make_dims(3, H, 2, flags=flags))
+    try:
+        outs = {k: torch.zeros(n, H, device="cuda") for k, n in
+                (("h", N), ("e", E), ("agg_in", N), ("agg_out", N))}
+        G.gnn_debug_stages(h, dev(x), dev(ei), N, E, 1, outs["h"], outs["e"], outs["agg_in"],
+                           outs["agg_out"])
+        torch.cuda.synchronize()
+        for k in ("agg_in", "agg_out", "h", "e"):
+            assert_logits_close(outs[k].cpu().numpy(), ref[k], what=f"{k} after 1")
+    finally:
+        G.gnn_destroy(h)
+
+
 def test_full_deterministic_and_permutation_equivariant(G):
     c = I.CONFIGS["full"]
     g = I.make_graph(c)
