@@ -34,7 +34,7 @@ TRAFFIC_SOURCES = {
     "fp32_mfma": ["paper_2402_09633_amd/csrc/factored.hip",
                   "paper_2402_09633_amd/csrc/device_common.h"],
 }
-MEASURED_TRAFFIC = {"f4c4c9c468e2ba92": {"edge_update_bytes": 1.802e9},   # edge_split<4,3>
+MEASURED_TRAFFIC = {"12e108cb294d0230": {"edge_update_bytes": 1.800e9},   # edge_split<4,3>
                     "d13e7c0d9ceb8c2f": {"edge_update_bytes": 1.652e9}}   # edge_f32<4,1>
 
 
@@ -66,10 +66,12 @@ def edge_update_bytes(N, E, H, s=4, n_src=0):
     return E * (2 * H * s + 2 * H * 4 + 8) + n_src * H * s
 
 
-def node_update_bytes(N, H, s=4):
-    """h, agg_in, agg_out read and h written (s bytes per element); the
-    projection row written (fp32)."""
-    return N * (4 * H * s + 2 * H * 4)
+def node_update_bytes(N, H, s=4, T=1):
+    """Average per launch over the T launches of one event: h, agg_in,
+    agg_out read (s bytes per element) and the projection row written
+    (fp32) every time; h written by all but the last launch, whose h feeds
+    the classifier only through its projections."""
+    return N * (3 * H * s + 2 * H * 4) + N * H * s * (T - 1) / T
 
 
 def split_mfma_flops(N, E, H, bf16=False):
@@ -257,7 +259,7 @@ def main():
                          "achieved": round(eu_mfma, 1), "peak": PEAK_TFLOPS[mdt],
                          "unit": "TFLOP/s", "frac": round(eu_mfma / PEAK_TFLOPS[mdt], 4),
                          "fp32_equivalent_tflops": round(eu_flops / (eu_ms / 1000.0) / 1e12, 1)}}
-        nb = node_update_bytes(N, H, act_bytes)
+        nb = node_update_bytes(N, H, act_bytes, T)
         nu_gbs = nb / (nu_ms / 1000.0) / 1e9
         nu_mfma = mf["node_update"] / (nu_ms / 1000.0) / 1e12
         roof_node = {"kernel": ("node_split<4,false,1,bf16> (hi/lo bf16 weights streamed "

@@ -610,7 +610,8 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
     na.nchunks = fd.enc_chunks;
     na.s2 = fd.s2_ne;
     na.nproj = 2;
-    na.h_out = (float *)w.h;
+    // with no iteration h0 feeds the classifier only through pb
+    na.h_out = T == 0 && ro.stop_iter < 0 ? nullptr : (float *)w.h;
     na.p_out[0] = w.pa;
     na.p_out[1] = w.pb;
     na.eps = d.ln_eps;
@@ -694,7 +695,10 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
         nu.row_bound = fd.row_bound;
       }
       nu.nproj = 1;
-      nu.h_out = (float *)w.h;  // in place: a wave reads its rows before writing them
+      // In place: a wave reads its rows before writing them.  The last
+      // update's h reaches the classifier only through its projections, so
+      // it is not stored unless the stages are being exported.
+      nu.h_out = t == T - 1 && ro.stop_iter < 0 ? nullptr : (float *)w.h;
       nu.p_out[0] = w.pb;
       nu.eps = d.ln_eps;
       st.begin();
