@@ -49,6 +49,11 @@ __device__ __forceinline__ float sigmoidf_stable(float z) {
 // bias is already in the accumulators.  Accumulators that hold s * y for a
 // power-of-two s (split-precision products) pass bscale = s and eps * s^2:
 // LayerNorm of s * (y + b) with eps s^2 equals LayerNorm of y + b with eps.
+// 1 / sqrt(x) for the LayerNorm scale, x = variance + eps > 0: the hardware
+// reciprocal square root (v_rsq_f32, about 1 ulp), in place of a square root
+// followed by an IEEE division (two roundings and a dozen instructions).
+__device__ __forceinline__ float ln_rstd(float x) { return __builtin_amdgcn_rsqf(x); }
+
 template <int MB>
 __device__ __forceinline__ void bias_ln_relu(f16v (&acc)[MB], const float *__restrict__ b,
                                              const float *__restrict__ g,
@@ -79,7 +84,7 @@ __device__ __forceinline__ void bias_ln_relu(f16v (&acc)[MB], const float *__res
       var += d * d;
     }
   var += __shfl_xor(var, 32);
-  const float rstd = 1.0f / sqrtf(var * inv_h + eps);
+  const float rstd = ln_rstd(var * inv_h + eps);
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -125,7 +130,7 @@ __device__ __forceinline__ void ln_relu_lds(f16v (&acc)[MB], const float *prm, f
       var += d * d;
     }
   var += __shfl_xor(var, 32);
-  const float rstd = 1.0f / sqrtf(var * inv_h + eps);
+  const float rstd = ln_rstd(var * inv_h + eps);
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll

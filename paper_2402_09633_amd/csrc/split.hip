@@ -168,7 +168,7 @@ __device__ __forceinline__ void ln_relu_t(f16v (&t)[MB], const float *prm, float
         const float d = t[mb][v0 + j] - mean[j];
         q += d * d;
       }
-      rstd[j] = 1.0f / sqrtf(sum32(q) * inv_h + eps);
+      rstd[j] = ln_rstd(sum32(q) * inv_h + eps);
     }
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
