@@ -212,6 +212,51 @@ def test_constant_messages_aggregate_to_degrees_full_scale(G, dtype):
         G.gnn_destroy(h)
 
 
+@pytest.mark.parametrize("dtype", [0, 1])
+def test_large_event_edge_rows_beyond_4gib(G, dtype):
+    # 2M nodes, 10M uniform edges: the fp32 edge-row buffer is 5.1 GB, so
+    # every per-edge row offset must be 64-bit (a 32-bit byte offset wraps
+    # after 8.4M fp32 rows).  Constant messages (edge MLP layer 2 W = 0,
+    # beta = 1) make every message exactly 1 and the aggregates exact
+    # degrees; the unmodified model is then run twice for bitwise
+    # determinism and scores in [0, 1].
+    N, E, H = 2_000_000, 10_000_000, 128
+    rng = np.random.default_rng(4242)
+    ei = rng.integers(0, N, size=(2, E), dtype=np.int32)
+    x = rng.normal(size=(N, 3)).astype(np.float32)
+    xd, eid = dev(x), dev(ei)
+    print(f"large event N={N} E={E} dtype={dtype}", flush=True)
+    w = I.make_weights(3, H, 1, 4242)
+    wc = w.copy()
+    v = I.blob_views(wc, 3, H, 1)
+    v["edge_mlp0.1.W"][:] = 0.0
+    v["edge_mlp0.1.beta"][:] = 1.0
+    h = G.gnn_create(wc, G.make_dims(3, H, 2, dtype=dtype))
+    try:
+        e = torch.zeros(E, H, device="cuda")
+        ain = torch.zeros(N, H, device="cuda")
+        aout = torch.zeros(N, H, device="cuda")
+        G.gnn_debug_stages(h, xd, eid, N, E, 1, None, e, ain, aout)
+        torch.cuda.synchronize()
+        assert bool((e == 1).all())
+        del e
+        indeg = torch.bincount(eid[1].long(), minlength=N).float()
+        outdeg = torch.bincount(eid[0].long(), minlength=N).float()
+        assert torch.equal(ain, indeg[:, None].expand(N, H))
+        assert torch.equal(aout, outdeg[:, None].expand(N, H))
+    finally:
+        G.gnn_destroy(h)
+    m = G.Model(w, G.make_dims(3, H, 2, dtype=dtype))
+    try:
+        s1 = m(xd, eid, logits=False).clone()
+        s2 = m(xd, eid, logits=False)
+        torch.cuda.synchronize()
+        assert torch.equal(s1, s2)
+        assert bool(((s1 >= 0) & (s1 <= 1)).all())
+    finally:
+        m.close()
+
+
 @pytest.mark.parametrize("dtype,flags", [(0, f) for f in PATHS] + [(1, f) for f in BF16_PATHS])
 @pytest.mark.parametrize("H", [64, 128])
 def test_out_sums_every_run_offset_exact(G, dtype, flags, H):
