@@ -27,15 +27,18 @@ PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2500.0, "fp16": 2500.0}
 
 # HBM bytes per launch of the edge-update kernel on the full event, from
 # rocprofv3 FETCH_SIZE / WRITE_SIZE passes scaled by a plain-copy calibration
-# (profiles/full_event_fp32_kernels_and_counters.md).  Valid only for the kernel sources they were measured on
-# (hash of the files of that path).
+# (profiles/full_event_fp32_kernels_and_counters.md, profiles/full_event_bf16_kernels_and_counters.md).
+# Valid only for the kernel sources they were measured on (hash of the files of that path).
 TRAFFIC_SOURCES = {
     "split": ["paper_2402_09633_amd/csrc/split.hip", "paper_2402_09633_amd/csrc/device_common.h"],
+    "bf16": ["paper_2402_09633_amd/csrc/split.hip", "paper_2402_09633_amd/csrc/device_common.h"],
     "fp32_mfma": ["paper_2402_09633_amd/csrc/factored.hip",
                   "paper_2402_09633_amd/csrc/device_common.h"],
 }
-MEASURED_TRAFFIC = {"12e108cb294d0230": {"edge_update_bytes": 1.800e9},   # edge_split<4,3>
-                    "d13e7c0d9ceb8c2f": {"edge_update_bytes": 1.652e9}}   # edge_f32<4,1>
+# (path, source hash) -> HBM bytes per edge-update launch on the full event
+MEASURED_TRAFFIC = {("split", "8675edf0b4ec909b"): 1.801e9,       # edge_split<4,3>
+                    ("bf16", "8675edf0b4ec909b"): 1.216e9,        # edge_split<4,3,bf16>
+                    ("fp32_mfma", "2a5ab5f168564cd8"): 1.651e9}   # edge_f32<4,1>
 
 
 def kernel_source_hash(path):
@@ -238,9 +241,8 @@ def main():
     nu_ms = nu["ms"] / max(nu["launches"], 1)
 
     traffic = None
-    if factored and cfg.name == "full" and path in TRAFFIC_SOURCES:
-        m_t = MEASURED_TRAFFIC.get(kernel_source_hash(path))
-        traffic = m_t["edge_update_bytes"] if m_t else None
+    if factored and cfg.name in ("full", "full_bf16") and path in TRAFFIC_SOURCES:
+        traffic = MEASURED_TRAFFIC.get((path, kernel_source_hash(path)))
     if split:
         eb = edge_update_bytes(N, E, H, act_bytes, n_src)
         gbs = eb / (eu_ms / 1000.0) / 1e9
