@@ -233,17 +233,6 @@ __device__ __forceinline__ void zero(f16v (&a)[MB]) {
 }
 
 template <int MB>
-__device__ __forceinline__ void store_rows(float *__restrict__ o, const f16v (&acc)[MB]) {
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const f4 val = {acc[mb][4 * q], acc[mb][4 * q + 1], acc[mb][4 * q + 2], acc[mb][4 * q + 3]};
-      *(f4 *)(o + mb * 32 + 8 * q) = val;
-    }
-}
-
-template <int MB>
 __device__ __forceinline__ void store_rows_bf16(__bf16 *__restrict__ o, const f16v (&acc)[MB]) {
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
@@ -538,9 +527,9 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
   constexpr bool HAS_E = MODE != (int)EdgeMode::Enc;
   constexpr bool HAS_L2 = MODE != (int)EdgeMode::Cls;
   constexpr bool FUSE = MODE == (int)EdgeMode::UpdAgg;
-  // Layer 2 transposed (step_ht / step_hlt) with row-contiguous e stores:
-  // the fused update and the encoder
-  constexpr bool TRANS = FUSE || MODE == (int)EdgeMode::Enc;
+  // The update always sums its rows per source here (UpdAgg); the plain
+  // update is the fp32-matrix-core kernel's (factored.hip).
+  static_assert(MODE != (int)EdgeMode::Upd, "split kernels have no plain update");
   __shared__ h8 lds[(HAS_E ? NR : 0) + (HAS_L2 ? NR : 0)];
   __shared__ float prm[6 * H];  // s1 b1, gamma1, beta1, s2 b2, gamma2, beta2
   h8 *lw_e = lds;
@@ -665,7 +654,9 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
         if (a.out_logit) a.out_logit[o] = z;
         if (a.out_score) a.out_score[o] = sigmoidf_stable(z);
       }
-    } else if constexpr (TRANS) {
+    } else {
+      // (the encoder and the fused update: layer 2 transposed, row-contiguous
+      // e stores)
       // Layer 2 transposed: lane l holds feature 32 mb + n of the unit's
       // rows 8 (v / 4) + 4 hh + v % 4.
       f16v t2[MB];
@@ -763,23 +754,6 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
       }
       if (u + nw < units) load_e(row_of(u + nw));
       }
-    } else {
-      f16v acc2[MB];
-      zero<MB>(acc2);
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        if constexpr (PREC == SPLIT)
-          step_h<MB>(acc2, lw_2 + g * 2 * MB * 64 + lane, acc_x<MB>(acc, g));
-        else
-          step_hl<MB>(acc2, (const bf8 *)(lw_2 + g * 2 * MB * 64 + lane), to_bf16(acc_x<MB>(acc, g)));
-      }
-      ln_relu_lds<MB>(acc2, prm + 3 * H, eps2, hh);
-      if (valid) {
-        if constexpr (PREC == SPLIT)
-          store_rows<MB>(a.e_out + row * H + 4 * hh, acc2);
-        else
-          store_rows_bf16<MB>((__bf16 *)a.e_out + row * H + 4 * hh, acc2);
-      }
     }
   }
 }
@@ -808,7 +782,7 @@ hipError_t edge_h(EdgeMode mode, const EdgeArgs &a, int grid, hipStream_t stream
   const unsigned nb = (unsigned)(need < grid ? need : grid);
   switch (mode) {
     case EdgeMode::Enc: edge_split<MB, 0, PREC><<<nb, 64 * SW, 0, stream>>>(a); break;
-    case EdgeMode::Upd: edge_split<MB, 1, PREC><<<nb, 64 * SW, 0, stream>>>(a); break;
+    case EdgeMode::Upd: return hipErrorInvalidValue;  // always UpdAgg here
     case EdgeMode::Cls: edge_split<MB, 2, PREC><<<nb, 64 * SW, 0, stream>>>(a); break;
     case EdgeMode::UpdAgg:
       if (!a.agg_out || !a.agg_part) return hipErrorInvalidValue;
@@ -822,11 +796,11 @@ template <int MB, int PREC>
 const void *edge_fn_mb(EdgeMode mode) {
   switch (mode) {
     case EdgeMode::Enc: return (const void *)edge_split<MB, 0, PREC>;
-    case EdgeMode::Upd: return (const void *)edge_split<MB, 1, PREC>;
     case EdgeMode::Cls: return (const void *)edge_split<MB, 2, PREC>;
+    case EdgeMode::Upd:  // not launched here (UpdAgg is)
     case EdgeMode::UpdAgg: return (const void *)edge_split<MB, 3, PREC>;
   }
-  return (const void *)edge_split<MB, 1, PREC>;
+  return (const void *)edge_split<MB, 3, PREC>;
 }
 
 template <int PREC>
