@@ -36,8 +36,8 @@ TRAFFIC_SOURCES = {
                   "paper_2402_09633_amd/csrc/device_common.h"],
 }
 # (path, source hash) -> HBM bytes per edge-update launch on the full event
-MEASURED_TRAFFIC = {("split", "8675edf0b4ec909b"): 1.801e9,       # edge_split<4,3>
-                    ("bf16", "8675edf0b4ec909b"): 1.216e9,        # edge_split<4,3,bf16>
+MEASURED_TRAFFIC = {("split", "b6ec3eb70f694e53"): 1.801e9,       # edge_split<4,3>
+                    ("bf16", "b6ec3eb70f694e53"): 1.215e9,        # edge_split<4,3,bf16>
                     ("fp32_mfma", "2a5ab5f168564cd8"): 1.651e9}   # edge_f32<4,1>
 
 
