@@ -166,6 +166,26 @@ def test_tiny_bf16_scores(G, oracle_mod, H, T, S, noise, flags):
     assert err <= BF16_SCORE_ATOL
 
 
+@pytest.mark.parametrize("dtype,flags", [(0, f) for f in PATHS] + [(1, f) for f in BF16_PATHS])
+@pytest.mark.parametrize("F,H", [(1, 64), (5, 128), (16, 64), (16, 128)])
+def test_feature_counts_other_than_three(G, oracle_mod, F, H, dtype, flags):
+    # The node encoder's first layer takes 1..16 input features (the hit
+    # features of other detectors); every other test uses 3.
+    rng = np.random.default_rng(100 + F)
+    n, e = 900, 3000
+    x = rng.normal(size=(n, F)).astype(np.float32)
+    ei = rng.integers(0, n, size=(2, e)).astype(np.int32)
+    w = I.make_weights(F, H, 1, 300 + F, affine_noise=0.3)
+    print(f"F={F} H={H} dtype={dtype} flags={flags}", flush=True)
+    ref = oracle_mod.forward(w, x, ei, H, 2)
+    dims = G.make_dims(F, H, 2, dtype=dtype, flags=flags)
+    if dtype == 0:
+        assert_logits_close(run_model(G, w, dims, x, ei), ref["logits"])
+    else:
+        sc = run_model(G, w, dims, x, ei, logits=False)
+        assert np.abs(sc - ref["scores"]).max() <= BF16_SCORE_ATOL
+
+
 @pytest.mark.parametrize("dtype", [0, 1])
 @pytest.mark.parametrize("bias", [0.0, 3.25, -80.0])
 def test_zero_weights_closed_form(G, dtype, bias):
