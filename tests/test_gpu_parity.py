@@ -186,6 +186,24 @@ def test_feature_counts_other_than_three(G, oracle_mod, F, H, dtype, flags):
         assert np.abs(sc - ref["scores"]).max() <= BF16_SCORE_ATOL
 
 
+@pytest.mark.parametrize("dtype,flags", [(0, f) for f in PATHS] + [(1, f) for f in BF16_PATHS])
+@pytest.mark.parametrize("eps", [0.5, 3.0e-3])
+def test_layernorm_eps(G, oracle_mod, eps, dtype, flags):
+    # A LayerNorm eps far from the default: the split kernels carry it as
+    # eps * s^2 next to accumulators scaled by a power of two s.
+    c = I.CONFIGS["tiny"]
+    g = I.make_graph(c)
+    w = I.make_weights(3, 128, 1, c.weight_seed, affine_noise=0.3)
+    print(f"eps={eps} dtype={dtype} flags={flags}", flush=True)
+    ref = oracle_mod.forward(w, g.x, g.edge_index, 128, 3, eps=eps)
+    dims = G.make_dims(3, 128, 3, dtype=dtype, ln_eps=eps, flags=flags)
+    if dtype == 0:
+        assert_logits_close(run_model(G, w, dims, g.x, g.edge_index), ref["logits"])
+    else:
+        sc = run_model(G, w, dims, g.x, g.edge_index, logits=False)
+        assert np.abs(sc - ref["scores"]).max() <= BF16_SCORE_ATOL
+
+
 @pytest.mark.parametrize("dtype", [0, 1])
 @pytest.mark.parametrize("bias", [0.0, 3.25, -80.0])
 def test_zero_weights_closed_form(G, dtype, bias):
