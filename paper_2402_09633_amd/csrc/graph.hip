@@ -14,10 +14,9 @@
 //             radius, so a pair within the radius sits in the same or
 //             adjacent cells; cells are hashed into a power-of-two table that
 //             is turned into buckets by the CSR builder (a stable sort of the
-//             points by bucket).  A point scans the 3^g neighbouring cells
-//             and keeps a candidate only if the candidate's own cell is the
-//             one being scanned, so hash collisions never produce a pair
-//             twice.  A count pass, an exclusive scan and a fill pass write
+//             points by bucket).  A point scans the buckets of the 3^g
+//             neighbouring cells, each bucket once, so hash collisions never
+//             produce a pair twice.  A count pass, an exclusive scan and a fill pass write
 //             the pairs grouped by i (within one i in cell-scan order), which
 //             is deterministic.
 #include "device_common.h"
@@ -102,15 +101,40 @@ __global__ __launch_bounds__(FTHREADS) void frnn_gather(FrnnArgs a, float *__res
 // neighbouring cells' buckets are scanned once each (a bucket that two
 // cells share through the hash is skipped the second time), so every other
 // point is tested at most once; a point of a colliding far cell simply fails
-// the distance test.
-template <bool FILL>
+// the distance test.  Candidates are taken U at a time: their ids and
+// coordinates are requested together before any distance is formed, so a
+// bucket costs one round of cache latency per U candidates rather than two
+// dependent ones per candidate (positions past the bucket's end repeat its
+// last point and are not counted).  The dimension D is a template argument:
+// the coordinate loads and the distance chain unroll, with 16-byte loads
+// when D is a multiple of 4 (rows of zs then start on 16-byte boundaries).
+template <bool FILL, int D>
 __global__ __launch_bounds__(FTHREADS) void frnn_pairs(FrnnArgs a, const float *__restrict__ zs) {
+  constexpr int U = 4;
+  constexpr int DZ = D < 3 ? 3 : D;  // cell_of reads up to 3 coordinates
   const int64_t p = (int64_t)blockIdx.x * FTHREADS + threadIdx.x;
   if (p >= a.n) return;
   const int32_t i = a.perm[p];
-  float zi[16];
+  auto load_row = [&](int64_t q, float *dst) {
+    const float *src = zs + q * D;
+    if constexpr (D % 4 == 0) {
 #pragma unroll
-  for (int k = 0; k < 16; ++k) zi[k] = k < a.D ? zs[p * a.D + k] : 0.f;
+      for (int k = 0; k < D; k += 4) {
+        const f4 v = *(const f4 *)(src + k);
+        dst[k] = v[0];
+        dst[k + 1] = v[1];
+        dst[k + 2] = v[2];
+        dst[k + 3] = v[3];
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < D; ++k) dst[k] = src[k];
+    }
+  };
+  float zi[DZ];
+#pragma unroll
+  for (int k = D; k < DZ; ++k) zi[k] = 0.f;
+  load_row(p, zi);
   int ci[3];
   cell_of(zi, a.g, a.inv_cell, ci);
   int64_t o = FILL ? a.offs[i] : 0;
@@ -127,28 +151,53 @@ __global__ __launch_bounds__(FTHREADS) void frnn_pairs(FrnnArgs a, const float *
         for (int u = 0; u < ns; ++u) dup |= seen[u] == key;
         if (dup) continue;
         seen[ns++] = key;
-        const int32_t qe = a.rp[key + 1];
-        for (int32_t q = a.rp[key]; q < qe; ++q) {
-          const int32_t j = a.perm[q];
-          if (j <= i) continue;
-          const float *zj = zs + (int64_t)q * a.D;
-          float acc = 0.f;
-          for (int k = 0; k < a.D; ++k) {
-            const float t = zi[k] - zj[k];
-            acc = __builtin_fmaf(t, t, acc);
+        const int32_t qb = a.rp[key], qe = a.rp[key + 1];
+        for (int32_t q0 = qb; q0 < qe; q0 += U) {
+          int32_t jj[U];
+          float zz[U][D];
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            const int32_t q = q0 + u < qe ? q0 + u : qe - 1;
+            jj[u] = a.perm[q];
+            load_row(q, zz[u]);
           }
-          if (acc < a.r2) {
-            if constexpr (FILL) {
-              a.out[o] = i;
-              a.out[a.total + o] = j;
-              ++o;
-            } else {
-              ++cnt;
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            if (q0 + u >= qe || jj[u] <= i) continue;
+            float acc = 0.f;
+#pragma unroll
+            for (int k = 0; k < D; ++k) {
+              const float t = zi[k] - zz[u][k];
+              acc = __builtin_fmaf(t, t, acc);
+            }
+            if (acc < a.r2) {
+              if constexpr (FILL) {
+                a.out[o] = i;
+                a.out[a.total + o] = jj[u];
+                ++o;
+              } else {
+                ++cnt;
+              }
             }
           }
         }
       }
   if constexpr (!FILL) a.count[i] = cnt;
+}
+
+template <bool FILL>
+hipError_t launch_pairs(const FrnnArgs &a, const float *zs, hipStream_t stream) {
+  const unsigned blocks = (unsigned)((a.n + FTHREADS - 1) / FTHREADS);
+  switch (a.D) {
+#define GNN_FRNN_D(d) \
+  case d: frnn_pairs<FILL, d><<<blocks, FTHREADS, 0, stream>>>(a, zs); break;
+    GNN_FRNN_D(1) GNN_FRNN_D(2) GNN_FRNN_D(3) GNN_FRNN_D(4) GNN_FRNN_D(5) GNN_FRNN_D(6)
+    GNN_FRNN_D(7) GNN_FRNN_D(8) GNN_FRNN_D(9) GNN_FRNN_D(10) GNN_FRNN_D(11) GNN_FRNN_D(12)
+    GNN_FRNN_D(13) GNN_FRNN_D(14) GNN_FRNN_D(15) GNN_FRNN_D(16)
+#undef GNN_FRNN_D
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 // Exclusive scan of the per-point counts into offs (int64), total -> *total:
@@ -249,8 +298,8 @@ hipError_t launch_frnn_count(const FrnnArgs &a, float *zs, hipStream_t stream) {
   if (a.n <= 0) return hipSuccess;
   const int64_t nz = a.n * a.D;
   frnn_gather<<<(unsigned)((nz + FTHREADS - 1) / FTHREADS), FTHREADS, 0, stream>>>(a, zs);
-  const unsigned blocks = (unsigned)((a.n + FTHREADS - 1) / FTHREADS);
-  frnn_pairs<false><<<blocks, FTHREADS, 0, stream>>>(a, zs);
+  hipError_t e = launch_pairs<false>(a, zs, stream);
+  if (e != hipSuccess) return e;
   const int64_t nb = (int64_t)frnn_scan_blocks(a.n);
   scan_tiles<<<(unsigned)nb, ST, 0, stream>>>(a.count, a.n, a.bsum);
   scan_sums<<<1, ST, 0, stream>>>(a.bsum, nb, a.total_dev);
@@ -260,8 +309,7 @@ hipError_t launch_frnn_count(const FrnnArgs &a, float *zs, hipStream_t stream) {
 
 hipError_t launch_frnn_fill(const FrnnArgs &a, const float *zs, hipStream_t stream) {
   if (a.n <= 0) return hipSuccess;
-  frnn_pairs<true><<<(unsigned)((a.n + FTHREADS - 1) / FTHREADS), FTHREADS, 0, stream>>>(a, zs);
-  return hipGetLastError();
+  return launch_pairs<true>(a, zs, stream);
 }
 
 }  // namespace gnn
