@@ -371,8 +371,17 @@ def bench_filter(G, I, cfg):
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t) * 1000.0 / 5
     G.gnn_filter_destroy(f)
+    # multiply-adds x 2 per candidate: layer 1 (2F -> 64, VALU), layer 2
+    # (64 -> 64, fp32 matrix cores), head (64 -> 1)
+    flop = 2.0 * g.n_edges * (2 * 3 * 64 + 64 * 64 + 64)
+    tf = flop / (ms / 1000.0) / 1e12
     return {"ms_per_event": round(ms, 4), "candidates": g.n_edges, "kept": kept,
             "candidate_edges_per_s": round(g.n_edges / (ms / 1000.0), 1),
+            "roofline": {"bound": "mfma", "achieved": round(tf, 2), "peak": PEAK_TFLOPS["fp32"],
+                         "unit": "TFLOP/s", "frac": round(tf / PEAK_TFLOPS["fp32"], 4),
+                         "flops_per_call": flop,
+                         "note": "wall time of the whole call (scoring, compaction, count "
+                                 "read-back)"},
             "note": "filter MLP (2F->64->64->1) + stable compaction at 0.5 on the same hits "
                     "with the wide windows (wall time incl. the count read-back); not part "
                     "of value"}
@@ -404,7 +413,15 @@ def bench_graph_construction(G, I, g):
         ei = G.radius_graph(pts, r2)
     torch.cuda.synchronize()
     frnn_ms = (time.perf_counter() - t) * 200.0
+    # multiply-adds x 2 per point: 3 -> 128 (VALU), 128 -> 128 (fp32 matrix
+    # cores), 128 -> 8 (VALU)
+    eflop = 2.0 * g.n_nodes * (3 * 128 + 128 * 128 + 128 * 8)
+    etf = eflop / (embed_ms / 1000.0) / 1e12
     return {"embed_ms": round(embed_ms, 4), "embed_points": int(g.n_nodes),
+            "embed_roofline": {"bound": "mfma", "achieved": round(etf, 2),
+                               "peak": PEAK_TFLOPS["fp32"], "unit": "TFLOP/s",
+                               "frac": round(etf / PEAK_TFLOPS["fp32"], 4),
+                               "flops_per_call": eflop},
             "frnn_ms": round(frnn_ms, 4), "frnn_points": 300_000, "frnn_dim": 8,
             "frnn_pairs": int(ei.shape[1]),
             "note": "embedding MLP 3->128->128->8 on the event's hits; fixed-radius pairs "
