@@ -1500,26 +1500,30 @@ int gnn_wcc(const int32_t *edge_index, const float *edge_scores, float threshold
   // Hooking onto the smaller root plus full compression converges in a few
   // rounds on graphs of tracks (and in O(log n) on typical graphs); a call
   // that has not converged after max_rounds fails instead of returning
-  // partial labels.
-  const int max_rounds = 256;
+  // partial labels.  Rounds are queued GROUP at a time, each with its own
+  // flag (zeroed up front); a round after one that joined nothing returns at
+  // once, so the host reads one flag per group instead of one per round.
+  const int max_rounds = 256, GROUP = 4;
   int rc = GNN_OK;
   bool converged = n_edges == 0;
   int32_t *changed = nullptr;
   {
-    hipError_t ae = hipMallocAsync((void **)&changed, sizeof(int32_t), stream);
+    hipError_t ae = hipMallocAsync((void **)&changed, max_rounds * sizeof(int32_t), stream);
     if (ae != hipSuccess) {
       (void)hipGetLastError();
       return fail(GNN_E_OOM, "hipMallocAsync failed: %s", hipGetErrorString(ae));
     }
   }
   HIP_TRY(wcc_launch_init(labels, n, stream));
-  for (int r = 0; r < max_rounds && n_edges > 0; ++r) {
+  HIP_TRY(launch_fill_i32(changed, max_rounds, 0, stream));
+  for (int r0 = 0; r0 < max_rounds && n_edges > 0; r0 += GROUP) {
+    const int r1 = r0 + GROUP < max_rounds ? r0 + GROUP : max_rounds;
+    for (int r = r0; r < r1; ++r)
+      HIP_TRY(wcc_launch_round(edge_index, edge_scores, threshold, n_edges, n, labels,
+                               r > 0 ? changed + r - 1 : nullptr, changed + r, stream));
     int32_t host_changed = 0;
-    HIP_TRY(launch_fill_i32(changed, 1, 0, stream));
-    HIP_TRY(wcc_launch_round(edge_index, edge_scores, threshold, n_edges, n, labels, changed,
-                             stream));
-    HIP_TRY(hipMemcpyAsync(&host_changed, changed, sizeof(int32_t), hipMemcpyDeviceToHost,
-                           stream));
+    HIP_TRY(hipMemcpyAsync(&host_changed, changed + r1 - 1, sizeof(int32_t),
+                           hipMemcpyDeviceToHost, stream));
     HIP_TRY(hipStreamSynchronize(stream));
     if (!host_changed) {
       converged = true;

@@ -221,12 +221,13 @@ hipError_t launch_frnn_count(const FrnnArgs &a, float *zs, hipStream_t stream);
 hipError_t launch_frnn_fill(const FrnnArgs &a, const float *zs, hipStream_t stream);
 
 // Weakly-connected components (wcc.hip): labels <- identity, then rounds of
-// hooking over the kept edges and pointer jumping; `changed` is set to 1 by
-// a round that joined two trees.
+// hooking over the kept edges and pointer jumping; `changed` (zero on entry)
+// is set to 1 by a round that joined two trees.  A round whose `prev` (the
+// previous round's flag; nullptr in the first round) is 0 does nothing.
 hipError_t wcc_launch_init(int32_t *labels, int32_t n, hipStream_t stream);
 hipError_t wcc_launch_round(const int32_t *edge_index, const float *scores, float threshold,
                             int64_t n_edges, int32_t n_nodes, int32_t *labels,
-                            int32_t *changed, hipStream_t stream);
+                            const int32_t *prev, int32_t *changed, hipStream_t stream);
 
 // flag <- 1 if any of the 2*n_edges indices lies outside [0, n_nodes).
 hipError_t launch_validate(const int32_t *edge_index, int64_t n_edges, int32_t n_nodes,

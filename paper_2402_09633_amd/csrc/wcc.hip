@@ -51,10 +51,14 @@ __global__ void wcc_init(int32_t *__restrict__ parent, int32_t n) {
 
 // `changed` is raised once per workgroup: one store per joining edge to a
 // single word would serialise on its L2 channel (milliseconds in the first
-// round, when most kept edges join two trees).
+// round, when most kept edges join two trees).  `prev` is the previous
+// round's flag (nullptr in the first round): once a round has joined
+// nothing the labels are final, and the rounds queued after it return at
+// once, so several rounds can be queued between two host checks.
 __global__ void wcc_hook(const int32_t *__restrict__ ei, const float *__restrict__ scores,
                          float threshold, int64_t n_edges, int32_t n_nodes, int32_t *parent,
-                         int32_t *__restrict__ changed) {
+                         const int32_t *prev, int32_t *__restrict__ changed) {
+  if (prev && __hip_atomic_load(prev, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) return;
   __shared__ int32_t joined;
   if (threadIdx.x == 0) joined = 0;
   __syncthreads();
@@ -74,7 +78,9 @@ __global__ void wcc_hook(const int32_t *__restrict__ ei, const float *__restrict
   if (threadIdx.x == 0 && joined) *changed = 1;
 }
 
-__global__ void wcc_compress(int32_t *parent, int32_t n) {
+// Skipped after a round that joined nothing (the links are roots already).
+__global__ void wcc_compress(int32_t *parent, int32_t n, const int32_t *changed) {
+  if (__hip_atomic_load(changed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) return;
   const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (v < n) parent[v] = find_root(parent, (int32_t)v);
 }
@@ -90,11 +96,13 @@ hipError_t wcc_launch_init(int32_t *labels, int32_t n, hipStream_t stream) {
 
 hipError_t wcc_launch_round(const int32_t *edge_index, const float *scores, float threshold,
                             int64_t n_edges, int32_t n_nodes, int32_t *labels,
-                            int32_t *changed, hipStream_t stream) {
+                            const int32_t *prev, int32_t *changed, hipStream_t stream) {
   if (n_edges > 0)
     wcc_hook<<<blocks_for(n_edges, 256), 256, 0, stream>>>(edge_index, scores, threshold,
-                                                          n_edges, n_nodes, labels, changed);
-  if (n_nodes > 0) wcc_compress<<<blocks_for(n_nodes, 256), 256, 0, stream>>>(labels, n_nodes);
+                                                          n_edges, n_nodes, labels, prev,
+                                                          changed);
+  if (n_nodes > 0)
+    wcc_compress<<<blocks_for(n_nodes, 256), 256, 0, stream>>>(labels, n_nodes, changed);
   return hipGetLastError();
 }
 
