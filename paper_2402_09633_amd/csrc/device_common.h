@@ -203,5 +203,58 @@ __device__ __forceinline__ void gemm_acc_f32(f16v (&out)[MB], const f16v (&act)[
   }
 }
 
+
+// ---- split-precision products (split.hip, filter.hip) ----
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef float f8 __attribute__((ext_vector_type(8)));
+
+// x = x1 + x2 with x1 = fp16(x), x2 = fp16(x - x1), both rounded to nearest.
+__device__ __forceinline__ void split2(const f8 &x, h8 &x1, h8 &x2) {
+  x1 = __builtin_convertvector(x, h8);
+  x2 = __builtin_convertvector(x - __builtin_convertvector(x1, f8), h8);
+}
+
+__device__ __forceinline__ f16v mma_h(const h8 &a, const h8 &b, const f16v &c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+// Weight records.  One record holds the A operands of one 16-wide k-step for
+// all MB output blocks, laid out [mb][part][lane] (16 bytes per slot), so
+// that lane l reads its parts of block mb at rec[(parts * mb + part) * 64].
+//
+// acc[mb] += (w1 + w2) (x1 + x2) over one k-step, x given split.
+template <int MB>
+__device__ __forceinline__ void step_h(f16v (&acc)[MB], const h8 *rec, const h8 &x1,
+                                       const h8 &x2) {
+  h8 w1[MB], w2[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    w1[mb] = rec[(2 * mb) * 64];
+    w2[mb] = rec[(2 * mb + 1) * 64];
+  }
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = mma_h(w1[mb], x1, acc[mb]);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = mma_h(w2[mb], x1, acc[mb]);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = mma_h(w1[mb], x2, acc[mb]);
+}
+
+template <int MB>
+__device__ __forceinline__ void step_h(f16v (&acc)[MB], const h8 *rec, const f8 &x) {
+  h8 x1, x2;
+  split2(x, x1, x2);
+  step_h<MB>(acc, rec, x1, x2);
+}
+
+// The eight accumulator values a lane supplies as the B operand of k-step
+// g = 2 mb + p when the operand is the previous layer's accumulators: the
+// features 16 g + 8 (j / 4) + 4 hh + j % 4, j = 0..7.
+template <int MB>
+__device__ __forceinline__ f8 acc_x(const f16v (&a)[MB], int g) {
+  const int mb = g / 2, o = 8 * (g % 2);
+  return f8{a[mb][o], a[mb][o + 1], a[mb][o + 2], a[mb][o + 3],
+            a[mb][o + 4], a[mb][o + 5], a[mb][o + 6], a[mb][o + 7]};
+}
+
 }  // namespace
 }  // namespace gnn

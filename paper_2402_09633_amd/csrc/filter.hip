@@ -2,10 +2,17 @@
 // step a Filtering MLP scores the candidate edges and applyFiltering keeps
 // the edges above a fixed threshold).
 //
-// filter_f32  one wave per 32 candidate edges: gather the raw features of
+// filter     one wave per 32 candidate edges: gather the raw features of
 //             both endpoints, layer 1 ([x_src; x_dst], 2F -> H) on VALU,
 //             LayerNorm/ReLU, layer 2 (H -> H) on the matrix cores,
-//             LayerNorm/ReLU, H -> 1 head, sigmoid.
+//             LayerNorm/ReLU, H -> 1 head, sigmoid.  Layer 2 runs on the
+//             fp16 matrix cores from split operands (SPLIT, as in split.hip:
+//             f16x2 records of s W1 with s a power of two, the LayerNorm/ReLU
+//             output as x1 + x2, three products per k-step, every partial
+//             product accumulated in fp32; the LayerNorm then takes the bias
+//             as s b1 and eps as eps s^2, which is the LayerNorm of W1 x + b1
+//             exactly), or on the fp32 matrix cores when the handle found the
+//             layer-1 LayerNorm output bound outside the fp16 range.
 // compaction  keep = score > threshold, in input order: per-block counts,
 //             one exclusive scan of the block counts, then a stable scatter
 //             (wave ballots inside a block); the kept edges are written as a
@@ -20,8 +27,8 @@ constexpr int CTHREADS = 256;
 constexpr int CITEMS = 4;
 constexpr int CTILE = CTHREADS * CITEMS;
 
-template <int MB>
-__global__ __launch_bounds__(64 * FWAVES) void filter_f32(FilterArgs a) {
+template <int MB, bool SPLIT>
+__global__ __launch_bounds__(64 * FWAVES) void filter_mlp(FilterArgs a) {
   constexpr int H = 32 * MB;
   const int lane = threadIdx.x & 63, hh = lane >> 5, n = lane & 31;
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
@@ -57,8 +64,19 @@ __global__ __launch_bounds__(64 * FWAVES) void filter_f32(FilterArgs a) {
   }
   bias_ln_relu<MB>(acc, nullptr, a.g0, a.beta0, a.eps, hh, false);
   f16v acc2[MB];
-  gemm_acc_f32<MB, MB>(acc2, acc, (const f4 *)a.w1 + lane, 0);
-  bias_ln_relu<MB>(acc2, a.b1, a.g1, a.beta1, a.eps, hh, true);
+  if constexpr (SPLIT) {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc2[mb][v] = 0.f;
+    const h8 *rec = (const h8 *)a.w1r + lane;
+#pragma unroll
+    for (int g = 0; g < 2 * MB; ++g) step_h<MB>(acc2, rec + g * 2 * MB * 64, acc_x<MB>(acc, g));
+    bias_ln_relu<MB>(acc2, a.b1, a.g1, a.beta1, a.eps * a.s1 * a.s1, hh, true, a.s1);
+  } else {
+    gemm_acc_f32<MB, MB>(acc2, acc, (const f4 *)a.w1 + lane, 0);
+    bias_ln_relu<MB>(acc2, a.b1, a.g1, a.beta1, a.eps, hh, true);
+  }
   float part = 0.f;
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
@@ -169,8 +187,14 @@ hipError_t launch_filter_scores(int hidden, const FilterArgs &a, hipStream_t str
   if (blocks <= 0) return hipSuccess;
   if (blocks > INT32_MAX) return hipErrorInvalidValue;
   switch (hidden) {
-    case 64: filter_f32<2><<<(unsigned)blocks, 64 * FWAVES, 0, stream>>>(a); break;
-    case 128: filter_f32<4><<<(unsigned)blocks, 64 * FWAVES, 0, stream>>>(a); break;
+    case 64:
+      if (a.w1r) filter_mlp<2, true><<<(unsigned)blocks, 64 * FWAVES, 0, stream>>>(a);
+      else filter_mlp<2, false><<<(unsigned)blocks, 64 * FWAVES, 0, stream>>>(a);
+      break;
+    case 128:
+      if (a.w1r) filter_mlp<4, true><<<(unsigned)blocks, 64 * FWAVES, 0, stream>>>(a);
+      else filter_mlp<4, false><<<(unsigned)blocks, 64 * FWAVES, 0, stream>>>(a);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -1278,6 +1278,15 @@ gnn_filter *gnn_filter_create(const float *weights, const gnn_filter_dims *dims)
   LayerOff o0 = stage_layer(st, l0, WKind::PlainT, false, true);
   LayerOff o1 = stage_layer(st, l1, WKind::FragAcc, false, true);
   LayerOff o2 = stage_layer(st, l2, WKind::Plain, false, false);
+  // Layer 2 on the fp16 matrix cores from split operands when its input, a
+  // LayerNorm/ReLU output, stays inside half the fp16 range (else fp32).
+  const bool split = ln_out_bound(l0) <= 32768.0;
+  const float s1 = split ? pow2_scale(l1) : 1.f;
+  size_t o_w1r = 0;
+  if (split) {
+    const std::vector<uint16_t> r = rec_f16x2(l1, 0, H, s1, true);
+    o_w1r = st.add(r.data(), r.size() * sizeof(uint16_t));
+  }
   gnn_filter *f = new gnn_filter();
   f->dims = *dims;
   f->device = dev;
@@ -1303,6 +1312,10 @@ gnn_filter *gnn_filter_create(const float *weights, const gnn_filter_dims *dims)
   f->tmpl.beta1 = d1.beta;
   f->tmpl.w2 = (const float *)d2.w;
   f->tmpl.b2 = d2.b;
+  if (split) {
+    f->tmpl.w1r = base + o_w1r;
+    f->tmpl.s1 = s1;
+  }
   return f;
 }
 

@@ -63,3 +63,20 @@ def test_filter_then_gnn_then_components(G, oracle_mod):
         m.close()
     zr = oracle_mod.forward(w, g.x, kept_ei, 64, 2)["logits"]
     assert_logits_close(z, zr)
+
+
+@pytest.mark.parametrize("H,gamma", [(64, 3000.0), (128, 2000.0), (64, 1.0e4)])
+def test_filter_large_layernorm_outputs(G, oracle_mod, H, gamma):
+    # The first LayerNorm's gain scaled up: outputs up to gamma * sqrt(H - 1).
+    # Near 2.8e4 (the first two cases) layer 2 keeps the split fp16 products
+    # (bound <= 2^15); near 9e4 the handle takes the fp32 matrix cores.  Both
+    # must match the oracle.
+    rng = np.random.default_rng(7)
+    n, e = 2000, 6000
+    x = rng.normal(size=(n, 3)).astype(np.float32)
+    ei = rng.integers(0, n, size=(2, e)).astype(np.int32)
+    w = I.make_filter_weights(3, H, 7, affine_noise=0.2)
+    I.filter_blob_views(w, 3, H)["filter.0.g"][:] *= np.float32(gamma)
+    sc, _ = run_filter(G, w, H, x, ei, 0.5)
+    ref, _ = oracle_mod.filter_edges(w, x, ei, H, 0.5)
+    np.testing.assert_allclose(sc, ref, rtol=0, atol=2e-6)
