@@ -380,8 +380,9 @@ def bench_filter(G, I, cfg):
             "roofline": {"bound": "mfma", "achieved": round(tf, 2), "peak": PEAK_TFLOPS["fp32"],
                          "unit": "TFLOP/s", "frac": round(tf / PEAK_TFLOPS["fp32"], 4),
                          "flops_per_call": flop,
-                         "note": "wall time of the whole call (scoring, compaction, count "
-                                 "read-back)"},
+                         "note": "algorithmic fp32 FLOP over the wall time of the whole call "
+                                 "(scoring, compaction, count read-back); layer 2 runs on the "
+                                 "fp16 matrix cores from split operands"},
             "note": "filter MLP (2F->64->64->1) + stable compaction at 0.5 on the same hits "
                     "with the wide windows (wall time incl. the count read-back); not part "
                     "of value"}
@@ -421,7 +422,9 @@ def bench_graph_construction(G, I, g):
             "embed_roofline": {"bound": "mfma", "achieved": round(etf, 2),
                                "peak": PEAK_TFLOPS["fp32"], "unit": "TFLOP/s",
                                "frac": round(etf / PEAK_TFLOPS["fp32"], 4),
-                               "flops_per_call": eflop},
+                               "flops_per_call": eflop,
+                               "note": "algorithmic fp32 FLOP; layer 2 runs on the fp16 matrix "
+                                       "cores from split operands"},
             "frnn_ms": round(frnn_ms, 4), "frnn_points": 300_000, "frnn_dim": 8,
             "frnn_pairs": int(ei.shape[1]),
             "note": "embedding MLP 3->128->128->8 on the event's hits; fixed-radius pairs "

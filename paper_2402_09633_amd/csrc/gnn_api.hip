@@ -1394,6 +1394,14 @@ gnn_embedder *gnn_embed_create(const float *weights, const gnn_embed_dims *dims)
   LayerOff o0 = stage_layer(st, l0, WKind::PlainT, false, true);
   LayerOff o1 = stage_layer(st, l1, WKind::FragAcc, false, true);
   LayerOff o2 = stage_layer(st, l2, WKind::Plain, false, false);
+  // layer 2 on split fp16 products unless its input leaves the fp16 range
+  const bool split = ln_out_bound(l0) <= 32768.0;
+  const float s1 = split ? pow2_scale(l1) : 1.f;
+  size_t o_w1r = 0;
+  if (split) {
+    const std::vector<uint16_t> r = rec_f16x2(l1, 0, H, s1, true);
+    o_w1r = st.add(r.data(), r.size() * sizeof(uint16_t));
+  }
   gnn_embedder *m = new gnn_embedder();
   m->dims = *dims;
   m->device = dev;
@@ -1418,6 +1426,10 @@ gnn_embedder *gnn_embed_create(const float *weights, const gnn_embed_dims *dims)
   m->tmpl.b1 = d1.b;
   m->tmpl.g1 = d1.g;
   m->tmpl.beta1 = d1.beta;
+  if (split) {
+    m->tmpl.w1r = base + o_w1r;
+    m->tmpl.s1 = s1;
+  }
   m->tmpl.w2 = (const float *)d2.w;
   m->tmpl.b2 = d2.b;
   return m;

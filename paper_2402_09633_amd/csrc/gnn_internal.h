@@ -197,6 +197,10 @@ struct EmbedArgs {
   int32_t F = 0, D = 0;
   const float *w0t = nullptr, *b0 = nullptr, *g0 = nullptr, *beta0 = nullptr;  // W0 as [F][H]
   const float *w1 = nullptr, *b1 = nullptr, *g1 = nullptr, *beta1 = nullptr;   // fragments
+  // f16x2 records of s1 W1 (layer 2 on the fp16 matrix cores); nullptr: the
+  // fp32 fragments w1 are used
+  const void *w1r = nullptr;
+  float s1 = 1.f;
   const float *w2 = nullptr, *b2 = nullptr;                                   // [D][H], [D]
   float *z = nullptr;                                                         // [n][D]
   float eps = 1e-5f;

@@ -3,10 +3,13 @@
 // fixed-radius nearest-neighbour search there proposes the candidate edges
 // that the filter and the GNN then score).
 //
-// embed_f32   one wave per 32 points: layer 1 (F -> H) on VALU, LayerNorm/
-//             ReLU, layer 2 (H -> H) on the fp32 matrix cores through the
+// embed       one wave per 32 points: layer 1 (F -> H) on VALU, LayerNorm/
+//             ReLU, layer 2 (H -> H) on the matrix cores through the
 //             accumulator chain, LayerNorm/ReLU, then the D outputs as VALU
-//             dot products (D <= 16).
+//             dot products (D <= 16).  Layer 2 takes the split fp16 products
+//             of split.hip (SPLIT: f16x2 records of s W1, bias s b1, eps
+//             eps s^2) when the first LayerNorm's output bound fits the fp16
+//             range, the fp32 matrix cores otherwise.
 // frnn        every pair i < j with d2(i, j) < r2, where d2 is evaluated in
 //             fp32 as d = fmaf(t, t, d) over the coordinates in ascending
 //             order (t = z_i[k] - z_j[k]).  Points are binned on a grid over
@@ -27,8 +30,8 @@ namespace {
 constexpr int EWAVES = 4;
 constexpr int FTHREADS = 256;
 
-template <int MB>
-__global__ __launch_bounds__(64 * EWAVES) void embed_f32(EmbedArgs a) {
+template <int MB, bool SPLIT>
+__global__ __launch_bounds__(64 * EWAVES) void embed_mlp(EmbedArgs a) {
   constexpr int H = 32 * MB;
   const int lane = threadIdx.x & 63, hh = lane >> 5, n = lane & 31;
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
@@ -42,8 +45,19 @@ __global__ __launch_bounds__(64 * EWAVES) void embed_f32(EmbedArgs a) {
   small_k_layer<MB>(acc, a.x, a.F, (int)r, a.w0t, a.b0, hh);
   bias_ln_relu<MB>(acc, nullptr, a.g0, a.beta0, a.eps, hh, false);
   f16v acc2[MB];
-  gemm_acc_f32<MB, MB>(acc2, acc, (const f4 *)a.w1 + lane, 0);
-  bias_ln_relu<MB>(acc2, a.b1, a.g1, a.beta1, a.eps, hh, true);
+  if constexpr (SPLIT) {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc2[mb][v] = 0.f;
+    const h8 *rec = (const h8 *)a.w1r + lane;
+#pragma unroll
+    for (int g = 0; g < 2 * MB; ++g) step_h<MB>(acc2, rec + g * 2 * MB * 64, acc_x<MB>(acc, g));
+    bias_ln_relu<MB>(acc2, a.b1, a.g1, a.beta1, a.eps * a.s1 * a.s1, hh, true, a.s1);
+  } else {
+    gemm_acc_f32<MB, MB>(acc2, acc, (const f4 *)a.w1 + lane, 0);
+    bias_ln_relu<MB>(acc2, a.b1, a.g1, a.beta1, a.eps, hh, true);
+  }
   for (int d = 0; d < a.D; ++d) {
     const float *wd = a.w2 + (int64_t)d * H + 4 * hh;
     float part = 0.f;
@@ -279,8 +293,14 @@ hipError_t launch_embed(int hidden, const EmbedArgs &a, hipStream_t stream) {
   const int64_t waves = (a.n + 31) / 32;
   const unsigned blocks = (unsigned)((waves + EWAVES - 1) / EWAVES);
   switch (hidden) {
-    case 64: embed_f32<2><<<blocks, 64 * EWAVES, 0, stream>>>(a); break;
-    case 128: embed_f32<4><<<blocks, 64 * EWAVES, 0, stream>>>(a); break;
+    case 64:
+      if (a.w1r) embed_mlp<2, true><<<blocks, 64 * EWAVES, 0, stream>>>(a);
+      else embed_mlp<2, false><<<blocks, 64 * EWAVES, 0, stream>>>(a);
+      break;
+    case 128:
+      if (a.w1r) embed_mlp<4, true><<<blocks, 64 * EWAVES, 0, stream>>>(a);
+      else embed_mlp<4, false><<<blocks, 64 * EWAVES, 0, stream>>>(a);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

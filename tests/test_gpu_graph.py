@@ -46,6 +46,23 @@ def test_embed_matches_oracle(G, oracle_mod, H, D, seed):
     np.testing.assert_allclose(z, ref, rtol=1e-4, atol=1e-4)
 
 
+@pytest.mark.parametrize("H,gamma", [(64, 3000.0), (128, 2000.0), (128, 1.0e4)])
+def test_embed_large_layernorm_outputs(G, oracle_mod, H, gamma):
+    # The first LayerNorm's gain scaled up: outputs up to gamma * sqrt(H - 1).
+    # Below 2^15 (the first two cases) layer 2 keeps the split fp16
+    # products; above it (the third) the handle takes the fp32 matrix cores.
+    g = I.make_graph(I.CONFIGS["tiny"])
+    w = I.make_embed_weights(3, H, 8, 61, affine_noise=0.2)
+    I.embed_blob_views(w, 3, H, 8)["embed.0.g"][:] *= np.float32(gamma)
+    ref = oracle_mod.embed(w, g.x, H, 8)
+    m = G.Embedder(w, G.make_embed_dims(3, H, 8))
+    try:
+        z = m(torch.as_tensor(g.x).cuda()).cpu().numpy()
+    finally:
+        m.close()
+    np.testing.assert_allclose(z, ref, rtol=1e-4, atol=1e-4)
+
+
 @pytest.mark.parametrize("n,D,r,seed", [(2000, 8, 0.05, 0), (3001, 3, 0.02, 1), (500, 1, 0.001, 2),
                                         (1500, 2, 0.01, 3), (2500, 5, 0.04, 4), (800, 16, 0.15, 5),
                                         (20000, 8, 0.08, 6), (2, 4, 10.0, 7)])
