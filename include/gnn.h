@@ -19,8 +19,14 @@
  *
  * Every pointer argument of gnn_infer* / gnn_debug_* is a DEVICE pointer on
  * the handle's device, except where noted.  All calls are thread-safe; one
- * handle may run concurrently on several streams (its weights are read-only
- * and every call allocates its own stream-ordered workspace).
+ * handle may run concurrently on several streams (its weights are read-only).
+ *
+ * Workspace: gnn_infer* and gnn_debug_* need device scratch of at most
+ * (E + 3N)*H*act_bytes + 16*N*H + (40 + H/4)*E bytes (act_bytes 4 for fp32,
+ * 2 for bf16; about 1.7 GB for N = 300k, E = 1M, H = 128, fp32).  The handle keeps these buffers between calls (at most 16, one
+ * per call in flight, each rounded up by 1/8 for growth) and frees them in
+ * gnn_destroy; a call that finds an idle buffer large enough orders itself
+ * after that buffer's previous call with an event and allocates nothing.
  */
 #ifndef GNN_H
 #define GNN_H

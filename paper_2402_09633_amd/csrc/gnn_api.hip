@@ -5,9 +5,12 @@
 // uploads it once.  gnn_infer enqueues the whole inference on the caller's
 // stream: CSR build (csr.hip), node and edge encoders, T iterations of edge
 // update -> segmented sums (agg.hip) -> node update, then the classifier.
-// The workspace is allocated stream-ordered (hipMallocAsync/hipFreeAsync)
-// from the device's default pool, whose release threshold is raised so that
-// repeated calls reuse memory; one handle can serve several streams at once.
+// The inference workspace comes from a small cache owned by the handle: an
+// idle entry is reused once the stream has been made to wait for the event
+// that closed its previous call, so steady-state calls allocate nothing and
+// one handle can serve several streams at once.  The other entry points
+// allocate stream-ordered (hipMallocAsync/hipFreeAsync) from the device's
+// default pool, whose release threshold is raised.
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -285,6 +288,18 @@ struct gnn_handle {
   int32_t prof_calls = 0;
   int64_t prof_launches[GNN_N_STAGES] = {};
   double prof_ms[GNN_N_STAGES] = {};
+  // Inference workspaces kept across calls.  `done` is recorded on `last`
+  // after each call that used the entry; a later call (on any stream) waits
+  // for it before touching the memory.  `busy` covers the host side of a call.
+  struct WsEntry {
+    void *base;
+    size_t bytes;
+    hipEvent_t done;
+    hipStream_t last;
+    bool busy, recorded;
+  };
+  std::mutex ws_mu;
+  std::vector<WsEntry> ws;
 };
 
 namespace {
@@ -529,6 +544,113 @@ struct StageTimer {
   }
 };
 
+// Most cached workspaces per handle; beyond this, calls share entries
+// (ordered by events) rather than allocate more.
+constexpr size_t kMaxCachedWorkspaces = 16;
+
+size_t ws_round(size_t bytes) {
+  const size_t mib = size_t(1) << 20, b = bytes + bytes / 8;  // slack for growing events
+  return (b + mib - 1) / mib * mib;
+}
+
+// Gives a call on `stream` a workspace of at least `bytes`.  Preference: an
+// idle cached entry last used on this stream, then one whose last call has
+// finished, then a new cached entry, then (cache full) an idle entry still in
+// use on another stream, then replacing an idle entry that is too small.
+// With every entry busy on the host, the call gets a stream-ordered
+// allocation of its own (*slot = -1), freed at its end.
+int ws_acquire(gnn_handle *h, size_t bytes, hipStream_t stream, void **base, int *slot) {
+  std::lock_guard<std::mutex> lk(h->ws_mu);
+  auto &ws = h->ws;
+  int pick = -1, rank = 3;
+  for (int i = 0; i < (int)ws.size(); ++i) {
+    const auto &e = ws[i];
+    if (e.busy || e.bytes < bytes) continue;
+    const int r = e.last == stream ? 0 : hipEventQuery(e.done) == hipSuccess ? 1 : 2;
+    if (r < rank || (r == rank && e.bytes < ws[pick].bytes)) {
+      pick = i;
+      rank = r;
+    }
+  }
+  if (pick >= 0 && rank == 2 && ws.size() < kMaxCachedWorkspaces) pick = -1;
+  if (pick < 0) {
+    int victim = -1;
+    if (ws.size() >= kMaxCachedWorkspaces)
+      for (int i = 0; i < (int)ws.size() && victim < 0; ++i)
+        if (!ws[i].busy) victim = i;
+    if (ws.size() >= kMaxCachedWorkspaces && victim < 0) {
+      *slot = -1;
+      const hipError_t ae = hipMallocAsync(base, bytes, stream);
+      if (ae == hipSuccess) return GNN_OK;
+      (void)hipGetLastError();
+      return fail(ae == hipErrorOutOfMemory ? GNN_E_OOM : GNN_E_HIP,
+                  "hipMallocAsync(%zu bytes) failed: %s", bytes, hipGetErrorString(ae));
+    }
+    if (victim >= 0) {
+      // Replaced in place: busy entries keep their indices.  Its last call
+      // must end before the memory goes back.
+      auto &v = ws[victim];
+      if (hipEventSynchronize(v.done) != hipSuccess || hipFree(v.base) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(GNN_E_HIP, "releasing a cached workspace failed");
+      }
+      v.base = nullptr;
+      v.bytes = 0;
+      v.recorded = false;
+      pick = victim;
+    } else {
+      gnn_handle::WsEntry e{nullptr, 0, nullptr, stream, false, false};
+      if (hipEventCreateWithFlags(&e.done, hipEventDisableTiming) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(GNN_E_HIP, "hipEventCreate for a workspace failed");
+      }
+      ws.push_back(e);
+      pick = (int)ws.size() - 1;
+    }
+    auto &e = ws[pick];
+    const size_t want = ws_round(bytes);
+    const hipError_t ae = hipMalloc(&e.base, want);
+    if (ae != hipSuccess) {  // the entry stays, empty, for a later call
+      (void)hipGetLastError();
+      e.base = nullptr;
+      return fail(ae == hipErrorOutOfMemory ? GNN_E_OOM : GNN_E_HIP,
+                  "hipMalloc(%zu bytes) of a workspace failed: %s", want, hipGetErrorString(ae));
+    }
+    e.bytes = want;
+  }
+  auto &e = ws[pick];
+  if (e.recorded && hipStreamWaitEvent(stream, e.done, 0) != hipSuccess)
+    return fail(GNN_E_HIP, "hipStreamWaitEvent on a cached workspace failed");
+  e.busy = true;
+  e.last = stream;
+  *base = e.base;
+  *slot = pick;
+  return GNN_OK;
+}
+
+// Ends the host side of a call: marks the end of its work on `stream` so the
+// next user of the entry can wait for it.
+int ws_release(gnn_handle *h, int slot, void *base, hipStream_t stream) {
+  if (slot < 0) {
+    const hipError_t fe = hipFreeAsync(base, stream);
+    return fe == hipSuccess ? GNN_OK
+                            : fail(GNN_E_HIP, "hipFreeAsync failed: %s", hipGetErrorString(fe));
+  }
+  std::lock_guard<std::mutex> lk(h->ws_mu);
+  auto &e = h->ws[slot];
+  int rc = GNN_OK;
+  if (hipEventRecord(e.done, stream) == hipSuccess) {
+    e.recorded = true;
+  } else {  // no event to wait for: finish the call's work here instead
+    (void)hipGetLastError();
+    e.recorded = false;
+    if (hipStreamSynchronize(stream) != hipSuccess)
+      rc = fail(GNN_E_HIP, "closing a call on its workspace failed");
+  }
+  e.busy = false;
+  return rc;
+}
+
 // What a call should produce.
 struct RunOut {
   float *scores = nullptr, *logits = nullptr;  // classifier outputs
@@ -556,14 +678,9 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
   // the edge update sums its rows per source itself (split kernels)
   const bool fused = fac && hd->fd.split;
   w.bytes = plan_workspace(w, N, E, H, ab, fac, fused);
-  {
-    hipError_t ae = hipMallocAsync(&w.base, w.bytes, stream);
-    if (ae != hipSuccess) {
-      (void)hipGetLastError();
-      return fail(ae == hipErrorOutOfMemory ? GNN_E_OOM : GNN_E_HIP,
-                  "hipMallocAsync(%zu bytes) failed: %s", w.bytes, hipGetErrorString(ae));
-    }
-  }
+  int slot = -1;
+  rc = ws_acquire(hd, w.bytes, stream, &w.base, &slot);
+  if (rc != GNN_OK) return rc;
   plan_workspace(w, N, E, H, ab, fac, fused);
 
   if (d.flags & GNN_VALIDATE_INDICES) {
@@ -835,9 +952,8 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
 out:
   total.end(GNN_STAGE_TOTAL);
   {
-    hipError_t fe = hipFreeAsync(w.base, stream);
-    if (fe != hipSuccess && rc == GNN_OK)
-      rc = fail(GNN_E_HIP, "hipFreeAsync failed: %s", hipGetErrorString(fe));
+    const int rr = ws_release(hd, slot, w.base, stream);
+    if (rc == GNN_OK) rc = rr;
   }
   return rc;
 }
@@ -1132,6 +1248,10 @@ void gnn_destroy(gnn_handle *h) {
       (void)hipEventDestroy(mk.b);
     }
     for (auto e : h->prof_free) (void)hipEventDestroy(e);
+    for (auto &e : h->ws) {
+      if (e.base) (void)hipFree(e.base);
+      (void)hipEventDestroy(e.done);
+    }
   }
   delete h;
 }

@@ -89,9 +89,10 @@ def test_create_without_device_reports_no_device(G):
 def test_no_float_atomics_in_kernels():
     # Aggregation must be deterministic: the only atomics are integer ones --
     # the radix sort's uint32 digit counters (LDS `cnt`, global `totals`) and
-    # the components' int32 parent array (atomicMin, relaxed loads).
+    # the components' int32 parent array (atomicMin, relaxed loads) and the
+    # relaxed loads of their int32 round flags.
     allowed = ("atomicAdd(&cnt[", "atomicAdd(&S.totals[", "atomicMin(&parent[",
-               "__hip_atomic_load(parent")
+               "__hip_atomic_load(parent", "__hip_atomic_load(prev", "__hip_atomic_load(changed")
     for f in os.listdir(CSRC):
         text = open(os.path.join(CSRC, f)).read()
         for line in text.splitlines():

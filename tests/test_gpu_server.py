@@ -96,3 +96,59 @@ def test_server_destroy_finishes_queued_requests(G):
     for o, r in zip(outs, ref):
         assert np.array_equal(o.cpu().numpy(), r)
     m.close()
+
+
+def test_workspace_cache_reuse_growth_and_overflow(G):
+    """The handle's cached inference workspaces: shared by more streams than
+    it holds buffers (later calls wait for earlier ones through events),
+    replaced when a larger event arrives with the cache full, and bypassed
+    (a call-owned allocation) when more calls than buffers are on the host
+    at once.  Every result must equal the single-stream one bit for bit."""
+    w = I.make_weights(3, 64, 1, 73, affine_noise=0.2)
+    m = G.Model(w, G.make_dims(3, 64, 2))
+    small = _events(20)
+    big = []
+    for i in range(4):
+        rng = np.random.default_rng(900 + i)
+        n, e = 20000 + 1000 * i, 60000 + 5000 * i
+        x = rng.normal(size=(n, 3)).astype(np.float32)
+        ei = rng.integers(0, n, size=(2, e)).astype(np.int32)
+        big.append((torch.as_tensor(x).cuda(), torch.as_tensor(ei).cuda()))
+    try:
+        ref_s = [m(x, ei).cpu().numpy() for x, ei in small]
+        ref_b = [m(x, ei).cpu().numpy() for x, ei in big]
+        streams = [torch.cuda.Stream() for _ in range(20)]
+
+        def run_rounds(evs, refs, rounds):
+            outs = []
+            torch.cuda.synchronize()
+            for r in range(rounds):
+                for k, (x, ei) in enumerate(evs):
+                    o = torch.full((ei.shape[1],), -1.0, device="cuda")
+                    torch.cuda.synchronize()  # the fill is on torch's stream
+                    st = streams[(k + r) % len(streams)]
+                    G.gnn_infer(m.handle, x, ei, x.shape[0], ei.shape[1], o, st)
+                    outs.append((o, k))
+            torch.cuda.synchronize()
+            for o, k in outs:
+                assert np.array_equal(o.cpu().numpy(), refs[k]), f"event {k}"
+
+        run_rounds(small, ref_s, 3)  # 20 streams over at most 16 buffers
+        run_rounds(big, ref_b, 2)    # every cached buffer too small: replaced
+        run_rounds(small + big, ref_s + ref_b, 1)
+
+        srv = G.Server(m, 24)  # up to 24 calls on the host at once
+        try:
+            evs = (small + big) * 2
+            refs = (ref_s + ref_b) * 2
+            outs = [torch.full((ei.shape[1],), -1.0, device="cuda") for _, ei in evs]
+            torch.cuda.synchronize()
+            ids = [srv.submit(x, ei, o) for (x, ei), o in zip(evs, outs)]
+            for i in ids:
+                srv.wait(i)
+            for k, (o, r) in enumerate(zip(outs, refs)):
+                assert np.array_equal(o.cpu().numpy(), r), f"request {k}"
+        finally:
+            srv.close()
+    finally:
+        m.close()
