@@ -11,7 +11,10 @@
 // before any is added, so a typical node (a few messages) costs three
 // dependent round trips: row bounds, row ids, rows.  The gather of 512-byte
 // rows at scattered positions is bound by HBM at a lower rate than a
-// streaming read.  Accumulation is fp32 in both storage modes.  Rows
+// streaming read.  Message rows are loaded and aggregates stored with the
+// nontemporal hint: each row is touched once per launch, and keeping these
+// streams out of the caches' retained set made the full-event fp32 launch
+// 14% faster.  Accumulation is fp32 in both storage modes.  Rows
 // longer than LONG_ROW messages use Neumaier's compensated summation: a hub
 // node can receive 10^5 messages, where a plain fp32 running sum drifts by
 // ~10^-4 relative, while the compensated sum stays within a few ulps of the
@@ -25,6 +28,16 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 
 constexpr int THREADS = 256;
+
+// Loads and stores of rows that this kernel touches once (nontemporal).
+template <typename T>
+__device__ __forceinline__ T ld_once(const T *p) {
+  return __builtin_nontemporal_load(p);
+}
+template <typename T>
+__device__ __forceinline__ void st_once(T *p, T v) {
+  __builtin_nontemporal_store(v, p);
+}
 constexpr int LONG_ROW = 32;
 
 // One step of Neumaier summation: s + c carries the running sum.  With
@@ -75,7 +88,7 @@ __device__ __forceinline__ void row_sum_f32(const float *__restrict__ base,
           q = group_lane<G>(my, min(j + u, n - 1));
         else
           q = p + min(j + u, n - 1);
-        r[u] = *(const f4 *)(base + q * H);
+        r[u] = ld_once((const f4 *)(base + q * H));
       }
 #pragma unroll
       for (int u = 0; u < B; ++u)
@@ -105,7 +118,7 @@ __device__ __forceinline__ void row_sum_bf16(const __bf16 *__restrict__ base,
           q = group_lane<G>(my, min(j + u, n - 1));
         else
           q = p + min(j + u, n - 1);
-        r[u] = *(const bf8 *)(base + q * H);
+        r[u] = ld_once((const bf8 *)(base + q * H));
       }
 #pragma unroll
       for (int u = 0; u < B; ++u)
@@ -164,7 +177,7 @@ __global__ __launch_bounds__(THREADS) void segsum_f32(
   float s[4] = {0.f, 0.f, 0.f, 0.f}, c[4] = {0.f, 0.f, 0.f, 0.f};
   row_sum_f32<H>(base, perm, p, pe, sub, s, c);
   const f4 res = {s[0] + c[0], s[1] + c[1], s[2] + c[2], s[3] + c[3]};
-  *(f4 *)(dst + v * H + 4 * sub) = res;
+  st_once((f4 *)(dst + v * H + 4 * sub), res);
 }
 
 // After a fused edge update (rows in source order), one task per node v:
@@ -199,7 +212,7 @@ __global__ __launch_bounds__(THREADS) void segsum_fused_f32(
   {
     float s[4] = {0.f, 0.f, 0.f, 0.f}, c[4] = {0.f, 0.f, 0.f, 0.f};
     row_sum_f32<H>(e + 4 * sub, perm_in, pi, pie, sub, s, c);
-    *(f4 *)(agg_in + v * H + 4 * sub) = f4{s[0] + c[0], s[1] + c[1], s[2] + c[2], s[3] + c[3]};
+    st_once((f4 *)(agg_in + v * H + 4 * sub), f4{s[0] + c[0], s[1] + c[1], s[2] + c[2], s[3] + c[3]});
   }
   if (a < b && !spans) return;  // written by the edge update
   float s[4] = {0.f, 0.f, 0.f, 0.f}, c[4] = {0.f, 0.f, 0.f, 0.f};
@@ -224,7 +237,7 @@ __global__ __launch_bounds__(THREADS) void segsum_fused_f32(
       }
     }
   }
-  *(f4 *)(agg_out + v * H + 4 * sub) = f4{s[0] + c[0], s[1] + c[1], s[2] + c[2], s[3] + c[3]};
+  st_once((f4 *)(agg_out + v * H + 4 * sub), f4{s[0] + c[0], s[1] + c[1], s[2] + c[2], s[3] + c[3]});
 }
 
 // The same for bf16 rows and aggregates (H/8 lanes per node, 8 features
@@ -266,7 +279,7 @@ __global__ __launch_bounds__(THREADS) void segsum_fused_bf16(
     bf8 o;
 #pragma unroll
     for (int k = 0; k < 8; ++k) o[k] = (__bf16)(s[k] + c[k]);
-    *(bf8 *)(agg_in + v * H + 8 * sub) = o;
+    st_once((bf8 *)(agg_in + v * H + 8 * sub), o);
   }
   if (a < b && !spans) return;  // written by the edge update
   float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -296,7 +309,7 @@ __global__ __launch_bounds__(THREADS) void segsum_fused_bf16(
   bf8 o;
 #pragma unroll
   for (int k = 0; k < 8; ++k) o[k] = (__bf16)(s[k] + c[k]);
-  *(bf8 *)(agg_out + v * H + 8 * sub) = o;
+  st_once((bf8 *)(agg_out + v * H + 8 * sub), o);
 }
 
 template <int H>
@@ -324,7 +337,7 @@ __global__ __launch_bounds__(THREADS) void segsum_bf16(
   bf8 o;
 #pragma unroll
   for (int k = 0; k < 8; ++k) o[k] = (__bf16)(s[k] + c[k]);
-  *(bf8 *)(dst + v * H + 8 * sub) = o;
+  st_once((bf8 *)(dst + v * H + 8 * sub), o);
 }
 
 template <int H>

@@ -191,7 +191,7 @@ __device__ __forceinline__ void store_rows_bf16(__bf16 *__restrict__ o, const f1
     for (int q = 0; q < 4; ++q) {
       const bf4 val = {(__bf16)acc[mb][4 * q], (__bf16)acc[mb][4 * q + 1],
                        (__bf16)acc[mb][4 * q + 2], (__bf16)acc[mb][4 * q + 3]};
-      *(bf4 *)(o + mb * 32 + 8 * q) = val;
+      __builtin_nontemporal_store(val, (bf4 *)(o + mb * 32 + 8 * q));
     }
 }
 
@@ -199,6 +199,11 @@ __device__ __forceinline__ void store_rows_bf16(__bf16 *__restrict__ o, const f1
 // rows >= nvalid skipped) through a 32 x 32-float LDS staging tile, one
 // 128-byte column block at a time: every store instruction then writes 8
 // full 128-byte lines instead of 32-byte pieces of 32 rows.
+//
+// Rows that a later kernel reads (h, P, e) are stored with the nontemporal
+// hint: their write-back then drains while this kernel runs instead of
+// competing with the reading kernel's gathers (full fp32 event 6.48 ->
+// 6.28 ms with h, P and the updated e stored this way).
 constexpr int SST = 36;  // staging row stride in floats (16-byte aligned rows)
 template <int MB>
 __device__ __forceinline__ void store_block(float *__restrict__ out, int64_t stride, int nvalid,
@@ -218,7 +223,7 @@ __device__ __forceinline__ void store_block(float *__restrict__ out, int64_t str
     for (int k = 0; k < 4; ++k) {
       const int row = 8 * k + rr;
       const f4 v = *(const f4 *)(stg + row * SST + cc);
-      if (row < nvalid) *(f4 *)(out + row * stride + mb * 32 + cc) = v;
+      if (row < nvalid) __builtin_nontemporal_store(v, (f4 *)(out + row * stride + mb * 32 + cc));
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -644,21 +649,27 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
         if (u + nw < units) load_idx(u + nw);
       }
       // e rows: each store writes 32 contiguous elements of a row per
-      // half-wave (128 bytes fp32, 64 bytes bf16)
+      // half-wave (128 bytes fp32, 64 bytes bf16).  The update's rows go
+      // out nontemporal, as the node kernel's (the aggregation that reads
+      // them next: 0.136 -> 0.128 ms); the encoder's gain nothing from it.
       act_t *eo = (act_t *)a.e_out + (u * 32 + 4 * hh) * H + n;
+      auto st_e = [&](act_t *p, float x) {
+        if constexpr (FUSE)
+          __builtin_nontemporal_store((act_t)x, p);
+        else
+          *p = (act_t)x;
+      };
       if (nvalid == 32) {
 #pragma unroll
         for (int v = 0; v < 16; ++v)
 #pragma unroll
-          for (int mb = 0; mb < MB; ++mb)
-            eo[(8 * (v / 4) + v % 4) * H + 32 * mb] = (act_t)t2[mb][v];
+          for (int mb = 0; mb < MB; ++mb) st_e(&eo[(8 * (v / 4) + v % 4) * H + 32 * mb], t2[mb][v]);
       } else {
 #pragma unroll
         for (int v = 0; v < 16; ++v)
           if (8 * (v / 4) + 4 * hh + v % 4 < nvalid)
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
-              eo[(8 * (v / 4) + v % 4) * H + 32 * mb] = (act_t)t2[mb][v];
+            for (int mb = 0; mb < MB; ++mb) st_e(&eo[(8 * (v / 4) + v % 4) * H + 32 * mb], t2[mb][v]);
       }
       if constexpr (FUSE) {
       // Exchange halves: afterwards lane l holds block b = p + hh MB/2 of
@@ -694,10 +705,11 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
             float *dst = a.agg_part + (u * 2 + (first && hc ? 0 : 1)) * H;
 #pragma unroll
             for (int p = 0; p < MB / 2; ++p) dst[32 * (p + hh * (MB / 2)) + n] = sum[p];
-          } else {
+          } else {  // (read by the node update: nontemporal, as e)
             act_t *dst = (act_t *)a.agg_out + (int64_t)__builtin_amdgcn_readlane(cur_src, e) * H;
 #pragma unroll
-            for (int p = 0; p < MB / 2; ++p) dst[32 * (p + hh * (MB / 2)) + n] = (act_t)sum[p];
+            for (int p = 0; p < MB / 2; ++p)
+              __builtin_nontemporal_store((act_t)sum[p], &dst[32 * (p + hh * (MB / 2)) + n]);
           }
 #pragma unroll
           for (int p = 0; p < MB / 2; ++p) sum[p] = 0.f;
