@@ -27,7 +27,11 @@ namespace {
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 
-constexpr int THREADS = 256;
+// Block sizes: small blocks schedule the short, uneven node tasks best
+// (full event, against 256 threads: fp32 0.1248 -> 0.1236 ms with 128,
+// bf16 0.0745 -> 0.0694 ms with 64).
+constexpr int THREADS_F32 = 128;
+constexpr int THREADS_BF16 = 64;
 
 // Loads and stores of rows that this kernel touches once (nontemporal).
 template <typename T>
@@ -156,13 +160,13 @@ __device__ __forceinline__ void row_sum_bf16(const __bf16 *base, const int32_t *
 }
 
 template <int H>
-__global__ __launch_bounds__(THREADS) void segsum_f32(
+__global__ __launch_bounds__(THREADS_F32) void segsum_f32(
     const float *__restrict__ e, const int32_t *__restrict__ rp_in,
     const int32_t *__restrict__ perm_in, const int32_t *__restrict__ rp_out,
     const int32_t *__restrict__ perm_out, float *__restrict__ agg_in,
     float *__restrict__ agg_out, int32_t n_nodes) {
   constexpr int LPR = H / 4;
-  constexpr int TPB = THREADS / LPR;
+  constexpr int TPB = THREADS_F32 / LPR;
   const int sub = threadIdx.x % LPR;
   const int64_t task = (int64_t)blockIdx.x * TPB + threadIdx.x / LPR;
   if (task >= 2 * (int64_t)n_nodes) return;
@@ -187,13 +191,13 @@ __global__ __launch_bounds__(THREADS) void segsum_f32(
 // of the last unit, added in that order), zeroed when v has no out-edges,
 // and otherwise left as the edge update wrote it.
 template <int H>
-__global__ __launch_bounds__(THREADS) void segsum_fused_f32(
+__global__ __launch_bounds__(THREADS_F32) void segsum_fused_f32(
     const float *__restrict__ e, const int32_t *__restrict__ rp_in,
     const int32_t *__restrict__ perm_in, const int32_t *__restrict__ rp_out,
     const float *__restrict__ part, float *__restrict__ agg_in, float *__restrict__ agg_out,
     int32_t n_nodes) {
   constexpr int LPR = H / 4;
-  constexpr int TPB = THREADS / LPR;
+  constexpr int TPB = THREADS_F32 / LPR;
   const int sub = threadIdx.x % LPR;
   const int64_t v = (int64_t)blockIdx.x * TPB + threadIdx.x / LPR;
   if (v >= n_nodes) return;
@@ -241,13 +245,13 @@ __global__ __launch_bounds__(THREADS) void segsum_fused_f32(
 // The same for bf16 rows and aggregates (H/8 lanes per node, 8 features
 // each); the pieces are fp32, the sums fp32, the stored aggregates bf16.
 template <int H>
-__global__ __launch_bounds__(THREADS) void segsum_fused_bf16(
+__global__ __launch_bounds__(THREADS_BF16) void segsum_fused_bf16(
     const __bf16 *__restrict__ e, const int32_t *__restrict__ rp_in,
     const int32_t *__restrict__ perm_in, const int32_t *__restrict__ rp_out,
     const float *__restrict__ part, __bf16 *__restrict__ agg_in, __bf16 *__restrict__ agg_out,
     int32_t n_nodes) {
   constexpr int LPR = H / 8;
-  constexpr int TPB = THREADS / LPR;
+  constexpr int TPB = THREADS_BF16 / LPR;
   const int sub = threadIdx.x % LPR;
   const int64_t v = (int64_t)blockIdx.x * TPB + threadIdx.x / LPR;
   if (v >= n_nodes) return;
@@ -308,13 +312,13 @@ __global__ __launch_bounds__(THREADS) void segsum_fused_bf16(
 }
 
 template <int H>
-__global__ __launch_bounds__(THREADS) void segsum_bf16(
+__global__ __launch_bounds__(THREADS_BF16) void segsum_bf16(
     const __bf16 *__restrict__ e, const int32_t *__restrict__ rp_in,
     const int32_t *__restrict__ perm_in, const int32_t *__restrict__ rp_out,
     const int32_t *__restrict__ perm_out, __bf16 *__restrict__ agg_in,
     __bf16 *__restrict__ agg_out, int32_t n_nodes) {
   constexpr int LPR = H / 8;
-  constexpr int TPB = THREADS / LPR;
+  constexpr int TPB = THREADS_BF16 / LPR;
   const int sub = threadIdx.x % LPR;
   const int64_t task = (int64_t)blockIdx.x * TPB + threadIdx.x / LPR;
   if (task >= 2 * (int64_t)n_nodes) return;
@@ -340,16 +344,17 @@ hipError_t launch_h(Act act, const void *e, const int32_t *rp_in, const int32_t 
                     const int32_t *rp_out, const int32_t *perm_out, void *agg_in, void *agg_out,
                     int32_t n_nodes, hipStream_t stream) {
   const int lpr = act == Act::F32 ? H / 4 : H / 8;
-  const int tpb = THREADS / lpr;
+  const int threads = act == Act::F32 ? THREADS_F32 : THREADS_BF16;
+  const int tpb = threads / lpr;
   const int64_t tasks = 2 * (int64_t)n_nodes;
   const unsigned blocks = (unsigned)((tasks + tpb - 1) / tpb);
   if (blocks == 0) return hipSuccess;
   if (act == Act::F32)
-    segsum_f32<H><<<blocks, THREADS, 0, stream>>>((const float *)e, rp_in, perm_in, rp_out,
+    segsum_f32<H><<<blocks, THREADS_F32, 0, stream>>>((const float *)e, rp_in, perm_in, rp_out,
                                                   perm_out, (float *)agg_in, (float *)agg_out,
                                                   n_nodes);
   else
-    segsum_bf16<H><<<blocks, THREADS, 0, stream>>>((const __bf16 *)e, rp_in, perm_in, rp_out,
+    segsum_bf16<H><<<blocks, THREADS_BF16, 0, stream>>>((const __bf16 *)e, rp_in, perm_in, rp_out,
                                                    perm_out, (__bf16 *)agg_in, (__bf16 *)agg_out,
                                                    n_nodes);
   return hipGetLastError();
@@ -359,18 +364,18 @@ template <int H>
 hipError_t launch_fused_h(Act act, const void *e, const int32_t *rp_in, const int32_t *perm_in,
                           const int32_t *rp_out, const float *part, void *agg_in, void *agg_out,
                           int32_t n_nodes, int64_t n_edges, hipStream_t stream) {
-  const int tpb = THREADS / (act == Act::F32 ? H / 4 : H / 8);
+  const int tpb = act == Act::F32 ? THREADS_F32 / (H / 4) : THREADS_BF16 / (H / 8);
   const int64_t tasks = n_nodes;
   const unsigned blocks = (unsigned)((tasks + tpb - 1) / tpb);
   if (blocks == 0) return hipSuccess;
   // the pieces come from an edge update over a non-empty edge list
   if (n_edges < 1 || n_edges > INT32_MAX) return hipErrorInvalidValue;
   if (act == Act::F32)
-    segsum_fused_f32<H><<<blocks, THREADS, 0, stream>>>((const float *)e, rp_in, perm_in, rp_out,
+    segsum_fused_f32<H><<<blocks, THREADS_F32, 0, stream>>>((const float *)e, rp_in, perm_in, rp_out,
                                                         part, (float *)agg_in, (float *)agg_out,
                                                         n_nodes);
   else
-    segsum_fused_bf16<H><<<blocks, THREADS, 0, stream>>>((const __bf16 *)e, rp_in, perm_in,
+    segsum_fused_bf16<H><<<blocks, THREADS_BF16, 0, stream>>>((const __bf16 *)e, rp_in, perm_in,
                                                          rp_out, part, (__bf16 *)agg_in,
                                                          (__bf16 *)agg_out, n_nodes);
   return hipGetLastError();
