@@ -181,6 +181,15 @@ int gnn_infer_labels(gnn_handle *h, const float *node_feat, const int32_t *edge_
 /* Waits for the device, then frees everything the handle owns.  NULL-safe. */
 void gnn_destroy(gnn_handle *h);
 
+/* Memory management, not a step of the method: frees the inference
+ * workspaces the handle keeps between calls (see the note at the top of
+ * this file) that no call is using, each after the work of its last call
+ * has finished (the function waits for that work).  Buffers held by calls
+ * in progress on other threads stay.  Later calls allocate again as needed.
+ * Returns the number of bytes freed (0 if none), or GNN_E_INVALID_ARG for a
+ * NULL handle, GNN_E_HIP if waiting or freeing fails. */
+int64_t gnn_release_workspaces(gnn_handle *h);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char *gnn_last_error(void);
 

@@ -575,7 +575,9 @@ int ws_acquire(gnn_handle *h, size_t bytes, hipStream_t stream, void **base, int
   if (pick >= 0 && rank == 2 && ws.size() < kMaxCachedWorkspaces) pick = -1;
   if (pick < 0) {
     int victim = -1;
-    if (ws.size() >= kMaxCachedWorkspaces)
+    for (int i = 0; i < (int)ws.size() && victim < 0; ++i)  // emptied by a release
+      if (!ws[i].busy && !ws[i].base) victim = i;
+    if (victim < 0 && ws.size() >= kMaxCachedWorkspaces)
       for (int i = 0; i < (int)ws.size() && victim < 0; ++i)
         if (!ws[i].busy) victim = i;
     if (ws.size() >= kMaxCachedWorkspaces && victim < 0) {
@@ -1235,6 +1237,25 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
     fd.grid_node = node_f32_grid(n_cu);
   }
   return h;
+}
+
+int64_t gnn_release_workspaces(gnn_handle *h) {
+  if (!h) return fail(GNN_E_INVALID_ARG, "handle is NULL");
+  DeviceGuard guard(h->device);
+  std::lock_guard<std::mutex> lk(h->ws_mu);
+  int64_t freed = 0;
+  for (auto &e : h->ws) {
+    if (e.busy || !e.base) continue;
+    if (hipEventSynchronize(e.done) != hipSuccess || hipFree(e.base) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(GNN_E_HIP, "releasing a cached workspace failed");
+    }
+    freed += (int64_t)e.bytes;
+    e.base = nullptr;
+    e.bytes = 0;
+    e.recorded = false;
+  }
+  return freed;
 }
 
 void gnn_destroy(gnn_handle *h) {

@@ -32,7 +32,8 @@ GNN_FP32_MFMA = 4
 
 EXPORTS = ("gnn_weight_count", "gnn_create", "gnn_infer", "gnn_infer_logits",
            "gnn_filter_weight_count", "gnn_filter_create", "gnn_filter_apply",
-           "gnn_filter_destroy", "gnn_wcc", "gnn_infer_labels", "gnn_destroy", "gnn_last_error",
+           "gnn_filter_destroy", "gnn_wcc", "gnn_infer_labels", "gnn_destroy",
+           "gnn_release_workspaces", "gnn_last_error",
            "gnn_profile_enable", "gnn_profile_read", "gnn_debug_csr", "gnn_debug_stages",
            "gnn_server_create", "gnn_server_submit", "gnn_server_wait", "gnn_server_destroy",
            "gnn_embed_weight_count", "gnn_embed_create", "gnn_embed_apply", "gnn_embed_destroy",
@@ -110,6 +111,8 @@ def _load():
     L.gnn_infer_labels.argtypes = [vp, vp, vp, i64, i64, ctypes.c_float, vp, vp, vp]
     L.gnn_destroy.restype = None
     L.gnn_destroy.argtypes = [vp]
+    L.gnn_release_workspaces.restype = ctypes.c_int64
+    L.gnn_release_workspaces.argtypes = [vp]
     L.gnn_last_error.restype = ctypes.c_char_p
     L.gnn_last_error.argtypes = []
     L.gnn_profile_enable.restype = ctypes.c_int
@@ -197,6 +200,14 @@ def gnn_create(weights: np.ndarray, dims: gnn_dims) -> int:
 
 def gnn_destroy(handle) -> None:
     lib.gnn_destroy(handle)
+
+
+def gnn_release_workspaces(handle) -> int:
+    """Frees the handle's idle cached workspaces; returns the bytes freed."""
+    r = lib.gnn_release_workspaces(handle)
+    if r < 0:
+        raise GnnError(int(r), gnn_last_error())
+    return int(r)
 
 
 def _check_io(node_feat, edge_index, out):

@@ -152,3 +152,32 @@ def test_workspace_cache_reuse_growth_and_overflow(G):
             srv.close()
     finally:
         m.close()
+
+
+def test_release_workspaces(G):
+    """gnn_release_workspaces frees the idle cached buffers (once), and later
+    calls allocate again and give the same results."""
+    w = I.make_weights(3, 64, 1, 74, affine_noise=0.2)
+    m = G.Model(w, G.make_dims(3, 64, 2))
+    try:
+        evs = _events(3)
+        streams = [torch.cuda.Stream() for _ in evs]
+        ref = [m(x, ei).cpu().numpy() for x, ei in evs]
+        outs = [torch.empty(ei.shape[1], device="cuda") for _, ei in evs]
+        torch.cuda.synchronize()
+        for (x, ei), o, st in zip(evs, outs, streams):
+            G.gnn_infer(m.handle, x, ei, x.shape[0], ei.shape[1], o, st)
+        freed = G.gnn_release_workspaces(m.handle)  # waits for those calls
+        assert freed > 0
+        assert G.gnn_release_workspaces(m.handle) == 0
+        for o, r in zip(outs, ref):
+            assert np.array_equal(o.cpu().numpy(), r)
+        again = [m(x, ei).cpu().numpy() for x, ei in evs]
+        for a, r in zip(again, ref):
+            assert np.array_equal(a, r)
+        assert G.gnn_release_workspaces(m.handle) > 0
+        with pytest.raises(G.GnnError) as e:
+            G.gnn_release_workspaces(None)
+        assert e.value.code == G.GNN_E_INVALID_ARG
+    finally:
+        m.close()
