@@ -127,8 +127,9 @@ def main():
         print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "copies": 3}))
         return
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(events are independent; see the sharding notes). Use --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(events are independent: one process per GPU serves them). Use --gpus 1.",
+              file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

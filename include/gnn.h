@@ -47,7 +47,7 @@ extern "C" {
 #define GNN_E_OOM (-3)         /* device or host allocation failed             */
 #define GNN_E_INDEX (-4)       /* edge index out of range (validation on)      */
 #define GNN_E_HIP (-5)         /* a HIP runtime call or kernel launch failed   */
-#define GNN_E_UNSUPPORTED (-6) /* dims or device this build does not support   */
+#define GNN_E_UNSUPPORTED (-6) /* dims or device the library does not support */
 
 /* ---- model description ------------------------------------------------- */
 #define GNN_FP32 0 /* weights and activations fp32                           */
