@@ -1,0 +1,67 @@
+"""Host-side logic of bench.py (no GPU): the one-GPU guard and the
+algorithmic byte and matrix-work counts behind its roofline figures, each
+checked against the per-unit definition written out by hand for the full
+event (300,000 hits, 1,000,513 edges, H = 128, T = 8; 247,893 hits have
+out-edges)."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+N, E, H, T, N_SRC = 300_000, 1_000_513, 128, 8, 247_893
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def test_edge_update_bytes_per_launch():
+    # per edge: e row read and written (2 x 512 B), the two gathered
+    # projection half-rows (2 x 512 B), two int32 indices; per source node
+    # one agg_out row (512 B)
+    per_edge = 2 * 512 + 2 * 512 + 8
+    assert bench.edge_update_bytes(N, E, H, 4, N_SRC) == E * per_edge + N_SRC * 512
+    assert bench.edge_update_bytes(N, E, H, 4, N_SRC) == 2_183_975_944
+    # bf16 rows: e and agg_out halve, the fp32 projections stay
+    assert bench.edge_update_bytes(N, E, H, 2, N_SRC) == E * (2 * 256 + 2 * 512 + 8) + N_SRC * 256
+
+
+def test_aggregate_bytes_per_launch():
+    # fused form: message rows (in-direction) and their int32 positions,
+    # agg_in rows, both row-pointer arrays, a zero agg_out row per hit
+    # without out-edges
+    want = E * 512 + E * 4 + N * 512 + 2 * (N + 1) * 4 + (N - N_SRC) * 512
+    assert bench.aggregate_bytes(N, E, H, 4, N_SRC) == want == 698_943_500
+    # unfused form: both directions of everything
+    assert bench.aggregate_bytes(N, E, H, 4) == 2 * (E * 512 + N * 512 + E * 4 + (N + 1) * 4)
+
+
+def test_node_update_bytes_average_launch():
+    # h, agg_in, agg_out read and the 2H-float projection row written every
+    # launch; h written in 7 of the 8 launches
+    want = N * (3 * 512 + 1024) + N * 512 * 7 / 8
+    assert bench.node_update_bytes(N, H, 4, T) == pytest.approx(want, rel=0, abs=1e-6)
+    assert bench.node_update_bytes(N, H, 4, T) == 902_400_000
+
+
+def test_matrix_work_per_launch():
+    # split fp32: three fp16 products per fp32 product; the edge update runs
+    # W_e e and layer 2 (2 H^2 per edge), the node update layer 1 (3 H^2),
+    # layer 2 (H^2) and the projections (2 H^2)
+    f = bench.split_mfma_flops(N, E, H)
+    assert f["edge_update"] == 3 * 2 * E * 2 * H * H == 196_708_859_904
+    assert f["node_update"] == 3 * 2 * N * 6 * H * H
+    b = bench.split_mfma_flops(N, E, H, bf16=True)
+    assert b["edge_update"] == 2 * 2 * E * 2 * H * H
+    # the fp32 model's algorithmic work: regrouped 2 H^2 per edge, per-edge 4 H^2
+    assert bench.edge_update_flops(E, H, True) == 2 * E * 2 * H * H
+    assert bench.edge_update_flops(E, H, False) == 2 * E * 4 * H * H
