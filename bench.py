@@ -36,8 +36,8 @@ TRAFFIC_SOURCES = {
                   "paper_2402_09633_amd/csrc/device_common.h"],
 }
 # (path, source hash) -> HBM bytes per edge-update launch on the full event
-MEASURED_TRAFFIC = {("split", "33771b6ab0f2de18"): 1.789e9,       # edge_split<4,3>
-                    ("bf16", "33771b6ab0f2de18"): 1.207e9,        # edge_split<4,3,bf16>
+MEASURED_TRAFFIC = {("split", "183abb9ba4c53724"): 1.789e9,       # edge_split<4,3>
+                    ("bf16", "183abb9ba4c53724"): 1.207e9,        # edge_split<4,3,bf16>
                     ("fp32_mfma", "d6fe23f044f63d7b"): 1.651e9}   # edge_f32<4,1>
 
 

@@ -201,9 +201,9 @@ __device__ __forceinline__ void store_rows_bf16(__bf16 *__restrict__ o, const f1
 // full 128-byte lines instead of 32-byte pieces of 32 rows.
 //
 // Rows that a later kernel reads (h, P, e) are stored with the nontemporal
-// hint: their write-back then drains while this kernel runs instead of
-// competing with the reading kernel's gathers (full fp32 event 6.48 ->
-// 6.28 ms with h, P and the updated e stored this way).
+// hint.  Measured on the full fp32 event: 6.48 -> 6.28 ms with h, P and the
+// updated e stored this way, the time saved showing up mostly in the
+// kernels that read those rows next.
 constexpr int SST = 36;  // staging row stride in floats (16-byte aligned rows)
 template <int MB>
 __device__ __forceinline__ void store_block(float *__restrict__ out, int64_t stride, int nvalid,
