@@ -94,6 +94,9 @@ typedef struct gnn_dims {
 typedef struct gnn_handle gnn_handle;
 
 /* Number of floats in the packed weight blob for `dims`, 0 if dims invalid.
+ * Paper section 2.1: the edge-classification step is an interaction network
+ * whose trained weights the pipeline loads (section 2.1: trained PyTorch
+ * models run through libTorch); this blob is that model's parameter set.
  * Blob order (fp32; W is [out][in] row-major, PyTorch Linear convention):
  *   node_enc (F->H->H), edge_enc (2H->H->H),
  *   n_mp_weight_sets x [edge_mlp (3H->H->H), node_mlp (3H->H->H)],
@@ -102,7 +105,10 @@ typedef struct gnn_handle gnn_handle;
  * stores W[1][H] and b[1]. */
 size_t gnn_weight_count(const gnn_dims *dims);
 
-/* Validate dims, convert and upload the HOST fp32 blob `weights` (copied;
+/* Loads one model instance (paper section 2.1: the pipeline loads the trained
+ * interaction network once and runs it for every event; section 3.2: one GPU
+ * may hold several instances, which here share one handle).
+ * Validate dims, convert and upload the HOST fp32 blob `weights` (copied;
  * the caller may free it on return) to the current HIP device.  Returns NULL
  * on error (see gnn_last_error): GNN_E_INVALID_ARG for bad dims or NULL
  * pointers, GNN_E_NO_DEVICE, GNN_E_UNSUPPORTED for a device that is not
@@ -124,7 +130,11 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims);
 int gnn_infer(gnn_handle *h, const float *node_feat, const int32_t *edge_index,
               int64_t n_nodes, int64_t n_edges, float *edge_scores, hipStream_t stream);
 
-/* As gnn_infer, writing the pre-sigmoid logits z instead of the scores. */
+/* As gnn_infer, writing the pre-sigmoid logits z instead of the scores
+ * (paper section 2.1: the classifier's raw output before the sigmoid that
+ * turns it into an edge score; exposed for parity checks, where a logit
+ * keeps precision that a saturated score loses).  Same arguments, layouts,
+ * ownership and errors as gnn_infer. */
 int gnn_infer_logits(gnn_handle *h, const float *node_feat, const int32_t *edge_index,
                      int64_t n_nodes, int64_t n_edges, float *edge_logits,
                      hipStream_t stream);
@@ -158,9 +168,9 @@ int gnn_filter_apply(gnn_filter *f, const float *node_feat, const int32_t *edge_
                      int64_t n_nodes, int64_t n_edges, float threshold, float *edge_scores,
                      int32_t *edge_index_out, int64_t *n_kept, hipStream_t stream);
 
-/* Track candidates from edge scores (paper section 2.1: the GNN edge scores
- * are passed to the weakly-connected-components step; section 2.3: one
- * integer label per space point).  Keeps the edges with
+/* Track candidates from edge scores (paper section 2.1: weakly-connected
+ * components of the scored graph form the track candidates; section 2.3:
+ * the service returns one integer label per space point).  Keeps the edges with
  * edge_scores[j] > threshold (every edge when edge_scores is NULL), treats
  * them as undirected and writes labels[v] = the smallest node id of v's
  * connected component -- unique, so results are bitwise reproducible.
@@ -178,7 +188,10 @@ int gnn_infer_labels(gnn_handle *h, const float *node_feat, const int32_t *edge_
                      int64_t n_nodes, int64_t n_edges, float threshold, float *edge_scores,
                      int32_t *labels, hipStream_t stream);
 
-/* Waits for the device, then frees everything the handle owns.  NULL-safe. */
+/* Unloads the model instance loaded by gnn_create (paper section 2.1).
+ * Waits for the device, then frees everything the handle owns: its weights
+ * and its cached workspaces.  Calls in progress on other threads must have
+ * returned.  NULL-safe. */
 void gnn_destroy(gnn_handle *h);
 
 /* Memory management, not a step of the method: frees the inference
@@ -190,7 +203,22 @@ void gnn_destroy(gnn_handle *h);
  * NULL handle, GNN_E_HIP if waiting or freeing fails. */
 int64_t gnn_release_workspaces(gnn_handle *h);
 
-/* Message of the last failed call on this thread ("" if none). */
+/* Memory management, not a step of the method: caps the bytes of inference
+ * workspace the handle may hold at once (its cached buffers plus buffers of
+ * calls in progress); 0 removes the cap.  A call whose workspace would take
+ * the handle past the cap allocates nothing and returns GNN_E_OOM before
+ * enqueuing any work (outputs untouched); the handle stays usable.  The
+ * initial cap comes from the environment variable GNN_WORKSPACE_LIMIT at
+ * gnn_create (digits with an optional k, m or g suffix, binary units; a
+ * malformed value makes gnn_create fail with GNN_E_INVALID_ARG), else none.
+ * Lowering the cap frees nothing already held (see
+ * gnn_release_workspaces).  Returns GNN_OK, or GNN_E_INVALID_ARG for a NULL
+ * handle or a negative count. */
+int gnn_set_workspace_limit(gnn_handle *h, int64_t bytes);
+
+/* Error reporting, not a step of the method (the paper describes none):
+ * the message of the last failed call on this thread ("" if none).  The
+ * pointer stays valid until the next failing call on the same thread. */
 const char *gnn_last_error(void);
 
 /* ---- graph construction ---------------------------------------------------
@@ -251,19 +279,43 @@ typedef struct gnn_server gnn_server;
 gnn_server *gnn_server_create(gnn_handle *h, int n_instances);
 
 /* Queue one event, with the arguments and device-pointer layouts of
- * gnn_infer.  The buffers must stay valid and the outputs untouched until
+ * gnn_infer.  The workers' streams are not ordered after any stream of the
+ * caller: the inputs must already hold their values on the device when
+ * submit is called (for example, synchronise the stream that produced them
+ * first), and the buffers must stay valid and the outputs untouched until
  * the request is waited for.  Returns the request id (>= 0), or a negative
- * status: GNN_E_INVALID_ARG for NULL pointers, counts outside
- * 0..INT32_MAX or a server that is shutting down. */
+ * status: GNN_E_INVALID_ARG for NULL pointers, counts outside 0..INT32_MAX
+ * or a server that is shutting down. */
 int64_t gnn_server_submit(gnn_server *s, const float *node_feat, const int32_t *edge_index,
                           int64_t n_nodes, int64_t n_edges, float *edge_scores);
 
 /* Block until request `id` has completed and release it; returns the status
  * of its gnn_infer (its message becomes this thread's gnn_last_error).  With
  * latency_ms non-NULL, stores the time from submission to completion
- * (queueing included) in milliseconds.  An id that is unknown or already
- * waited for gives GNN_E_INVALID_ARG. */
+ * (queueing included) in milliseconds.  Only one thread may wait for a
+ * request: an id that is unknown, already released, or being waited for by
+ * another thread gives GNN_E_INVALID_ARG (that other wait is unaffected). */
 int gnn_server_wait(gnn_server *s, int64_t id, double *latency_ms);
+
+/* What gnn_server_wait_info reports about one request.  The device interval
+ * comes from two events the worker records on its stream just before and
+ * just after the request's gnn_infer, in milliseconds since an event
+ * recorded when the server was created; the union of these intervals over
+ * a run, divided by its wall time, is the fraction of that time the GPU
+ * spent on requests (paper section 3.2, Fig. 4b: GPU utilisation against
+ * the number of model instances).  Both are -1 if the request failed. */
+typedef struct gnn_request_info {
+  uint32_t struct_size;   /* = sizeof(gnn_request_info)                        */
+  int32_t status;         /* status of the request's gnn_infer                 */
+  double latency_ms;      /* submission to completion, host clock              */
+  double device_start_ms; /* device interval of the request's work, relative   */
+  double device_end_ms;   /* to the server's creation                          */
+} gnn_request_info;
+
+/* gnn_server_wait, filling *info (struct_size set by the caller).  Returns
+ * the request's status as gnn_server_wait does; GNN_E_INVALID_ARG also for
+ * a NULL info or a wrong struct_size. */
+int gnn_server_wait_info(gnn_server *s, int64_t id, gnn_request_info *info);
 
 /* Finish every queued request, stop the workers, free the server.  Results
  * of requests not waited for are discarded.  NULL-safe. */

@@ -6,6 +6,7 @@ objects are linked into ``paper_2402_09633_amd/libgnn.so``.
 from __future__ import annotations
 
 import glob
+import json
 import os
 import subprocess
 import sys
@@ -16,6 +17,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libgnn.so")
+INFO = os.path.join(HERE, "build_info.json")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -39,6 +41,25 @@ def _compile(src: str) -> str:
     return obj
 
 
+def _git(*args: str) -> str:
+    try:
+        r = subprocess.run(["git", "-C", ROOT, *args], capture_output=True, text=True, timeout=30)
+        return r.stdout.strip() if r.returncode == 0 else ""
+    except Exception:  # no git: the revision is left empty
+        return ""
+
+
+def _write_info() -> None:
+    """Records what the library was built from (reported by bench.py)."""
+    hip = subprocess.run([HIPCC, "--version"], capture_output=True, text=True).stdout
+    info = {"git_sha": _git("rev-parse", "HEAD"),
+            "git_dirty": bool(_git("status", "--porcelain", "--untracked-files=no")),
+            "hipcc_flags": " ".join(FLAGS[:-2]),
+            "hipcc": next((l.strip() for l in hip.splitlines() if "HIP version" in l), "")}
+    with open(INFO, "w") as f:
+        json.dump(info, f)
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
@@ -48,6 +69,7 @@ def build(verbose: bool = False) -> str:
     subprocess.run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp],
                    check=True)
     os.replace(tmp, LIB)
+    _write_info()
     if verbose:
         print("built", LIB)
     return LIB

@@ -11,9 +11,11 @@
 // one handle can serve several streams at once.  The other entry points
 // allocate stream-ordered (hipMallocAsync/hipFreeAsync) from the device's
 // default pool, whose release threshold is raised.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <string>
@@ -300,6 +302,10 @@ struct gnn_handle {
   };
   std::mutex ws_mu;
   std::vector<WsEntry> ws;
+  // Most bytes of workspace the handle may hold at once (cached entries plus
+  // call-owned allocations in flight); 0 = no limit.
+  size_t ws_limit = 0;
+  size_t ws_held = 0;
 };
 
 namespace {
@@ -544,6 +550,44 @@ struct StageTimer {
   }
 };
 
+// Parses a byte count: decimal digits with an optional binary suffix k, m or
+// g (either case).  Returns false for anything else or on overflow.
+bool parse_bytes(const char *txt, size_t *out) {
+  if (!txt || !*txt) return false;
+  size_t v = 0;
+  const char *p = txt;
+  for (; *p >= '0' && *p <= '9'; ++p) {
+    const size_t d = (size_t)(*p - '0');
+    if (v > (SIZE_MAX - d) / 10) return false;
+    v = v * 10 + d;
+  }
+  if (p == txt) return false;
+  int shift = 0;
+  if (*p) {
+    switch (*p) {
+      case 'k': case 'K': shift = 10; break;
+      case 'm': case 'M': shift = 20; break;
+      case 'g': case 'G': shift = 30; break;
+      default: return false;
+    }
+    if (p[1]) return false;
+  }
+  if (shift && v > (SIZE_MAX >> shift)) return false;
+  *out = v << shift;
+  return true;
+}
+
+// Fails with GNN_E_OOM if taking `more` bytes would exceed the handle's
+// workspace limit (caller holds ws_mu).
+int ws_check_limit(gnn_handle *h, size_t more) {
+  if (h->ws_limit && h->ws_held + more > h->ws_limit)
+    return fail(GNN_E_OOM,
+                "workspace limit of %zu bytes reached: the handle holds %zu bytes and this call "
+                "needs %zu more (see gnn_set_workspace_limit)",
+                h->ws_limit, h->ws_held, more);
+  return GNN_OK;
+}
+
 // Most cached workspaces per handle; beyond this, calls share entries
 // (ordered by events) rather than allocate more.
 constexpr size_t kMaxCachedWorkspaces = 16;
@@ -572,7 +616,11 @@ int ws_acquire(gnn_handle *h, size_t bytes, hipStream_t stream, void **base, int
       rank = r;
     }
   }
-  if (pick >= 0 && rank == 2 && ws.size() < kMaxCachedWorkspaces) pick = -1;
+  // A buffer still in use on another stream is taken (after its work) only
+  // when the cache has no room for a new one, or the workspace limit none.
+  if (pick >= 0 && rank == 2 && ws.size() < kMaxCachedWorkspaces &&
+      !(h->ws_limit && h->ws_held + ws_round(bytes) > h->ws_limit))
+    pick = -1;
   if (pick < 0) {
     int victim = -1;
     for (int i = 0; i < (int)ws.size() && victim < 0; ++i)  // emptied by a release
@@ -582,8 +630,12 @@ int ws_acquire(gnn_handle *h, size_t bytes, hipStream_t stream, void **base, int
         if (!ws[i].busy) victim = i;
     if (ws.size() >= kMaxCachedWorkspaces && victim < 0) {
       *slot = -1;
+      if (const int lr = ws_check_limit(h, bytes)) return lr;
       const hipError_t ae = hipMallocAsync(base, bytes, stream);
-      if (ae == hipSuccess) return GNN_OK;
+      if (ae == hipSuccess) {
+        h->ws_held += bytes;
+        return GNN_OK;
+      }
       (void)hipGetLastError();
       return fail(ae == hipErrorOutOfMemory ? GNN_E_OOM : GNN_E_HIP,
                   "hipMallocAsync(%zu bytes) failed: %s", bytes, hipGetErrorString(ae));
@@ -592,15 +644,20 @@ int ws_acquire(gnn_handle *h, size_t bytes, hipStream_t stream, void **base, int
       // Replaced in place: busy entries keep their indices.  Its last call
       // must end before the memory goes back.
       auto &v = ws[victim];
-      if (hipEventSynchronize(v.done) != hipSuccess || hipFree(v.base) != hipSuccess) {
+      if (v.base && ws_check_limit(h, ws_round(bytes) - std::min(v.bytes, ws_round(bytes))))
+        return GNN_E_OOM;
+      if (v.base &&
+          (hipEventSynchronize(v.done) != hipSuccess || hipFree(v.base) != hipSuccess)) {
         (void)hipGetLastError();
         return fail(GNN_E_HIP, "releasing a cached workspace failed");
       }
+      h->ws_held -= v.bytes;
       v.base = nullptr;
       v.bytes = 0;
       v.recorded = false;
       pick = victim;
     } else {
+      if (const int lr = ws_check_limit(h, ws_round(bytes))) return lr;
       gnn_handle::WsEntry e{nullptr, 0, nullptr, stream, false, false};
       if (hipEventCreateWithFlags(&e.done, hipEventDisableTiming) != hipSuccess) {
         (void)hipGetLastError();
@@ -611,6 +668,7 @@ int ws_acquire(gnn_handle *h, size_t bytes, hipStream_t stream, void **base, int
     }
     auto &e = ws[pick];
     const size_t want = ws_round(bytes);
+    if (const int lr = ws_check_limit(h, want)) return lr;
     const hipError_t ae = hipMalloc(&e.base, want);
     if (ae != hipSuccess) {  // the entry stays, empty, for a later call
       (void)hipGetLastError();
@@ -619,6 +677,7 @@ int ws_acquire(gnn_handle *h, size_t bytes, hipStream_t stream, void **base, int
                   "hipMalloc(%zu bytes) of a workspace failed: %s", want, hipGetErrorString(ae));
     }
     e.bytes = want;
+    h->ws_held += want;
   }
   auto &e = ws[pick];
   if (e.recorded && hipStreamWaitEvent(stream, e.done, 0) != hipSuccess)
@@ -632,8 +691,12 @@ int ws_acquire(gnn_handle *h, size_t bytes, hipStream_t stream, void **base, int
 
 // Ends the host side of a call: marks the end of its work on `stream` so the
 // next user of the entry can wait for it.
-int ws_release(gnn_handle *h, int slot, void *base, hipStream_t stream) {
+int ws_release(gnn_handle *h, int slot, void *base, size_t bytes, hipStream_t stream) {
   if (slot < 0) {
+    {
+      std::lock_guard<std::mutex> lk(h->ws_mu);
+      h->ws_held -= bytes;
+    }
     const hipError_t fe = hipFreeAsync(base, stream);
     return fe == hipSuccess ? GNN_OK
                             : fail(GNN_E_HIP, "hipFreeAsync failed: %s", hipGetErrorString(fe));
@@ -954,7 +1017,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
 out:
   total.end(GNN_STAGE_TOTAL);
   {
-    const int rr = ws_release(hd, slot, w.base, stream);
+    const int rr = ws_release(hd, slot, w.base, w.bytes, stream);
     if (rc == GNN_OK) rc = rr;
   }
   return rc;
@@ -985,6 +1048,14 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
   if (!weights) {
     fail(GNN_E_INVALID_ARG, "weights is NULL");
     return nullptr;
+  }
+  size_t ws_limit = 0;
+  if (const char *lim = getenv("GNN_WORKSPACE_LIMIT")) {
+    if (!parse_bytes(lim, &ws_limit)) {
+      fail(GNN_E_INVALID_ARG,
+           "GNN_WORKSPACE_LIMIT='%s' is not a byte count (digits, optional k/m/g suffix)", lim);
+      return nullptr;
+    }
   }
   int ndev = 0;
   if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0) {
@@ -1183,6 +1254,7 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
 
   gnn_handle *h = new gnn_handle();
   h->dims = d;
+  h->ws_limit = ws_limit;
   h->device = dev;
   if (hipMalloc(&h->dev_weights, st.bytes.size()) != hipSuccess) {
     (void)hipGetLastError();
@@ -1251,11 +1323,20 @@ int64_t gnn_release_workspaces(gnn_handle *h) {
       return fail(GNN_E_HIP, "releasing a cached workspace failed");
     }
     freed += (int64_t)e.bytes;
+    h->ws_held -= e.bytes;
     e.base = nullptr;
     e.bytes = 0;
     e.recorded = false;
   }
   return freed;
+}
+
+int gnn_set_workspace_limit(gnn_handle *h, int64_t bytes) {
+  if (!h) return fail(GNN_E_INVALID_ARG, "handle is NULL");
+  if (bytes < 0) return fail(GNN_E_INVALID_ARG, "negative workspace limit %lld", (long long)bytes);
+  std::lock_guard<std::mutex> lk(h->ws_mu);
+  h->ws_limit = (size_t)bytes;
+  return GNN_OK;
 }
 
 void gnn_destroy(gnn_handle *h) {

@@ -7,7 +7,11 @@
 // take requests from one FIFO queue; every request is one gnn_infer call on
 // the shared handle (the library is reentrant across streams), followed by a
 // synchronisation of the worker's stream.  Latency is measured on the host
-// from submission to completion, so it includes the time spent queued.
+// from submission to completion, so it includes the time spent queued.  Each
+// request is also bracketed by two events on the worker's stream, which give
+// its device interval relative to an event recorded when the server was
+// created: the union of those intervals over a run is the time the GPU spent
+// on requests (the utilisation of the paper's Fig. 4b).
 #include <chrono>
 #include <condition_variable>
 #include <cstdint>
@@ -31,7 +35,9 @@ struct Request {
   int64_t n_nodes = 0, n_edges = 0;
   float *out = nullptr;
   clock_t_::time_point submitted, done_at;
+  double dev_start_ms = -1.0, dev_end_ms = -1.0;  // device interval (< 0: unknown)
   bool done = false;
+  bool claimed = false;  // a thread is waiting for it (only that one may release it)
   int status = GNN_OK;
   std::string error;
 };
@@ -45,20 +51,28 @@ struct gnn_server {
   std::mutex mu;
   std::condition_variable cv_work, cv_done;
   std::deque<int64_t> queue;
+  // Node-based map: references to its elements stay valid when a submit
+  // rehashes it; only the claiming waiter erases an element.
   std::unordered_map<int64_t, Request> reqs;
   int64_t next_id = 0;
   bool stopping = false;
   int start_errors = 0;
+  hipEvent_t t0 = nullptr;  // time origin of the device intervals
 };
 
 namespace {
 
 void worker(gnn_server *s) {
   hipStream_t stream = nullptr;
+  hipEvent_t ev[2] = {nullptr, nullptr};
   const bool ok = hipSetDevice(s->device) == hipSuccess &&
-                  hipStreamCreateWithFlags(&stream, hipStreamNonBlocking) == hipSuccess;
+                  hipStreamCreateWithFlags(&stream, hipStreamNonBlocking) == hipSuccess &&
+                  hipEventCreate(&ev[0]) == hipSuccess && hipEventCreate(&ev[1]) == hipSuccess;
   if (!ok) {
     (void)hipGetLastError();
+    for (hipEvent_t e : ev)
+      if (e) (void)hipEventDestroy(e);
+    if (stream) (void)hipStreamDestroy(stream);
     std::lock_guard<std::mutex> lk(s->mu);
     ++s->start_errors;
     s->cv_done.notify_all();
@@ -73,9 +87,12 @@ void worker(gnn_server *s) {
       if (s->queue.empty()) break;  // stopping and drained
       id = s->queue.front();
       s->queue.pop_front();
-      r = s->reqs[id];
+      r = s->reqs.at(id);
     }
+    // (the events are reused: the previous request's work has finished)
+    const bool timed = hipEventRecord(ev[0], stream) == hipSuccess;
     int rc = gnn_infer(s->model, r.x, r.ei, r.n_nodes, r.n_edges, r.out, stream);
+    const bool timed_end = timed && hipEventRecord(ev[1], stream) == hipSuccess;
     std::string err;
     if (rc == GNN_OK) {
       const hipError_t e = hipStreamSynchronize(stream);
@@ -86,17 +103,53 @@ void worker(gnn_server *s) {
     } else {
       err = gnn_last_error();
     }
+    float t_a = -1.f, t_b = -1.f;
+    if (!(rc == GNN_OK && timed_end && hipEventSynchronize(ev[1]) == hipSuccess &&
+          hipEventElapsedTime(&t_a, s->t0, ev[0]) == hipSuccess &&
+          hipEventElapsedTime(&t_b, s->t0, ev[1]) == hipSuccess)) {
+      (void)hipGetLastError();
+      t_a = t_b = -1.f;
+    }
     {
       std::lock_guard<std::mutex> lk(s->mu);
-      Request &q = s->reqs[id];
+      Request &q = s->reqs.at(id);
       q.status = rc;
       q.error = err;
       q.done_at = clock_t_::now();
+      q.dev_start_ms = t_a;
+      q.dev_end_ms = t_b;
       q.done = true;
     }
     s->cv_done.notify_all();
   }
+  for (hipEvent_t e : ev) (void)hipEventDestroy(e);
   (void)hipStreamDestroy(stream);
+}
+
+// Waits for request `id`, releases it and returns a copy.  Only one thread
+// may wait for a given request: a second one gets GNN_E_INVALID_ARG.
+int take_request(gnn_server *s, int64_t id, Request *out) {
+  if (!s) return gnn::set_error(GNN_E_INVALID_ARG, "server is NULL");
+  std::unique_lock<std::mutex> lk(s->mu);
+  {
+    auto it = s->reqs.find(id);
+    if (it == s->reqs.end()) return gnn::set_error(GNN_E_INVALID_ARG, "unknown request id");
+    if (it->second.claimed)
+      return gnn::set_error(GNN_E_INVALID_ARG, "another thread is waiting for this request");
+    it->second.claimed = true;
+  }
+  // Looked up again after every wake-up: a submit may have rehashed the map.
+  s->cv_done.wait(lk, [&] {
+    return s->reqs.at(id).done || s->start_errors == (int)s->workers.size();
+  });
+  auto it = s->reqs.find(id);
+  if (!it->second.done) {
+    it->second.claimed = false;
+    return gnn::set_error(GNN_E_HIP, "no worker could create its stream");
+  }
+  *out = it->second;
+  s->reqs.erase(it);
+  return GNN_OK;
 }
 
 }  // namespace
@@ -113,6 +166,14 @@ gnn_server *gnn_server_create(gnn_handle *h, int n_instances) {
   if (hipGetDevice(&s->device) != hipSuccess) {
     delete s;
     gnn::set_error(GNN_E_NO_DEVICE, "hipGetDevice failed");
+    return nullptr;
+  }
+  if (hipEventCreate(&s->t0) != hipSuccess || hipEventRecord(s->t0, nullptr) != hipSuccess ||
+      hipEventSynchronize(s->t0) != hipSuccess) {
+    (void)hipGetLastError();
+    if (s->t0) (void)hipEventDestroy(s->t0);
+    delete s;
+    gnn::set_error(GNN_E_HIP, "creating the server's time-origin event failed");
     return nullptr;
   }
   for (int i = 0; i < n_instances; ++i) s->workers.emplace_back(worker, s);
@@ -144,19 +205,25 @@ int64_t gnn_server_submit(gnn_server *s, const float *node_feat, const int32_t *
 }
 
 int gnn_server_wait(gnn_server *s, int64_t id, double *latency_ms) {
-  if (!s) return gnn::set_error(GNN_E_INVALID_ARG, "server is NULL");
-  std::unique_lock<std::mutex> lk(s->mu);
-  auto it = s->reqs.find(id);
-  if (it == s->reqs.end()) return gnn::set_error(GNN_E_INVALID_ARG, "unknown request id");
-  s->cv_done.wait(lk, [&] {
-    return it->second.done || s->start_errors == (int)s->workers.size();
-  });
-  if (!it->second.done) return gnn::set_error(GNN_E_HIP, "no worker could create its stream");
-  const Request r = it->second;
-  s->reqs.erase(it);
-  lk.unlock();
+  Request r;
+  const int rc = take_request(s, id, &r);
+  if (rc != GNN_OK) return rc;
   if (latency_ms)
     *latency_ms = std::chrono::duration<double, std::milli>(r.done_at - r.submitted).count();
+  if (r.status != GNN_OK) return gnn::set_error(r.status, r.error.c_str());
+  return GNN_OK;
+}
+
+int gnn_server_wait_info(gnn_server *s, int64_t id, gnn_request_info *info) {
+  if (!info || info->struct_size != sizeof(gnn_request_info))
+    return gnn::set_error(GNN_E_INVALID_ARG, "info is NULL or info->struct_size is wrong");
+  Request r;
+  const int rc = take_request(s, id, &r);
+  if (rc != GNN_OK) return rc;
+  info->status = r.status;
+  info->latency_ms = std::chrono::duration<double, std::milli>(r.done_at - r.submitted).count();
+  info->device_start_ms = r.dev_start_ms;
+  info->device_end_ms = r.dev_end_ms;
   if (r.status != GNN_OK) return gnn::set_error(r.status, r.error.c_str());
   return GNN_OK;
 }
@@ -169,6 +236,7 @@ void gnn_server_destroy(gnn_server *s) {
   }
   s->cv_work.notify_all();
   for (auto &t : s->workers) t.join();
+  (void)hipEventDestroy(s->t0);
   delete s;
 }
 

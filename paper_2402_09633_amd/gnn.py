@@ -35,7 +35,8 @@ EXPORTS = ("gnn_weight_count", "gnn_create", "gnn_infer", "gnn_infer_logits",
            "gnn_filter_destroy", "gnn_wcc", "gnn_infer_labels", "gnn_destroy",
            "gnn_release_workspaces", "gnn_last_error",
            "gnn_profile_enable", "gnn_profile_read", "gnn_debug_csr", "gnn_debug_stages",
-           "gnn_server_create", "gnn_server_submit", "gnn_server_wait", "gnn_server_destroy",
+           "gnn_server_create", "gnn_server_submit", "gnn_server_wait", "gnn_server_wait_info",
+           "gnn_server_destroy", "gnn_set_workspace_limit",
            "gnn_embed_weight_count", "gnn_embed_create", "gnn_embed_apply", "gnn_embed_destroy",
            "gnn_frnn")
 STAGES = ("csr", "node_enc", "edge_enc", "edge_update", "aggregate", "node_update",
@@ -73,6 +74,12 @@ def make_filter_dims(in_features=3, hidden=64, ln_eps=1e-5) -> gnn_filter_dims:
 class gnn_profile_stats(ctypes.Structure):
     _fields_ = [("struct_size", ctypes.c_uint32), ("n_calls", ctypes.c_int32),
                 ("launches", ctypes.c_int64 * 8), ("ms", ctypes.c_double * 8)]
+
+
+class gnn_request_info(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("status", ctypes.c_int32),
+                ("latency_ms", ctypes.c_double), ("device_start_ms", ctypes.c_double),
+                ("device_end_ms", ctypes.c_double)]
 
 
 class GnnError(RuntimeError):
@@ -113,6 +120,8 @@ def _load():
     L.gnn_destroy.argtypes = [vp]
     L.gnn_release_workspaces.restype = ctypes.c_int64
     L.gnn_release_workspaces.argtypes = [vp]
+    L.gnn_set_workspace_limit.restype = ctypes.c_int
+    L.gnn_set_workspace_limit.argtypes = [vp, i64]
     L.gnn_last_error.restype = ctypes.c_char_p
     L.gnn_last_error.argtypes = []
     L.gnn_profile_enable.restype = ctypes.c_int
@@ -141,6 +150,8 @@ def _load():
     L.gnn_server_submit.argtypes = [vp, vp, vp, i64, i64, vp]
     L.gnn_server_wait.restype = ctypes.c_int
     L.gnn_server_wait.argtypes = [vp, i64, ctypes.POINTER(ctypes.c_double)]
+    L.gnn_server_wait_info.restype = ctypes.c_int
+    L.gnn_server_wait_info.argtypes = [vp, i64, ctypes.POINTER(gnn_request_info)]
     L.gnn_server_destroy.restype = None
     L.gnn_server_destroy.argtypes = [vp]
     return L
@@ -208,6 +219,11 @@ def gnn_release_workspaces(handle) -> int:
     if r < 0:
         raise GnnError(int(r), gnn_last_error())
     return int(r)
+
+
+def gnn_set_workspace_limit(handle, n_bytes: int) -> int:
+    """Caps the handle's inference workspace bytes (0 = no cap)."""
+    return _check(lib.gnn_set_workspace_limit(handle, int(n_bytes)))
 
 
 def _check_io(node_feat, edge_index, out):
@@ -418,6 +434,14 @@ def gnn_server_wait(server, request_id: int) -> float:
     return lat.value
 
 
+def gnn_server_wait_info(server, request_id: int) -> dict:
+    """Wait for one request; returns its status, latency and device interval (ms)."""
+    info = gnn_request_info(ctypes.sizeof(gnn_request_info), 0, 0.0, -1.0, -1.0)
+    _check(lib.gnn_server_wait_info(server, int(request_id), ctypes.byref(info)))
+    return {"status": info.status, "latency_ms": info.latency_ms,
+            "device_start_ms": info.device_start_ms, "device_end_ms": info.device_end_ms}
+
+
 def gnn_server_destroy(server) -> None:
     lib.gnn_server_destroy(server)
 
@@ -434,6 +458,9 @@ class Server:
 
     def wait(self, request_id: int) -> float:
         return gnn_server_wait(self.server, request_id)
+
+    def wait_info(self, request_id: int) -> dict:
+        return gnn_server_wait_info(self.server, request_id)
 
     def close(self):
         if self.server:

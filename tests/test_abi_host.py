@@ -118,3 +118,37 @@ def test_product_path_never_touches_the_oracle():
 def test_filter_weight_count_matches_generator(G, F, H):
     assert G.gnn_filter_weight_count(G.make_filter_dims(F, H)) == I.filter_weight_count(F, H)
     assert G.gnn_filter_weight_count(G.make_filter_dims(F, 96)) == 0
+
+
+@pytest.mark.parametrize("value", ["12x", "", "-5", "1.5g", "k", "99999999999999999999999"])
+def test_malformed_workspace_limit_rejected_at_create(G, value, monkeypatch):
+    # The workspace cap is read from GNN_WORKSPACE_LIMIT before any device
+    # call, so a malformed value fails gnn_create on any machine.
+    monkeypatch.setenv("GNN_WORKSPACE_LIMIT", value)
+    d = G.make_dims(3, 64, 2)
+    w = I.make_weights(3, 64, 1, 0)
+    assert G.lib.gnn_create(w.ctypes.data, ctypes.byref(d)) is None
+    assert "GNN_WORKSPACE_LIMIT" in G.gnn_last_error()
+
+
+@pytest.mark.skipif(torch.cuda.device_count() > 0, reason="a GPU is visible")
+@pytest.mark.parametrize("value", ["0", "1048576", "64k", "512M", "2G"])
+def test_wellformed_workspace_limit_passes_parsing(G, value, monkeypatch):
+    # a valid cap is accepted; without a device the call then stops there
+    monkeypatch.setenv("GNN_WORKSPACE_LIMIT", value)
+    d = G.make_dims(3, 64, 2)
+    w = I.make_weights(3, 64, 1, 0)
+    assert G.lib.gnn_create(w.ctypes.data, ctypes.byref(d)) is None
+    assert "device" in G.gnn_last_error()
+
+
+def test_workspace_limit_and_server_calls_reject_null(G):
+    assert G.lib.gnn_set_workspace_limit(None, 0) == G.GNN_E_INVALID_ARG
+    assert "NULL" in G.gnn_last_error()
+    info = G.gnn_request_info(ctypes.sizeof(G.gnn_request_info), 0, 0.0, -1.0, -1.0)
+    assert G.lib.gnn_server_wait_info(None, 0, ctypes.byref(info)) == G.GNN_E_INVALID_ARG
+    bad = G.gnn_request_info(4, 0, 0.0, -1.0, -1.0)
+    assert G.lib.gnn_server_wait_info(None, 0, ctypes.byref(bad)) == G.GNN_E_INVALID_ARG
+    assert "struct_size" in G.gnn_last_error()
+    assert G.lib.gnn_server_wait(None, 0, None) == G.GNN_E_INVALID_ARG
+    assert G.lib.gnn_server_submit(None, None, None, 1, 1, None) == G.GNN_E_INVALID_ARG

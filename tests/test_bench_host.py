@@ -65,3 +65,19 @@ def test_matrix_work_per_launch():
     # the fp32 model's algorithmic work: regrouped 2 H^2 per edge, per-edge 4 H^2
     assert bench.edge_update_flops(E, H, True) == 2 * E * 2 * H * H
     assert bench.edge_update_flops(E, H, False) == 2 * E * 4 * H * H
+
+
+def test_union_of_device_intervals():
+    # the utilisation figure: overlapping requests count once, gaps not at all
+    assert bench.union_ms([]) == 0.0
+    assert bench.union_ms([(0.0, 1.0)]) == 1.0
+    assert bench.union_ms([(0.0, 1.0), (0.5, 2.0), (3.0, 4.0), (3.5, 3.6)]) == 3.0
+    assert bench.union_ms([(3.0, 4.0), (0.0, 1.0), (1.0, 2.0)]) == 3.0  # order-free, touching
+
+
+def test_max_scaled_error_definition():
+    # |z - z_ref| / max(1, |z_ref|): absolute below 1, relative above
+    assert bench.max_scaled_err([0.5, 10.0], [0.5, 10.0]) == 0.0
+    assert bench.max_scaled_err([0.0], [1e-3]) == pytest.approx(1e-3)
+    assert bench.max_scaled_err([101.0], [100.0]) == pytest.approx(1e-2)
+    assert bench.max_scaled_err([], []) == 0.0

@@ -46,3 +46,7 @@ def test_bench_json_line_tiny_workload():
     cb = rec["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["cores"] >= 1 and cb["value"] > 0
     assert cb["unit"] == "edges/s" and cb["sample"]
+    assert cb["host"]["physical_cores_in_affinity"] >= 1
+    par = rec["parity"]
+    assert par["n_edges_compared"] == g.n_edges and par["pass"] is True
+    assert par["max_scaled_logit_err"] <= 1e-4

@@ -1,0 +1,158 @@
+"""Every edge of the full-size workloads against a live run of the fp64
+oracle, through the C ABI.
+
+- The 300k-hit / 1.0M-edge layered event (H = 128, T = 8): fp32 logits of
+  all three fp32 kernel sets within 1e-4 * max(1, |z|); bf16 scores of both
+  bf16 kernel sets within 2e-2 of the oracle of the same fp32 weights; the
+  same event with its edge list shuffled, against the oracle's logits moved
+  with the edges.
+- The ragged service batch (8 events of 0.8-1.36M edges): all 8 events on 8
+  streams of one handle, each bitwise equal to its single-stream run and to
+  the request queue's result with 8 instances, and every edge of every event
+  against the oracle.
+
+The oracle runs once per event (module fixtures) on the host's threads.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2402_09633_amd import inputs as I
+from tests.gpu_util import BF16_SCORE_ATOL, assert_logits_close, dev
+
+pytestmark = pytest.mark.gpu
+
+# fp32 kernel sets: split products (0), fp32 matrix cores (GNN_FP32_MFMA = 4),
+# per-edge first layer (GNN_LITERAL_GATHER = 2); bf16: regrouped (0), per-edge (2)
+FP32_PATHS = [0, 4, 2]
+BF16_PATHS = [0, 2]
+# |s - s_ref| implied by the logit bar: sigma' <= 1/4, and max(1, |z|) sigma'(z) <= 1/4
+FP32_SCORE_ATOL = 2.5e-5
+
+
+@pytest.fixture(scope="module")
+def G():
+    from paper_2402_09633_amd import gnn
+    return gnn
+
+
+@pytest.fixture(scope="module")
+def full_event(oracle_mod):
+    c = I.CONFIGS["full"]
+    g = I.make_graph(c)
+    w = I.make_weights(3, c.hidden, 1, c.weight_seed)
+    print(f"full event N={g.n_nodes} E={g.n_edges}: oracle on {oracle_mod.max_threads()} "
+          f"threads", flush=True)
+    ref = oracle_mod.forward(w, g.x, g.edge_index, c.hidden, c.n_iters)
+    return c, g, w, ref
+
+
+def _infer(G, m, xd, eid, logits):
+    out = torch.full((eid.shape[1],), float("nan"), device="cuda")
+    torch.cuda.synchronize()
+    m(xd, eid, out=out, logits=logits)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+@pytest.mark.parametrize("flags", FP32_PATHS)
+def test_full_fp32_every_edge(G, full_event, flags):
+    c, g, w, ref = full_event
+    m = G.Model(w, G.make_dims(3, c.hidden, c.n_iters, flags=flags))
+    try:
+        xd, eid = dev(g.x), dev(g.edge_index)
+        z = _infer(G, m, xd, eid, True)
+        s = _infer(G, m, xd, eid, False)
+    finally:
+        m.close()
+    err = assert_logits_close(z, ref["logits"], what=f"full fp32 flags={flags}")
+    serr = float(np.abs(s - ref["scores"]).max())
+    print(f"full fp32 flags={flags}: {g.n_edges} edges, max scaled logit error {err:.2e}, "
+          f"max score error {serr:.2e}", flush=True)
+    assert serr <= FP32_SCORE_ATOL
+
+
+@pytest.mark.parametrize("flags", BF16_PATHS)
+def test_full_bf16_every_edge(G, full_event, flags):
+    c, g, w, ref = full_event
+    m = G.Model(w, G.make_dims(3, c.hidden, c.n_iters, dtype=G.GNN_BF16, flags=flags))
+    try:
+        s = _infer(G, m, dev(g.x), dev(g.edge_index), False)
+    finally:
+        m.close()
+    err = np.abs(s.astype(np.float64) - ref["scores"])
+    print(f"full bf16 flags={flags}: {g.n_edges} edges, max score error {err.max():.3e}, "
+          f"p99 {np.percentile(err, 99):.3e}", flush=True)
+    assert err.max() <= BF16_SCORE_ATOL
+
+
+def test_full_shuffled_edge_order_every_edge(G, full_event):
+    # The oracle is equivariant under edge permutations (pinned on the CPU),
+    # so the shuffled event's logits are the oracle's moved with the edges.
+    c, g, w, ref = full_event
+    gs, p = I.shuffled(g, 21)
+    m = G.Model(w, G.make_dims(3, c.hidden, c.n_iters))
+    try:
+        z = _infer(G, m, dev(gs.x), dev(gs.edge_index), True)
+    finally:
+        m.close()
+    err = assert_logits_close(z, ref["logits"][p], what="full, shuffled edges")
+    print(f"full shuffled: max scaled logit error {err:.2e}", flush=True)
+
+
+@pytest.fixture(scope="module")
+def batch_run(G):
+    """All 8 ragged events: one at a time on one stream, then all 8 on 8
+    streams at once, then through the request queue with 8 instances."""
+    c = I.CONFIGS["batch"]
+    events = I.make_batch(c)
+    w = I.make_weights(3, c.hidden, 1, c.weight_seed)
+    print(f"batch: E = {[g.n_edges for g in events]}", flush=True)
+    m = G.Model(w, G.make_dims(3, c.hidden, c.n_iters))
+    try:
+        xs = [dev(g.x) for g in events]
+        eis = [dev(g.edge_index) for g in events]
+        single_z = [_infer(G, m, x, ei, True) for x, ei in zip(xs, eis)]
+        single_s = [_infer(G, m, x, ei, False) for x, ei in zip(xs, eis)]
+        outs = [torch.full((ei.shape[1],), float("nan"), device="cuda") for ei in eis]
+        streams = [torch.cuda.Stream() for _ in events]
+        torch.cuda.synchronize()
+        for x, ei, o, st in zip(xs, eis, outs, streams):
+            G.gnn_infer_logits(m.handle, x, ei, x.shape[0], ei.shape[1], o, st)
+        torch.cuda.synchronize()
+        multi_z = [o.cpu().numpy() for o in outs]
+        outs = [torch.full((ei.shape[1],), float("nan"), device="cuda") for ei in eis]
+        torch.cuda.synchronize()  # the workers' streams do not wait for torch's
+        srv = G.Server(m, 8)
+        try:
+            ids = [srv.submit(x, ei, o) for x, ei, o in zip(xs, eis, outs)]
+            for i in ids:
+                srv.wait(i)
+        finally:
+            srv.close()
+        server_s = [o.cpu().numpy() for o in outs]
+    finally:
+        m.close()
+    return {"cfg": c, "events": events, "w": w, "single_z": single_z, "single_s": single_s,
+            "multi_z": multi_z, "server_s": server_s}
+
+
+def test_batch_8_streams_bitwise_equal_single_stream(batch_run):
+    for k in range(8):
+        assert np.array_equal(batch_run["multi_z"][k], batch_run["single_z"][k]), f"event {k}"
+
+
+def test_batch_server_8_instances_bitwise_equal_single_stream(batch_run):
+    for k in range(8):
+        assert np.array_equal(batch_run["server_s"][k], batch_run["single_s"][k]), f"event {k}"
+
+
+@pytest.mark.parametrize("k", range(8))
+def test_batch_event_every_edge_vs_oracle(batch_run, oracle_mod, k):
+    c, g, w = batch_run["cfg"], batch_run["events"][k], batch_run["w"]
+    ref = oracle_mod.forward(w, g.x, g.edge_index, c.hidden, c.n_iters)
+    err = assert_logits_close(batch_run["multi_z"][k], ref["logits"], what=f"batch event {k}")
+    serr = float(np.abs(batch_run["server_s"][k] - ref["scores"]).max())
+    print(f"batch event {k}: N={g.n_nodes} E={g.n_edges} max scaled logit error {err:.2e}, "
+          f"server max score error {serr:.2e}", flush=True)
+    assert serr <= FP32_SCORE_ATOL

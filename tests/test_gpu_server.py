@@ -1,12 +1,19 @@
 """The request queue in front of several model instances (gnn_server_*),
 called through the C ABI: every request must give exactly what a direct
 gnn_infer call gives (the kernels are deterministic), whatever the number of
-instances and the order in which the workers take the requests."""
+instances and the order in which the workers take the requests, and both
+must match the fp64 oracle.  Also: concurrent submitters and waiters, the
+device intervals behind the utilisation figure, and the workspace limit
+that forces the out-of-memory path."""
+import threading
+import time
+
 import numpy as np
 import pytest
 import torch
 
 from paper_2402_09633_amd import inputs as I
+from tests.gpu_util import dev
 
 pytestmark = pytest.mark.gpu
 
@@ -30,11 +37,14 @@ def _events(k):
 
 
 @pytest.mark.parametrize("n_inst", [1, 3, 8])
-def test_server_results_equal_direct_calls(G, n_inst):
+def test_server_results_equal_direct_calls(G, oracle_mod, n_inst):
     w = I.make_weights(3, 64, 1, 71, affine_noise=0.2)
     m = G.Model(w, G.make_dims(3, 64, 2))
     evs = _events(12)
     ref = [m(x, ei).cpu().numpy() for x, ei in evs]
+    for k, (x, ei) in enumerate(evs):
+        orc = oracle_mod.forward(w, x.cpu().numpy(), ei.cpu().numpy(), 64, 2)["scores"]
+        assert np.abs(ref[k] - orc).max() <= 2.5e-5, f"event {k} vs oracle"
     torch.cuda.synchronize()
     srv = G.Server(m, n_inst)
     try:
@@ -179,5 +189,157 @@ def test_release_workspaces(G):
         with pytest.raises(G.GnnError) as e:
             G.gnn_release_workspaces(None)
         assert e.value.code == G.GNN_E_INVALID_ARG
+    finally:
+        m.close()
+
+
+def test_server_concurrent_submitter_and_two_waiters(G, oracle_mod):
+    # One thread submits while two others wait on distinct ids (even / odd)
+    # as the ids appear; every request must succeed and equal the direct call.
+    w = I.make_weights(3, 64, 1, 75, affine_noise=0.2)
+    m = G.Model(w, G.make_dims(3, 64, 2))
+    evs = _events(16)
+    ref = [m(x, ei).cpu().numpy() for x, ei in evs]
+    outs = [torch.full((ei.shape[1],), -1.0, device="cuda") for _, ei in evs]
+    torch.cuda.synchronize()
+    srv = G.Server(m, 3)
+    ids, cv, errors = [None] * 16, threading.Condition(), []
+
+    def submitter():
+        for k, ((x, ei), o) in enumerate(zip(evs, outs)):
+            rid = srv.submit(x, ei, o)  # the map of requests grows while others wait
+            with cv:
+                ids[k] = rid
+                cv.notify_all()
+            time.sleep(0.001)
+
+    def waiter(par):
+        try:
+            for k in range(par, 16, 2):
+                with cv:
+                    cv.wait_for(lambda: ids[k] is not None)
+                srv.wait(ids[k])
+        except Exception as e:  # reported by the main thread
+            errors.append(e)
+
+    th = [threading.Thread(target=submitter)] + [threading.Thread(target=waiter, args=(p,))
+                                                   for p in (0, 1)]
+    try:
+        for t in th:
+            t.start()
+        for t in th:
+            t.join(60)
+        assert not any(t.is_alive() for t in th)
+        assert not errors, errors
+        for o, r in zip(outs, ref):
+            assert np.array_equal(o.cpu().numpy(), r)
+    finally:
+        srv.close()
+        m.close()
+
+
+def test_server_second_waiter_on_one_id_is_rejected(G):
+    # A request queued behind long ones is claimed by a waiting thread; a
+    # second wait on the same id must fail with GNN_E_INVALID_ARG (claimed,
+    # or already released) and leave the first wait's result intact.
+    w = I.make_weights(3, 128, 1, 76)
+    m = G.Model(w, G.make_dims(3, 128, 8))
+    g = I.layered_graph(100_000, 5, I.DPHI_MID * 0.35, I.DZ_MID * 0.35)
+    xd, eid = dev(g.x), dev(g.edge_index)
+    small = _events(1)[0]
+    ref = m(*small).cpu().numpy()
+    srv = G.Server(m, 1)
+    try:
+        big_out = [torch.empty(g.n_edges, device="cuda") for _ in range(4)]
+        out = torch.full((small[1].shape[1],), -1.0, device="cuda")
+        torch.cuda.synchronize()
+        big_ids = [srv.submit(xd, eid, o) for o in big_out]
+        rid = srv.submit(small[0], small[1], out)
+        res = {}
+        t = threading.Thread(target=lambda: res.setdefault("lat", srv.wait(rid)))
+        t.start()
+        time.sleep(0.005)
+        with pytest.raises(G.GnnError) as e:
+            srv.wait(rid)
+        assert e.value.code == G.GNN_E_INVALID_ARG
+        print(f"second waiter: {e.value}", flush=True)
+        t.join(60)
+        assert res["lat"] > 0
+        assert np.array_equal(out.cpu().numpy(), ref)
+        for i in big_ids:
+            srv.wait(i)
+    finally:
+        srv.close()
+        m.close()
+
+
+def test_server_device_intervals(G):
+    # The device interval of every request lies inside its host latency
+    # window, and requests on one instance do not overlap on the device.
+    w = I.make_weights(3, 64, 1, 77, affine_noise=0.2)
+    m = G.Model(w, G.make_dims(3, 64, 2))
+    evs = _events(10)
+    outs = [torch.empty(ei.shape[1], device="cuda") for _, ei in evs]
+    torch.cuda.synchronize()
+    for n_inst in (1, 4):
+        srv = G.Server(m, n_inst)
+        try:
+            ids = [srv.submit(x, ei, o) for (x, ei), o in zip(evs, outs)]
+            infos = [srv.wait_info(i) for i in ids]
+        finally:
+            srv.close()
+        for inf in infos:
+            assert inf["status"] == 0
+            assert 0.0 <= inf["device_start_ms"] < inf["device_end_ms"]
+            assert inf["device_end_ms"] - inf["device_start_ms"] <= inf["latency_ms"] + 0.5
+        if n_inst == 1:
+            iv = sorted((i["device_start_ms"], i["device_end_ms"]) for i in infos)
+            assert all(a[1] <= b[0] for a, b in zip(iv, iv[1:]))
+    m.close()
+
+
+def test_workspace_limit_gives_oom_and_handle_recovers(G, monkeypatch):
+    # GNN_WORKSPACE_LIMIT caps the handle's workspace: the tiny event needs
+    # about 6 MB, so under a 1 MiB cap the call returns GNN_E_OOM without
+    # writing; lifting the cap on the same handle makes it work, bit for bit
+    # as an uncapped handle.  A cap of one workspace still serves two
+    # streams (the second waits for the first's buffer).
+    c = I.CONFIGS["tiny"]
+    g = I.make_graph(c)
+    w = I.make_weights(3, c.hidden, 1, c.weight_seed, affine_noise=0.2)
+    dims = G.make_dims(3, c.hidden, c.n_iters)
+    xd, eid = dev(g.x), dev(g.edge_index)
+    ref = G.Model(w, dims)
+    want = ref(xd, eid).cpu().numpy()
+    ref.close()
+    monkeypatch.setenv("GNN_WORKSPACE_LIMIT", "1M")
+    m = G.Model(w, dims)
+    monkeypatch.delenv("GNN_WORKSPACE_LIMIT")
+    try:
+        out = torch.full((g.n_edges,), 7.0, device="cuda")
+        torch.cuda.synchronize()
+        with pytest.raises(G.GnnError) as e:
+            m(xd, eid, out=out)
+        assert e.value.code == G.GNN_E_OOM
+        assert "workspace limit" in str(e.value)
+        torch.cuda.synchronize()
+        assert bool((out == 7.0).all())
+        G.gnn_set_workspace_limit(m.handle, 0)
+        assert np.array_equal(m(xd, eid, out=out).cpu().numpy(), want)
+        # exactly one cached buffer allowed: two streams share it
+        G.gnn_release_workspaces(m.handle)
+        m(xd, eid, out=out)
+        torch.cuda.synchronize()
+        held = G.gnn_release_workspaces(m.handle)
+        assert held > 0
+        G.gnn_set_workspace_limit(m.handle, held)
+        o2 = [torch.full((g.n_edges,), -1.0, device="cuda") for _ in range(2)]
+        st = [torch.cuda.Stream() for _ in range(2)]
+        torch.cuda.synchronize()
+        for o, s_ in zip(o2, st):
+            G.gnn_infer(m.handle, xd, eid, g.n_nodes, g.n_edges, o, s_)
+        torch.cuda.synchronize()
+        for o in o2:
+            assert np.array_equal(o.cpu().numpy(), want)
     finally:
         m.close()
