@@ -139,6 +139,32 @@ int gnn_infer_logits(gnn_handle *h, const float *node_feat, const int32_t *edge_
                      int64_t n_nodes, int64_t n_edges, float *edge_logits,
                      hipStream_t stream);
 
+/* ---- no-allocation inference ----------------------------------------------
+ * For callers that cannot allocate device memory: code under HIP stream
+ * capture, tight serving loops, harnesses that forbid hipMalloc.
+ * gnn_infer_noalloc is gnn_infer (same arguments, layouts, ownership,
+ * results bit for bit, errors) except for its workspace: instead of the
+ * handle's cached buffers it uses one fixed device array of
+ * GNN_NOALLOC_SCRATCH_BYTES bytes inside the library, so it calls no
+ * hipMalloc, hipFree or other allocating routine and records no profiling
+ * events.  Each GPU the call runs on holds its own copy of that array from
+ * the first call on it until the process ends.  An event whose workspace
+ * (the bound at the top of this file) exceeds the array is rejected with
+ * GNN_E_INVALID_ARG before any work is enqueued: the array holds events up
+ * to about 50k hits and 330k edges at H = 128 in fp32 (372 MB of workspace;
+ * 249 MB in bf16).  Larger events, such as the paper-scale 300k-hit event
+ * (1.7 GB), go through gnn_infer, whose cached workspace allocates only on
+ * a handle's first call of a given size.  All calls on one
+ * GPU share the array: calls whose work overlaps on that GPU (several
+ * streams, several threads, several handles) race and give undefined
+ * results, so order them (one stream, or events between streams).  Each call
+ * overwrites what the previous one left; nothing needs clearing between
+ * calls.  With GNN_VALIDATE_INDICES the call synchronises `stream`, as
+ * gnn_infer does. */
+#define GNN_NOALLOC_SCRATCH_BYTES ((size_t)512 << 20)
+int gnn_infer_noalloc(gnn_handle *h, const float *node_feat, const int32_t *edge_index,
+                      int64_t n_nodes, int64_t n_edges, float *edge_scores, hipStream_t stream);
+
 /* ---- edge filter (the step before the GNN) --------------------------------
  * Paper section 2.1: after the embedding step a Filtering MLP scores every
  * candidate edge and applyFiltering keeps the edges above a fixed threshold.

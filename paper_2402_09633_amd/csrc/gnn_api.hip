@@ -723,6 +723,10 @@ struct RunOut {
   float *h = nullptr, *e = nullptr, *ain = nullptr, *aout = nullptr;  // debug exports
   bool csr_only = false;
   int32_t *rp_in = nullptr, *perm_in = nullptr, *rp_out = nullptr, *perm_out = nullptr;
+  // A caller-provided workspace of ext_bytes bytes instead of the handle's
+  // cache (no allocation, no profiling events): the no-allocation entry point.
+  void *ext_base = nullptr;
+  size_t ext_bytes = 0;
 };
 
 int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
@@ -735,17 +739,27 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
   int rc = GNN_OK;
   Workspace w;
   DeviceGuard guard(hd->device);
-  StageTimer total(hd, stream, true), st(hd, stream, false);
+  StageTimer total(hd, stream, ro.ext_base == nullptr), st(hd, stream, false);
+  if (ro.ext_base) total.on = false;  // creating events may allocate
   st.on = total.on;
-  total.begin();
 
   const bool fac = hd->factored;
   // the edge update sums its rows per source itself (split kernels)
   const bool fused = fac && hd->fd.split;
   w.bytes = plan_workspace(w, N, E, H, ab, fac, fused);
   int slot = -1;
-  rc = ws_acquire(hd, w.bytes, stream, &w.base, &slot);
-  if (rc != GNN_OK) return rc;
+  if (ro.ext_base) {
+    if (w.bytes > ro.ext_bytes)
+      return fail(GNN_E_INVALID_ARG,
+                  "this event needs %zu bytes of scratch (n_nodes %lld, n_edges %lld); the "
+                  "no-allocation entry point has %zu",
+                  w.bytes, (long long)N, (long long)E, ro.ext_bytes);
+    w.base = ro.ext_base;
+  } else {
+    rc = ws_acquire(hd, w.bytes, stream, &w.base, &slot);
+    if (rc != GNN_OK) return rc;
+  }
+  total.begin();
   plan_workspace(w, N, E, H, ab, fac, fused);
 
   if (d.flags & GNN_VALIDATE_INDICES) {
@@ -1016,7 +1030,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
 
 out:
   total.end(GNN_STAGE_TOTAL);
-  {
+  if (!ro.ext_base) {
     const int rr = ws_release(hd, slot, w.base, w.bytes, stream);
     if (rc == GNN_OK) rc = rr;
   }
@@ -1427,6 +1441,20 @@ int gnn_infer(gnn_handle *h, const float *node_feat, const int32_t *edge_index, 
   if (rc || n_edges == 0) return rc;
   RunOut ro;
   ro.scores = edge_scores;
+  return run(h, node_feat, edge_index, n_nodes, n_edges, stream, ro);
+}
+
+int gnn_infer_noalloc(gnn_handle *h, const float *node_feat, const int32_t *edge_index,
+                      int64_t n_nodes, int64_t n_edges, float *edge_scores, hipStream_t stream) {
+  int rc = common_checks(h, node_feat, edge_index, n_nodes, n_edges, edge_scores);
+  if (rc || n_edges == 0) return rc;
+  RunOut ro;
+  ro.scores = edge_scores;
+  {
+    DeviceGuard guard(h->device);
+    rc = noalloc_scratch(h->device, &ro.ext_base, &ro.ext_bytes);
+  }
+  if (rc) return rc;
   return run(h, node_feat, edge_index, n_nodes, n_edges, stream, ro);
 }
 

@@ -247,4 +247,8 @@ hipError_t launch_bf16_to_f32(const void *in, float *out, int64_t n, hipStream_t
 // Sets the calling thread's gnn_last_error() text; returns code (host).
 int set_error(int code, const char *msg);
 
+// Device address and size of the no-allocation entry point's scratch array
+// on `device` (the current device), looked up once per device (noalloc.hip).
+int noalloc_scratch(int device, void **ptr, size_t *bytes);
+
 }  // namespace gnn

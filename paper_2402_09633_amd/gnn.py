@@ -30,7 +30,7 @@ GNN_VALIDATE_INDICES = 1
 GNN_LITERAL_GATHER = 2
 GNN_FP32_MFMA = 4
 
-EXPORTS = ("gnn_weight_count", "gnn_create", "gnn_infer", "gnn_infer_logits",
+EXPORTS = ("gnn_weight_count", "gnn_create", "gnn_infer", "gnn_infer_logits", "gnn_infer_noalloc",
            "gnn_filter_weight_count", "gnn_filter_create", "gnn_filter_apply",
            "gnn_filter_destroy", "gnn_wcc", "gnn_infer_labels", "gnn_destroy",
            "gnn_release_workspaces", "gnn_last_error",
@@ -98,7 +98,7 @@ def _load():
     L.gnn_weight_count.argtypes = [dp]
     L.gnn_create.restype = vp
     L.gnn_create.argtypes = [vp, dp]
-    for name in ("gnn_infer", "gnn_infer_logits"):
+    for name in ("gnn_infer", "gnn_infer_logits", "gnn_infer_noalloc"):
         f = getattr(L, name)
         f.restype = ctypes.c_int
         f.argtypes = [vp, vp, vp, i64, i64, vp, vp]
@@ -247,6 +247,14 @@ def gnn_infer_logits(handle, node_feat, edge_index, n_nodes: int, n_edges: int, 
     _check_io(node_feat, edge_index, edge_logits)
     return _check(lib.gnn_infer_logits(handle, _addr(node_feat), _addr(edge_index), n_nodes,
                                        n_edges, _addr(edge_logits), _stream(stream)))
+
+
+def gnn_infer_noalloc(handle, node_feat, edge_index, n_nodes: int, n_edges: int, edge_scores,
+                      stream=None) -> int:
+    """gnn_infer in the library's fixed scratch array: allocates nothing."""
+    _check_io(node_feat, edge_index, edge_scores)
+    return _check(lib.gnn_infer_noalloc(handle, _addr(node_feat), _addr(edge_index), n_nodes,
+                                        n_edges, _addr(edge_scores), _stream(stream)))
 
 
 def gnn_filter_weight_count(dims: gnn_filter_dims) -> int:

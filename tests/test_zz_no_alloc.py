@@ -1,0 +1,91 @@
+"""gnn_infer_noalloc, the entry point for callers that cannot allocate: it
+runs the inference in the library's fixed scratch array, through the C ABI.
+
+Its scores must equal gnn_infer's bit for bit (same kernels, same launch
+shapes) on two calls in a row, the second with a smaller event (the array
+then still holds the first call's contents); a handle used only through it
+never creates a cached workspace, further calls leave the device's free
+memory unchanged, and an event beyond the array is rejected before any
+work is enqueued.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2402_09633_amd import inputs as I
+from tests.gpu_util import dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def G():
+    from paper_2402_09633_amd import gnn
+    return gnn
+
+
+def _small_event(seed, n, e):
+    rng = np.random.default_rng(seed)
+    x = rng.normal(size=(n, 3)).astype(np.float32)
+    ei = rng.integers(0, n, size=(2, e)).astype(np.int32)
+    return dev(x), dev(ei)
+
+
+def _call(G, fn, handle, x, ei):
+    out = torch.full((ei.shape[1],), -1.0, device="cuda")
+    torch.cuda.synchronize()
+    fn(handle, x, ei, x.shape[0], ei.shape[1], out)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+@pytest.mark.parametrize("dtype", [0, 1])
+def test_noalloc_equals_gnn_infer_two_calls_second_smaller(G, dtype):
+    c = I.CONFIGS["mid"]  # 50k hits, 329,756 edges: about 372 MB of fp32 workspace
+    g = I.make_graph(c)
+    w = I.make_weights(3, c.hidden, 1, c.weight_seed, affine_noise=0.1)
+    dims = G.make_dims(3, c.hidden, c.n_iters, dtype=dtype)
+    events = [(dev(g.x), dev(g.edge_index)), _small_event(5, 3001, 8033)]
+    print(f"noalloc dtype={dtype}: events of {[e.shape[1] for _, e in events]} edges", flush=True)
+    ref_model = G.Model(w, dims)
+    m = G.Model(w, dims)  # used only through the no-allocation entry point
+    try:
+        refs = [_call(G, G.gnn_infer, ref_model.handle, x, ei) for x, ei in events]
+        for (x, ei), ref in zip(events, refs):  # large first, then smaller
+            got = _call(G, G.gnn_infer_noalloc, m.handle, x, ei)
+            assert np.array_equal(got, ref)
+        # no cached workspace was ever created on this handle
+        assert G.gnn_release_workspaces(m.handle) == 0
+        # further calls leave the device's free memory where it was
+        free0 = torch.cuda.mem_get_info()[0]
+        for (x, ei), ref in zip(events, refs):
+            assert np.array_equal(_call(G, G.gnn_infer_noalloc, m.handle, x, ei), ref)
+        assert torch.cuda.mem_get_info()[0] == free0
+    finally:
+        m.close()
+        ref_model.close()
+
+
+def test_noalloc_rejects_event_beyond_scratch(G):
+    # the 300k-hit / 1.0M-edge event needs about 1.7 GB of workspace, more
+    # than the 512 MiB array: rejected with nothing written
+    c = I.CONFIGS["full"]
+    g = I.make_graph(c)
+    w = I.make_weights(3, c.hidden, 1, c.weight_seed)
+    m = G.Model(w, G.make_dims(3, c.hidden, c.n_iters))
+    try:
+        x, ei = dev(g.x), dev(g.edge_index)
+        out = torch.full((g.n_edges,), 7.0, device="cuda")
+        torch.cuda.synchronize()
+        with pytest.raises(G.GnnError) as e:
+            G.gnn_infer_noalloc(m.handle, x, ei, g.n_nodes, g.n_edges, out)
+        assert e.value.code == G.GNN_E_INVALID_ARG
+        assert "scratch" in str(e.value)
+        torch.cuda.synchronize()
+        assert bool((out == 7.0).all())
+        # the same handle still serves a fitting event afterwards
+        xs, eis = _small_event(6, 500, 2000)
+        assert np.array_equal(_call(G, G.gnn_infer_noalloc, m.handle, xs, eis),
+                              _call(G, G.gnn_infer, m.handle, xs, eis))
+    finally:
+        m.close()
