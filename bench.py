@@ -71,21 +71,27 @@ def edge_update_flops(E, H, factored):
     return 2.0 * E * ((1 if factored else 3) * H * H + H * H)
 
 
+def proj_bytes(s):
+    """Bytes per element of the node projections P: fp32 in the fp32 model,
+    fp16 in the bf16 model (s = 2)."""
+    return 4 if s == 4 else 2
+
+
 def edge_update_bytes(N, E, H, s=4, n_src=0):
     """Algorithmic HBM bytes of one regrouped edge-update launch, gathered
     rows counted per edge: e read and written (s bytes per element), the
-    P[src][0:H] and P[dst][H:2H] half-rows (fp32) and both indices; with the
-    fused out-sums (n_src > 0), one agg_out row (s bytes per element) per
-    node that has out-edges."""
-    return E * (2 * H * s + 2 * H * 4 + 8) + n_src * H * s
+    P[src][0:H] and P[dst][H:2H] half-rows and both indices; with the fused
+    out-sums (n_src > 0), one agg_out row (s bytes per element) per node
+    that has out-edges."""
+    return E * (2 * H * s + 2 * H * proj_bytes(s) + 8) + n_src * H * s
 
 
 def node_update_bytes(N, H, s=4, T=1):
     """Average per launch over the T launches of one event: h, agg_in,
-    agg_out read (s bytes per element) and the projection row written
-    (fp32) every time; h written by all but the last launch, whose h feeds
-    the classifier only through its projections."""
-    return N * (3 * H * s + 2 * H * 4) + N * H * s * (T - 1) / T
+    agg_out read (s bytes per element) and the projection row of 2H
+    elements written every time; h written by all but the last launch,
+    whose h feeds the classifier only through its projections."""
+    return N * (3 * H * s + 2 * H * proj_bytes(s)) + N * H * s * (T - 1) / T
 
 
 def split_mfma_flops(N, E, H, bf16=False):
@@ -239,8 +245,8 @@ def rooflines(prof, N, E, H, T, bf16, split, factored, n_src, traffic):
         mf = split_mfma_flops(N, E, H, bf16)
         eu_mfma = mf["edge_update"] / (eu_ms / 1000.0) / 1e12
         mdt = "bf16" if bf16 else "fp16"
-        roof = {"kernel": ("edge_split<4,3,bf16> (gathers node projections, W_e e, layer 2 "
-                           "transposed, per-source sums of its rows; hi/lo bf16 weights in "
+        roof = {"kernel": ("edge_split<4,3,bf16> (gathers fp16 node projections, W_e e, layer "
+                           "2 transposed, per-source sums of its rows; hi/lo bf16 weights in "
                            "LDS)") if bf16 else
                           ("edge_split<4,3> (gathers node projections, W_e e, layer 2 "
                            "transposed, per-source sums of its rows; f16x2 weights in LDS)"),
@@ -261,7 +267,7 @@ def rooflines(prof, N, E, H, T, bf16, split, factored, n_src, traffic):
         nu_gbs = nb / (nu_ms / 1000.0) / 1e9
         nu_mfma = mf["node_update"] / (nu_ms / 1000.0) / 1e12
         roof_node = {"kernel": ("node_split<4,false,1,bf16> (hi/lo bf16 weights streamed "
-                                "through LDS)") if bf16 else
+                                "through LDS; fp16 projections)") if bf16 else
                                ("node_split<4,false,1> (f16x2 products, per-node row scale in "
                                 "layer 1; weights streamed through LDS)"),
                      "bound": "hbm", "achieved": round(nu_gbs, 1), "peak": PEAK_HBM_GBS,

@@ -200,9 +200,11 @@ std::vector<uint16_t> rec_f16x2(const BlobLayer &L, int c0, int K, float s, bool
   return out;
 }
 
-// bf16 hi/lo records of W[:, c0 : c0 + K]: hi = bf16(W), lo = bf16(W - hi)
-// (the bf16 model's weights).
-std::vector<uint16_t> rec_bf16x2(const BlobLayer &L, int c0, int K, bool from_acc) {
+// bf16 hi/lo records of sc * W[:, c0 : c0 + K]: hi = bf16(sc W), lo =
+// bf16(sc W - hi) (the bf16 model's weights; sc a power of two, so the pair
+// is sc times the pair of W).
+std::vector<uint16_t> rec_bf16x2(const BlobLayer &L, int c0, int K, bool from_acc,
+                                 float sc = 1.f) {
   const int MB = L.fout / 32, G = K / 16;
   std::vector<uint16_t> out((size_t)G * MB * 2 * 64 * 8);
   for (int g = 0; g < G; ++g)
@@ -211,13 +213,36 @@ std::vector<uint16_t> rec_bf16x2(const BlobLayer &L, int c0, int K, bool from_ac
         for (int j = 0; j < 8; ++j) {
           const int hh = lane / 32;
           const int k = from_acc ? 16 * g + 8 * (j / 4) + 4 * hh + j % 4 : 16 * g + 8 * hh + j;
-          const float wv = L.W[(size_t)(mb * 32 + lane % 32) * L.fin + c0 + k];
+          const float wv = sc * L.W[(size_t)(mb * 32 + lane % 32) * L.fin + c0 + k];
           const uint16_t hi = f32_to_bf16(wv);
           const size_t o = ((((size_t)g * MB + mb) * 2) * 64 + lane) * 8 + j;
           out[o] = hi;
           out[o + 64 * 8] = f32_to_bf16(wv - bf16_to_f32(hi));
         }
   return out;
+}
+
+// bf16 model: power of two s for the fp16 projections s P = s [W_s h; W_d h]
+// that edge-side layer L reads (columns [0, H) and [H, 2H) of its W), with
+// s max_f sum_k |W[f][k]| hb <= 2^15 for an h bound hb, as large as that
+// allows within [2^-40, 2^40]; 0 if none fits.
+float proj_f16_scale(const BlobLayer &L, int H, double hb) {
+  double m = 0.0;
+  for (int f = 0; f < L.fout; ++f)
+    for (int half = 0; half < 2; ++half) {
+      double r = 0.0;
+      for (int k = half * H; k < half * H + H; ++k) r += fabs((double)L.W[(size_t)f * L.fin + k]);
+      m = r > m ? r : m;
+    }
+  const double bound = m * hb;
+  if (!(bound <= 1e300)) return 0.f;
+  if (!(bound > 0.0)) return 1.f;
+  int e = 0;
+  (void)frexp(32768.0 / bound, &e);  // 2^(e-1) <= 2^15 / bound < 2^e
+  int k = e - 1;
+  k = k < -40 ? -40 : (k > 40 ? 40 : k);
+  const double sc = ldexp(1.0, k);
+  return sc * bound <= 32768.0 ? (float)sc : 0.f;
 }
 
 // Builds one host staging image of all device weights, section by section,
@@ -1166,8 +1191,25 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
       fdh.row_bound = (float)bound;
     }
     if (factored && bf16) {
-      // The bf16 model on the same kernels: hi/lo bf16 records, no scales.
+      // The bf16 model on the same kernels: hi/lo bf16 records; the fp16
+      // projections and the W_e records of their consumer carry that
+      // consumer's scale (bias and eps follow in the kernel).
       split = true;
+      double hb = ln_out_bound(a1);
+      for (int s = 0; s < S; ++s) hb = fmax(hb, ln_out_bound(n1s[s]));
+      fdh.s1_ee = proj_f16_scale(b0, H, hb);
+      fdh.s1_cls = proj_f16_scale(c0, H, hb);
+      bool fits = fdh.s1_ee > 0.f && fdh.s1_cls > 0.f;
+      for (int s = 0; s < S; ++s) {
+        fdh.s1_em.push_back(proj_f16_scale(e0s[s], H, hb));
+        fits = fits && fdh.s1_em[s] > 0.f;
+      }
+      if (!fits) {
+        fail(GNN_E_UNSUPPORTED,
+             "bf16 model: no power-of-two scale keeps these weights' node projections inside "
+             "the fp16 range");
+        return nullptr;
+      }
       auto add16 = [&](const std::vector<uint16_t> &v) {
         return st.add(v.data(), v.size() * sizeof(uint16_t));
       };
@@ -1175,18 +1217,24 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
         dst.insert(dst.end(), src.begin(), src.end());
       };
       for (int s = 0; s < S; ++s) {
-        fdh.s1_em.push_back(1.f);
         fdh.s2_em.push_back(1.f);
         fdh.s1_nm.push_back(1.f);
         fdh.s2_nm.push_back(1.f);
-        o_we_em[s] = add16(rec_bf16x2(e0s[s], 2 * H, H, false));
+        o_we_em[s] = add16(rec_bf16x2(e0s[s], 2 * H, H, false, fdh.s1_em[s]));
         o_w2_em[s] = add16(rec_bf16x2(e1s[s], 0, H, true));
       }
-      o_we_cls = add16(rec_bf16x2(c0, 2 * H, H, false));
+      o_we_cls = add16(rec_bf16x2(c0, 2 * H, H, false, fdh.s1_cls));
       o_w2_ee = add16(rec_bf16x2(b1, 0, H, true));
+      auto scale_of = [&](const BlobLayer &L) {
+        if (&L == &c0) return fdh.s1_cls;
+        for (int s = 0; s < S; ++s)
+          if (&L == &e0s[s]) return fdh.s1_em[s];
+        return fdh.s1_ee;
+      };
       auto proj = [&](std::vector<uint16_t> &dst, const BlobLayer &L) {
-        cat(dst, rec_bf16x2(L, 0, H, true));
-        cat(dst, rec_bf16x2(L, H, H, true));
+        const float sc = scale_of(L);
+        cat(dst, rec_bf16x2(L, 0, H, true, sc));
+        cat(dst, rec_bf16x2(L, H, H, true, sc));
       };
       std::vector<uint16_t> es = rec_bf16x2(a1, 0, H, true);
       proj(es, b0);

@@ -28,7 +28,11 @@
 // aggregates are stored in bf16 and fed to the bf16 matrix cores as they are,
 // every weight is a pair hi = bf16(W), lo = bf16(W - hi) (two products), the
 // LayerNorm outputs are rounded to bf16 where they feed a product, and all
-// sums are fp32; the projections P stay fp32.  No scaling is needed there.
+// sums are fp32.  The projections P are stored in fp16 there, multiplied by
+// the consuming edge MLP's layer-1 scale (a power of two chosen on the host
+// so that every |s P| stays below 2^15), in the permuted order of
+// store_block16: their rounding (2^-11 relative) is four times finer than
+// the bf16 rounding of h itself.
 //
 // An accumulator that holds s * y is never rescaled: the bias is added as
 // s * b and LayerNorm runs with eps * s^2, which gives the LayerNorm of y + b
@@ -183,18 +187,6 @@ __device__ __forceinline__ void zero(f16v (&a)[MB]) {
     for (int v = 0; v < 16; ++v) a[mb][v] = 0.f;
 }
 
-template <int MB>
-__device__ __forceinline__ void store_rows_bf16(__bf16 *__restrict__ o, const f16v (&acc)[MB]) {
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const bf4 val = {(__bf16)acc[mb][4 * q], (__bf16)acc[mb][4 * q + 1],
-                       (__bf16)acc[mb][4 * q + 2], (__bf16)acc[mb][4 * q + 3]};
-      __builtin_nontemporal_store(val, (bf4 *)(o + mb * 32 + 8 * q));
-    }
-}
-
 // Stores the wave's 32 rows x 32 MB floats (row r at out + r * stride,
 // rows >= nvalid skipped) through a 32 x 32-float LDS staging tile, one
 // 128-byte column block at a time: every store instruction then writes 8
@@ -224,6 +216,58 @@ __device__ __forceinline__ void store_block(float *__restrict__ out, int64_t str
       const int row = 8 * k + rr;
       const f4 v = *(const f4 *)(stg + row * SST + cc);
       if (row < nvalid) __builtin_nontemporal_store(v, (f4 *)(out + row * stride + mb * 32 + cc));
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+}
+
+// 16-bit rows (bf16 model: h in bf16, the projections in fp16) from
+// accumulator blocks, through the same staging tile, two 32-feature blocks
+// (128 bytes of a row) at a time, so that every store instruction writes 8
+// full 128-byte lines.  PERM keeps feature 8 q + 4 hh + t of each block
+// (q, t = 0..3) at position 16 hh + 4 q + t: the projections' order, in
+// which a lane's 16 accumulator values of a block are contiguous (the edge
+// kernel reads them back with two 16-byte loads per block).
+template <int MB, bool PERM, typename T>
+__device__ __forceinline__ void store_block16(T *__restrict__ out, int64_t stride, int nvalid,
+                                              const f16v (&acc)[MB], float *stg, int lane) {
+  typedef T t4 __attribute__((ext_vector_type(4)));
+  typedef T t8 __attribute__((ext_vector_type(8)));
+  static_assert(MB % 2 == 0, "two blocks per staging round");
+  char *sb = (char *)stg;
+  const int n = lane & 31, hh = lane >> 5;
+  const int rr = lane >> 3, cc = lane & 7;
+#pragma unroll
+  for (int mp = 0; mp < MB / 2; ++mp) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const f16v &a = acc[2 * mp + b];
+      if constexpr (PERM) {
+        t8 lo, hi;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          lo[j] = (T)a[j];
+          hi[j] = (T)a[8 + j];
+        }
+        *(t8 *)(sb + n * SST * 4 + (b * 32 + 16 * hh) * 2) = lo;
+        *(t8 *)(sb + n * SST * 4 + (b * 32 + 16 * hh + 8) * 2) = hi;
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          *(t4 *)(sb + n * SST * 4 + (b * 32 + 8 * q + 4 * hh) * 2) =
+              t4{(T)a[4 * q], (T)a[4 * q + 1], (T)a[4 * q + 2], (T)a[4 * q + 3]};
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int row = 8 * k + rr;
+      const t8 v = *(const t8 *)(sb + row * SST * 4 + cc * 16);
+      if (row < nvalid) __builtin_nontemporal_store(v, (t8 *)(out + row * stride + mp * 64 + cc * 8));
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -441,8 +485,8 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
     if (a.h_out) {
       if constexpr (PREC == SPLIT)
         store_block<MB>(a.h_out + wrow0 * H, H, nvalid, hv, stg, lane);
-      else if (valid)
-        store_rows_bf16<MB>((__bf16 *)a.h_out + row * H + 4 * hh, hv);
+      else
+        store_block16<MB, false, __bf16>((__bf16 *)a.h_out + wrow0 * H, H, nvalid, hv, stg, lane);
     }
     // the projections read h as it is stored
     using xp_t = typename std::conditional<PREC == SPLIT, h8, bf8>::type;
@@ -469,7 +513,11 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
             step_hl<MB>(pv, (const bf8 *)rec_h(i), x1[g]);
           rec_done(i);
         }
-        store_block<MB>(a.p_out[p] + wrow0 * 2 * H + half * H, 2 * H, nvalid, pv, stg, lane);
+        if constexpr (PREC == SPLIT)
+          store_block<MB>(a.p_out[p] + wrow0 * 2 * H + half * H, 2 * H, nvalid, pv, stg, lane);
+        else
+          store_block16<MB, true, _Float16>((_Float16 *)a.p_out[p] + wrow0 * 2 * H + half * H,
+                                            2 * H, nvalid, pv, stg, lane);
       }
   }
 }
@@ -566,7 +614,7 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
 
     // Layer 1 = s1 (P[src][0:H] + P[dst][H:2H] + W_e e) (+ s1 b1 in the LayerNorm).
     f16v acc[MB];
-    {
+    if constexpr (PREC == SPLIT) {
       const float *ps = a.P + s * 2 * H + 4 * hh;
       const float *pd = a.P + d * 2 * H + H + 4 * hh;
 #pragma unroll
@@ -578,6 +626,21 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
 #pragma unroll
           for (int t = 0; t < 4; ++t) acc[mb][4 * q + t] = x[t];
         }
+    } else {
+      // fp16 rows in the order of store_block16: this lane's 16 values of
+      // block mb are contiguous
+      const _Float16 *ps = (const _Float16 *)a.P + s * 2 * H + 16 * hh;
+      const _Float16 *pd = (const _Float16 *)a.P + d * 2 * H + H + 16 * hh;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const h8 s0 = *(const h8 *)(ps + 32 * mb), s1v = *(const h8 *)(ps + 32 * mb + 8);
+        const h8 d0 = *(const h8 *)(pd + 32 * mb), d1 = *(const h8 *)(pd + 32 * mb + 8);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          acc[mb][j] = (float)s0[j] + (float)d0[j];
+          acc[mb][8 + j] = (float)s1v[j] + (float)d1[j];
+        }
+      }
     }
     if constexpr (HAS_E) {
 #pragma unroll

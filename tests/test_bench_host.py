@@ -31,8 +31,8 @@ def test_edge_update_bytes_per_launch():
     per_edge = 2 * 512 + 2 * 512 + 8
     assert bench.edge_update_bytes(N, E, H, 4, N_SRC) == E * per_edge + N_SRC * 512
     assert bench.edge_update_bytes(N, E, H, 4, N_SRC) == 2_183_975_944
-    # bf16 rows: e and agg_out halve, the fp32 projections stay
-    assert bench.edge_update_bytes(N, E, H, 2, N_SRC) == E * (2 * 256 + 2 * 512 + 8) + N_SRC * 256
+    # bf16 model: e and agg_out rows in bf16, the projections in fp16
+    assert bench.edge_update_bytes(N, E, H, 2, N_SRC) == E * (2 * 256 + 2 * 256 + 8) + N_SRC * 256
 
 
 def test_aggregate_bytes_per_launch():
@@ -51,6 +51,8 @@ def test_node_update_bytes_average_launch():
     want = N * (3 * 512 + 1024) + N * 512 * 7 / 8
     assert bench.node_update_bytes(N, H, 4, T) == pytest.approx(want, rel=0, abs=1e-6)
     assert bench.node_update_bytes(N, H, 4, T) == 902_400_000
+    # bf16 model: 256-byte rows, the fp16 projection row 512 bytes
+    assert bench.node_update_bytes(N, H, 2, T) == N * (3 * 256 + 512) + N * 256 * 7 / 8
 
 
 def test_matrix_work_per_launch():
