@@ -102,8 +102,9 @@ __device__ __forceinline__ void bias_ln_relu(f16v (&acc)[MB], const float *__res
 
 // LayerNorm epilogue with its parameters (b, gamma, beta; H floats each)
 // read from LDS (the bias already multiplied by the accumulators' scale,
-// eps by its square).
-template <int MB>
+// eps by its square).  ADD_BIAS false: the bias is in the accumulators
+// already (b is then not read).
+template <int MB, bool ADD_BIAS = true>
 __device__ __forceinline__ void ln_relu_lds(f16v (&acc)[MB], const float *prm, float eps, int hh) {
   constexpr int H = 32 * MB;
   constexpr float inv_h = 1.0f / H;
@@ -112,10 +113,11 @@ __device__ __forceinline__ void ln_relu_lds(f16v (&acc)[MB], const float *prm, f
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const f4 bb = *(const f4 *)(prm + mb * 32 + 8 * q + 4 * hh);
+      f4 bb = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (ADD_BIAS) bb = *(const f4 *)(prm + mb * 32 + 8 * q + 4 * hh);
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        acc[mb][4 * q + t] += bb[t];
+        if constexpr (ADD_BIAS) acc[mb][4 * q + t] += bb[t];
         s += acc[mb][4 * q + t];
       }
     }

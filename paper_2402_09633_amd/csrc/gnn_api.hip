@@ -835,6 +835,24 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
     na.h_out = T == 0 && ro.stop_iter < 0 ? nullptr : (float *)w.h;
     na.p_out[0] = w.pa;
     na.p_out[1] = w.pb;
+    // the edge MLP that reads the projections stored after node update t
+    // (t = -1: the node encoder's second projection)
+    auto consumer = [&](int t, const MlpDev **m, float *s1) {
+      if (t + 1 < T) {
+        *m = &hd->edge_mlp[set_of(t + 1)];
+        *s1 = fd.split ? fd.s1_em[set_of(t + 1)] : 1.f;
+      } else {
+        *m = &hd->cls;
+        *s1 = fd.split ? fd.s1_cls : 1.f;
+      }
+    };
+    {
+      na.pbias[0] = hd->edge_enc.l0.b;
+      na.ps1[0] = fd.split ? fd.s1_ee : 1.f;
+      const MlpDev *m2 = nullptr;
+      consumer(-1, &m2, &na.ps1[1]);
+      na.pbias[1] = m2->l0.b;
+    }
     na.eps = d.ln_eps;
     st.begin();
     HIP_TRY(fd.split ? launch_node_split(true, H, na, fd.grid_node, fd.bf16, stream)
@@ -921,6 +939,11 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       // it is not stored unless the stages are being exported.
       nu.h_out = t == T - 1 && ro.stop_iter < 0 ? nullptr : (float *)w.h;
       nu.p_out[0] = w.pb;
+      {
+        const MlpDev *mc = nullptr;
+        consumer(t, &mc, &nu.ps1[0]);
+        nu.pbias[0] = mc->l0.b;
+      }
       nu.eps = d.ln_eps;
       st.begin();
       HIP_TRY(fd.split ? launch_node_split(false, H, nu, fd.grid_node, fd.bf16, stream)

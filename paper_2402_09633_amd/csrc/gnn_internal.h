@@ -72,6 +72,11 @@ struct NodeArgs {
   float s1 = 1.f, s2 = 1.f;
   const int32_t *rp_in = nullptr, *rp_out = nullptr;
   float row_bound = 0.f;
+  // split kernels: the layer-1 bias of the edge MLP that reads projection
+  // p, and that MLP's layer-1 scale; the bias goes into the source half
+  // P[v][0:H] as the rows are stored, so the edge kernels add none
+  const float *pbias[2] = {nullptr, nullptr};
+  float ps1[2] = {1.f, 1.f};
 };
 
 // UpdAgg: the edge update that also sums its output rows per source node

@@ -175,6 +175,19 @@ __device__ __forceinline__ void step_hlt(f16v (&acc)[MB], const bf8 *rec, const 
 
 __device__ __forceinline__ bf8 to_bf16(const f8 &x) { return __builtin_convertvector(x, bf8); }
 
+// a + b in fp32 for two fp16 values held in the low (HI = false) or high
+// halves of 32-bit registers: one mixed-precision fma, a * 1 + b, whose fp16
+// sources are converted exactly (instead of two conversions and an add).
+template <bool HI>
+__device__ __forceinline__ float add_f16(unsigned a, unsigned b) {
+  float r;
+  if constexpr (HI)
+    asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel:[1,0,1] op_sel_hi:[1,0,1]" : "=v"(r) : "v"(a), "v"(b));
+  else
+    asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel_hi:[1,0,1]" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
 // Operand precision of the kernels below.
 constexpr int SPLIT = 0;  // fp32 activations, split products
 constexpr int BF16 = 1;   // bf16 activations, hi/lo bf16 weights
@@ -338,8 +351,10 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
   // each bias multiplied by its accumulator scale; the encoder adds its
   // first-layer bias and W^T ([F][H]).  Read from LDS, they stay off the
   // vector-memory counter that the row loads and stores wait on.
-  constexpr int NPRM = 6 * H + (ENC ? H + MAX_F * H : 0);
+  constexpr int NPRM = 6 * H + NPROJ * H + (ENC ? H + MAX_F * H : 0);
   __shared__ float prm[NPRM];
+  // (the projections' consumer biases, scaled, at prm + PB)
+  constexpr int PB = 6 * H + (ENC ? H + MAX_F * H : 0);
   const int tid = threadIdx.x, lane = tid & 63, hh = lane >> 5, n = lane & 31;
   const int wave = tid >> 6;
   float *stg = stage[wave];
@@ -351,6 +366,8 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
     prm[4 * H + i] = a.mlp.l1.g[i];
     prm[5 * H + i] = a.mlp.l1.beta[i];
     if constexpr (ENC) prm[6 * H + i] = a.mlp.l0.b[i];
+#pragma unroll
+    for (int p = 0; p < NPROJ; ++p) prm[PB + p * H + i] = a.pbias[p][i] * a.ps1[p];
   }
   if constexpr (ENC)
     for (int i = tid; i < a.F * H; i += 64 * SW) prm[7 * H + i] = ((const float *)a.mlp.l0.w)[i];
@@ -513,6 +530,18 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
             step_hl<MB>(pv, (const bf8 *)rec_h(i), x1[g]);
           rec_done(i);
         }
+        if (half == 0) {
+          // the consumer's layer-1 bias, added once per node here rather
+          // than once per edge in the edge kernel
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const f4 bb = *(const f4 *)(prm + PB + p * H + mb * 32 + 8 * q + 4 * hh);
+#pragma unroll
+              for (int t = 0; t < 4; ++t) pv[mb][4 * q + t] += bb[t];
+            }
+        }
         if constexpr (PREC == SPLIT)
           store_block<MB>(a.p_out[p] + wrow0 * 2 * H + half * H, 2 * H, nvalid, pv, stg, lane);
         else
@@ -543,7 +572,7 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
     if constexpr (HAS_L2) lw_2[i] = ((const h8 *)a.w2)[i];
   }
   for (int i = threadIdx.x; i < H; i += 64 * SW) {
-    prm[i] = a.b1[i] * a.s1;
+    prm[i] = 0.f;  // (layer-1 bias: inside the gathered P[src] rows)
     prm[H + i] = a.g1[i];
     prm[2 * H + i] = a.beta1[i];
     if constexpr (HAS_L2) {
@@ -633,12 +662,15 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
       const _Float16 *pd = (const _Float16 *)a.P + d * 2 * H + H + 16 * hh;
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
-        const h8 s0 = *(const h8 *)(ps + 32 * mb), s1v = *(const h8 *)(ps + 32 * mb + 8);
-        const h8 d0 = *(const h8 *)(pd + 32 * mb), d1 = *(const h8 *)(pd + 32 * mb + 8);
+        const u4 s0 = *(const u4 *)(ps + 32 * mb), s1v = *(const u4 *)(ps + 32 * mb + 8);
+        const u4 d0 = *(const u4 *)(pd + 32 * mb), d1 = *(const u4 *)(pd + 32 * mb + 8);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          acc[mb][j] = (float)s0[j] + (float)d0[j];
-          acc[mb][8 + j] = (float)s1v[j] + (float)d1[j];
+        for (int j = 0; j < 4; ++j) {
+          const unsigned a0 = s0[j], b0 = d0[j], a1 = s1v[j], b1 = d1[j];
+          acc[mb][2 * j] = add_f16<false>(a0, b0);
+          acc[mb][2 * j + 1] = add_f16<true>(a0, b0);
+          acc[mb][8 + 2 * j] = add_f16<false>(a1, b1);
+          acc[mb][8 + 2 * j + 1] = add_f16<true>(a1, b1);
         }
       }
     }
@@ -654,7 +686,7 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
     // (FUSE: after layer 2's LayerNorm, which needs the registers)
     if constexpr (!FUSE)
       if (u + nw < units) load_idx(u + nw);
-    ln_relu_lds<MB>(acc, prm, eps1, hh);
+    ln_relu_lds<MB, false>(acc, prm, eps1, hh);  // bias inside P[src]
 
     if constexpr (!HAS_L2) {
       float part = 0.f;
