@@ -209,17 +209,25 @@ __device__ __forceinline__ void zero(f16v (&a)[MB]) {
 // hint.  Measured on the full fp32 event: 6.48 -> 6.28 ms with h, P and the
 // updated e stored this way, the time saved showing up mostly in the
 // kernels that read those rows next.
-constexpr int SST = 36;  // staging row stride in floats (16-byte aligned rows)
+//
+// The tile has 32 rows of 128 bytes (eight 16-byte chunks); chunk c of row r
+// sits at chunk c ^ swz(r), swz(r) = r & 7.  Measured with this access
+// pattern (row writes, one chunk per lane; column-block reads, eight lanes
+// per row): no LDS bank conflicts, against 1.0M per 64k writes and reads
+// for rows padded to 36 floats, 14.7M for unpadded rows and 2.1M for the
+// swizzle (r >> 1) & 7.
+constexpr int SST = 32;  // staging row stride in floats
+__device__ __forceinline__ int swz(int r) { return r & 7; }
 template <int MB>
 __device__ __forceinline__ void store_block(float *__restrict__ out, int64_t stride, int nvalid,
                                             const f16v (&acc)[MB], float *stg, int lane) {
   const int n = lane & 31, hh = lane >> 5;
-  const int rr = lane >> 3, cc = 4 * (lane & 7);
+  const int rr = lane >> 3, cc = lane & 7;
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      *(f4 *)(stg + n * SST + 8 * q + 4 * hh) =
+      *(f4 *)(stg + n * SST + 4 * ((2 * q + hh) ^ swz(n))) =
           f4{acc[mb][4 * q], acc[mb][4 * q + 1], acc[mb][4 * q + 2], acc[mb][4 * q + 3]};
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -227,8 +235,9 @@ __device__ __forceinline__ void store_block(float *__restrict__ out, int64_t str
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int row = 8 * k + rr;
-      const f4 v = *(const f4 *)(stg + row * SST + cc);
-      if (row < nvalid) __builtin_nontemporal_store(v, (f4 *)(out + row * stride + mb * 32 + cc));
+      const f4 v = *(const f4 *)(stg + row * SST + 4 * (cc ^ swz(row)));
+      if (row < nvalid)
+        __builtin_nontemporal_store(v, (f4 *)(out + row * stride + mb * 32 + 4 * cc));
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -257,6 +266,7 @@ __device__ __forceinline__ void store_block16(T *__restrict__ out, int64_t strid
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       const f16v &a = acc[2 * mp + b];
+      // (chunk = 8 values; chunk c of row n at c ^ swz(n), as in store_block)
       if constexpr (PERM) {
         t8 lo, hi;
 #pragma unroll
@@ -264,12 +274,12 @@ __device__ __forceinline__ void store_block16(T *__restrict__ out, int64_t strid
           lo[j] = (T)a[j];
           hi[j] = (T)a[8 + j];
         }
-        *(t8 *)(sb + n * SST * 4 + (b * 32 + 16 * hh) * 2) = lo;
-        *(t8 *)(sb + n * SST * 4 + (b * 32 + 16 * hh + 8) * 2) = hi;
+        *(t8 *)(sb + n * SST * 4 + 16 * ((4 * b + 2 * hh) ^ swz(n))) = lo;
+        *(t8 *)(sb + n * SST * 4 + 16 * ((4 * b + 2 * hh + 1) ^ swz(n))) = hi;
       } else {
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-          *(t4 *)(sb + n * SST * 4 + (b * 32 + 8 * q + 4 * hh) * 2) =
+          *(t4 *)(sb + n * SST * 4 + 16 * ((4 * b + q) ^ swz(n)) + 8 * hh) =
               t4{(T)a[4 * q], (T)a[4 * q + 1], (T)a[4 * q + 2], (T)a[4 * q + 3]};
       }
     }
@@ -279,7 +289,7 @@ __device__ __forceinline__ void store_block16(T *__restrict__ out, int64_t strid
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int row = 8 * k + rr;
-      const t8 v = *(const t8 *)(sb + row * SST * 4 + cc * 16);
+      const t8 v = *(const t8 *)(sb + row * SST * 4 + 16 * (cc ^ swz(row)));
       if (row < nvalid) __builtin_nontemporal_store(v, (t8 *)(out + row * stride + mp * 64 + cc * 8));
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
