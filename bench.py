@@ -47,8 +47,8 @@ TRAFFIC_SOURCES = {
                   "paper_2402_09633_amd/csrc/device_common.h"],
 }
 # (path, source hash) -> HBM bytes per edge-update launch on the full event
-MEASURED_TRAFFIC = {("split", "183abb9ba4c53724"): 1.789e9,       # edge_split<4,3>
-                    ("bf16", "183abb9ba4c53724"): 1.207e9,        # edge_split<4,3,bf16>
+MEASURED_TRAFFIC = {("split", "f44aaaf4a983a653"): 1.790e9,       # edge_split<4,3>
+                    ("bf16", "f44aaaf4a983a653"): 0.8937e9,       # edge_split<4,3,bf16>
                     ("fp32_mfma", "d6fe23f044f63d7b"): 1.651e9}   # edge_f32<4,1>
 
 
@@ -172,7 +172,6 @@ def host_info():
     except Exception:  # no cgroup v2 quota visible
         pass
     gcc = (_run(["gcc", "--version"]).splitlines() or [""])[0]
-    hip = [l for l in _run(["/opt/rocm/bin/hipcc", "--version"]).splitlines() if "HIP version" in l]
     bi = {}
     try:
         with open(os.path.join(ROOT, "paper_2402_09633_amd", "build_info.json")) as f:
@@ -182,8 +181,7 @@ def host_info():
     return {"cpu_model": info.get("Model name", ""), "logical_cpus_in_affinity": len(aff),
             "physical_cores_in_affinity": len(cores) or len(aff),
             "cgroup_cpu_quota": quota, "omp_num_threads_env": os.environ.get("OMP_NUM_THREADS"),
-            "gcc": gcc, "hipcc": hip[0].strip() if hip else "",
-            "libgnn_build": bi}
+            "gcc": gcc, "hipcc": bi.get("hipcc", ""), "libgnn_build": bi}
 
 
 # ------------------------------------------------------------ GPU legs ---
