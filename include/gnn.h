@@ -22,8 +22,8 @@
  * handle may run concurrently on several streams (its weights are read-only).
  *
  * Workspace: gnn_infer* and gnn_debug_* need device scratch of at most
- * (E + 3N)*H*act_bytes + 16*N*H + (40 + H/4)*E bytes (act_bytes 4 for fp32,
- * 2 for bf16; about 1.7 GB for N = 300k, E = 1M, H = 128, fp32).  The handle keeps these buffers between calls (at most 16, one
+ * (E + 3N)*H*act_bytes + 16*N*H + (60 + H/4)*E + 64 KiB bytes (act_bytes 4
+ * for fp32, 2 for bf16; about 1.7 GB for N = 300k, E = 1M, H = 128, fp32).  The handle keeps these buffers between calls (at most 16, one
  * per call in flight, each rounded up by 1/8 for growth) and frees them in
  * gnn_destroy; a call that finds an idle buffer large enough orders itself
  * after that buffer's previous call with an event and allocates nothing.
@@ -124,9 +124,10 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims);
  * and outputs untouched until the stream passes this work.  Results are
  * bitwise deterministic for a given input.  Returns GNN_OK with no writes
  * when n_edges == 0; GNN_E_INVALID_ARG for n_nodes == 0 < n_edges, negative
- * counts, counts above INT32_MAX or NULL pointers.  An index outside
- * [0, n_nodes) is reported as GNN_E_INDEX when GNN_VALIDATE_INDICES is set;
- * otherwise it is clamped into range (no fault, meaningless scores). */
+ * counts, counts above INT32_MAX or NULL pointers; GNN_E_UNSUPPORTED for
+ * n_edges >= 2^30 (the CSR sort's counters are 30 bits wide).  An index
+ * outside [0, n_nodes) is reported as GNN_E_INDEX when GNN_VALIDATE_INDICES
+ * is set; otherwise it is clamped into range (no fault, meaningless scores). */
 int gnn_infer(gnn_handle *h, const float *node_feat, const int32_t *edge_index,
               int64_t n_nodes, int64_t n_edges, float *edge_scores, hipStream_t stream);
 
@@ -151,8 +152,8 @@ int gnn_infer_logits(gnn_handle *h, const float *node_feat, const int32_t *edge_
  * the first call on it until the process ends.  An event whose workspace
  * (the bound at the top of this file) exceeds the array is rejected with
  * GNN_E_INVALID_ARG before any work is enqueued: the array holds events up
- * to about 50k hits and 330k edges at H = 128 in fp32 (372 MB of workspace;
- * 249 MB in bf16).  Larger events, such as the paper-scale 300k-hit event
+ * to about 50k hits and 330k edges at H = 128 in fp32 (378 MB of workspace;
+ * 255 MB in bf16).  Larger events, such as the paper-scale 300k-hit event
  * (1.7 GB), go through gnn_infer, whose cached workspace allocates only on
  * a handle's first call of a given size.  All calls on one
  * GPU share the array: calls whose work overlaps on that GPU (several
@@ -378,7 +379,9 @@ int gnn_profile_read(gnn_handle *h, gnn_profile_stats *out);
  * Destination- and source-sorted CSR of edge_index, as the inference path
  * builds it: row_ptr_in [n_nodes+1], perm_in [n_edges] (edge ids with
  * dst == v in ascending id order at row_ptr_in[v] .. row_ptr_in[v+1]-1),
- * and the same by source.  Any output pointer may be NULL. */
+ * and the same by source.  Any output pointer may be NULL.  Waits for the
+ * build; GNN_E_HIP if a sort pass gave up waiting on an earlier tile (its
+ * wait is bounded; running workgroups always end it in practice). */
 int gnn_debug_csr(gnn_handle *h, const int32_t *edge_index, int64_t n_nodes, int64_t n_edges,
                   int32_t *row_ptr_in, int32_t *perm_in, int32_t *row_ptr_out,
                   int32_t *perm_out, hipStream_t stream);

@@ -440,9 +440,9 @@ struct Workspace {
   int32_t *rp_in = nullptr, *rp_out = nullptr, *perm_in = nullptr, *perm_out = nullptr;
   CsrScratch csr{};
   int32_t *flag = nullptr;
-  // regrouped path: edges in source order ([2][E], in the sort scratch once
-  // the CSR is built), the in-CSR over that order, and the unit pieces of
-  // the fused out-sums ([units][2][H] fp32)
+  // regrouped path: edges in source order ([2][E], written by the CSR
+  // build), the in-CSR over that order, and the unit pieces of the fused
+  // out-sums ([units][2][H] fp32)
   int32_t *eis = nullptr, *inv = nullptr, *q_in = nullptr;
   float *part = nullptr;
 };
@@ -461,10 +461,11 @@ size_t plan_workspace(Workspace &w, int64_t N, int64_t E, int H, size_t act_byte
   const size_t o_ao = take((size_t)N * H * act_bytes);
   const size_t o_rpi = take((size_t)(N + 1) * 4), o_rpo = take((size_t)(N + 1) * 4);
   const size_t o_pi = take((size_t)E * 4), o_po = take((size_t)E * 4);
-  const size_t o_ka = take((size_t)E * 8), o_kb = take((size_t)E * 8);
-  const size_t o_va = take((size_t)E * 8), o_vb = take((size_t)E * 8);
-  const size_t o_hist = take(csr_hist_len(E) * 8);
-  const size_t o_tot = take(2 * 256 * 4 * 4);
+  const size_t o_sa = take((size_t)E * 16), o_sb = take((size_t)E * 16);
+  const size_t o_st = take(csr_scratch_bytes(E, N));
+  const size_t o_eis = factored ? take((size_t)E * 8) : 0;
+  const size_t o_inv = factored ? take((size_t)E * 4) : 0;
+  const size_t o_qin = factored ? take((size_t)E * 4) : 0;
   const size_t o_flag = take(4);
   const size_t o_pa = factored ? take((size_t)N * 2 * H * 4) : 0;
   const size_t o_pb = factored ? take((size_t)N * 2 * H * 4) : 0;
@@ -484,16 +485,15 @@ size_t plan_workspace(Workspace &w, int64_t N, int64_t E, int H, size_t act_byte
     w.rp_out = (int32_t *)(b + o_rpo);
     w.perm_in = (int32_t *)(b + o_pi);
     w.perm_out = (int32_t *)(b + o_po);
-    w.csr.keys_a = (uint32_t *)(b + o_ka);
-    w.csr.keys_b = (uint32_t *)(b + o_kb);
-    w.csr.vals_a = (uint32_t *)(b + o_va);
-    w.csr.vals_b = (uint32_t *)(b + o_vb);
-    w.csr.hist = (uint32_t *)(b + o_hist);
-    w.csr.totals = (uint32_t *)(b + o_tot);
+    w.csr.pairs_a = (uint2 *)(b + o_sa);
+    w.csr.pairs_b = (uint2 *)(b + o_sb);
+    w.csr.status = (uint32_t *)(b + o_st);
     w.flag = (int32_t *)(b + o_flag);
-    w.eis = (int32_t *)w.csr.keys_a;
-    w.inv = (int32_t *)w.csr.keys_b;
-    w.q_in = w.inv + E;
+    if (factored) {
+      w.eis = (int32_t *)(b + o_eis);
+      w.inv = (int32_t *)(b + o_inv);
+      w.q_in = (int32_t *)(b + o_qin);
+    }
   }
   return off;
 }
@@ -505,6 +505,9 @@ int check_counts(gnn_handle *h, int64_t N, int64_t E) {
   if (N > INT32_MAX || E > INT32_MAX)
     return fail(GNN_E_INVALID_ARG, "count above INT32_MAX");
   if (E > 0 && N == 0) return fail(GNN_E_INVALID_ARG, "n_edges > 0 with n_nodes == 0");
+  if (E >= CSR_MAX_ITEMS)
+    return fail(GNN_E_UNSUPPORTED, "n_edges %lld: the CSR build takes at most 2^30 - 1 edges",
+                (long long)E);
   return GNN_OK;
 }
 
@@ -803,16 +806,23 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
     int32_t *rpi = ro.rp_in ? ro.rp_in : w.rp_in, *pi = ro.perm_in ? ro.perm_in : w.perm_in;
     int32_t *rpo = ro.rp_out ? ro.rp_out : w.rp_out, *po = ro.perm_out ? ro.perm_out : w.perm_out;
     st.begin();
-    HIP_TRY(build_csr(ei, m, n, rpi, pi, rpo, po, w.csr, stream));
+    // The regrouped kernels keep the edge rows in source order (a node's
+    // out-edges are consecutive); outputs go back to input order.  The CSR
+    // build writes that order as well.
+    HIP_TRY(build_csr(ei, m, n, rpi, pi, rpo, po, w.csr, w.eis, w.inv, w.q_in, stream));
     st.end(GNN_STAGE_CSR);
-    if (ro.csr_only) goto out;
+    if (ro.csr_only) {
+      // the sort's look-back wait is bounded; report a pass that gave up
+      uint32_t err = 0;
+      HIP_TRY(hipMemcpyAsync(&err, csr_err_word(w.csr, m, n), 4, hipMemcpyDeviceToHost, stream));
+      HIP_TRY(hipStreamSynchronize(stream));
+      if (err) rc = fail(GNN_E_HIP, "CSR sort: a tile's look-back wait ran out");
+      goto out;
+    }
     w.rp_in = rpi;
     w.perm_in = pi;
     w.rp_out = rpo;
     w.perm_out = po;
-    // The regrouped kernels keep the edge rows in source order (a node's
-    // out-edges are consecutive); outputs go back to input order.
-    if (fac) HIP_TRY(launch_edge_order(ei, po, pi, m, n, w.eis, w.inv, w.q_in, stream));
   }
 
   if (fac) {

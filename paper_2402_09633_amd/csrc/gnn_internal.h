@@ -152,20 +152,27 @@ hipError_t launch_segsum_fused(Act act, int hidden, const void *e, const int32_t
 // (row_ptr_out, perm_out); row_ptr has n_nodes+1 entries, perm lists edge
 // ids ascending within each row.  Both sorts run in the same launches.
 struct CsrScratch {
-  uint32_t *keys_a, *keys_b, *vals_a, *vals_b;  // 2*n_edges each
-  uint32_t *hist;                               // 2*csr_hist_len(n_edges)
-  uint32_t *totals;                             // 2*256*4
+  uint2 *pairs_a, *pairs_b;  // 2*n_edges (key, edge id) pairs each
+  // look-back words of the sort passes, digit totals, tile counters and an
+  // error word: csr_scratch_bytes(n_edges, n_nodes) bytes, 4-byte aligned
+  uint32_t *status;
 };
-size_t csr_hist_len(int64_t n_edges);
+// The sort's look-back words hold counts below 2^30: builds of at most
+// CSR_MAX_ITEMS - 1 edges (larger ones return hipErrorInvalidValue).
+constexpr int32_t CSR_MAX_ITEMS = 1 << 30;
+size_t csr_scratch_bytes(int64_t n_edges, int64_t n_nodes);
+// Nonzero after a build in which a sort pass gave up waiting for an earlier
+// tile (a bounded wait that forward progress of running workgroups ends).
+uint32_t *csr_err_word(const CsrScratch &s, int64_t n_edges, int64_t n_nodes);
+// Destination- and source-sorted CSR of edge_index (stable: ascending edge id
+// within a row).  With eis set (regrouped kernels) it also writes the edges
+// in source order, eis[0][p] = src[perm_out[p]], eis[1][p] = dst[perm_out[p]]
+// (clamped into [0, n_nodes)), inv[j] = source-order position of edge j, and
+// q_in[k] = inv[perm_in[k]].
 hipError_t build_csr(const int32_t *edge_index, int32_t n_edges, int32_t n_nodes,
                      int32_t *row_ptr_in, int32_t *perm_in, int32_t *row_ptr_out,
-                     int32_t *perm_out, const CsrScratch &s, hipStream_t stream);
-// The edges in source order: eis[0][p] = src[perm_out[p]], eis[1][p] =
-// dst[perm_out[p]] (clamped into [0, n_nodes)), and q_in[k] = the source-order
-// position of edge perm_in[k]; inv ([n_edges]) is scratch.
-hipError_t launch_edge_order(const int32_t *edge_index, const int32_t *perm_out,
-                             const int32_t *perm_in, int32_t n_edges, int32_t n_nodes,
-                             int32_t *eis, int32_t *inv, int32_t *q_in, hipStream_t stream);
+                     int32_t *perm_out, const CsrScratch &s, int32_t *eis, int32_t *inv,
+                     int32_t *q_in, hipStream_t stream);
 // dst[idx[r]][:] = src[r][:] (fp32 or bf16 rows of width H, written as fp32).
 hipError_t launch_scatter_rows(Act act, const void *src, const int32_t *idx, float *dst,
                                int64_t rows, int H, hipStream_t stream);

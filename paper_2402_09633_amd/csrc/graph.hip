@@ -354,6 +354,8 @@ extern "C" int gnn_frnn(const float *z, int64_t n_nodes, int32_t dim, float r2,
   *n_pairs = 0;
   if (n_nodes < 0 || n_nodes > INT32_MAX)
     return set_error(GNN_E_INVALID_ARG, "n_nodes outside 0..INT32_MAX");
+  if (n_nodes >= CSR_MAX_ITEMS)
+    return set_error(GNN_E_UNSUPPORTED, "the cell sort takes at most 2^30 - 1 points");
   if (dim < 1 || dim > 16) return set_error(GNN_E_INVALID_ARG, "dim outside 1..16");
   if (max_pairs < 0) return set_error(GNN_E_INVALID_ARG, "max_pairs is negative");
   if (n_nodes > 0 && !z) return set_error(GNN_E_INVALID_ARG, "z is NULL");
@@ -384,9 +386,8 @@ extern "C" int gnn_frnn(const float *z, int64_t n_nodes, int32_t dim, float r2,
   const size_t o_keys = take((size_t)2 * n * 4);
   const size_t o_rpi = take(((size_t)m + 1) * 4), o_pi = take((size_t)n * 4);
   const size_t o_rpo = take(((size_t)m + 1) * 4), o_po = take((size_t)n * 4);
-  const size_t o_ka = take((size_t)2 * n * 4), o_kb = take((size_t)2 * n * 4);
-  const size_t o_va = take((size_t)2 * n * 4), o_vb = take((size_t)2 * n * 4);
-  const size_t o_hist = take(2 * csr_hist_len(n) * 4), o_tot = take(2 * 256 * 4 * 4);
+  const size_t o_pa = take((size_t)2 * n * 8), o_pb = take((size_t)2 * n * 8);
+  const size_t o_st = take(csr_scratch_bytes(n, m));
   const size_t o_cnt = take((size_t)n * 4), o_offs = take((size_t)n * 8), o_total = take(8);
   const size_t o_bsum = take(frnn_scan_blocks(n) * 8);
   const size_t o_zs = take((size_t)n * dim * 4);
@@ -398,12 +399,9 @@ extern "C" int gnn_frnn(const float *z, int64_t n_nodes, int32_t dim, float r2,
   unsigned char *b = (unsigned char *)base;
   int32_t *keys = (int32_t *)(b + o_keys);
   CsrScratch cs;
-  cs.keys_a = (uint32_t *)(b + o_ka);
-  cs.keys_b = (uint32_t *)(b + o_kb);
-  cs.vals_a = (uint32_t *)(b + o_va);
-  cs.vals_b = (uint32_t *)(b + o_vb);
-  cs.hist = (uint32_t *)(b + o_hist);
-  cs.totals = (uint32_t *)(b + o_tot);
+  cs.pairs_a = (uint2 *)(b + o_pa);
+  cs.pairs_b = (uint2 *)(b + o_pb);
+  cs.status = (uint32_t *)(b + o_st);
   a.rp = (const int32_t *)(b + o_rpi);
   a.perm = (const int32_t *)(b + o_pi);
   a.count = (int32_t *)(b + o_cnt);
@@ -416,7 +414,8 @@ extern "C" int gnn_frnn(const float *z, int64_t n_nodes, int32_t dim, float r2,
   hipError_t e = launch_frnn_keys(a, keys, stream);
   if (e == hipSuccess)
     e = build_csr(keys, (int32_t)n, (int32_t)m, (int32_t *)(b + o_rpi), (int32_t *)(b + o_pi),
-                  (int32_t *)(b + o_rpo), (int32_t *)(b + o_po), cs, stream);
+                  (int32_t *)(b + o_rpo), (int32_t *)(b + o_po), cs, nullptr, nullptr, nullptr,
+                  stream);
   float *zs = (float *)(b + o_zs);
   if (e == hipSuccess) e = launch_frnn_count(a, zs, stream);
   if (e == hipSuccess) e = hipMemcpyAsync(&total, a.total_dev, 8, hipMemcpyDeviceToHost, stream);

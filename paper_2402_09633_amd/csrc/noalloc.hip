@@ -24,7 +24,7 @@ namespace gnn {
 namespace {
 
 // 512 MiB: events up to about 50k hits and 330k edges at H = 128 in fp32
-// (workspace 372 MB; 249 MB in bf16).  The host side keeps a shadow of
+// (workspace 378 MB; 255 MB in bf16).  The host side keeps a shadow of
 // every device variable at full size (address space only, never touched),
 // which is one reason to keep the array modest.
 constexpr size_t kScratchBytes = size_t(512) << 20;

@@ -88,10 +88,12 @@ def test_create_without_device_reports_no_device(G):
 
 def test_no_float_atomics_in_kernels():
     # Aggregation must be deterministic: the only atomics are integer ones --
-    # the radix sort's uint32 digit counters (LDS `cnt`, global `totals`) and
+    # the radix sort's uint32 digit histograms (LDS `h`, global `totals`),
+    # its tile counters and error word, its uint32 look-back words (`st`),
     # the components' int32 parent array (atomicMin, relaxed loads) and the
     # relaxed loads of their int32 round flags.
-    allowed = ("atomicAdd(&cnt[", "atomicAdd(&S.totals[", "atomicMin(&parent[",
+    allowed = ("atomicAdd(&h[", "atomicAdd(&totals[", "atomicAdd(&O.ctr[", "atomicOr(O.err",
+               "__hip_atomic_store(st", "__hip_atomic_load(st", "atomicMin(&parent[",
                "__hip_atomic_load(parent", "__hip_atomic_load(prev", "__hip_atomic_load(changed")
     for f in os.listdir(CSRC):
         text = open(os.path.join(CSRC, f)).read()
@@ -100,7 +102,7 @@ def test_no_float_atomics_in_kernels():
             if "atomic" in code:
                 assert any(a in code for a in allowed), f"{f}: {line.strip()}"
     csr = open(os.path.join(CSRC, "csr.hip")).read()
-    assert "uint32_t cnt[" in csr and "uint32_t *totals[2]" in csr
+    assert "uint32_t h[" in csr and "uint32_t *totals" in csr and "uint32_t *status" in csr
     wcc = open(os.path.join(CSRC, "wcc.hip")).read()
     assert "int32_t *parent" in wcc and "float *parent" not in wcc
 

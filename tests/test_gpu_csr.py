@@ -58,7 +58,7 @@ def test_csr_shuffled_full(G, handle, oracle_mod):
 
 @pytest.mark.parametrize("n,e,seed", [(1, 5, 0), (2, 1, 1), (255, 1000, 2), (256, 4097, 3),
                                       (257, 2048, 4), (65536, 70001, 5), (65537, 3, 6),
-                                      (100_000, 333_333, 7)])
+                                      (100_000, 333_333, 7), ((1 << 24) + 1, 5000, 8)])
 def test_csr_edge_cases(G, handle, oracle_mod, n, e, seed):
     rng = np.random.default_rng(seed)
     ei = rng.integers(0, n, size=(2, e)).astype(np.int32)
@@ -72,3 +72,17 @@ def test_csr_hub(G, handle, oracle_mod):
     ei[1, rng.random(e) < 0.5] = 17       # in-degree ~150k
     ei[0, rng.random(e) < 0.2] = 4999     # out-degree ~60k
     check(G, handle, oracle_mod, ei, n)
+
+
+def test_csr_edge_limit(G, handle):
+    # 2^30 edges or more are refused before any device work (the sort's
+    # look-back words hold 30-bit counts); the small buffers are never read.
+    x = torch.zeros((4, 3), device="cuda")
+    ei = torch.zeros((2, 4), dtype=torch.int32, device="cuda")
+    out = torch.zeros(4, device="cuda")
+    with pytest.raises(G.GnnError) as e:
+        G.gnn_infer(handle, x, ei, 4, 1 << 30, out)
+    assert e.value.code == G.GNN_E_UNSUPPORTED
+    with pytest.raises(G.GnnError) as e:
+        G.gnn_debug_csr(handle, ei, 4, 1 << 30, None, None, None, None)
+    assert e.value.code == G.GNN_E_UNSUPPORTED
