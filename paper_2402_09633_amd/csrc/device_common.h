@@ -123,13 +123,15 @@ __device__ __forceinline__ void ln_relu_lds(f16v (&acc)[MB], const float *prm, f
     }
   s += __shfl_xor(s, 32);
   const float mean = s * inv_h;
+  // centred in place: the normalisation reuses x - mean (same roundings as
+  // recomputing it, one subtraction fewer per value)
   float var = 0.f;
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const float d = acc[mb][v] - mean;
-      var += d * d;
+      acc[mb][v] -= mean;
+      var += acc[mb][v] * acc[mb][v];
     }
   var += __shfl_xor(var, 32);
   const float rstd = ln_rstd(var * inv_h + eps);
@@ -142,7 +144,7 @@ __device__ __forceinline__ void ln_relu_lds(f16v (&acc)[MB], const float *prm, f
       const f4 bt = *(const f4 *)(prm + 2 * H + f);
 #pragma unroll
       for (int t = 0; t < 4; ++t)
-        acc[mb][4 * q + t] = fmaxf((acc[mb][4 * q + t] - mean) * rstd * gg[t] + bt[t], 0.f);
+        acc[mb][4 * q + t] = fmaxf(acc[mb][4 * q + t] * rstd * gg[t] + bt[t], 0.f);
     }
 }
 

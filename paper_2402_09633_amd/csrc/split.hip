@@ -130,8 +130,8 @@ __device__ __forceinline__ void ln_relu_t(f16v (&t)[MB], const float *prm, float
       float q = 0.f;
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
-        const float d = t[mb][v0 + j] - mean[j];
-        q += d * d;
+        t[mb][v0 + j] -= mean[j];  // centred in place, reused below
+        q += t[mb][v0 + j] * t[mb][v0 + j];
       }
       rstd[j] = ln_rstd(sum32(q) * inv_h + eps);
     }
@@ -139,7 +139,7 @@ __device__ __forceinline__ void ln_relu_t(f16v (&t)[MB], const float *prm, float
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        t[mb][v0 + j] = fmaxf((t[mb][v0 + j] - mean[j]) * rstd[j] * gg[mb] + bt[mb], 0.f);
+        t[mb][v0 + j] = fmaxf(t[mb][v0 + j] * rstd[j] * gg[mb] + bt[mb], 0.f);
   }
 }
 
