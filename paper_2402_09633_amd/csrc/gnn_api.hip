@@ -181,7 +181,21 @@ double ln_out_bound(const BlobLayer &L) {
 }
 
 // f16x2 records of s * W[:, c0 : c0 + K]: parts w1 = fp16(sW), w2 = fp16(sW - w1).
-std::vector<uint16_t> rec_f16x2(const BlobLayer &L, int c0, int K, float s, bool from_acc) {
+// Input feature of slot j (0..7) of lane half hh in k-step g of a record
+// stream (rec_f16x2, rec_bf16x2), by how the kernel supplies the operand:
+//   grp = 0: row slices from memory, k = 16 g + 8 hh + j;
+//   grp < 0: the previous layer's accumulators, k = 16 g + 8 (j / 4) + 4 hh + j % 4;
+//   grp > 0: line order (the node update's layer-1 rows): groups of grp
+//            k-steps cover 16 grp consecutive features, lane half hh the
+//            8 grp features from 8 grp hh on, k-step g % grp of the group its
+//            8 features from 8 (g % grp) on.
+inline int node_line_k(int g, int hh, int j, int grp) {
+  if (grp < 0) return 16 * g + 8 * (j / 4) + 4 * hh + j % 4;
+  if (grp == 0) return 16 * g + 8 * hh + j;
+  return 16 * grp * (g / grp) + 8 * grp * hh + 8 * (g % grp) + j;
+}
+
+std::vector<uint16_t> rec_f16x2(const BlobLayer &L, int c0, int K, float s, int grp) {
   const int MB = L.fout / 32, G = K / 16;
   std::vector<uint16_t> out((size_t)G * MB * 2 * 64 * 8);
   for (int g = 0; g < G; ++g)
@@ -189,7 +203,7 @@ std::vector<uint16_t> rec_f16x2(const BlobLayer &L, int c0, int K, float s, bool
       for (int lane = 0; lane < 64; ++lane)
         for (int j = 0; j < 8; ++j) {
           const int hh = lane / 32;
-          const int k = from_acc ? 16 * g + 8 * (j / 4) + 4 * hh + j % 4 : 16 * g + 8 * hh + j;
+          const int k = node_line_k(g, hh, j, grp);
           const float wv = s * L.W[(size_t)(mb * 32 + lane % 32) * L.fin + c0 + k];
           const _Float16 p1 = (_Float16)wv;
           const _Float16 p2 = (_Float16)(wv - (float)p1);
@@ -203,8 +217,7 @@ std::vector<uint16_t> rec_f16x2(const BlobLayer &L, int c0, int K, float s, bool
 // bf16 hi/lo records of sc * W[:, c0 : c0 + K]: hi = bf16(sc W), lo =
 // bf16(sc W - hi) (the bf16 model's weights; sc a power of two, so the pair
 // is sc times the pair of W).
-std::vector<uint16_t> rec_bf16x2(const BlobLayer &L, int c0, int K, bool from_acc,
-                                 float sc = 1.f) {
+std::vector<uint16_t> rec_bf16x2(const BlobLayer &L, int c0, int K, int grp, float sc = 1.f) {
   const int MB = L.fout / 32, G = K / 16;
   std::vector<uint16_t> out((size_t)G * MB * 2 * 64 * 8);
   for (int g = 0; g < G; ++g)
@@ -212,7 +225,7 @@ std::vector<uint16_t> rec_bf16x2(const BlobLayer &L, int c0, int K, bool from_ac
       for (int lane = 0; lane < 64; ++lane)
         for (int j = 0; j < 8; ++j) {
           const int hh = lane / 32;
-          const int k = from_acc ? 16 * g + 8 * (j / 4) + 4 * hh + j % 4 : 16 * g + 8 * hh + j;
+          const int k = node_line_k(g, hh, j, grp);
           const float wv = sc * L.W[(size_t)(mb * 32 + lane % 32) * L.fin + c0 + k];
           const uint16_t hi = f32_to_bf16(wv);
           const size_t o = ((((size_t)g * MB + mb) * 2) * 64 + lane) * 8 + j;
@@ -1253,11 +1266,11 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
         fdh.s2_em.push_back(1.f);
         fdh.s1_nm.push_back(1.f);
         fdh.s2_nm.push_back(1.f);
-        o_we_em[s] = add16(rec_bf16x2(e0s[s], 2 * H, H, false, fdh.s1_em[s]));
-        o_w2_em[s] = add16(rec_bf16x2(e1s[s], 0, H, true));
+        o_we_em[s] = add16(rec_bf16x2(e0s[s], 2 * H, H, 0, fdh.s1_em[s]));
+        o_w2_em[s] = add16(rec_bf16x2(e1s[s], 0, H, -1));
       }
-      o_we_cls = add16(rec_bf16x2(c0, 2 * H, H, false, fdh.s1_cls));
-      o_w2_ee = add16(rec_bf16x2(b1, 0, H, true));
+      o_we_cls = add16(rec_bf16x2(c0, 2 * H, H, 0, fdh.s1_cls));
+      o_w2_ee = add16(rec_bf16x2(b1, 0, H, -1));
       auto scale_of = [&](const BlobLayer &L) {
         if (&L == &c0) return fdh.s1_cls;
         for (int s = 0; s < S; ++s)
@@ -1266,17 +1279,17 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
       };
       auto proj = [&](std::vector<uint16_t> &dst, const BlobLayer &L) {
         const float sc = scale_of(L);
-        cat(dst, rec_bf16x2(L, 0, H, true, sc));
-        cat(dst, rec_bf16x2(L, H, H, true, sc));
+        cat(dst, rec_bf16x2(L, 0, H, -1, sc));
+        cat(dst, rec_bf16x2(L, H, H, -1, sc));
       };
-      std::vector<uint16_t> es = rec_bf16x2(a1, 0, H, true);
+      std::vector<uint16_t> es = rec_bf16x2(a1, 0, H, -1);
       proj(es, b0);
       proj(es, next_edge_l1(-1));
       o_enc_stream = add16(es);
       for (int t = 0; t < T; ++t) {
         const int k = S == 1 ? 0 : t;
-        std::vector<uint16_t> us = rec_bf16x2(n0s[k], 0, 3 * H, false);
-        cat(us, rec_bf16x2(n1s[k], 0, H, true));
+        std::vector<uint16_t> us = rec_bf16x2(n0s[k], 0, 3 * H, 4);
+        cat(us, rec_bf16x2(n1s[k], 0, H, -1));
         proj(us, next_edge_l1(t));
         o_upd_stream[t] = add16(us);
       }
@@ -1296,11 +1309,11 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
         fdh.s2_em.push_back(pow2_scale(e1s[s]));
         fdh.s1_nm.push_back(pow2_scale(n0s[s]));
         fdh.s2_nm.push_back(pow2_scale(n1s[s]));
-        o_we_em[s] = add16(rec_f16x2(e0s[s], 2 * H, H, fdh.s1_em[s], false));
-        o_w2_em[s] = add16(rec_f16x2(e1s[s], 0, H, fdh.s2_em[s], true));
+        o_we_em[s] = add16(rec_f16x2(e0s[s], 2 * H, H, fdh.s1_em[s], 0));
+        o_w2_em[s] = add16(rec_f16x2(e1s[s], 0, H, fdh.s2_em[s], -1));
       }
-      o_we_cls = add16(rec_f16x2(c0, 2 * H, H, fdh.s1_cls, false));
-      o_w2_ee = add16(rec_f16x2(b1, 0, H, fdh.s2_ee, true));
+      o_we_cls = add16(rec_f16x2(c0, 2 * H, H, fdh.s1_cls, 0));
+      o_w2_ee = add16(rec_f16x2(b1, 0, H, fdh.s2_ee, -1));
       // Projections of h (B operand from the accumulators), scaled by the
       // consumer's first-layer scale.
       auto scale_of = [&](const BlobLayer &L) {
@@ -1311,17 +1324,17 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
       };
       auto proj = [&](std::vector<uint16_t> &dst, const BlobLayer &L) {
         const float sc = scale_of(L);
-        cat(dst, rec_f16x2(L, 0, H, sc, true));
-        cat(dst, rec_f16x2(L, H, H, sc, true));
+        cat(dst, rec_f16x2(L, 0, H, sc, -1));
+        cat(dst, rec_f16x2(L, H, H, sc, -1));
       };
-      std::vector<uint16_t> es = rec_f16x2(a1, 0, H, fdh.s2_ne, true);
+      std::vector<uint16_t> es = rec_f16x2(a1, 0, H, fdh.s2_ne, -1);
       proj(es, b0);
       proj(es, next_edge_l1(-1));
       o_enc_stream = add16(es);
       for (int t = 0; t < T; ++t) {
         const int k = S == 1 ? 0 : t;
-        std::vector<uint16_t> us = rec_f16x2(n0s[k], 0, 3 * H, fdh.s1_nm[k], false);
-        cat(us, rec_f16x2(n1s[k], 0, H, fdh.s2_nm[k], true));
+        std::vector<uint16_t> us = rec_f16x2(n0s[k], 0, 3 * H, fdh.s1_nm[k], 2);
+        cat(us, rec_f16x2(n1s[k], 0, H, fdh.s2_nm[k], -1));
         proj(us, next_edge_l1(t));
         o_upd_stream[t] = add16(us);
       }
@@ -1615,7 +1628,7 @@ gnn_filter *gnn_filter_create(const float *weights, const gnn_filter_dims *dims)
   const float s1 = split ? pow2_scale(l1) : 1.f;
   size_t o_w1r = 0;
   if (split) {
-    const std::vector<uint16_t> r = rec_f16x2(l1, 0, H, s1, true);
+    const std::vector<uint16_t> r = rec_f16x2(l1, 0, H, s1, -1);
     o_w1r = st.add(r.data(), r.size() * sizeof(uint16_t));
   }
   gnn_filter *f = new gnn_filter();
@@ -1730,7 +1743,7 @@ gnn_embedder *gnn_embed_create(const float *weights, const gnn_embed_dims *dims)
   const float s1 = split ? pow2_scale(l1) : 1.f;
   size_t o_w1r = 0;
   if (split) {
-    const std::vector<uint16_t> r = rec_f16x2(l1, 0, H, s1, true);
+    const std::vector<uint16_t> r = rec_f16x2(l1, 0, H, s1, -1);
     o_w1r = st.add(r.data(), r.size() * sizeof(uint16_t));
   }
   gnn_embedder *m = new gnn_embedder();

@@ -343,6 +343,12 @@ constexpr int rpc_h() { return ENC ? 4 : 6; }
 template <int MB, bool ENC>
 constexpr int node_nf4() { return (ENC ? 4 * 2 : 4 * 3) * MB * 64 / 512; }
 
+// Records per 128-byte line pair of the node update's layer-1 inputs (two
+// lanes read one line of a row): 2 for fp32 rows, 4 for bf16 rows.  The
+// host packs those records in the same order (node_line_k in gnn_api.hip).
+template <int PREC>
+constexpr int line_group() { return PREC == SPLIT ? 2 : 4; }
+
 template <int MB, bool ENC, int NPROJ, int PREC>
 __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
   constexpr int H = 32 * MB;
@@ -426,29 +432,36 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
       small_k_layer<MB>(acc, a.x, a.F, (int)r, prm + 7 * H, prm + 6 * H, hh);
       ln_relu_lds<MB>(acc, prm, a.eps, hh);
     } else {
-      // Layer 1 over [h; agg_in; agg_out]: 3G records.  The node row
-      // slices are loaded LA records ahead into a ring of LA + 1 slots.
+      // Layer 1 over [h; agg_in; agg_out]: 3G records.  The k-steps of each
+      // source are taken in line order (node_line_k): the GRP records of a
+      // group cover 16 GRP consecutive features, lanes n and n + 32 reading
+      // the two 64-byte halves of one 128-byte line of row n, and a group's
+      // records are requested together, one group ahead, into a ring of
+      // two groups.
       zero<MB>(acc);
-      constexpr int NREC = 3 * G, LA = 3;
+      constexpr int NREC = 3 * G, GRP = line_group<PREC>(), RING = 2 * GRP;
+      static_assert(G % GRP == 0, "groups inside one source");
       // Addresses are a per-tile scalar base plus one 32-bit lane offset
       // shared by the three sources: 64-bit per-lane pointers cost the
       // registers that the look-ahead needs (a spill reload would wait for
       // every load in flight).
       const int64_t t0 = wrow0;
-      const uint32_t roff = (uint32_t)((r - t0) * H + 8 * hh) * (uint32_t)sizeof(act_t);
+      const uint32_t roff =
+          (uint32_t)((r - t0) * H + 8 * GRP * hh) * (uint32_t)sizeof(act_t);
       const act_t *const *srcs = (const act_t *const *)a.src;
       using xrec_t = typename std::conditional<PREC == SPLIT, f8, bf8>::type;
       auto load_rec = [&](int rec) {
+        const int g = rec % G;
         const char *p = (const char *)(srcs[rec / G] + t0 * H) + roff +
-                        16 * (int)sizeof(act_t) * (rec % G);
+                        (int)sizeof(act_t) * (16 * GRP * (g / GRP) + 8 * (g % GRP));
         if constexpr (PREC == SPLIT)
           return cat8(*(const f4 *)p, *(const f4 *)(p + 16));
         else
           return *(const bf8 *)p;
       };
-      xrec_t xr[LA + 1];
+      xrec_t xr[RING];
 #pragma unroll
-      for (int i = 0; i < LA; ++i) xr[i] = load_rec(i);
+      for (int i = 0; i < GRP; ++i) xr[i] = load_rec(i);
       // Split: the node's whole input row is multiplied by a power of two
       // sv <= 1 that keeps it inside the fp16 range of the split parts: the
       // aggregates are bounded by max(deg_in, deg_out) times the bound of a
@@ -470,15 +483,17 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
       const f4 *w = nullptr;
 #pragma unroll
       for (int i = 0; i < NREC; ++i) {
-        if (i + LA < NREC) xr[(i + LA) % (LA + 1)] = load_rec(i + LA);
-        // keeps the load here: under register pressure the scheduler would
-        // sink it next to its use and the look-ahead would be lost
+        if (i % GRP == 0 && i + GRP < NREC)
+#pragma unroll
+          for (int j = 0; j < GRP; ++j) xr[(i + GRP + j) % RING] = load_rec(i + GRP + j);
+        // keeps the loads here: under register pressure the scheduler would
+        // sink them next to their use and the look-ahead would be lost
         __builtin_amdgcn_sched_barrier(0);
         if (i % RPC_1 == 0) w = ws.begin(tid) + lane;
         if constexpr (PREC == SPLIT)
-          step_h<MB>(acc, (const h8 *)(w + (i % RPC_1) * REC_1), xr[i % (LA + 1)] * sv);
+          step_h<MB>(acc, (const h8 *)(w + (i % RPC_1) * REC_1), xr[i % RING] * sv);
         else
-          step_hl<MB>(acc, (const bf8 *)(w + (i % RPC_1) * REC_1), xr[i % (LA + 1)]);
+          step_hl<MB>(acc, (const bf8 *)(w + (i % RPC_1) * REC_1), xr[i % RING]);
         if (i % RPC_1 == RPC_1 - 1) ws.end(tid);
       }
       if constexpr (PREC == SPLIT) {
