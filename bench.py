@@ -46,10 +46,11 @@ TRAFFIC_SOURCES = {
     "fp32_mfma": ["paper_2402_09633_amd/csrc/factored.hip",
                   "paper_2402_09633_amd/csrc/device_common.h"],
 }
-# (path, source hash) -> HBM bytes per edge-update launch on the full event
-MEASURED_TRAFFIC = {("split", "f44aaaf4a983a653"): 1.790e9,       # edge_split<4,3>
-                    ("bf16", "f44aaaf4a983a653"): 0.8937e9,       # edge_split<4,3,bf16>
-                    ("fp32_mfma", "d6fe23f044f63d7b"): 1.651e9}   # edge_f32<4,1>
+# (path, source hash) -> (HBM bytes read, written) per edge-update launch on
+# the full event
+MEASURED_TRAFFIC = {("split", "f44aaaf4a983a653"): (1.139e9, 0.651e9),     # edge_split<4,3>
+                    ("bf16", "f44aaaf4a983a653"): (0.5504e9, 0.3433e9),    # edge_split<4,3,bf16>
+                    ("fp32_mfma", "d6fe23f044f63d7b"): (1.000e9, 0.651e9)}  # edge_f32<4,1>
 
 
 def kernel_source_hash(path):
@@ -84,6 +85,55 @@ def edge_update_bytes(N, E, H, s=4, n_src=0):
     out-sums (n_src > 0), one agg_out row (s bytes per element) per node
     that has out-edges."""
     return E * (2 * H * s + 2 * H * proj_bytes(s) + 8) + n_src * H * s
+
+
+def edge_update_rw(N, E, H, s=4, n_src=0):
+    """edge_update_bytes split into (read, written)."""
+    return (E * (H * s + 2 * H * proj_bytes(s) + 8), E * H * s + n_src * H * s)
+
+
+def node_update_rw(N, H, s=4, T=1):
+    """node_update_bytes split into (read, written)."""
+    return (N * 3 * H * s, N * 2 * H * proj_bytes(s) + N * H * s * (T - 1) / T)
+
+
+def aggregate_rw(N, E, H, s, n_src):
+    """aggregate_bytes after the fused edge update, split into (read, written)."""
+    return (E * H * s + E * 4 + 2.0 * (N + 1) * 4, N * H * s + (N - n_src) * H * s)
+
+
+def practical(rw, seconds, ceil):
+    """The launch's HBM rate against what plain streaming kernels reach on
+    this device: a launch that reads R and writes W bytes needs at least
+    R / read_rate + W / write_rate."""
+    if not ceil:
+        return None
+    r, w = rw
+    t_min = r / (ceil["read_gbs"] * 1e9) + w / (ceil["write_gbs"] * 1e9)
+    return {"read_bytes": r, "write_bytes": w,
+            "ceiling_gbs": round((r + w) / t_min / 1e9, 1),
+            "achieved_gbs": round((r + w) / seconds / 1e9, 1),
+            "frac": round(t_min / seconds, 4)}
+
+
+def hbm_ceiling(G, torch):
+    """Fastest read, write and copy rates of the library's streaming probe
+    (1 GiB, nontemporal 16-byte accesses) over a few grid sizes."""
+    nb = 1 << 30
+    a = torch.empty(nb // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty(nb // 4, dtype=torch.float32, device="cuda")
+    a.zero_()
+    out = {"bytes": nb}
+    for kind, name, moved in ((G.GNN_PROBE_READ, "read_gbs", nb), (G.GNN_PROBE_WRITE, "write_gbs", nb),
+                              (G.GNN_PROBE_COPY, "copy_gbs", 2 * nb)):
+        best = min(G.gnn_hbm_probe(kind, a, b, nb, grid, 5) for grid in (512, 1024, 2048, 4096))
+        out[name] = round(moved / (best / 1000.0) / 1e9, 1)
+    del a, b
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    out["note"] = ("plain grid-stride kernels (gnn_hbm_probe), best of 5 launches at 512-4096 "
+                   "workgroups of 256 threads; copy_gbs counts bytes read plus written")
+    return out
 
 
 def node_update_bytes(N, H, s=4, T=1):
@@ -223,7 +273,7 @@ def timed_leg(G, torch, np, g, w, H, T, dtype, flags, steps, warmup):
             "logits": zt.cpu().numpy(), "model": m, "x": x, "ei": ei, "out": out}
 
 
-def rooflines(prof, N, E, H, T, bf16, split, factored, n_src, traffic):
+def rooflines(prof, N, E, H, T, bf16, split, factored, n_src, traffic, ceil=None):
     """Edge-update (dominant), node-update and aggregation rooflines from the
     library's per-stage HIP-event times over the timed region."""
     act_bytes = 2 if bf16 else 4
@@ -249,7 +299,7 @@ def rooflines(prof, N, E, H, T, bf16, split, factored, n_src, traffic):
                           ("edge_split<4,3> (gathers node projections, W_e e, layer 2 "
                            "transposed, per-source sums of its rows; f16x2 weights in LDS)"),
                 "bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
+                "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": sum(traffic) if traffic else None,
                 "bytes_per_launch": eb, "avg_launch_ms": round(eu_ms, 4),
                 "mfma": {"dtype": mdt, "executed_tflop_per_launch": mf["edge_update"] / 1e12,
                          "achieved": round(eu_mfma, 1), "peak": PEAK_TFLOPS[mdt],
@@ -258,9 +308,16 @@ def rooflines(prof, N, E, H, T, bf16, split, factored, n_src, traffic):
         if traffic:
             # the counter-measured HBM stream of the same launch, beside the
             # algorithmic rate (on-die reuse of the gathered rows makes it lower)
-            tg = traffic / (eu_ms / 1000.0) / 1e9
+            tg = sum(traffic) / (eu_ms / 1000.0) / 1e9
             roof["traffic_gbs"] = round(tg, 1)
             roof["traffic_frac"] = round(tg / PEAK_HBM_GBS, 4)
+        # against the measured streaming ceilings: the counter split when the
+        # counters match these sources, else the algorithmic one (gathered
+        # rows counted per edge, an upper bound of the bytes moved)
+        pr = practical(traffic or edge_update_rw(N, E, H, act_bytes, n_src), eu_ms / 1000.0, ceil)
+        if pr:
+            pr["bytes"] = "counters" if traffic else "algorithmic"
+            roof["practical"] = pr
         nb = node_update_bytes(N, H, act_bytes, T)
         nu_gbs = nb / (nu_ms / 1000.0) / 1e9
         nu_mfma = mf["node_update"] / (nu_ms / 1000.0) / 1e12
@@ -275,6 +332,9 @@ def rooflines(prof, N, E, H, T, bf16, split, factored, n_src, traffic):
                               "executed_tflop_per_launch": mf["node_update"] / 1e12,
                               "achieved": round(nu_mfma, 1), "peak": PEAK_TFLOPS["fp16"],
                               "unit": "TFLOP/s", "frac": round(nu_mfma / PEAK_TFLOPS["fp16"], 4)}}
+        pr = practical(node_update_rw(N, H, act_bytes, T), nu_ms / 1000.0, ceil)
+        if pr:
+            roof_node["practical"] = pr
     else:
         achieved = eu_flops / (eu_ms / 1000.0) / 1e12
         peak = PEAK_TFLOPS["fp32"]
@@ -282,7 +342,7 @@ def rooflines(prof, N, E, H, T, bf16, split, factored, n_src, traffic):
                            "weights in LDS)") if factored else
                           ("gmlp edge update (gathers [h_src; h_dst; e], 3H->H->H)"),
                 "bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
-                "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": traffic,
+                "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": sum(traffic) if traffic else None,
                 "flops_per_launch": eu_flops, "avg_launch_ms": round(eu_ms, 4)}
     roof_agg = {"kernel": ("aggregate (in-direction CSR sums; out-direction rows the edge update "
                            "left in pieces completed, empty rows zeroed)") if n_src else
@@ -290,6 +350,10 @@ def rooflines(prof, N, E, H, T, bf16, split, factored, n_src, traffic):
                 "bound": "hbm", "achieved": round(ag_gbs, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(ag_gbs / PEAK_HBM_GBS, 4),
                 "bytes_per_launch": ag_bytes, "avg_launch_ms": round(ag_ms, 4)}
+    if n_src:
+        pr = practical(aggregate_rw(N, E, H, act_bytes, n_src), ag_ms / 1000.0, ceil)
+        if pr:
+            roof_agg["practical"] = pr
     return roof, roof_node, roof_agg
 
 
@@ -622,8 +686,9 @@ def main():
     traffic = None
     if factored and cfg.name in ("full", "full_bf16") and path in TRAFFIC_SOURCES:
         traffic = MEASURED_TRAFFIC.get((path, kernel_source_hash(path)))
+    ceil = hbm_ceiling(G, torch)
     roof, roof_node, roof_agg = rooflines(leg["prof"], N, E, H, T, bf16, split, factored,
-                                          n_src, traffic)
+                                          n_src, traffic, ceil)
     per = leg["per"]
     rec = {
         "metric": METRIC,
@@ -652,6 +717,7 @@ def main():
         "ms_per_event_min": round(float(per.min()), 4),
         "roofline": roof,
         "roofline_aggregate": roof_agg,
+        "hbm_ceiling": ceil,
         "stages_ms_per_event": stages(leg["prof"]),
         "components": {"ms_per_event": round(wcc_ms, 4), "threshold": 0.5,
                        "n_components": n_comp,
@@ -686,7 +752,7 @@ def main():
         bleg["model"].close()
         btraffic = MEASURED_TRAFFIC.get(("bf16", kernel_source_hash("bf16")))
         broof, broof_node, broof_agg = rooflines(bleg["prof"], N, E, H, T, True, True, True,
-                                                 n_src, btraffic)
+                                                 n_src, btraffic, ceil)
         rec["bf16"] = {
             "ms_per_event": round(bleg["ms_per_step"], 4),
             "edges_per_s": round(E / (bleg["ms_per_step"] / 1000.0), 1),

@@ -375,6 +375,27 @@ int gnn_profile_enable(gnn_handle *h, int enable);
 /* Synchronise the recorded events and fill *out (struct_size must be set). */
 int gnn_profile_read(gnn_handle *h, gnn_profile_stats *out);
 
+/* ---- measurement aid: achievable HBM streaming rates --------------------
+ * Not an operation of the method: it gives the roofline figures a measured
+ * ceiling beside the 8 TB/s peak.  One launch of a plain grid-stride kernel
+ * of 256-thread workgroups streams `bytes` (a positive multiple of 16)
+ * through device memory in 16-byte nontemporal accesses:
+ *   GNN_PROBE_READ   reads buf; buf2 (>= 4 bytes) is a sink written only
+ *                    when the sum equals -1.5e38 (never, for finite data);
+ *   GNN_PROBE_WRITE  fills buf (buf2 unused but must be non-NULL);
+ *   GNN_PROBE_COPY   copies buf to buf2 (both `bytes` long, disjoint).
+ * grid = workgroups (0: 4 per compute unit).  After one untimed launch,
+ * `reps` launches (1..1000) are timed with HIP events on `stream`; *ms gets
+ * the fastest.  Waits for the stream.  buf and buf2 are device pointers
+ * owned by the caller; their contents afterwards are unspecified.  Returns
+ * GNN_E_INVALID_ARG for a bad kind, size, grid, reps or NULL pointer,
+ * GNN_E_HIP if a launch or event call fails. */
+#define GNN_PROBE_READ 0
+#define GNN_PROBE_WRITE 1
+#define GNN_PROBE_COPY 2
+int gnn_hbm_probe(int kind, void *buf, void *buf2, int64_t bytes, int32_t grid, int32_t reps,
+                  float *ms, hipStream_t stream);
+
 /* ---- test hooks ---------------------------------------------------------
  * Destination- and source-sorted CSR of edge_index, as the inference path
  * builds it: row_ptr_in [n_nodes+1], perm_in [n_edges] (edge ids with

@@ -38,7 +38,7 @@ EXPORTS = ("gnn_weight_count", "gnn_create", "gnn_infer", "gnn_infer_logits", "g
            "gnn_server_create", "gnn_server_submit", "gnn_server_wait", "gnn_server_wait_info",
            "gnn_server_destroy", "gnn_set_workspace_limit",
            "gnn_embed_weight_count", "gnn_embed_create", "gnn_embed_apply", "gnn_embed_destroy",
-           "gnn_frnn")
+           "gnn_frnn", "gnn_hbm_probe")
 STAGES = ("csr", "node_enc", "edge_enc", "edge_update", "aggregate", "node_update",
           "classifier", "total")
 
@@ -128,6 +128,9 @@ def _load():
     L.gnn_profile_enable.argtypes = [vp, ctypes.c_int]
     L.gnn_profile_read.restype = ctypes.c_int
     L.gnn_profile_read.argtypes = [vp, ctypes.POINTER(gnn_profile_stats)]
+    L.gnn_hbm_probe.restype = ctypes.c_int
+    L.gnn_hbm_probe.argtypes = [ctypes.c_int, vp, vp, i64, i32, i32, ctypes.POINTER(ctypes.c_float),
+                                vp]
     L.gnn_debug_csr.restype = ctypes.c_int
     L.gnn_debug_csr.argtypes = [vp, vp, i64, i64, vp, vp, vp, vp, vp]
     L.gnn_debug_stages.restype = ctypes.c_int
@@ -319,6 +322,18 @@ def gnn_profile_read(handle) -> dict:
     for i, name in enumerate(STAGES):
         out[name] = {"launches": int(st.launches[i]), "ms": float(st.ms[i])}
     return out
+
+
+GNN_PROBE_READ, GNN_PROBE_WRITE, GNN_PROBE_COPY = 0, 1, 2
+
+
+def gnn_hbm_probe(kind: int, buf, buf2, nbytes: int, grid: int = 0, reps: int = 5,
+                  stream=None) -> float:
+    """Fastest of `reps` timed launches of the streaming probe, in ms."""
+    ms = ctypes.c_float(0.0)
+    _check(lib.gnn_hbm_probe(kind, _addr(buf), _addr(buf2), nbytes, grid, reps, ctypes.byref(ms),
+                             _stream(stream)))
+    return float(ms.value)
 
 
 def gnn_debug_csr(handle, edge_index, n_nodes: int, n_edges: int, row_ptr_in=None, perm_in=None,

@@ -154,3 +154,17 @@ def test_workspace_limit_and_server_calls_reject_null(G):
     assert "struct_size" in G.gnn_last_error()
     assert G.lib.gnn_server_wait(None, 0, None) == G.GNN_E_INVALID_ARG
     assert G.lib.gnn_server_submit(None, None, None, 1, 1, None) == G.GNN_E_INVALID_ARG
+
+
+@pytest.mark.parametrize("kind,nbytes,grid,reps,null", [(3, 1024, 0, 1, False), (0, 1000, 0, 1, False),
+                                                         (0, 0, 0, 1, False), (1, 1024, -1, 1, False),
+                                                         (2, 1024, 0, 0, False), (2, 1024, 0, 1001, False),
+                                                         (0, 1024, 0, 1, True)])
+def test_hbm_probe_rejects_bad_arguments(G, kind, nbytes, grid, reps, null):
+    # checked before any device call (no GPU needed)
+    buf = None if null else 16
+    ms = ctypes.c_float(-1.0)
+    rc = G.lib.gnn_hbm_probe(kind, buf, 16, nbytes, grid, reps, ctypes.byref(ms), None)
+    assert rc == G.GNN_E_INVALID_ARG
+    assert ms.value == 0.0
+    assert G.gnn_last_error() != ""

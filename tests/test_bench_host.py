@@ -83,3 +83,24 @@ def test_max_scaled_error_definition():
     assert bench.max_scaled_err([0.0], [1e-3]) == pytest.approx(1e-3)
     assert bench.max_scaled_err([101.0], [100.0]) == pytest.approx(1e-2)
     assert bench.max_scaled_err([], []) == 0.0
+
+
+def test_practical_ceiling_is_the_serial_read_write_bound():
+    # 1 GB read at 8 GB/s and 0.5 GB written at 4 GB/s need at least
+    # 0.125 + 0.125 s: a launch of 0.5 s reaches half of that ceiling
+    ceil = {"read_gbs": 8.0, "write_gbs": 4.0}
+    pr = bench.practical((1e9, 0.5e9), 0.5, ceil)
+    assert pr["ceiling_gbs"] == pytest.approx(1.5e9 / 0.25 / 1e9)
+    assert pr["achieved_gbs"] == pytest.approx(3.0)
+    assert pr["frac"] == pytest.approx(0.5)
+    assert bench.practical((1e9, 0.5e9), 0.5, None) is None
+
+
+def test_read_write_splits_add_up_to_the_byte_counts():
+    for s in (4, 2):
+        r, w = bench.edge_update_rw(N, E, H, s, N_SRC)
+        assert r + w == pytest.approx(bench.edge_update_bytes(N, E, H, s, N_SRC))
+        r, w = bench.node_update_rw(N, H, s, T)
+        assert r + w == pytest.approx(bench.node_update_bytes(N, H, s, T))
+        r, w = bench.aggregate_rw(N, E, H, s, N_SRC)
+        assert r + w == pytest.approx(bench.aggregate_bytes(N, E, H, s, N_SRC))
