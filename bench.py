@@ -48,9 +48,8 @@ TRAFFIC_SOURCES = {
 }
 # (path, source hash) -> (HBM bytes read, written) per edge-update launch on
 # the full event
-MEASURED_TRAFFIC = {("split", "f44aaaf4a983a653"): (1.139e9, 0.651e9),     # edge_split<4,3>
-                    ("bf16", "f44aaaf4a983a653"): (0.5504e9, 0.3433e9),    # edge_split<4,3,bf16>
-                    ("fp32_mfma", "d6fe23f044f63d7b"): (1.000e9, 0.651e9)}  # edge_f32<4,1>
+MEASURED_TRAFFIC = {("split", "270c0bc20d53cec3"): (1.138e9, 0.651e9),    # edge_split<4,3>
+                    ("bf16", "270c0bc20d53cec3"): (0.551e9, 0.343e9)}     # edge_split<4,3,bf16>
 
 
 def kernel_source_hash(path):
