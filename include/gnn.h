@@ -77,6 +77,20 @@ extern "C" {
                                    max|gamma| sqrt(H-1) + max|beta| <= 2^15;
                                    weights that break it select this path by
                                    themselves. */
+#define GNN_F16_WEIGHTS 8u      /* GNN_BF16 only (not with GNN_LITERAL_GATHER or
+                                   GNN_FP32_MFMA): each weight carried as one
+                                   fp16 number (times a power of two) instead
+                                   of the bf16 pair hi/lo, so every product is
+                                   one fp16 matrix-core operation instead of
+                                   two bf16 ones.  Activations stay bf16 in
+                                   memory and are rounded to bf16 where they
+                                   feed a product, then converted exactly to
+                                   fp16 (a node's aggregate row scaled by a
+                                   power of two when its degree would leave the
+                                   fp16 range).  Needs every LayerNorm output
+                                   bound (as above) <= 2^15 and every scaled
+                                   weight inside the fp16 range; otherwise
+                                   gnn_create fails with GNN_E_UNSUPPORTED. */
 
 typedef struct gnn_dims {
   uint32_t struct_size;     /* = sizeof(gnn_dims) (ABI versioning)              */
@@ -88,7 +102,7 @@ typedef struct gnn_dims {
   int32_t dtype;            /* GNN_FP32 or GNN_BF16                             */
   float ln_eps;             /* LayerNorm epsilon (1e-5)                         */
   uint32_t flags;           /* OR of GNN_VALIDATE_INDICES, GNN_LITERAL_GATHER,
-                               GNN_FP32_MFMA, or 0                              */
+                               GNN_FP32_MFMA, GNN_F16_WEIGHTS, or 0             */
 } gnn_dims;
 
 typedef struct gnn_handle gnn_handle;

@@ -69,8 +69,13 @@ int check_dims(const gnn_dims *d) {
     return fail(GNN_E_INVALID_ARG, "dtype %d unknown", d->dtype);
   if (!(d->ln_eps > 0.f) || !(d->ln_eps < 1.f))
     return fail(GNN_E_INVALID_ARG, "ln_eps %g outside (0, 1)", (double)d->ln_eps);
-  if (d->flags & ~(GNN_VALIDATE_INDICES | GNN_LITERAL_GATHER | GNN_FP32_MFMA))
+  if (d->flags & ~(GNN_VALIDATE_INDICES | GNN_LITERAL_GATHER | GNN_FP32_MFMA | GNN_F16_WEIGHTS))
     return fail(GNN_E_INVALID_ARG, "unknown flags");
+  if ((d->flags & GNN_F16_WEIGHTS) &&
+      (d->dtype != GNN_BF16 || (d->flags & (GNN_LITERAL_GATHER | GNN_FP32_MFMA))))
+    return fail(GNN_E_INVALID_ARG,
+                "GNN_F16_WEIGHTS needs dtype GNN_BF16 and neither GNN_LITERAL_GATHER nor "
+                "GNN_FP32_MFMA");
   return GNN_OK;
 }
 
@@ -217,6 +222,22 @@ std::vector<uint16_t> rec_f16x2(const BlobLayer &L, int c0, int K, float s, int 
 // bf16 hi/lo records of sc * W[:, c0 : c0 + K]: hi = bf16(sc W), lo =
 // bf16(sc W - hi) (the bf16 model's weights; sc a power of two, so the pair
 // is sc times the pair of W).
+// One-part fp16 records of s * W[:, c0 : c0 + K] (the bf16 model with fp16
+// weights), laid out as rec_f16x2's first part: [g][mb][lane] x 8 values.
+std::vector<uint16_t> rec_f16x1(const BlobLayer &L, int c0, int K, float s, int grp) {
+  const int MB = L.fout / 32, G = K / 16;
+  std::vector<uint16_t> out((size_t)G * MB * 64 * 8);
+  for (int g = 0; g < G; ++g)
+    for (int mb = 0; mb < MB; ++mb)
+      for (int lane = 0; lane < 64; ++lane)
+        for (int j = 0; j < 8; ++j) {
+          const int k = node_line_k(g, lane / 32, j, grp);
+          const float wv = s * L.W[(size_t)(mb * 32 + lane % 32) * L.fin + c0 + k];
+          out[(((size_t)g * MB + mb) * 64 + lane) * 8 + j] = f16_bits((_Float16)wv);
+        }
+  return out;
+}
+
 std::vector<uint16_t> rec_bf16x2(const BlobLayer &L, int c0, int K, int grp, float sc = 1.f) {
   const int MB = L.fout / 32, G = K / 16;
   std::vector<uint16_t> out((size_t)G * MB * 2 * 64 * 8);
@@ -287,6 +308,7 @@ struct MlpOff {
 struct FactDev {
   bool split = false;  // split.hip kernels (fp32 split products, or the bf16 model)
   bool bf16 = false;   // with split: the bf16 model
+  int prec = 0;        // split.hip precision: 0 fp32, 1 bf16 hi/lo, 2 bf16 with fp16 weights
   const void *we_cls = nullptr;
   std::vector<const void *> we_em;
   // node-kernel streams: encoder (W2 | two projections) and, per
@@ -878,7 +900,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
     }
     na.eps = d.ln_eps;
     st.begin();
-    HIP_TRY(fd.split ? launch_node_split(true, H, na, fd.grid_node, fd.bf16, stream)
+    HIP_TRY(fd.split ? launch_node_split(true, H, na, fd.grid_node, fd.prec, stream)
                      : launch_node_f32(true, H, na, fd.grid_node, stream));
     st.end(GNN_STAGE_NODE_ENC);
 
@@ -900,7 +922,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       return ea;
     };
     auto launch_edge = [&](EdgeMode mode, const EdgeArgs &ea, int grid) {
-      return fd.split ? launch_edge_split(mode, H, ea, grid, fd.bf16, stream)
+      return fd.split ? launch_edge_split(mode, H, ea, grid, fd.prec, stream)
                       : launch_edge_f32(mode, H, ea, grid, stream);
     };
     {
@@ -969,7 +991,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       }
       nu.eps = d.ln_eps;
       st.begin();
-      HIP_TRY(fd.split ? launch_node_split(false, H, nu, fd.grid_node, fd.bf16, stream)
+      HIP_TRY(fd.split ? launch_node_split(false, H, nu, fd.grid_node, fd.prec, stream)
                        : launch_node_f32(false, H, nu, fd.grid_node, stream));
       st.end(GNN_STAGE_NODE_UPDATE);
     }
@@ -1174,6 +1196,7 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
   const gnn_dims &d = *dims;
   const int F = d.in_features, H = d.hidden, S = d.n_mp_weight_sets;
   const bool bf16 = d.dtype == GNN_BF16;
+  const bool f16w = bf16 && (d.flags & GNN_F16_WEIGHTS);
   const float *p = weights;
   auto next = [&](int fin, int fout, bool ln) {
     BlobLayer L{p, nullptr, nullptr, nullptr, fin, fout};
@@ -1237,10 +1260,27 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
       fdh.row_bound = (float)bound;
     }
     if (factored && bf16) {
-      // The bf16 model on the same kernels: hi/lo bf16 records; the fp16
-      // projections and the W_e records of their consumer carry that
-      // consumer's scale (bias and eps follow in the kernel).
+      // The bf16 model on the same kernels: hi/lo bf16 records (or, with
+      // GNN_F16_WEIGHTS, one fp16 record part); the fp16 projections and the
+      // W_e records of their consumer carry that consumer's scale (bias and
+      // eps follow in the kernel).
       split = true;
+      if (f16w) {
+        // fp16 operands: every LayerNorm output that feeds a product must
+        // lie inside the fp16 range (as for the split products), and the
+        // node update scales aggregate rows by the message-row bound
+        double bound = 0.0;
+        for (const BlobLayer *L : {&a0, &a1, &b0, &b1}) bound = fmax(bound, ln_out_bound(*L));
+        for (int s = 0; s < S; ++s)
+          for (const BlobLayer *L : {&e0s[s], &e1s[s], &n0s[s], &n1s[s]})
+            bound = fmax(bound, ln_out_bound(*L));
+        if (!(bound <= 32768.0)) {
+          fail(GNN_E_UNSUPPORTED,
+               "GNN_F16_WEIGHTS: a LayerNorm output bound %g exceeds the fp16 range", bound);
+          return nullptr;
+        }
+        fdh.row_bound = (float)bound;
+      }
       double hb = ln_out_bound(a1);
       for (int s = 0; s < S; ++s) hb = fmax(hb, ln_out_bound(n1s[s]));
       fdh.s1_ee = proj_f16_scale(b0, H, hb);
@@ -1262,15 +1302,30 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
       auto cat = [](std::vector<uint16_t> &dst, const std::vector<uint16_t> &src) {
         dst.insert(dst.end(), src.begin(), src.end());
       };
+      // Records: hi/lo bf16 pairs, or with GNN_F16_WEIGHTS one fp16 part of
+      // the weights times a power of two (W2, the node MLPs and the node
+      // encoder's W2 then carry pow2_scale; the projections and W_e carry
+      // the fp16 projections' consumer scale either way).
+      bool f16_fits = true;
+      auto rec = [&](const BlobLayer &L, int c0, int K, int grp, float sc) {
+        if (!f16w) return rec_bf16x2(L, c0, K, grp, sc);
+        for (int f = 0; f < L.fout; ++f)
+          for (int k = c0; k < c0 + K; ++k)
+            if (!(fabsf(sc * L.W[(size_t)f * L.fin + k]) <= 65504.f)) f16_fits = false;
+        return rec_f16x1(L, c0, K, sc, grp);
+      };
+      auto s2_of = [&](const BlobLayer &L) { return f16w ? pow2_scale(L) : 1.f; };
+      fdh.s2_ee = s2_of(b1);
+      fdh.s2_ne = s2_of(a1);
       for (int s = 0; s < S; ++s) {
-        fdh.s2_em.push_back(1.f);
-        fdh.s1_nm.push_back(1.f);
-        fdh.s2_nm.push_back(1.f);
-        o_we_em[s] = add16(rec_bf16x2(e0s[s], 2 * H, H, 0, fdh.s1_em[s]));
-        o_w2_em[s] = add16(rec_bf16x2(e1s[s], 0, H, -1));
+        fdh.s2_em.push_back(s2_of(e1s[s]));
+        fdh.s1_nm.push_back(s2_of(n0s[s]));
+        fdh.s2_nm.push_back(s2_of(n1s[s]));
+        o_we_em[s] = add16(rec(e0s[s], 2 * H, H, 0, fdh.s1_em[s]));
+        o_w2_em[s] = add16(rec(e1s[s], 0, H, -1, fdh.s2_em[s]));
       }
-      o_we_cls = add16(rec_bf16x2(c0, 2 * H, H, 0, fdh.s1_cls));
-      o_w2_ee = add16(rec_bf16x2(b1, 0, H, -1));
+      o_we_cls = add16(rec(c0, 2 * H, H, 0, fdh.s1_cls));
+      o_w2_ee = add16(rec(b1, 0, H, -1, fdh.s2_ee));
       auto scale_of = [&](const BlobLayer &L) {
         if (&L == &c0) return fdh.s1_cls;
         for (int s = 0; s < S; ++s)
@@ -1279,19 +1334,23 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
       };
       auto proj = [&](std::vector<uint16_t> &dst, const BlobLayer &L) {
         const float sc = scale_of(L);
-        cat(dst, rec_bf16x2(L, 0, H, -1, sc));
-        cat(dst, rec_bf16x2(L, H, H, -1, sc));
+        cat(dst, rec(L, 0, H, -1, sc));
+        cat(dst, rec(L, H, H, -1, sc));
       };
-      std::vector<uint16_t> es = rec_bf16x2(a1, 0, H, -1);
+      std::vector<uint16_t> es = rec(a1, 0, H, -1, fdh.s2_ne);
       proj(es, b0);
       proj(es, next_edge_l1(-1));
       o_enc_stream = add16(es);
       for (int t = 0; t < T; ++t) {
         const int k = S == 1 ? 0 : t;
-        std::vector<uint16_t> us = rec_bf16x2(n0s[k], 0, 3 * H, 4);
-        cat(us, rec_bf16x2(n1s[k], 0, H, -1));
+        std::vector<uint16_t> us = rec(n0s[k], 0, 3 * H, 4, fdh.s1_nm[k]);
+        cat(us, rec(n1s[k], 0, H, -1, fdh.s2_nm[k]));
         proj(us, next_edge_l1(t));
         o_upd_stream[t] = add16(us);
+      }
+      if (!f16_fits) {
+        fail(GNN_E_UNSUPPORTED, "GNN_F16_WEIGHTS: a scaled weight exceeds the fp16 range");
+        return nullptr;
       }
     } else if (factored && split) {
       auto add16 = [&](const std::vector<uint16_t> &v) {
@@ -1401,11 +1460,12 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
     if (split) {
       fd.w2_ee = base + o_w2_ee;
       for (int s = 0; s < S; ++s) fd.w2_em.push_back(base + o_w2_em[s]);
-      fd.enc_chunks = node_split_chunks(true, H, 2, bf16);
-      fd.upd_chunks = node_split_chunks(false, H, 1, bf16);
-      fd.grid_enc = edge_split_grid(EdgeMode::Enc, H, bf16, n_cu);
-      fd.grid_upd = edge_split_grid(EdgeMode::UpdAgg, H, bf16, n_cu);
-      fd.grid_cls = edge_split_grid(EdgeMode::Cls, H, bf16, n_cu);
+      fd.prec = !bf16 ? 0 : (f16w ? 2 : 1);
+      fd.enc_chunks = node_split_chunks(true, H, 2, fd.prec);
+      fd.upd_chunks = node_split_chunks(false, H, 1, fd.prec);
+      fd.grid_enc = edge_split_grid(EdgeMode::Enc, H, fd.prec, n_cu);
+      fd.grid_upd = edge_split_grid(EdgeMode::UpdAgg, H, fd.prec, n_cu);
+      fd.grid_cls = edge_split_grid(EdgeMode::Cls, H, fd.prec, n_cu);
     } else {
       const int kg = H / 8;  // k-groups of one H-wide operand; 8 per chunk
       fd.enc_chunks = (kg + 4 * kg) / 8;

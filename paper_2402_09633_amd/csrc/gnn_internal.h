@@ -119,16 +119,17 @@ hipError_t launch_edge_f32(EdgeMode mode, int hidden, const EdgeArgs &a, int gri
                            hipStream_t stream);
 int edge_f32_grid(EdgeMode mode, int hidden, int n_cu);
 
-// The same kernels with split-precision products on the fp16/bf16 matrix
-// cores (split.hip), or, with bf16 = true, for the bf16 model (h, e and the
-// aggregates in bf16, hi/lo bf16 weights).  Weights come as 16-bit records;
-// P rows are fp32, stored multiplied by the consumer's s1.
-hipError_t launch_node_split(bool enc, int hidden, const NodeArgs &a, int grid, bool bf16,
+// The same kernels on the fp16/bf16 matrix cores (split.hip), by `prec`:
+// 0 = fp32 model, split-precision products (fp32 P rows); 1 = bf16 model
+// (h, e and the aggregates in bf16, hi/lo bf16 weights, fp16 P rows);
+// 2 = the bf16 model with fp16 weights (one product per weight).  Weights
+// come as 16-bit records; P rows are stored multiplied by the consumer's s1.
+hipError_t launch_node_split(bool enc, int hidden, const NodeArgs &a, int grid, int prec,
                              hipStream_t stream);
-int node_split_chunks(bool enc, int hidden, int nproj, bool bf16);
-hipError_t launch_edge_split(EdgeMode mode, int hidden, const EdgeArgs &a, int grid, bool bf16,
+int node_split_chunks(bool enc, int hidden, int nproj, int prec);
+hipError_t launch_edge_split(EdgeMode mode, int hidden, const EdgeArgs &a, int grid, int prec,
                              hipStream_t stream);
-int edge_split_grid(EdgeMode mode, int hidden, bool bf16, int n_cu);
+int edge_split_grid(EdgeMode mode, int hidden, int prec, int n_cu);
 
 // Deterministic CSR segmented sums of the edge rows `e` ([n_edges][H]):
 // agg_in[v] = sum over p in [rp_in[v], rp_in[v+1]) of e[perm_in[p]], in

@@ -191,6 +191,45 @@ __device__ __forceinline__ float add_f16(unsigned a, unsigned b) {
 // Operand precision of the kernels below.
 constexpr int SPLIT = 0;  // fp32 activations, split products
 constexpr int BF16 = 1;   // bf16 activations, hi/lo bf16 weights
+constexpr int F16W = 2;   // bf16 activations, fp16 weights (one product per weight)
+
+// Parts per weight record: two (f16x2 or bf16 hi/lo) or one (fp16 weights).
+template <int PREC>
+constexpr int rec_parts() { return PREC == F16W ? 1 : 2; }
+
+// acc[mb] += w x over one k-step, one fp16 weight part (F16W).
+template <int MB>
+__device__ __forceinline__ void step_f(f16v (&acc)[MB], const h8 *rec, const h8 &x) {
+  h8 w[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) w[mb] = rec[mb * 64];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = mma_h(w[mb], x, acc[mb]);
+}
+
+// step_f with the operands exchanged (transposed accumulators, as step_ht).
+template <int MB>
+__device__ __forceinline__ void step_ft(f16v (&acc)[MB], const h8 *rec, const h8 &x) {
+  h8 w[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) w[mb] = rec[mb * 64];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = mma_h(x, w[mb], acc[mb]);
+}
+
+// F16W operands: a stored bf16 value is exactly an fp16 value once it lies
+// in the fp16 range (the callers keep it there, scaling a node's aggregate
+// row by a power of two where needed); an fp32 accumulator value is rounded
+// to bf16 first (the model's activation precision) and then converted.
+__device__ __forceinline__ h8 bf_to_h(const bf8 &x) {
+  return __builtin_convertvector(__builtin_convertvector(x, f8), h8);
+}
+__device__ __forceinline__ h8 bf_to_h(const bf8 &x, float sv) {
+  return __builtin_convertvector(__builtin_convertvector(x, f8) * sv, h8);
+}
+__device__ __forceinline__ h8 acc_to_h(const f8 &x) {
+  return __builtin_convertvector(__builtin_convertvector(__builtin_convertvector(x, bf8), f8), h8);
+}
 
 template <int MB>
 __device__ __forceinline__ void zero(f16v (&a)[MB]) {
@@ -332,16 +371,19 @@ struct Stream {
   }
 };
 
-// Records per chunk: every record has 2 parts (f16x2, or bf16 hi/lo).  A
-// chunk is 48 KB (MB = 4) in the update and 32 KB in the encoder.
-template <int PREC>
-constexpr int rpc_l1() { return 6; }
-template <int PREC>
-constexpr int parts_l1() { return 2; }
-template <bool ENC>
-constexpr int rpc_h() { return ENC ? 4 : 6; }
-template <int MB, bool ENC>
-constexpr int node_nf4() { return (ENC ? 4 * 2 : 4 * 3) * MB * 64 / 512; }
+// Chunks of the node kernels' weight stream.  Two-part records (f16x2, bf16
+// hi/lo): 6 records, 48 KB (MB = 4), per update chunk and 4, 32 KB, per
+// encoder chunk.  One-part records (fp16 weights): the same chunk bytes hold
+// twice the records, except in the H = 64 encoder, whose 20 records take 4
+// per chunk (16 KB-per-thread-slot chunks) so that the count divides.
+template <int MB, bool ENC, int PREC>
+constexpr int node_nf4() {
+  return PREC == F16W && ENC && MB == 2 ? 1 : (ENC ? 4 * 2 : 4 * 3) * MB * 64 / 512;
+}
+template <int MB, bool ENC, int PREC>
+constexpr int rpc_h() { return node_nf4<MB, ENC, PREC>() * 512 / (rec_parts<PREC>() * MB * 64); }
+template <int MB, int PREC>
+constexpr int rpc_l1() { return rpc_h<MB, false, PREC>(); }
 
 // Records per 128-byte line pair of the node update's layer-1 inputs (two
 // lanes read one line of a row): 2 for fp32 rows, 4 for bf16 rows.  The
@@ -353,13 +395,13 @@ template <int MB, bool ENC, int NPROJ, int PREC>
 __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
   constexpr int H = 32 * MB;
   constexpr int G = H / 16;  // k-steps per H-wide operand
-  constexpr int NF4 = node_nf4<MB, ENC>();
-  constexpr int RPC_H = rpc_h<ENC>();
-  constexpr int RPC_1 = rpc_l1<PREC>();
-  constexpr int REC_H = 2 * MB * 64;                 // 16-byte slots per 2-part record
-  constexpr int REC_1 = parts_l1<PREC>() * MB * 64;  // slots per layer-1 record
-  static_assert(RPC_H * REC_H == NF4 * 512, "2-part chunk size");
-  static_assert(ENC || RPC_1 * REC_1 == NF4 * 512, "layer-1 chunk size");
+  constexpr int NF4 = node_nf4<MB, ENC, PREC>();
+  constexpr int RPC_H = rpc_h<MB, ENC, PREC>();
+  constexpr int RPC_1 = rpc_l1<MB, PREC>();
+  constexpr int REC_H = rec_parts<PREC>() * MB * 64;  // 16-byte slots per record
+  constexpr int REC_1 = REC_H;
+  static_assert(RPC_H * REC_H == NF4 * 512, "chunk size");
+  static_assert(ENC || (3 * G) % RPC_1 == 0, "layer-1 records fill whole chunks");
   using act_t = typename std::conditional<PREC == SPLIT, float, __bf16>::type;
   __shared__ f4 wbuf[2 * NF4 * 512];
   __shared__ float stage[SW][32 * SST];
@@ -462,13 +504,14 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
       xrec_t xr[RING];
 #pragma unroll
       for (int i = 0; i < GRP; ++i) xr[i] = load_rec(i);
-      // Split: the node's whole input row is multiplied by a power of two
-      // sv <= 1 that keeps it inside the fp16 range of the split parts: the
-      // aggregates are bounded by max(deg_in, deg_out) times the bound of a
-      // message row.  Column n of the product is then sv times the node's,
-      // and is divided by sv again after the last record (exact).
+      // Split and fp16 weights: the node's whole input row is multiplied by
+      // a power of two sv <= 1 that keeps it inside the fp16 range of the
+      // operands: the aggregates are bounded by max(deg_in, deg_out) times
+      // the bound of a message row.  Column n of the product is then sv
+      // times the node's, and is divided by sv again after the last record
+      // (exact).
       float sv = 1.f, inv_sv = 1.f;
-      if constexpr (PREC == SPLIT) {
+      if constexpr (PREC != BF16) {
         const int32_t din = a.rp_in[r + 1] - a.rp_in[r];
         const int32_t dout = a.rp_out[r + 1] - a.rp_out[r];
         const float m = (float)(din > dout ? (din > 1 ? din : 1) : (dout > 1 ? dout : 1)) *
@@ -492,19 +535,21 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
         if (i % RPC_1 == 0) w = ws.begin(tid) + lane;
         if constexpr (PREC == SPLIT)
           step_h<MB>(acc, (const h8 *)(w + (i % RPC_1) * REC_1), xr[i % RING] * sv);
-        else
+        else if constexpr (PREC == BF16)
           step_hl<MB>(acc, (const bf8 *)(w + (i % RPC_1) * REC_1), xr[i % RING]);
+        else
+          step_f<MB>(acc, (const h8 *)(w + (i % RPC_1) * REC_1), bf_to_h(xr[i % RING], sv));
         if (i % RPC_1 == RPC_1 - 1) ws.end(tid);
       }
-      if constexpr (PREC == SPLIT) {
+      if constexpr (PREC != BF16) {
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) acc[mb] *= inv_sv;
       }
       ln_relu_lds<MB>(acc, prm, a.eps * a.s1 * a.s1, hh);
     }
 
-    // The 2-part records: layer 2, then the projection halves.  Record i of
-    // this part sits in chunk i / RPC_H at slot i % RPC_H.
+    // Layer 2, then the projection halves.  Record i of this part sits in
+    // chunk i / RPC_H at slot i % RPC_H.
     const f4 *wcur = nullptr;
     auto rec_h = [&](int i) {
       if (i % RPC_H == 0) wcur = ws.begin(tid) + lane;
@@ -519,8 +564,10 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
     for (int g = 0; g < G; ++g) {
       if constexpr (PREC == SPLIT)
         step_h<MB>(hv, (const h8 *)rec_h(g), acc_x<MB>(acc, g));
-      else
+      else if constexpr (PREC == BF16)
         step_hl<MB>(hv, (const bf8 *)rec_h(g), to_bf16(acc_x<MB>(acc, g)));
+      else
+        step_f<MB>(hv, (const h8 *)rec_h(g), acc_to_h(acc_x<MB>(acc, g)));
       rec_done(g);
     }
     ln_relu_lds<MB>(hv, prm + 3 * H, eps2, hh);
@@ -531,14 +578,16 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
         store_block16<MB, false, __bf16>((__bf16 *)a.h_out + wrow0 * H, H, nvalid, hv, stg, lane);
     }
     // the projections read h as it is stored
-    using xp_t = typename std::conditional<PREC == SPLIT, h8, bf8>::type;
+    using xp_t = typename std::conditional<PREC == BF16, bf8, h8>::type;
     xp_t x1[G], x2[PREC == SPLIT ? G : 1];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       if constexpr (PREC == SPLIT)
         split2(acc_x<MB>(hv, g), x1[g], x2[g]);
-      else
+      else if constexpr (PREC == BF16)
         x1[g] = to_bf16(acc_x<MB>(hv, g));
+      else
+        x1[g] = acc_to_h(acc_x<MB>(hv, g));
     }
 #pragma unroll
     for (int p = 0; p < NPROJ; ++p)
@@ -551,8 +600,10 @@ __global__ __launch_bounds__(64 * SW) void node_split(NodeArgs a) {
           const int i = G * (1 + 2 * p + half) + g;
           if constexpr (PREC == SPLIT)
             step_h<MB>(pv, (const h8 *)rec_h(i), x1[g], x2[g]);
-          else
+          else if constexpr (PREC == BF16)
             step_hl<MB>(pv, (const bf8 *)rec_h(i), x1[g]);
+          else
+            step_f<MB>(pv, (const h8 *)rec_h(i), x1[g]);
           rec_done(i);
         }
         if (half == 0) {
@@ -580,7 +631,8 @@ template <int MB, int MODE, int PREC>
 __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
   constexpr int H = 32 * MB;
   constexpr int G = H / 16;
-  constexpr int NR = G * MB * 2 * 64;  // 16-byte slots of one H x H matrix (2-part records)
+  constexpr int RP = rec_parts<PREC>();
+  constexpr int NR = G * MB * RP * 64;  // 16-byte slots of one H x H matrix
   using act_t = typename std::conditional<PREC == SPLIT, float, __bf16>::type;
   constexpr bool HAS_E = MODE != (int)EdgeMode::Enc;
   constexpr bool HAS_L2 = MODE != (int)EdgeMode::Cls;
@@ -703,9 +755,11 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         if constexpr (PREC == SPLIT)
-          step_h<MB>(acc, lw_e + g * 2 * MB * 64 + lane, ev[g]);
+          step_h<MB>(acc, lw_e + g * RP * MB * 64 + lane, ev[g]);
+        else if constexpr (PREC == BF16)
+          step_hl<MB>(acc, (const bf8 *)(lw_e + g * RP * MB * 64 + lane), ev[g]);
         else
-          step_hl<MB>(acc, (const bf8 *)(lw_e + g * 2 * MB * 64 + lane), ev[g]);
+          step_f<MB>(acc, lw_e + g * RP * MB * 64 + lane, bf_to_h(ev[g]));
       }
     }
     // (FUSE: after layer 2's LayerNorm, which needs the registers)
@@ -740,12 +794,14 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         if constexpr (PREC == SPLIT)
-          step_ht<MB>(t2, lw_2 + g * 2 * MB * 64 + lane, acc_x<MB>(acc, g));
+          step_ht<MB>(t2, lw_2 + g * RP * MB * 64 + lane, acc_x<MB>(acc, g));
+        else if constexpr (PREC == BF16)
+          step_hlt<MB>(t2, (const bf8 *)(lw_2 + g * RP * MB * 64 + lane), to_bf16(acc_x<MB>(acc, g)));
         else
-          step_hlt<MB>(t2, (const bf8 *)(lw_2 + g * 2 * MB * 64 + lane), to_bf16(acc_x<MB>(acc, g)));
+          step_ft<MB>(t2, lw_2 + g * RP * MB * 64 + lane, acc_to_h(acc_x<MB>(acc, g)));
       }
       ln_relu_t<MB>(t2, prm + 3 * H, eps2, n);
-      if constexpr (PREC == BF16) {
+      if constexpr (PREC != SPLIT) {
         // the stored rows are the bf16 values; the sums add exactly those
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
@@ -896,27 +952,47 @@ const void *edge_fn(EdgeMode mode, int hidden) {
 // Chunks of a node stream: the encoder holds (1 + 2 nproj) H x H matrices
 // of 2-part records; the update 3H/16 layer-1 records (3 parts when split, 2
 // in bf16) and three H x H matrices.
-int node_split_chunks(bool enc, int hidden, int nproj, bool bf16) {
+int node_split_chunks(bool enc, int hidden, int nproj, int prec) {
   const int G = hidden / 16;
-  (void)bf16;
-  if (enc) return (G * (1 + 2 * nproj)) / 4;
-  return (3 * G) / rpc_l1<SPLIT>() + (3 * G) / 6;
+  auto chunks = [&](auto mbc, auto pc) {
+    constexpr int MB = decltype(mbc)::value, PREC = decltype(pc)::value;
+    return enc ? (G * (1 + 2 * nproj)) / rpc_h<MB, true, PREC>()
+               : (3 * G) / rpc_l1<MB, PREC>() + (3 * G) / rpc_h<MB, false, PREC>();
+  };
+  using I2 = std::integral_constant<int, 2>;
+  using I4 = std::integral_constant<int, 4>;
+  using PS = std::integral_constant<int, SPLIT>;
+  using PB = std::integral_constant<int, BF16>;
+  using PF = std::integral_constant<int, F16W>;
+  if (hidden == 64) return prec == 2 ? chunks(I2{}, PF{}) : prec == 1 ? chunks(I2{}, PB{}) : chunks(I2{}, PS{});
+  return prec == 2 ? chunks(I4{}, PF{}) : prec == 1 ? chunks(I4{}, PB{}) : chunks(I4{}, PS{});
 }
 
-hipError_t launch_node_split(bool enc, int hidden, const NodeArgs &a, int grid, bool bf16,
-                             hipStream_t stream) {
-  if (a.F > MAX_F || a.nproj < 1 || a.nproj > 2 || (!enc && a.nproj != 1) || grid <= 0)
-    return hipErrorInvalidValue;
-  if (a.nchunks != node_split_chunks(enc, hidden, a.nproj, bf16)) return hipErrorInvalidValue;
-  switch (hidden) {
-    case 64: return bf16 ? node_h<2, BF16>(enc, a, grid, stream) : node_h<2, SPLIT>(enc, a, grid, stream);
-    case 128: return bf16 ? node_h<4, BF16>(enc, a, grid, stream) : node_h<4, SPLIT>(enc, a, grid, stream);
+template <int MB>
+hipError_t node_p(int prec, bool enc, const NodeArgs &a, int grid, hipStream_t stream) {
+  switch (prec) {
+    case 0: return node_h<MB, SPLIT>(enc, a, grid, stream);
+    case 1: return node_h<MB, BF16>(enc, a, grid, stream);
+    case 2: return node_h<MB, F16W>(enc, a, grid, stream);
   }
   return hipErrorInvalidValue;
 }
 
-int edge_split_grid(EdgeMode mode, int hidden, bool bf16, int n_cu) {
-  const void *fn = bf16 ? edge_fn<BF16>(mode, hidden) : edge_fn<SPLIT>(mode, hidden);
+hipError_t launch_node_split(bool enc, int hidden, const NodeArgs &a, int grid, int prec,
+                             hipStream_t stream) {
+  if (a.F > MAX_F || a.nproj < 1 || a.nproj > 2 || (!enc && a.nproj != 1) || grid <= 0)
+    return hipErrorInvalidValue;
+  if (a.nchunks != node_split_chunks(enc, hidden, a.nproj, prec)) return hipErrorInvalidValue;
+  switch (hidden) {
+    case 64: return node_p<2>(prec, enc, a, grid, stream);
+    case 128: return node_p<4>(prec, enc, a, grid, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+int edge_split_grid(EdgeMode mode, int hidden, int prec, int n_cu) {
+  const void *fn = prec == 2 ? edge_fn<F16W>(mode, hidden)
+                             : prec == 1 ? edge_fn<BF16>(mode, hidden) : edge_fn<SPLIT>(mode, hidden);
   int per_cu = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 64 * SW, 0) != hipSuccess ||
       per_cu < 1)
@@ -924,12 +1000,22 @@ int edge_split_grid(EdgeMode mode, int hidden, bool bf16, int n_cu) {
   return per_cu * (n_cu > 0 ? n_cu : 1);
 }
 
-hipError_t launch_edge_split(EdgeMode mode, int hidden, const EdgeArgs &a, int grid, bool bf16,
+template <int MB>
+hipError_t edge_p(int prec, EdgeMode mode, const EdgeArgs &a, int grid, hipStream_t stream) {
+  switch (prec) {
+    case 0: return edge_h<MB, SPLIT>(mode, a, grid, stream);
+    case 1: return edge_h<MB, BF16>(mode, a, grid, stream);
+    case 2: return edge_h<MB, F16W>(mode, a, grid, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_edge_split(EdgeMode mode, int hidden, const EdgeArgs &a, int grid, int prec,
                              hipStream_t stream) {
   if (grid <= 0) return hipErrorInvalidValue;
   switch (hidden) {
-    case 64: return bf16 ? edge_h<2, BF16>(mode, a, grid, stream) : edge_h<2, SPLIT>(mode, a, grid, stream);
-    case 128: return bf16 ? edge_h<4, BF16>(mode, a, grid, stream) : edge_h<4, SPLIT>(mode, a, grid, stream);
+    case 64: return edge_p<2>(prec, mode, a, grid, stream);
+    case 128: return edge_p<4>(prec, mode, a, grid, stream);
   }
   return hipErrorInvalidValue;
 }

@@ -29,6 +29,7 @@ GNN_BF16 = 1
 GNN_VALIDATE_INDICES = 1
 GNN_LITERAL_GATHER = 2
 GNN_FP32_MFMA = 4
+GNN_F16_WEIGHTS = 8
 
 EXPORTS = ("gnn_weight_count", "gnn_create", "gnn_infer", "gnn_infer_logits", "gnn_infer_noalloc",
            "gnn_filter_weight_count", "gnn_filter_create", "gnn_filter_apply",

@@ -54,7 +54,7 @@ def test_weight_count_matches_generator(G, F, H, T, S):
 @pytest.mark.parametrize("kw", [dict(hidden=48), dict(hidden=96), dict(hidden=0),
                                 dict(n_iters=-1), dict(n_iters=8, n_mp_weight_sets=3),
                                 dict(dtype=7), dict(ln_eps=0.0), dict(in_features=0),
-                                dict(in_features=17), dict(flags=8)])
+                                dict(in_features=17), dict(flags=16)])
 def test_bad_dims_are_rejected(G, kw):
     d = G.make_dims(**kw)
     assert G.gnn_weight_count(d) == 0
@@ -168,3 +168,11 @@ def test_hbm_probe_rejects_bad_arguments(G, kind, nbytes, grid, reps, null):
     assert rc == G.GNN_E_INVALID_ARG
     assert ms.value == 0.0
     assert G.gnn_last_error() != ""
+
+
+@pytest.mark.parametrize("dtype,flags", [(0, 8), (1, 8 | 2), (1, 8 | 4)])
+def test_f16_weights_flag_only_with_bf16_regrouped(G, dtype, flags):
+    d = G.make_dims(dtype=dtype, flags=flags)
+    assert G.gnn_weight_count(d) == 0
+    assert "GNN_F16_WEIGHTS" in G.gnn_last_error()
+    assert G.gnn_weight_count(G.make_dims(dtype=1, flags=8)) > 0

@@ -25,7 +25,7 @@ pytestmark = pytest.mark.gpu
 # fp32 kernel sets: split products (0), fp32 matrix cores (GNN_FP32_MFMA = 4),
 # per-edge first layer (GNN_LITERAL_GATHER = 2); bf16: regrouped (0), per-edge (2)
 FP32_PATHS = [0, 4, 2]
-BF16_PATHS = [0, 2]
+BF16_PATHS = [0, 2, 8]  # default, per-edge first layer, fp16 weights
 # |s - s_ref| implied by the logit bar: sigma' <= 1/4, and max(1, |z|) sigma'(z) <= 1/4
 FP32_SCORE_ATOL = 2.5e-5
 

@@ -40,7 +40,7 @@ def _tiny_random(seed, n, e, loops=False):
 # (GNN_FP32_MFMA = 4), and the per-edge gather (GNN_LITERAL_GATHER = 2).
 PATHS = [0, 4, 2]
 # bf16 runs the regrouped kernels (flags 0) and the per-edge gather (2).
-BF16_PATHS = [0, 2]
+BF16_PATHS = [0, 2, 8]  # default, per-edge first layer, fp16 weights
 
 
 @pytest.mark.parametrize("flags", PATHS)
