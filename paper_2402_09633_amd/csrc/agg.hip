@@ -103,10 +103,11 @@ __device__ __forceinline__ void row_sum_f32(const float *__restrict__ base,
   }
 }
 
-template <int H, int B, bool COMP, bool IDX>
-__device__ __forceinline__ void row_sum_bf16(const __bf16 *__restrict__ base,
+template <int H, int B, bool COMP, bool IDX, typename T>
+__device__ __forceinline__ void row_sum_bf16(const T *__restrict__ base,
                                              const int32_t *__restrict__ perm, int32_t p,
                                              int32_t pe, int sub, float (&s)[8], float (&c)[8]) {
+  typedef T t8 __attribute__((ext_vector_type(8)));
   constexpr int G = H / 8;
   static_assert(G % B == 0, "batch must divide the group");
   for (; p < pe; p += G) {
@@ -114,7 +115,7 @@ __device__ __forceinline__ void row_sum_bf16(const __bf16 *__restrict__ base,
     int32_t my = 0;
     if constexpr (IDX) my = perm[p + min(sub, n - 1)];
     for (int j = 0; j < n; j += B) {
-      bf8 r[B];
+      t8 r[B];
 #pragma unroll
       for (int u = 0; u < B; ++u) {
         int64_t q;
@@ -122,7 +123,7 @@ __device__ __forceinline__ void row_sum_bf16(const __bf16 *__restrict__ base,
           q = group_lane<G>(my, min(j + u, n - 1));
         else
           q = p + min(j + u, n - 1);
-        r[u] = ld_once((const bf8 *)(base + q * H));
+        r[u] = ld_once((const t8 *)(base + q * H));
       }
 #pragma unroll
       for (int u = 0; u < B; ++u)
@@ -146,16 +147,16 @@ __device__ __forceinline__ void row_sum_f32(const float *base, const int32_t *pe
   }
 }
 
-template <int H, int B = 4>
-__device__ __forceinline__ void row_sum_bf16(const __bf16 *base, const int32_t *perm, int32_t p,
+template <int H, int B = 4, typename T>
+__device__ __forceinline__ void row_sum_bf16(const T *base, const int32_t *perm, int32_t p,
                                              int32_t pe, int sub, float (&s)[8], float (&c)[8]) {
   const bool comp = pe - p > LONG_ROW;
   if (perm) {
-    if (comp) row_sum_bf16<H, B, true, true>(base, perm, p, pe, sub, s, c);
-    else row_sum_bf16<H, B, false, true>(base, perm, p, pe, sub, s, c);
+    if (comp) row_sum_bf16<H, B, true, true, T>(base, perm, p, pe, sub, s, c);
+    else row_sum_bf16<H, B, false, true, T>(base, perm, p, pe, sub, s, c);
   } else {
-    if (comp) row_sum_bf16<H, B, true, false>(base, perm, p, pe, sub, s, c);
-    else row_sum_bf16<H, B, false, false>(base, perm, p, pe, sub, s, c);
+    if (comp) row_sum_bf16<H, B, true, false, T>(base, perm, p, pe, sub, s, c);
+    else row_sum_bf16<H, B, false, false, T>(base, perm, p, pe, sub, s, c);
   }
 }
 
@@ -242,11 +243,12 @@ __global__ __launch_bounds__(THREADS_F32) void segsum_fused_f32(
   st_once((f4 *)(agg_out + v * H + 4 * sub), f4{s[0] + c[0], s[1] + c[1], s[2] + c[2], s[3] + c[3]});
 }
 
-// The same for bf16 rows and aggregates (H/8 lanes per node, 8 features
-// each); the pieces are fp32, the sums fp32, the stored aggregates bf16.
-template <int H>
+// The same for 16-bit rows and bf16 aggregates (H/8 lanes per node, 8
+// features each); the pieces are fp32, the sums fp32.  ET is the row type:
+// bf16, or fp16 for the edge rows of the bf16 model with fp16 weights.
+template <int H, typename ET>
 __global__ __launch_bounds__(THREADS_BF16) void segsum_fused_bf16(
-    const __bf16 *__restrict__ e, const int32_t *__restrict__ rp_in,
+    const ET *__restrict__ e, const int32_t *__restrict__ rp_in,
     const int32_t *__restrict__ perm_in, const int32_t *__restrict__ rp_out,
     const float *__restrict__ part, __bf16 *__restrict__ agg_in, __bf16 *__restrict__ agg_out,
     int32_t n_nodes) {
@@ -374,10 +376,14 @@ hipError_t launch_fused_h(Act act, const void *e, const int32_t *rp_in, const in
     segsum_fused_f32<H><<<blocks, THREADS_F32, 0, stream>>>((const float *)e, rp_in, perm_in, rp_out,
                                                         part, (float *)agg_in, (float *)agg_out,
                                                         n_nodes);
+  else if (act == Act::BF16)
+    segsum_fused_bf16<H, __bf16><<<blocks, THREADS_BF16, 0, stream>>>(
+        (const __bf16 *)e, rp_in, perm_in, rp_out, part, (__bf16 *)agg_in, (__bf16 *)agg_out,
+        n_nodes);
   else
-    segsum_fused_bf16<H><<<blocks, THREADS_BF16, 0, stream>>>((const __bf16 *)e, rp_in, perm_in,
-                                                         rp_out, part, (__bf16 *)agg_in,
-                                                         (__bf16 *)agg_out, n_nodes);
+    segsum_fused_bf16<H, _Float16><<<blocks, THREADS_BF16, 0, stream>>>(
+        (const _Float16 *)e, rp_in, perm_in, rp_out, part, (__bf16 *)agg_in, (__bf16 *)agg_out,
+        n_nodes);
   return hipGetLastError();
 }
 

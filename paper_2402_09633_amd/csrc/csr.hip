@@ -557,9 +557,12 @@ hipError_t launch_scatter_rows(Act act, const void *src, const int32_t *idx, flo
   if (act == Act::F32)
     scatter_rows_k<float><<<blocks_for(n, 256), 256, 0, stream>>>((const float *)src, idx, dst,
                                                                   rows, H);
-  else
+  else if (act == Act::BF16)
     scatter_rows_k<__bf16><<<blocks_for(n, 256), 256, 0, stream>>>((const __bf16 *)src, idx,
                                                                    dst, rows, H);
+  else
+    scatter_rows_k<_Float16><<<blocks_for(n, 256), 256, 0, stream>>>((const _Float16 *)src, idx,
+                                                                     dst, rows, H);
   return hipGetLastError();
 }
 

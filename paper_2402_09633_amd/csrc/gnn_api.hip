@@ -797,6 +797,8 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
   const gnn_dims &d = hd->dims;
   const int H = d.hidden;
   const Act act = d.dtype == GNN_BF16 ? Act::BF16 : Act::F32;
+  // the edge rows of the bf16 model with fp16 weights are held in fp16
+  const Act eact = hd->factored && hd->fd.split && hd->fd.prec == 2 ? Act::F16 : act;
   const size_t ab = act == Act::F32 ? 4 : 2;
   const int32_t n = (int32_t)N, m = (int32_t)E;
   int rc = GNN_OK;
@@ -957,7 +959,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       st.end(GNN_STAGE_EDGE_UPDATE);
       st.begin();
       if (fused)
-        HIP_TRY(launch_segsum_fused(act, H, w.e, w.rp_in, w.q_in, w.rp_out, w.part, w.ain,
+        HIP_TRY(launch_segsum_fused(eact, H, w.e, w.rp_in, w.q_in, w.rp_out, w.part, w.ain,
                                     w.aout, n, E, stream));
       else  // source-order rows: the out-CSR is the identity
         HIP_TRY(launch_segsum(act, H, w.e, w.rp_in, w.q_in, w.rp_out, nullptr, w.ain, w.aout,
@@ -1003,7 +1005,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       for (auto &x2 : ex) {
         if (!x2.dst || x2.n == 0 || (x2.agg && T == 0)) continue;
         if (x2.src == w.e)  // back to input order
-          HIP_TRY(launch_scatter_rows(act, w.e, w.perm_out, x2.dst, E, H, stream));
+          HIP_TRY(launch_scatter_rows(eact, w.e, w.perm_out, x2.dst, E, H, stream));
         else if (act == Act::F32)
           HIP_TRY(hipMemcpyAsync(x2.dst, x2.src, x2.n * 4, hipMemcpyDeviceToDevice, stream));
         else

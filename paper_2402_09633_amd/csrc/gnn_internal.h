@@ -10,7 +10,10 @@
 namespace gnn {
 
 // Activation storage type of a handle.
-enum class Act : int { F32 = 0, BF16 = 1 };
+// Row element types.  F16 is used only for the edge rows of the bf16 model
+// with fp16 weights: their values are bf16 numbers, held in fp16 encoding so
+// that the fp16 products read them as they are.
+enum class Act : int { F32 = 0, BF16 = 1, F16 = 2 };
 
 // One Linear layer on the device.  `w` is laid out for the kernel that reads
 // it: MFMA operand fragments for the dense layers, plain [out][in] rows for
@@ -142,7 +145,8 @@ hipError_t launch_segsum(Act act, int hidden, const void *e, const int32_t *rp_i
 // agg_out[v] is completed for the nodes whose out-edge positions
 // [rp_out[v], rp_out[v+1]) span several 32-row units (sum of the fp32 unit
 // pieces in agg_part, in unit order) and zeroed for nodes without out-edges;
-// the edge update wrote every other row.
+// the edge update wrote every other row.  act = Act::F16: fp16 edge rows,
+// bf16 aggregates.
 hipError_t launch_segsum_fused(Act act, int hidden, const void *e, const int32_t *rp_in,
                                const int32_t *perm_in, const int32_t *rp_out,
                                const float *agg_part, void *agg_in, void *agg_out,
@@ -174,7 +178,7 @@ hipError_t build_csr(const int32_t *edge_index, int32_t n_edges, int32_t n_nodes
                      int32_t *row_ptr_in, int32_t *perm_in, int32_t *row_ptr_out,
                      int32_t *perm_out, const CsrScratch &s, int32_t *eis, int32_t *inv,
                      int32_t *q_in, hipStream_t stream);
-// dst[idx[r]][:] = src[r][:] (fp32 or bf16 rows of width H, written as fp32).
+// dst[idx[r]][:] = src[r][:] (fp32, bf16 or fp16 rows of width H, written as fp32).
 hipError_t launch_scatter_rows(Act act, const void *src, const int32_t *idx, float *dst,
                                int64_t rows, int H, hipStream_t stream);
 

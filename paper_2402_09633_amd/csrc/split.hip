@@ -633,7 +633,9 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
   constexpr int G = H / 16;
   constexpr int RP = rec_parts<PREC>();
   constexpr int NR = G * MB * RP * 64;  // 16-byte slots of one H x H matrix
-  using act_t = typename std::conditional<PREC == SPLIT, float, __bf16>::type;
+  using act_t = typename std::conditional<PREC == SPLIT, float, __bf16>::type;  // aggregates
+  // edge rows: fp32, bf16, or bf16 values in fp16 encoding (F16W)
+  using et_t = typename std::conditional<PREC == F16W, _Float16, act_t>::type;
   constexpr bool HAS_E = MODE != (int)EdgeMode::Enc;
   constexpr bool HAS_L2 = MODE != (int)EdgeMode::Cls;
   constexpr bool FUSE = MODE == (int)EdgeMode::UpdAgg;
@@ -676,16 +678,17 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
   // The next unit's edge indices and e row are requested before the
   // current unit's stores (vector-memory completions are counted in issue
   // order, so a load issued after a store is waited for with that store).
-  using xrec_t = typename std::conditional<PREC == SPLIT, f8, bf8>::type;
+  using xrec_t = typename std::conditional<PREC == SPLIT, f8,
+                                           typename std::conditional<PREC == F16W, h8, bf8>::type>::type;
   xrec_t ev[HAS_E ? G : 1];
   auto load_e = [&](int64_t rr) {
-    const act_t *ep = (const act_t *)a.e_in + rr * H + 8 * hh;
+    const et_t *ep = (const et_t *)a.e_in + rr * H + 8 * hh;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       if constexpr (PREC == SPLIT)
         ev[g] = cat8(*(const f4 *)(ep + 16 * g), *(const f4 *)(ep + 16 * g + 4));
       else
-        ev[g] = *(const bf8 *)(ep + 16 * g);
+        ev[g] = *(const xrec_t *)(ep + 16 * g);
     }
   };
   // FUSE: the source of the rows just before and after this lane's row
@@ -759,7 +762,7 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
         else if constexpr (PREC == BF16)
           step_hl<MB>(acc, (const bf8 *)(lw_e + g * RP * MB * 64 + lane), ev[g]);
         else
-          step_f<MB>(acc, lw_e + g * RP * MB * 64 + lane, bf_to_h(ev[g]));
+          step_f<MB>(acc, lw_e + g * RP * MB * 64 + lane, ev[g]);
       }
     }
     // (FUSE: after layer 2's LayerNorm, which needs the registers)
@@ -828,12 +831,12 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
       // half-wave (128 bytes fp32, 64 bytes bf16).  The update's rows go
       // out nontemporal, as the node kernel's (the aggregation that reads
       // them next: 0.136 -> 0.128 ms); the encoder's gain nothing from it.
-      act_t *eo = (act_t *)a.e_out + (u * 32 + 4 * hh) * H + n;
-      auto st_e = [&](act_t *p, float x) {
+      et_t *eo = (et_t *)a.e_out + (u * 32 + 4 * hh) * H + n;
+      auto st_e = [&](et_t *p, float x) {
         if constexpr (FUSE)
-          __builtin_nontemporal_store((act_t)x, p);
+          __builtin_nontemporal_store((et_t)x, p);
         else
-          *p = (act_t)x;
+          *p = (et_t)x;
       };
       if (nvalid == 32) {
 #pragma unroll
