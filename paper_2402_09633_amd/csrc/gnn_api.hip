@@ -673,7 +673,16 @@ int ws_acquire(gnn_handle *h, size_t bytes, hipStream_t stream, void **base, int
   for (int i = 0; i < (int)ws.size(); ++i) {
     const auto &e = ws[i];
     if (e.busy || e.bytes < bytes) continue;
-    const int r = e.last == stream ? 0 : hipEventQuery(e.done) == hipSuccess ? 1 : 2;
+    // (a query that does not return hipSuccess, "not ready" included, is
+    // cleared from the thread's last-error state, which the launch wrappers
+    // of this call report)
+    int r = 1;
+    if (e.last == stream) {
+      r = 0;
+    } else if (e.recorded && hipEventQuery(e.done) != hipSuccess) {
+      (void)hipGetLastError();
+      r = 2;
+    }
     if (r < rank || (r == rank && e.bytes < ws[pick].bytes)) {
       pick = i;
       rank = r;
@@ -709,8 +718,8 @@ int ws_acquire(gnn_handle *h, size_t bytes, hipStream_t stream, void **base, int
       auto &v = ws[victim];
       if (v.base && ws_check_limit(h, ws_round(bytes) - std::min(v.bytes, ws_round(bytes))))
         return GNN_E_OOM;
-      if (v.base &&
-          (hipEventSynchronize(v.done) != hipSuccess || hipFree(v.base) != hipSuccess)) {
+      if (v.base && ((v.recorded && hipEventSynchronize(v.done) != hipSuccess) ||
+                     hipFree(v.base) != hipSuccess)) {
         (void)hipGetLastError();
         return fail(GNN_E_HIP, "releasing a cached workspace failed");
       }
@@ -804,6 +813,10 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
   int rc = GNN_OK;
   Workspace w;
   DeviceGuard guard(hd->device);
+  // The launch wrappers report hipGetLastError(): drop whatever an earlier
+  // runtime call of this thread left there, so that only this call's own
+  // launches are reported.
+  (void)hipGetLastError();
   StageTimer total(hd, stream, ro.ext_base == nullptr), st(hd, stream, false);
   if (ro.ext_base) total.on = false;  // creating events may allocate
   st.on = total.on;
@@ -1142,6 +1155,27 @@ int common_checks(gnn_handle *h, const float *x, const int32_t *ei, int64_t N, i
 }
 
 }  // namespace
+
+namespace gnn {
+
+// Detaches the handle's cached workspaces from `stream` before the caller
+// destroys it: entries whose last call ran there wait for that call (already
+// finished when the stream has been synchronised) and then hold no event
+// recorded on it, so no later call queries or waits on an event of a
+// destroyed stream.
+void ws_forget_stream(gnn_handle *h, hipStream_t stream) {
+  if (!h) return;
+  DeviceGuard guard(h->device);
+  std::lock_guard<std::mutex> lk(h->ws_mu);
+  for (auto &e : h->ws) {
+    if (e.busy || e.last != stream) continue;
+    if (e.recorded && hipEventSynchronize(e.done) != hipSuccess) (void)hipGetLastError();
+    e.recorded = false;
+    e.last = nullptr;
+  }
+}
+
+}  // namespace gnn
 
 extern "C" {
 
@@ -1488,7 +1522,8 @@ int64_t gnn_release_workspaces(gnn_handle *h) {
   int64_t freed = 0;
   for (auto &e : h->ws) {
     if (e.busy || !e.base) continue;
-    if (hipEventSynchronize(e.done) != hipSuccess || hipFree(e.base) != hipSuccess) {
+    if ((e.recorded && hipEventSynchronize(e.done) != hipSuccess) ||
+        hipFree(e.base) != hipSuccess) {
       (void)hipGetLastError();
       return fail(GNN_E_HIP, "releasing a cached workspace failed");
     }

@@ -7,6 +7,8 @@
 #include <cstddef>
 #include <cstdint>
 
+struct gnn_handle;
+
 namespace gnn {
 
 // Activation storage type of a handle.
@@ -260,6 +262,10 @@ hipError_t launch_validate(const int32_t *edge_index, int64_t n_edges, int32_t n
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t stream);
 // bf16 rows -> fp32 rows (debug export).
 hipError_t launch_bf16_to_f32(const void *in, float *out, int64_t n, hipStream_t stream);
+
+// Detaches a handle's cached workspaces from a stream about to be destroyed
+// (host; the stream's work must have finished).
+void ws_forget_stream(gnn_handle *h, hipStream_t stream);
 
 // Sets the calling thread's gnn_last_error() text; returns code (host).
 int set_error(int code, const char *msg);

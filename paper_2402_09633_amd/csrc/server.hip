@@ -91,6 +91,7 @@ void worker(gnn_server *s) {
     }
     // (the events are reused: the previous request's work has finished)
     const bool timed = hipEventRecord(ev[0], stream) == hipSuccess;
+    if (!timed) (void)hipGetLastError();
     int rc = gnn_infer(s->model, r.x, r.ei, r.n_nodes, r.n_edges, r.out, stream);
     const bool timed_end = timed && hipEventRecord(ev[1], stream) == hipSuccess;
     std::string err;
@@ -122,8 +123,12 @@ void worker(gnn_server *s) {
     }
     s->cv_done.notify_all();
   }
+  // the handle's cached workspaces must not keep events of this stream
+  (void)hipStreamSynchronize(stream);
+  gnn::ws_forget_stream(s->model, stream);
   for (hipEvent_t e : ev) (void)hipEventDestroy(e);
   (void)hipStreamDestroy(stream);
+  (void)hipGetLastError();
 }
 
 // Waits for request `id`, releases it and returns a copy.  Only one thread

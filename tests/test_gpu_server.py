@@ -343,3 +343,40 @@ def test_workspace_limit_gives_oom_and_handle_recovers(G, monkeypatch):
             assert np.array_equal(o.cpu().numpy(), want)
     finally:
         m.close()
+
+
+def test_servers_in_sequence_on_one_handle(G):
+    """Servers of 1, 2, 4 and 8 instances created and destroyed one after the
+    other on one handle, after calls on 8 torch streams: each server's
+    workers take cached workspaces last used on streams that no longer
+    exist (the previous server's).  Every request must still equal the
+    direct call bitwise."""
+    w = I.make_weights(3, 64, 1, 75, affine_noise=0.2)
+    m = G.Model(w, G.make_dims(3, 64, 2))
+    evs = _events(8)
+    try:
+        ref = [m(x, ei).cpu().numpy() for x, ei in evs]
+        streams = [torch.cuda.Stream() for _ in evs]
+        outs = [torch.full((ei.shape[1],), -1.0, device="cuda") for _, ei in evs]
+        torch.cuda.synchronize()
+        for (x, ei), o, st in zip(evs, outs, streams):
+            G.gnn_infer(m.handle, x, ei, x.shape[0], ei.shape[1], o, st)
+        torch.cuda.synchronize()
+        for o, r in zip(outs, ref):
+            assert np.array_equal(o.cpu().numpy(), r)
+        for k in (1, 2, 4, 8):
+            srv = G.Server(m, k)
+            try:
+                for rnd in range(2):
+                    for o in outs:
+                        o.fill_(-1.0)
+                    torch.cuda.synchronize()
+                    ids = [srv.submit(x, ei, o) for (x, ei), o in zip(evs, outs)]
+                    for i in ids:
+                        srv.wait(i)
+                    for j, (o, r) in enumerate(zip(outs, ref)):
+                        assert np.array_equal(o.cpu().numpy(), r), f"{k} instances, round {rnd}, event {j}"
+            finally:
+                srv.close()
+    finally:
+        m.close()
