@@ -363,10 +363,14 @@ int gnn_server_wait_info(gnn_server *s, int64_t id, gnn_request_info *info);
 void gnn_server_destroy(gnn_server *s);
 
 /* ---- profiling -----------------------------------------------------------
- * While profiling is enabled on a handle, every call brackets each stage's
- * kernel launches with HIP events on the call's stream (a few microseconds
- * of overhead per stage).  gnn_profile_read waits for those events and
- * returns the accumulated device time per stage since the last enable. */
+ * While profiling is enabled on a handle, every call times each stage with
+ * two HIP events bound to the dispatches of the stage's kernels
+ * (hipExtLaunchKernel): the first kernel's start and the last one's end, so
+ * a stage's time is the time its kernels ran.  Timed dispatches cost the
+ * stream a few microseconds each.  A call's total runs from its first
+ * stage's start to its last stage's end.  gnn_profile_read waits for those
+ * events and returns the accumulated device time per stage since the last
+ * enable. */
 #define GNN_STAGE_CSR 0         /* destination- and source-sorted CSR build  */
 #define GNN_STAGE_NODE_ENC 1    /* node encoder MLP                           */
 #define GNN_STAGE_EDGE_ENC 2    /* edge encoder MLP (gathers h_src, h_dst)    */
@@ -380,7 +384,7 @@ void gnn_server_destroy(gnn_server *s);
 typedef struct gnn_profile_stats {
   uint32_t struct_size;            /* = sizeof(gnn_profile_stats)          */
   int32_t n_calls;                 /* profiled calls accumulated           */
-  int64_t launches[GNN_N_STAGES];  /* bracketed launches per stage         */
+  int64_t launches[GNN_N_STAGES];  /* timed stages (one per stage run)     */
   double ms[GNN_N_STAGES];         /* accumulated device milliseconds      */
 } gnn_profile_stats;
 

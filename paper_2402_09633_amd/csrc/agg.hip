@@ -352,14 +352,10 @@ hipError_t launch_h(Act act, const void *e, const int32_t *rp_in, const int32_t 
   const unsigned blocks = (unsigned)((tasks + tpb - 1) / tpb);
   if (blocks == 0) return hipSuccess;
   if (act == Act::F32)
-    segsum_f32<H><<<blocks, THREADS_F32, 0, stream>>>((const float *)e, rp_in, perm_in, rp_out,
-                                                  perm_out, (float *)agg_in, (float *)agg_out,
-                                                  n_nodes);
-  else
-    segsum_bf16<H><<<blocks, THREADS_BF16, 0, stream>>>((const __bf16 *)e, rp_in, perm_in, rp_out,
-                                                   perm_out, (__bf16 *)agg_in, (__bf16 *)agg_out,
-                                                   n_nodes);
-  return hipGetLastError();
+    return launch(segsum_f32<H>, blocks, THREADS_F32, 0, stream, (const float *)e, rp_in, perm_in,
+                  rp_out, perm_out, (float *)agg_in, (float *)agg_out, n_nodes);
+  return launch(segsum_bf16<H>, blocks, THREADS_BF16, 0, stream, (const __bf16 *)e, rp_in, perm_in,
+                rp_out, perm_out, (__bf16 *)agg_in, (__bf16 *)agg_out, n_nodes);
 }
 
 template <int H>
@@ -373,18 +369,14 @@ hipError_t launch_fused_h(Act act, const void *e, const int32_t *rp_in, const in
   // the pieces come from an edge update over a non-empty edge list
   if (n_edges < 1 || n_edges > INT32_MAX) return hipErrorInvalidValue;
   if (act == Act::F32)
-    segsum_fused_f32<H><<<blocks, THREADS_F32, 0, stream>>>((const float *)e, rp_in, perm_in, rp_out,
-                                                        part, (float *)agg_in, (float *)agg_out,
-                                                        n_nodes);
-  else if (act == Act::BF16)
-    segsum_fused_bf16<H, __bf16><<<blocks, THREADS_BF16, 0, stream>>>(
-        (const __bf16 *)e, rp_in, perm_in, rp_out, part, (__bf16 *)agg_in, (__bf16 *)agg_out,
-        n_nodes);
-  else
-    segsum_fused_bf16<H, _Float16><<<blocks, THREADS_BF16, 0, stream>>>(
-        (const _Float16 *)e, rp_in, perm_in, rp_out, part, (__bf16 *)agg_in, (__bf16 *)agg_out,
-        n_nodes);
-  return hipGetLastError();
+    return launch(segsum_fused_f32<H>, blocks, THREADS_F32, 0, stream, (const float *)e, rp_in,
+                  perm_in, rp_out, part, (float *)agg_in, (float *)agg_out, n_nodes);
+  if (act == Act::BF16)
+    return launch(segsum_fused_bf16<H, __bf16>, blocks, THREADS_BF16, 0, stream, (const __bf16 *)e,
+                  rp_in, perm_in, rp_out, part, (__bf16 *)agg_in, (__bf16 *)agg_out, n_nodes);
+  return launch(segsum_fused_bf16<H, _Float16>, blocks, THREADS_BF16, 0, stream,
+                (const _Float16 *)e, rp_in, perm_in, rp_out, part, (__bf16 *)agg_in,
+                (__bf16 *)agg_out, n_nodes);
 }
 
 }  // namespace

@@ -495,7 +495,9 @@ hipError_t build_csr(const int32_t *edge_index, int32_t n, int32_t n_nodes, int3
   // region, zeroed by a fill kernel (also under stream capture)
   const size_t sw = csr_status_words(n, n_nodes);
   const int64_t words = (int64_t)(sw + CSR_TAIL_WORDS);
-  fill_i32<<<blocks_for(words, 256), 256, 0, stream>>>((int32_t *)s.status, words, 0);
+  if (const hipError_t e =
+          launch(fill_i32, blocks_for(words, 256), 256, 0, stream, (int32_t *)s.status, words, 0))
+    return e;
   uint32_t *totals = s.status + sw;
 
   SortSet S{};
@@ -512,13 +514,15 @@ hipError_t build_csr(const int32_t *edge_index, int32_t n, int32_t n_nodes, int3
     O.inv = inv;
     S.keys_i32[0] = edge_index + n;
     S.keys_i32[1] = edge_index;
-    rs_hist<<<dim3(blocks_for(n, HS_TILE), 2), HS_THREADS, 0, stream>>>(S, n, n_nodes, dg.passes,
-                                                                        dg.bits, totals);
+    if (const hipError_t e = launch(rs_hist, dim3(blocks_for(n, HS_TILE), 2), HS_THREADS, 0,
+                                    stream, S, n, n_nodes, dg.passes, dg.bits, totals))
+      return e;
     for (int p = 0; p < dg.passes; ++p) {
       const bool last = p == dg.passes - 1;
       for (int y = 0; y < 2; ++y) S.out[y] = (p & 1) ? pb[y] : pa[y];
-      rs_onesweep<<<dim3(ntiles, 2), OS_THREADS, 0, stream>>>(S, O, n, n_nodes, p, dg.bits,
-                                                              ntiles, last ? 1 : 0);
+      if (const hipError_t e = launch(rs_onesweep, dim3(ntiles, 2), OS_THREADS, 0, stream, S, O,
+                                      n, n_nodes, p, dg.bits, ntiles, last ? 1 : 0))
+        return e;
       for (int y = 0; y < 2; ++y) {
         S.keys_i32[y] = nullptr;
         S.in[y] = S.out[y];
@@ -533,43 +537,38 @@ hipError_t build_csr(const int32_t *edge_index, int32_t n, int32_t n_nodes, int3
   C.perm[1] = perm_out;
   C.inv = inv;
   C.q_in = eis ? q_in : nullptr;
-  csr_finish<<<dim3(blocks_for((int64_t)n + 1, FIN_POS), 2), FIN_THREADS, 0, stream>>>(
-      C, n, n_nodes);
-  return hipGetLastError();
+  return launch(csr_finish, dim3(blocks_for((int64_t)n + 1, FIN_POS), 2), FIN_THREADS, 0, stream,
+                C, n, n_nodes);
 }
 
 hipError_t launch_validate(const int32_t *edge_index, int64_t n_edges, int32_t n_nodes,
                            int32_t *flag, hipStream_t stream) {
   const int64_t n = 2 * n_edges;
-  validate_idx<<<blocks_for(n, 256), 256, 0, stream>>>(edge_index, n, n_nodes, flag);
-  return hipGetLastError();
+  return launch(validate_idx, blocks_for(n, 256), 256, 0, stream, edge_index, n, n_nodes, flag);
 }
 
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t stream) {
-  if (n > 0) fill_i32<<<blocks_for(n, 256), 256, 0, stream>>>(p, n, v);
-  return hipGetLastError();
+  if (n <= 0) return hipSuccess;
+  return launch(fill_i32, blocks_for(n, 256), 256, 0, stream, p, n, v);
 }
 
 hipError_t launch_scatter_rows(Act act, const void *src, const int32_t *idx, float *dst,
                                int64_t rows, int H, hipStream_t stream) {
   const int64_t n = rows * H;
   if (n <= 0) return hipSuccess;
+  const unsigned nb = (unsigned)blocks_for(n, 256);
   if (act == Act::F32)
-    scatter_rows_k<float><<<blocks_for(n, 256), 256, 0, stream>>>((const float *)src, idx, dst,
-                                                                  rows, H);
-  else if (act == Act::BF16)
-    scatter_rows_k<__bf16><<<blocks_for(n, 256), 256, 0, stream>>>((const __bf16 *)src, idx,
-                                                                   dst, rows, H);
-  else
-    scatter_rows_k<_Float16><<<blocks_for(n, 256), 256, 0, stream>>>((const _Float16 *)src, idx,
-                                                                     dst, rows, H);
-  return hipGetLastError();
+    return launch(scatter_rows_k<float>, nb, 256, 0, stream, (const float *)src, idx, dst, rows, H);
+  if (act == Act::BF16)
+    return launch(scatter_rows_k<__bf16>, nb, 256, 0, stream, (const __bf16 *)src, idx, dst, rows,
+                  H);
+  return launch(scatter_rows_k<_Float16>, nb, 256, 0, stream, (const _Float16 *)src, idx, dst,
+                rows, H);
 }
 
 hipError_t launch_bf16_to_f32(const void *in, float *out, int64_t n, hipStream_t stream) {
-  if (n > 0)
-    bf16_to_f32<<<blocks_for(n, 256), 256, 0, stream>>>((const __bf16 *)in, out, n);
-  return hipGetLastError();
+  if (n <= 0) return hipSuccess;
+  return launch(bf16_to_f32, blocks_for(n, 256), 256, 0, stream, (const __bf16 *)in, out, n);
 }
 
 }  // namespace gnn

@@ -386,15 +386,9 @@ hipError_t node_h(bool enc, const NodeArgs &a, int grid, hipStream_t stream) {
   const int64_t tiles = (a.n_rows + 32 * EDGE_WAVES - 1) / (32 * EDGE_WAVES);
   if (tiles <= 0) return hipSuccess;
   const unsigned nb = (unsigned)(tiles < grid ? tiles : grid);
-  if (enc) {
-    if (a.nproj == 2)
-      node_f32<MB, true, 2><<<nb, 64 * EDGE_WAVES, 0, stream>>>(a);
-    else
-      node_f32<MB, true, 1><<<nb, 64 * EDGE_WAVES, 0, stream>>>(a);
-  } else {
-    node_f32<MB, false, 1><<<nb, 64 * EDGE_WAVES, 0, stream>>>(a);
-  }
-  return hipGetLastError();
+  if (!enc) return launch(node_f32<MB, false, 1>, nb, 64 * EDGE_WAVES, 0, stream, a);
+  if (a.nproj == 2) return launch(node_f32<MB, true, 2>, nb, 64 * EDGE_WAVES, 0, stream, a);
+  return launch(node_f32<MB, true, 1>, nb, 64 * EDGE_WAVES, 0, stream, a);
 }
 
 template <int MB>
@@ -404,12 +398,11 @@ hipError_t edge_h(EdgeMode mode, const EdgeArgs &a, int grid, hipStream_t stream
   if (need <= 0) return hipSuccess;
   const unsigned nb = (unsigned)(need < grid ? need : grid);
   switch (mode) {
-    case EdgeMode::Enc: edge_f32<MB, 0><<<nb, 64 * EDGE_WAVES, 0, stream>>>(a); break;
-    case EdgeMode::Upd: edge_f32<MB, 1><<<nb, 64 * EDGE_WAVES, 0, stream>>>(a); break;
-    case EdgeMode::Cls: edge_f32<MB, 2><<<nb, 64 * EDGE_WAVES, 0, stream>>>(a); break;
+    case EdgeMode::Enc: return launch(edge_f32<MB, 0>, nb, 64 * EDGE_WAVES, 0, stream, a);
+    case EdgeMode::Upd: return launch(edge_f32<MB, 1>, nb, 64 * EDGE_WAVES, 0, stream, a);
+    case EdgeMode::Cls: return launch(edge_f32<MB, 2>, nb, 64 * EDGE_WAVES, 0, stream, a);
     default: return hipErrorInvalidValue;  // no fused sums on the fp32 matrix cores
   }
-  return hipGetLastError();
 }
 
 }  // namespace

@@ -335,13 +335,12 @@ struct gnn_handle {
   std::vector<MlpDev> edge_mlp, node_mlp;
   FactDev fd;
   // profiling: recorded (stage, start, end) event pairs not yet read, the
-  // running totals and a pool of reusable events.  Consecutive stages share
-  // the event between them (the mark of the later stage does not own its
-  // start event).
+  // running totals and a pool of reusable events.  A call's total shares the
+  // events of its first and last stages (its mark owns neither).
   struct Mark {
     int stage;
     hipEvent_t a, b;
-    bool own_a;
+    bool own_a, own_b;
   };
   std::mutex prof_mu;
   bool prof_on = false;
@@ -555,21 +554,25 @@ int check_counts(gnn_handle *h, int64_t N, int64_t E) {
     }                                                                                \
   } while (0)
 
-// Brackets stage launches with events when profiling is on.  A stage that
-// begins right where the previous one ended starts at that stage's end
-// event, so a call records one event per stage boundary (each record costs
-// the stream a few microseconds).
+// Times the stages of a call when profiling is on.  Each stage gets two
+// events that its kernels' dispatches mark themselves (StageEvents): the
+// first kernel's start and the last one's end, so a stage's time is the time
+// its kernels ran, with no marker work added to the stream.  The call's total
+// runs from its first stage's start to its last stage's end.
 struct StageTimer {
   gnn_handle *h;
-  hipStream_t s;
   bool on;
-  hipEvent_t a = nullptr;     // start of the open stage
-  bool own_a = false;
-  hipEvent_t last = nullptr;  // end of the previous stage
-  StageTimer(gnn_handle *h_, hipStream_t s_, bool count_call) : h(h_), s(s_) {
+  hipEvent_t a = nullptr, b = nullptr;          // the open stage's events
+  hipEvent_t first = nullptr, last_b = nullptr;  // the call's first start, last end
+  StageTimer(gnn_handle *h_, bool count_call) : h(h_) {
     std::lock_guard<std::mutex> lk(h->prof_mu);
     on = h->prof_on;
     if (on && count_call) ++h->prof_calls;
+  }
+  ~StageTimer() {  // a stage left open by an error
+    gnn::stage_events() = gnn::StageEvents{};
+    if (a) put(a);
+    if (b) put(b);
   }
   hipEvent_t get() {
     std::lock_guard<std::mutex> lk(h->prof_mu);
@@ -578,6 +581,7 @@ struct StageTimer {
       e = h->prof_free.back();
       h->prof_free.pop_back();
     } else if (hipEventCreate(&e) != hipSuccess) {
+      (void)hipGetLastError();
       e = nullptr;
     }
     return e;
@@ -588,28 +592,37 @@ struct StageTimer {
   }
   void begin() {
     if (!on) return;
-    if (last) {
-      a = last;
-      own_a = false;
+    a = get();
+    b = get();
+    if (!a || !b) {
+      if (a) put(a);
+      if (b) put(b);
+      a = b = nullptr;
       return;
     }
-    a = get();
-    own_a = true;
-    if (a) (void)hipEventRecord(a, s);
+    gnn::stage_events() = gnn::StageEvents{a, b, false};
   }
   void end(int stage) {
-    if (!on || !a) return;
-    hipEvent_t b = get();
-    if (!b) {
-      if (own_a) put(a);
-      a = last = nullptr;
-      return;
+    if (!a) return;
+    gnn::StageEvents &ev = gnn::stage_events();
+    const bool launched = ev.launched;
+    ev = gnn::StageEvents{};
+    if (!launched) {  // nothing ran in this stage
+      put(a);
+      put(b);
+    } else {
+      std::lock_guard<std::mutex> lk(h->prof_mu);
+      h->prof_pending.push_back({stage, a, b, true, true});
+      if (!first) first = a;
+      last_b = b;
     }
-    (void)hipEventRecord(b, s);
+    a = b = nullptr;
+  }
+  // Records the call's total (events owned by the first and last stages).
+  void finish(int stage) {
+    if (!first) return;
     std::lock_guard<std::mutex> lk(h->prof_mu);
-    h->prof_pending.push_back({stage, a, b, own_a});
-    last = b;
-    a = nullptr;
+    h->prof_pending.push_back({stage, first, last_b, false, false});
   }
 };
 
@@ -817,9 +830,8 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
   // runtime call of this thread left there, so that only this call's own
   // launches are reported.
   (void)hipGetLastError();
-  StageTimer total(hd, stream, ro.ext_base == nullptr), st(hd, stream, false);
-  if (ro.ext_base) total.on = false;  // creating events may allocate
-  st.on = total.on;
+  StageTimer st(hd, ro.ext_base == nullptr);
+  if (ro.ext_base) st.on = false;  // creating events may allocate
 
   const bool fac = hd->factored;
   // the edge update sums its rows per source itself (split kernels)
@@ -837,7 +849,6 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
     rc = ws_acquire(hd, w.bytes, stream, &w.base, &slot);
     if (rc != GNN_OK) return rc;
   }
-  total.begin();
   plan_workspace(w, N, E, H, ab, fac, fused);
 
   if (d.flags & GNN_VALIDATE_INDICES) {
@@ -1137,7 +1148,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
   }
 
 out:
-  total.end(GNN_STAGE_TOTAL);
+  st.finish(GNN_STAGE_TOTAL);
   if (!ro.ext_base) {
     const int rr = ws_release(hd, slot, w.base, w.bytes, stream);
     if (rc == GNN_OK) rc = rr;
@@ -1157,6 +1168,11 @@ int common_checks(gnn_handle *h, const float *x, const int32_t *ei, int64_t N, i
 }  // namespace
 
 namespace gnn {
+
+StageEvents &stage_events() {
+  static thread_local StageEvents ev;
+  return ev;
+}
 
 // Detaches the handle's cached workspaces from `stream` before the caller
 // destroys it: entries whose last call ran there wait for that call (already
@@ -1552,7 +1568,7 @@ void gnn_destroy(gnn_handle *h) {
     (void)hipFree(h->dev_weights);
     for (auto &mk : h->prof_pending) {
       if (mk.own_a) (void)hipEventDestroy(mk.a);
-      (void)hipEventDestroy(mk.b);
+      if (mk.own_b) (void)hipEventDestroy(mk.b);
     }
     for (auto e : h->prof_free) (void)hipEventDestroy(e);
     for (auto &e : h->ws) {
@@ -1614,7 +1630,7 @@ int gnn_profile_read(gnn_handle *h, gnn_profile_stats *out) {
   std::lock_guard<std::mutex> lk(h->prof_mu);
   for (auto &mk : marks) {
     if (mk.own_a) h->prof_free.push_back(mk.a);
-    h->prof_free.push_back(mk.b);
+    if (mk.own_b) h->prof_free.push_back(mk.b);
   }
   for (int i = 0; i < GNN_N_STAGES; ++i) {
     h->prof_ms[i] += add[i];

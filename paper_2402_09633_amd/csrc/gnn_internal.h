@@ -2,14 +2,54 @@
 // libgnn.so.  Nothing here is part of the public ABI (include/gnn.h).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstddef>
 #include <cstdint>
+#include <tuple>
+#include <utility>
 
 struct gnn_handle;
 
 namespace gnn {
+
+// Events of the stage being timed on this thread (profiling on), bound to the
+// dispatches of the stage's kernels rather than recorded between them: the
+// first kernel launched in the stage marks `start` when it begins, and every
+// kernel marks `stop` when it ends (the last one's stands).  Both are null
+// when no stage is being timed.
+struct StageEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+  bool launched = false;
+};
+StageEvents &stage_events();  // this thread's
+
+template <typename K, typename T, size_t... I>
+hipError_t launch_args(K k, dim3 grid, dim3 block, size_t shmem, hipStream_t stream, T &t,
+                       std::index_sequence<I...>) {
+  void *argv[] = {(void *)&std::get<I>(t)...};
+  StageEvents &ev = stage_events();
+  if (!ev.stop) return hipLaunchKernel((const void *)k, grid, block, argv, shmem, stream);
+  const hipError_t e =
+      hipExtLaunchKernel((const void *)k, grid, block, argv, shmem, stream, ev.start, ev.stop, 0);
+  if (e == hipSuccess) {
+    ev.start = nullptr;
+    ev.launched = true;
+  }
+  return e;
+}
+
+// Launches kernel k(args...) on `stream` with the timed stage's events, if
+// any (StageEvents).  Returns the launch status, which the runtime also
+// leaves for hipGetLastError().
+template <typename... P, typename... A>
+hipError_t launch(void (*k)(P...), dim3 grid, dim3 block, size_t shmem, hipStream_t stream,
+                  A &&...args) {
+  static_assert(sizeof...(P) == sizeof...(A), "kernel argument count");
+  std::tuple<P...> t(std::forward<A>(args)...);
+  return launch_args(k, grid, block, shmem, stream, t, std::index_sequence_for<P...>{});
+}
 
 // Activation storage type of a handle.
 // Row element types.  F16 is used only for the edge rows of the bf16 model

@@ -300,11 +300,10 @@ hipError_t launch_one(Act act, const GmlpArgs &a, hipStream_t stream) {
   const int64_t blocks = (waves + WAVES_PER_BLOCK - 1) / WAVES_PER_BLOCK;
   if (blocks <= 0) return hipSuccess;
   if (blocks > INT32_MAX) return hipErrorInvalidValue;
+  const unsigned nb = (unsigned)blocks;
   if (act == Act::F32)
-    gmlp_f32<MB, NSRC, SMALLK, CLS, KIND><<<(unsigned)blocks, 64 * WAVES_PER_BLOCK, 0, stream>>>(a);
-  else
-    gmlp_bf16<MB, NSRC, SMALLK, CLS, KIND><<<(unsigned)blocks, 64 * WAVES_PER_BLOCK, 0, stream>>>(a);
-  return hipGetLastError();
+    return launch(gmlp_f32<MB, NSRC, SMALLK, CLS, KIND>, nb, 64 * WAVES_PER_BLOCK, 0, stream, a);
+  return launch(gmlp_bf16<MB, NSRC, SMALLK, CLS, KIND>, nb, 64 * WAVES_PER_BLOCK, 0, stream, a);
 }
 
 template <int MB>

@@ -250,13 +250,17 @@ __device__ __forceinline__ void zero(f16v (&a)[MB]) {
 // kernels that read those rows next.
 //
 // The tile has 32 rows of 128 bytes (eight 16-byte chunks); chunk c of row r
-// sits at chunk c ^ swz(r), swz(r) = r & 7.  Measured with this access
-// pattern (row writes, one chunk per lane; column-block reads, eight lanes
-// per row): no LDS bank conflicts, against 1.0M per 64k writes and reads
-// for rows padded to 36 floats, 14.7M for unpadded rows and 2.1M for the
-// swizzle (r >> 1) & 7.
+// sits at chunk c ^ swz(r), swz(r) = (r ^ (r >> 3)) & 7.  Measured with the
+// 16-byte accesses (row writes, one chunk per lane; column-block reads,
+// eight lanes per row): no LDS bank conflicts with r & 7, against 1.0M per
+// 64k writes and reads for rows padded to 36 floats, 14.7M for unpadded rows
+// and 2.1M for the swizzle (r >> 1) & 7.  The 8-byte writes of 16-bit rows
+// (store_block16, h) are served 16 lanes at a time: with r & 7, rows n and
+// n + 8 then hit the same banks (1024 bytes apart, the same swizzle); the
+// extra r >> 3 term moves row n + 8 to the neighbouring chunk, which keeps
+// every pattern here conflict-free on 64 four-byte banks.
 constexpr int SST = 32;  // staging row stride in floats
-__device__ __forceinline__ int swz(int r) { return r & 7; }
+__device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
 template <int MB>
 __device__ __forceinline__ void store_block(float *__restrict__ out, int64_t stride, int nvalid,
                                             const f16v (&acc)[MB], float *stg, int lane) {
@@ -905,15 +909,9 @@ hipError_t node_h(bool enc, const NodeArgs &a, int grid, hipStream_t stream) {
   const int64_t tiles = (a.n_rows + 32 * SW - 1) / (32 * SW);
   if (tiles <= 0) return hipSuccess;
   const unsigned nb = (unsigned)(tiles < grid ? tiles : grid);
-  if (enc) {
-    if (a.nproj == 2)
-      node_split<MB, true, 2, PREC><<<nb, 64 * SW, 0, stream>>>(a);
-    else
-      node_split<MB, true, 1, PREC><<<nb, 64 * SW, 0, stream>>>(a);
-  } else {
-    node_split<MB, false, 1, PREC><<<nb, 64 * SW, 0, stream>>>(a);
-  }
-  return hipGetLastError();
+  if (!enc) return launch(node_split<MB, false, 1, PREC>, nb, 64 * SW, 0, stream, a);
+  if (a.nproj == 2) return launch(node_split<MB, true, 2, PREC>, nb, 64 * SW, 0, stream, a);
+  return launch(node_split<MB, true, 1, PREC>, nb, 64 * SW, 0, stream, a);
 }
 
 template <int MB, int PREC>
@@ -923,15 +921,14 @@ hipError_t edge_h(EdgeMode mode, const EdgeArgs &a, int grid, hipStream_t stream
   if (need <= 0) return hipSuccess;
   const unsigned nb = (unsigned)(need < grid ? need : grid);
   switch (mode) {
-    case EdgeMode::Enc: edge_split<MB, 0, PREC><<<nb, 64 * SW, 0, stream>>>(a); break;
+    case EdgeMode::Enc: return launch(edge_split<MB, 0, PREC>, nb, 64 * SW, 0, stream, a);
     case EdgeMode::Upd: return hipErrorInvalidValue;  // always UpdAgg here
-    case EdgeMode::Cls: edge_split<MB, 2, PREC><<<nb, 64 * SW, 0, stream>>>(a); break;
+    case EdgeMode::Cls: return launch(edge_split<MB, 2, PREC>, nb, 64 * SW, 0, stream, a);
     case EdgeMode::UpdAgg:
       if (!a.agg_out || !a.agg_part) return hipErrorInvalidValue;
-      edge_split<MB, 3, PREC><<<nb, 64 * SW, 0, stream>>>(a);
-      break;
+      return launch(edge_split<MB, 3, PREC>, nb, 64 * SW, 0, stream, a);
   }
-  return hipGetLastError();
+  return hipErrorInvalidValue;
 }
 
 template <int MB, int PREC>
