@@ -648,35 +648,25 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
   static_assert(MODE != (int)EdgeMode::Upd, "split kernels have no plain update");
   __shared__ h8 lds[(HAS_E ? NR : 0) + (HAS_L2 ? NR : 0)];
   __shared__ float prm[6 * H];  // s1 b1, gamma1, beta1, s2 b2, gamma2, beta2
-  h8 *lw_e = lds;
-  h8 *lw_2 = lds + (HAS_E ? NR : 0);
-  for (int i = threadIdx.x; i < NR; i += 64 * SW) {
-    if constexpr (HAS_E) lw_e[i] = ((const h8 *)a.we)[i];
-    if constexpr (HAS_L2) lw_2[i] = ((const h8 *)a.w2)[i];
-  }
-  for (int i = threadIdx.x; i < H; i += 64 * SW) {
-    prm[i] = 0.f;  // (layer-1 bias: inside the gathered P[src] rows)
-    prm[H + i] = a.g1[i];
-    prm[2 * H + i] = a.beta1[i];
-    if constexpr (HAS_L2) {
-      prm[3 * H + i] = a.b2[i] * a.s2;
-      prm[4 * H + i] = a.g2[i];
-      prm[5 * H + i] = a.beta2[i];
-    } else {
-      prm[3 * H + i] = ((const float *)a.w2)[i];  // classifier head row
-    }
-  }
-  __syncthreads();
-  const float eps1 = a.eps * a.s1 * a.s1, eps2 = a.eps * a.s2 * a.s2;
-
   const int lane = threadIdx.x & 63, hh = lane >> 5, n = lane & 31;
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
-  const int64_t gw = (int64_t)blk * SW + (threadIdx.x >> 6);
+  const int wv = threadIdx.x >> 6;
+  const int64_t gw = (int64_t)blk * SW + wv;
   const int64_t nw = (int64_t)gridDim.x * SW;
   const int64_t units = (a.n_rows + 31) / 32;
   auto row_of = [&](int64_t u) {
     const int64_t row = u * 32 + n;
     return row < a.n_rows ? row : a.n_rows - 1;  // tail lanes recompute the last row
+  };
+  // The unit of round rd for this wave (-1: none).  Full rounds go
+  // workgroup by workgroup (a workgroup's waves take consecutive units); the
+  // last, partial round is spread over all workgroups, one wave of each
+  // before any takes a second, so that it does not fall on a few CUs only.
+  const int64_t full_rounds = units / nw;
+  auto unit_at = [&](int64_t rd) -> int64_t {
+    if (rd < full_rounds) return rd * nw + gw;
+    const int64_t u = full_rounds * nw + (int64_t)wv * gridDim.x + blk;
+    return rd == full_rounds && u < units ? u : -1;
   };
 
   // The next unit's edge indices and e row are requested before the
@@ -712,11 +702,35 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
     // unit's stores anyway, and the registers are needed until then.
     if constexpr (HAS_E && !FUSE) load_e(r0);
   };
-  if (gw < units) {
-    load_idx(gw);
-    if constexpr (FUSE) load_e(row_of(gw));
+  // The first unit's loads go out before the weights are copied into LDS.
+  int64_t u = unit_at(0);
+  if (u >= 0) {
+    load_idx(u);
+    if constexpr (FUSE) load_e(row_of(u));
   }
-  for (int64_t u = gw; u < units; u += nw) {
+  h8 *lw_e = lds;
+  h8 *lw_2 = lds + (HAS_E ? NR : 0);
+  for (int i = threadIdx.x; i < NR; i += 64 * SW) {
+    if constexpr (HAS_E) lw_e[i] = ((const h8 *)a.we)[i];
+    if constexpr (HAS_L2) lw_2[i] = ((const h8 *)a.w2)[i];
+  }
+  for (int i = threadIdx.x; i < H; i += 64 * SW) {
+    prm[i] = 0.f;  // (layer-1 bias: inside the gathered P[src] rows)
+    prm[H + i] = a.g1[i];
+    prm[2 * H + i] = a.beta1[i];
+    if constexpr (HAS_L2) {
+      prm[3 * H + i] = a.b2[i] * a.s2;
+      prm[4 * H + i] = a.g2[i];
+      prm[5 * H + i] = a.beta2[i];
+    } else {
+      prm[3 * H + i] = ((const float *)a.w2)[i];  // classifier head row
+    }
+  }
+  __syncthreads();
+  const float eps1 = a.eps * a.s1 * a.s1, eps2 = a.eps * a.s2 * a.s2;
+
+  for (int64_t rd = 0; u >= 0; ++rd) {
+    const int64_t un = unit_at(rd + 1);  // the next unit (-1: none)
     // Keeps the LDS record reads inside the loop (they are loop-invariant;
     // hoisted, they would pin every weight in registers).
     asm volatile("" ::: "memory");
@@ -771,7 +785,7 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
     }
     // (FUSE: after layer 2's LayerNorm, which needs the registers)
     if constexpr (!FUSE)
-      if (u + nw < units) load_idx(u + nw);
+      if (un >= 0) load_idx(un);
     ln_relu_lds<MB, false>(acc, prm, eps1, hh);  // bias inside P[src]
 
     if constexpr (!HAS_L2) {
@@ -829,7 +843,7 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
         hc = __ballot(n == 0 && nprev == nsrc) != 0;
         tc = __ballot(n == 31 && nsrc == nnext) != 0;
         cur_src = nsrc;
-        if (u + nw < units) load_idx(u + nw);
+        if (un >= 0) load_idx(un);
       }
       // e rows: each store writes 32 contiguous elements of a row per
       // half-wave (128 bytes fp32, 64 bytes bf16).  The update's rows go
@@ -898,9 +912,10 @@ __global__ __launch_bounds__(64 * SW) void edge_split(EdgeArgs a) {
           for (int p = 0; p < MB / 2; ++p) sum[p] = 0.f;
         }
       }
-      if (u + nw < units) load_e(row_of(u + nw));
+      if (un >= 0) load_e(row_of(un));
       }
     }
+    u = un;
   }
 }
 
