@@ -43,6 +43,7 @@ BF16_SCORE_ATOL = 2e-2   # |s - s_ref| <= 2e-2 against the oracle of the fp32 we
 TRAFFIC_SOURCES = {
     "split": ["paper_2402_09633_amd/csrc/split.hip", "paper_2402_09633_amd/csrc/device_common.h"],
     "bf16": ["paper_2402_09633_amd/csrc/split.hip", "paper_2402_09633_amd/csrc/device_common.h"],
+    "f16w": ["paper_2402_09633_amd/csrc/split.hip", "paper_2402_09633_amd/csrc/device_common.h"],
     "fp32_mfma": ["paper_2402_09633_amd/csrc/factored.hip",
                   "paper_2402_09633_amd/csrc/device_common.h"],
 }
@@ -270,6 +271,21 @@ def timed_leg(G, torch, np, g, w, H, T, dtype, flags, steps, warmup):
     ms = (t1 - t0) * 1000.0 / steps
     return {"ms_per_step": ms, "per": per, "prof": prof, "scores": scores,
             "logits": zt.cpu().numpy(), "model": m, "x": x, "ei": ei, "out": out}
+
+
+def f16w_rooflines(roof, roof_node):
+    """The fp16-weight kernels execute one fp16 product per weight, half
+    the hi/lo bf16 kernels' matrix work (rooflines() counts the latter)."""
+    roof["kernel"] = "edge_split<4,3,f16w> (fp16 weights in LDS, bf16 rows converted exactly)"
+    for r in (roof, roof_node):
+        if r and "mfma" in r:
+            r["mfma"]["executed_tflop_per_launch"] /= 2.0
+            r["mfma"]["achieved"] = round(r["mfma"]["achieved"] / 2.0, 1)
+            r["mfma"]["frac"] = round(r["mfma"]["frac"] / 2.0, 4)
+            r["mfma"]["dtype"] = "fp16"
+    if roof_node:
+        roof_node["kernel"] = "node_split<4,false,1,f16w> (fp16 weights streamed through LDS; " \
+                              "fp16 projections)"
 
 
 def rooflines(prof, N, E, H, T, bf16, split, factored, n_src, traffic, ceil=None):
@@ -593,6 +609,8 @@ def main():
     ap.add_argument("--fp32-mfma", action="store_true",
                     help="fp32 products on the fp32 matrix cores (GNN_FP32_MFMA) instead of "
                          "split fp16/bf16 products")
+    ap.add_argument("--f16-weights", action="store_true",
+                    help="with --workload full_bf16: fp16 weights (GNN_F16_WEIGHTS)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 3 times (reference "
                          "kernel of known traffic for scaling HBM byte counters)")
@@ -641,11 +659,16 @@ def main():
     w = I.make_weights(3, H, 1, cfg.weight_seed)
     bf16 = cfg.dtype == "bf16"
     dtype = G.GNN_BF16 if bf16 else G.GNN_FP32
+    if args.f16_weights and not (bf16 and not args.literal and not args.fp32_mfma):
+        print("--f16-weights needs the bf16 workload on the regrouped kernels", file=sys.stderr)
+        sys.exit(2)
     flags = (G.GNN_LITERAL_GATHER if args.literal else 0) | \
-        (G.GNN_FP32_MFMA if args.fp32_mfma else 0)
+        (G.GNN_FP32_MFMA if args.fp32_mfma else 0) | \
+        (G.GNN_F16_WEIGHTS if args.f16_weights else 0)
     factored = not args.literal
     split = factored and (bf16 or not args.fp32_mfma)
-    path = ("bf16" if bf16 else "split") if split else ("fp32_mfma" if factored else "literal")
+    path = (("f16w" if args.f16_weights else "bf16") if bf16 else "split") if split else \
+        ("fp32_mfma" if factored else "literal")
     extra = cfg.name == "full" and not args.no_extra_legs
     print(f"# workload {cfg.name}: N={N} E={E} H={H} T={T} {cfg.dtype}", file=sys.stderr,
           flush=True)
@@ -688,6 +711,8 @@ def main():
     ceil = hbm_ceiling(G, torch)
     roof, roof_node, roof_agg = rooflines(leg["prof"], N, E, H, T, bf16, split, factored,
                                           n_src, traffic, ceil)
+    if path == "f16w":
+        f16w_rooflines(roof, roof_node)
     per = leg["per"]
     rec = {
         "metric": METRIC,
@@ -710,7 +735,9 @@ def main():
                                 "fp32_mfma": "fp32 matrix cores",
                                 "literal": "per-edge first layer",
                                 "bf16": "bf16 activations on the bf16 matrix cores, hi/lo "
-                                        "bf16 weights, fp32 accumulation"}[path]},
+                                        "bf16 weights, fp32 accumulation",
+                                "f16w": "bf16 activations converted exactly to fp16, fp16 "
+                                        "weights, fp16 matrix cores, fp32 accumulation"}[path]},
         "ms_per_event_p50": round(float(np.percentile(per, 50)), 4),
         "ms_per_event_p99": round(float(np.percentile(per, 99)), 4),
         "ms_per_event_min": round(float(per.min()), 4),
@@ -770,19 +797,17 @@ def main():
         fleg = timed_leg(G, torch, np, g, w, H, T, G.GNN_BF16, G.GNN_F16_WEIGHTS, args.steps,
                          args.warmup)
         fleg["model"].close()
+        ftraffic = MEASURED_TRAFFIC.get(("f16w", kernel_source_hash("f16w")))
         froof, froof_node, froof_agg = rooflines(fleg["prof"], N, E, H, T, True, True, True,
-                                                 n_src, None, ceil)
-        froof["kernel"] = "edge_split<4,3,f16w> (fp16 weights in LDS, bf16 rows converted)"
-        froof["mfma"]["executed_tflop_per_launch"] /= 2.0
-        froof["mfma"]["achieved"] = round(froof["mfma"]["achieved"] / 2.0, 1)
-        froof["mfma"]["frac"] = round(froof["mfma"]["frac"] / 2.0, 4)
-        froof["mfma"]["dtype"] = "fp16"
+                                                 n_src, ftraffic, ceil)
+        f16w_rooflines(froof, froof_node)
         rec["bf16"]["f16_weights"] = {
             "ms_per_event": round(fleg["ms_per_step"], 4),
             "edges_per_s": round(E / (fleg["ms_per_step"] / 1000.0), 1),
             "ms_per_event_p50": round(float(np.percentile(fleg["per"], 50)), 4),
             "ms_per_event_p99": round(float(np.percentile(fleg["per"], 99)), 4),
-            "roofline": froof, "stages_ms_per_event": stages(fleg["prof"]),
+            "roofline": froof, "roofline_node_update": froof_node,
+            "roofline_aggregate": froof_agg, "stages_ms_per_event": stages(fleg["prof"]),
             "weights": "GNN_F16_WEIGHTS: each weight one fp16 number times a power of two (one "
                        "fp16 product per weight); activations bf16 in HBM, rounded to bf16 "
                        "where they feed a product and converted exactly to fp16",
