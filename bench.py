@@ -38,7 +38,8 @@ BF16_SCORE_ATOL = 2e-2   # |s - s_ref| <= 2e-2 against the oracle of the fp32 we
 
 # HBM bytes per launch of the edge-update kernel on the full event, from
 # rocprofv3 FETCH_SIZE / WRITE_SIZE passes scaled by a plain-copy calibration
-# (profiles/full_event_fp32_kernels_and_counters.md, profiles/full_event_bf16_kernels_and_counters.md).
+# (profiles/full_event_fp32_kernels_and_counters.md, profiles/full_event_bf16_kernels_and_counters.md,
+# profiles/full_event_bf16_f16_weights_kernels_and_counters.md).
 # Valid only for the kernel sources they were measured on (hash of the files of that path).
 TRAFFIC_SOURCES = {
     "split": ["paper_2402_09633_amd/csrc/split.hip", "paper_2402_09633_amd/csrc/device_common.h"],
@@ -49,8 +50,9 @@ TRAFFIC_SOURCES = {
 }
 # (path, source hash) -> (HBM bytes read, written) per edge-update launch on
 # the full event
-MEASURED_TRAFFIC = {("split", "270c0bc20d53cec3"): (1.138e9, 0.651e9),    # edge_split<4,3>
-                    ("bf16", "270c0bc20d53cec3"): (0.551e9, 0.343e9)}     # edge_split<4,3,bf16>
+MEASURED_TRAFFIC = {("split", "ad4e97287fae85e0"): (1.136e9, 0.651e9),    # edge_split<4,3>
+                    ("bf16", "ad4e97287fae85e0"): (0.550e9, 0.342e9),     # edge_split<4,3,bf16>
+                    ("f16w", "ad4e97287fae85e0"): (0.592e9, 0.347e9)}     # edge_split<4,3,f16w>
 
 
 def kernel_source_hash(path):
