@@ -344,6 +344,7 @@ struct gnn_handle {
   };
   std::mutex prof_mu;
   bool prof_on = false;
+  bool prof_sample = false;  // GNN_PROFILE_SAMPLE: one iteration's stages per call
   std::vector<Mark> prof_pending;
   std::vector<hipEvent_t> prof_free;
   int32_t prof_calls = 0;
@@ -561,12 +562,13 @@ int check_counts(gnn_handle *h, int64_t N, int64_t E) {
 // runs from its first stage's start to its last stage's end.
 struct StageTimer {
   gnn_handle *h;
-  bool on;
+  bool on, sample;
   hipEvent_t a = nullptr, b = nullptr;          // the open stage's events
   hipEvent_t first = nullptr, last_b = nullptr;  // the call's first start, last end
   StageTimer(gnn_handle *h_, bool count_call) : h(h_) {
     std::lock_guard<std::mutex> lk(h->prof_mu);
     on = h->prof_on;
+    sample = h->prof_sample;
     if (on && count_call) ++h->prof_calls;
   }
   ~StageTimer() {  // a stage left open by an error
@@ -590,8 +592,10 @@ struct StageTimer {
     std::lock_guard<std::mutex> lk(h->prof_mu);
     h->prof_free.push_back(e);
   }
-  void begin() {
-    if (!on) return;
+  // in_sample: the stage belongs to the iteration that GNN_PROFILE_SAMPLE
+  // times (every stage is timed in the full mode)
+  void begin(bool in_sample = false) {
+    if (!on || (sample && !in_sample)) return;
     a = get();
     b = get();
     if (!a || !b) {
@@ -620,7 +624,7 @@ struct StageTimer {
   }
   // Records the call's total (events owned by the first and last stages).
   void finish(int stage) {
-    if (!first) return;
+    if (!first || sample) return;
     std::lock_guard<std::mutex> lk(h->prof_mu);
     h->prof_pending.push_back({stage, first, last_b, false, false});
   }
@@ -978,10 +982,10 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
         ea.agg_out = w.aout;
         ea.agg_part = w.part;
       }
-      st.begin();
+      st.begin(t == T / 2);
       HIP_TRY(launch_edge(fused ? EdgeMode::UpdAgg : EdgeMode::Upd, ea, fd.grid_upd));
       st.end(GNN_STAGE_EDGE_UPDATE);
-      st.begin();
+      st.begin(t == T / 2);
       if (fused)
         HIP_TRY(launch_segsum_fused(eact, H, w.e, w.rp_in, w.q_in, w.rp_out, w.part, w.ain,
                                     w.aout, n, E, stream));
@@ -1016,7 +1020,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
         nu.pbias[0] = mc->l0.b;
       }
       nu.eps = d.ln_eps;
-      st.begin();
+      st.begin(t == T / 2);
       HIP_TRY(fd.split ? launch_node_split(false, H, nu, fd.grid_node, fd.prec, stream)
                        : launch_node_f32(false, H, nu, fd.grid_node, stream));
       st.end(GNN_STAGE_NODE_UPDATE);
@@ -1094,10 +1098,10 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       a.src[2] = w.e;
       a.mlp = hd->edge_mlp[k];
       a.out = w.e;
-      st.begin();
+      st.begin(t == T / 2);
       HIP_TRY(launch_gmlp(GmlpKind::EdgeUpd, act, H, a, stream));
       st.end(GNN_STAGE_EDGE_UPDATE);
-      st.begin();
+      st.begin(t == T / 2);
       HIP_TRY(launch_segsum(act, H, w.e, w.rp_in, w.perm_in, w.rp_out, w.perm_out, w.ain,
                             w.aout, n, stream));
       st.end(GNN_STAGE_AGGREGATE);
@@ -1111,7 +1115,7 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       a.src[2] = w.aout;
       a.mlp = hd->node_mlp[k];
       a.out = w.h;
-      st.begin();
+      st.begin(t == T / 2);
       HIP_TRY(launch_gmlp(GmlpKind::NodeUpd, act, H, a, stream));
       st.end(GNN_STAGE_NODE_UPDATE);
     }
@@ -1585,13 +1589,17 @@ int gnn_profile_enable(gnn_handle *h, int enable) {
   scratch.struct_size = sizeof scratch;
   int rc = gnn_profile_read(h, &scratch);  // drains pending events
   if (rc) return rc;
+  if (enable < 0 || enable > GNN_PROFILE_SAMPLE)
+    return fail(GNN_E_INVALID_ARG, "profiling mode %d is not 0, 1 or GNN_PROFILE_SAMPLE", enable);
   std::lock_guard<std::mutex> lk(h->prof_mu);
   h->prof_on = enable != 0;
+  h->prof_sample = enable == GNN_PROFILE_SAMPLE;
   h->prof_calls = 0;
-  // events for about 64 calls, so that none is created while timing
+  // events for about 64 calls (two per timed stage), so that none is
+  // created while timing
   if (h->prof_on) {
     DeviceGuard guard(h->device);
-    while (h->prof_free.size() < 2048) {
+    while (h->prof_free.size() < 4096) {
       hipEvent_t e = nullptr;
       if (hipEventCreate(&e) != hipSuccess) break;
       h->prof_free.push_back(e);

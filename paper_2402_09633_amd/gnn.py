@@ -30,6 +30,7 @@ GNN_VALIDATE_INDICES = 1
 GNN_LITERAL_GATHER = 2
 GNN_FP32_MFMA = 4
 GNN_F16_WEIGHTS = 8
+GNN_PROFILE_SAMPLE = 2
 
 EXPORTS = ("gnn_weight_count", "gnn_create", "gnn_infer", "gnn_infer_logits", "gnn_infer_noalloc",
            "gnn_filter_weight_count", "gnn_filter_create", "gnn_filter_apply",
@@ -310,8 +311,10 @@ def gnn_infer_labels(handle, node_feat, edge_index, n_nodes: int, n_edges: int,
                                        _addr(labels), _stream(stream)))
 
 
-def gnn_profile_enable(handle, enable: bool = True) -> int:
-    return _check(lib.gnn_profile_enable(handle, 1 if enable else 0))
+def gnn_profile_enable(handle, enable=True) -> int:
+    """enable: False/0 off, True/1 every stage, GNN_PROFILE_SAMPLE."""
+    mode = int(enable) if not isinstance(enable, bool) else (1 if enable else 0)
+    return _check(lib.gnn_profile_enable(handle, mode))
 
 
 def gnn_profile_read(handle) -> dict:
