@@ -261,17 +261,16 @@ __device__ __forceinline__ void zero(f16v (&a)[MB]) {
 // kernels that read those rows next.
 //
 // The tile has 32 rows of 128 bytes (eight 16-byte chunks); chunk c of row r
-// sits at chunk c ^ swz(r), swz(r) = (r ^ (r >> 3)) & 7.  Measured with the
-// 16-byte accesses (row writes, one chunk per lane; column-block reads,
-// eight lanes per row): no LDS bank conflicts with r & 7, against 1.0M per
-// 64k writes and reads for rows padded to 36 floats, 14.7M for unpadded rows
-// and 2.1M for the swizzle (r >> 1) & 7.  The 8-byte writes of 16-bit rows
-// (store_block16, h) are served 16 lanes at a time: with r & 7, rows n and
-// n + 8 then hit the same banks (1024 bytes apart, the same swizzle); the
-// extra r >> 3 term moves row n + 8 to the neighbouring chunk, which keeps
-// every pattern here conflict-free on 64 four-byte banks.
+// sits at chunk c ^ swz(r), swz(r) = r & 7.  Measured with the 16-byte
+// accesses (row writes, one chunk per lane; column-block reads, eight lanes
+// per row): no LDS bank conflicts, against 1.0M per 64k writes and reads
+// for rows padded to 36 floats, 14.7M for unpadded rows and 2.1M for the
+// swizzle (r >> 1) & 7.  The 8-byte writes of 16-bit h rows (store_block16)
+// leave about 56 conflict cycles per 32-row unit (about 1 us of a 140 us
+// node update): each half-wave writes one half of every chunk it touches,
+// and the swizzle (r ^ (r >> 3)) & 7 gave the same count.
 constexpr int SST = 32;  // staging row stride in floats
-__device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
+__device__ __forceinline__ int swz(int r) { return r & 7; }
 template <int MB>
 __device__ __forceinline__ void store_block(float *__restrict__ out, int64_t stride, int nvalid,
                                             const f16v (&acc)[MB], float *stg, int lane) {
