@@ -78,3 +78,31 @@ def test_profile_modes_count_and_time_stages(G, dtype, flags):
         assert e.value.code == G.GNN_E_INVALID_ARG
     finally:
         m.close()
+
+
+@pytest.mark.parametrize("T", [0, 1])
+def test_profile_sampled_mode_few_iterations(G, T):
+    """T = 0 has no iteration to sample (no stage timed, calls still
+    counted); T = 1 samples its only iteration."""
+    w = I.make_weights(3, 64, 1, 34)
+    m = G.Model(w, G.make_dims(3, 64, T))
+    x, ei = _event()
+    out = torch.empty(ei.shape[1], device="cuda")
+    try:
+        G.gnn_profile_enable(m.handle, G.GNN_PROFILE_SAMPLE)
+        for _ in range(2):
+            m(x, ei, out)
+        q = G.gnn_profile_read(m.handle)
+        assert q["n_calls"] == 2
+        for k in PER_ITER:
+            assert q[k]["launches"] == (2 if T == 1 else 0), k
+        for k in ONCE + ("total",):
+            assert q[k]["launches"] == 0, k
+        G.gnn_profile_enable(m.handle, True)
+        m(x, ei, out)
+        p = G.gnn_profile_read(m.handle)
+        assert p["total"]["launches"] == 1 and p["classifier"]["launches"] == 1
+        for k in PER_ITER:
+            assert p[k]["launches"] == T, k
+    finally:
+        m.close()
