@@ -637,6 +637,10 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "copies": 3}))
         return
+    if args.f16_weights and (args.workload != "full_bf16" or args.literal or args.fp32_mfma):
+        print("--f16-weights needs --workload full_bf16 on the regrouped kernels (no --literal, "
+              "no --fp32-mfma)", file=sys.stderr)
+        sys.exit(2)
     if args.gpus != 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(events are independent: one process per GPU serves them). Use --gpus 1.",
@@ -670,9 +674,6 @@ def main():
     w = I.make_weights(3, H, 1, cfg.weight_seed)
     bf16 = cfg.dtype == "bf16"
     dtype = G.GNN_BF16 if bf16 else G.GNN_FP32
-    if args.f16_weights and not (bf16 and not args.literal and not args.fp32_mfma):
-        print("--f16-weights needs the bf16 workload on the regrouped kernels", file=sys.stderr)
-        sys.exit(2)
     flags = (G.GNN_LITERAL_GATHER if args.literal else 0) | \
         (G.GNN_FP32_MFMA if args.fp32_mfma else 0) | \
         (G.GNN_F16_WEIGHTS if args.f16_weights else 0)

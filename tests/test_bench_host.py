@@ -104,3 +104,12 @@ def test_read_write_splits_add_up_to_the_byte_counts():
         assert r + w == pytest.approx(bench.node_update_bytes(N, H, s, T))
         r, w = bench.aggregate_rw(N, E, H, s, N_SRC)
         assert r + w == pytest.approx(bench.aggregate_bytes(N, E, H, s, N_SRC))
+
+
+@pytest.mark.parametrize("extra", [["--workload", "full"], ["--workload", "full_bf16", "--literal"]])
+def test_f16_weights_needs_the_regrouped_bf16_workload(extra):
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--f16-weights", *extra],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "--f16-weights needs" in r.stderr
+    assert r.stdout == ""
