@@ -99,6 +99,14 @@ def node_update_rw(N, H, s=4, T=1):
     return (N * 3 * H * s, N * 2 * H * proj_bytes(s) + N * H * s * (T - 1) / T)
 
 
+def node_update_sampled_rw(N, H, s=4, T=1):
+    """(read, written) bytes of the node-update launch the sampled profiler
+    times, that of iteration T // 2 (0-based): it stores h unless it is the
+    last of the T iterations."""
+    writes_h = T // 2 != T - 1
+    return (N * 3 * H * s, N * 2 * H * proj_bytes(s) + (N * H * s if writes_h else 0))
+
+
 def aggregate_rw(N, E, H, s, n_src):
     """aggregate_bytes after the fused edge update, split into (read, written)."""
     return (E * H * s + E * 4 + 2.0 * (N + 1) * 4, N * H * s + (N - n_src) * H * s)
@@ -300,7 +308,10 @@ def f16w_rooflines(roof, roof_node):
 
 def rooflines(prof, N, E, H, T, bf16, split, factored, n_src, traffic, ceil=None):
     """Edge-update (dominant), node-update and aggregation rooflines from the
-    library's per-stage HIP-event times over the timed region."""
+    library's per-stage HIP-event times over the timed region (the sampled
+    profiler: one launch of each per event, that of iteration T // 2).  The
+    events bracket the dispatch, so each launch reads about 4 us above the
+    kernel's own duration in a kernel trace."""
     act_bytes = 2 if bf16 else 4
     eu = prof["edge_update"]
     eu_ms = eu["ms"] / max(eu["launches"], 1)
@@ -343,7 +354,8 @@ def rooflines(prof, N, E, H, T, bf16, split, factored, n_src, traffic, ceil=None
         if pr:
             pr["bytes"] = "counters" if traffic else "algorithmic"
             roof["practical"] = pr
-        nb = node_update_bytes(N, H, act_bytes, T)
+        # the sampled launch (iteration T // 2), not the average over T
+        nb = sum(node_update_sampled_rw(N, H, act_bytes, T))
         nu_gbs = nb / (nu_ms / 1000.0) / 1e9
         nu_mfma = mf["node_update"] / (nu_ms / 1000.0) / 1e12
         roof_node = {"kernel": ("node_split<4,false,1,bf16> (hi/lo bf16 weights streamed "
@@ -357,7 +369,7 @@ def rooflines(prof, N, E, H, T, bf16, split, factored, n_src, traffic, ceil=None
                               "executed_tflop_per_launch": mf["node_update"] / 1e12,
                               "achieved": round(nu_mfma, 1), "peak": PEAK_TFLOPS["fp16"],
                               "unit": "TFLOP/s", "frac": round(nu_mfma / PEAK_TFLOPS["fp16"], 4)}}
-        pr = practical(node_update_rw(N, H, act_bytes, T), nu_ms / 1000.0, ceil)
+        pr = practical(node_update_sampled_rw(N, H, act_bytes, T), nu_ms / 1000.0, ceil)
         if pr:
             roof_node["practical"] = pr
     else:

@@ -113,3 +113,14 @@ def test_f16_weights_needs_the_regrouped_bf16_workload(extra):
     assert r.returncode == 2
     assert "--f16-weights needs" in r.stderr
     assert r.stdout == ""
+
+
+def test_sampled_node_update_launch_bytes():
+    # the profiler times iteration T // 2 = 4 of 8, which stores h: reads h,
+    # agg_in, agg_out, writes the projection row and h
+    r, w = bench.node_update_sampled_rw(N, H, 4, T)
+    assert (r, w) == (N * 3 * 512, N * (1024 + 512))
+    # T = 1 and T = 2: the sampled launch is the last one and stores no h
+    assert bench.node_update_sampled_rw(N, H, 4, 1)[1] == N * 1024
+    assert bench.node_update_sampled_rw(N, H, 4, 2)[1] == N * 1024
+    assert bench.node_update_sampled_rw(N, H, 2, 3)[1] == N * (512 + 256)
