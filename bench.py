@@ -835,8 +835,10 @@ def main():
             "weights": "GNN_F16_WEIGHTS: each weight one fp16 number times a power of two (one "
                        "fp16 product per weight); activations bf16 in HBM, rounded to bf16 "
                        "where they feed a product and converted exactly to fp16",
-            "note": "the bf16 model with the other 16-bit weight format; timed like the main "
-                    "leg, after the bf16 leg; not part of value"}
+            "note": "the bf16 model with the other 16-bit weight format; the edge encoder "
+                    "runs inside the first edge update's kernel (its three weight matrices "
+                    "fit in LDS together; stages_ms_per_event counts it there); timed like the "
+                    "main leg, after the bf16 leg; not part of value"}
         del x, ei, out
         torch.cuda.empty_cache()
         rec["filter"] = bench_filter(G, I, cfg)

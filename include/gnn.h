@@ -90,7 +90,12 @@ extern "C" {
                                    fp16 range).  Needs every LayerNorm output
                                    bound (as above) <= 2^15 and every scaled
                                    weight inside the fp16 range; otherwise
-                                   gnn_create fails with GNN_E_UNSUPPORTED. */
+                                   gnn_create fails with GNN_E_UNSUPPORTED.
+                                   With T >= 1 the edge encoder then runs in
+                                   the first edge update's kernel (its output
+                                   stays on chip; the profiler counts it in
+                                   GNN_STAGE_EDGE_UPDATE), except in
+                                   gnn_debug_stages. */
 
 typedef struct gnn_dims {
   uint32_t struct_size;     /* = sizeof(gnn_dims) (ABI versioning)              */

@@ -324,6 +324,10 @@ struct FactDev {
   std::vector<float> s1_em, s2_em, s1_nm, s2_nm;
   float row_bound = 0.f;  // bound of any h or e entry (LayerNorm/ReLU outputs)
   int grid_enc = 0, grid_upd = 0, grid_cls = 0, grid_node = 0;  // persistent grids
+  // fp16 weights: the first update's W_e records with e0 taken from the
+  // accumulators (the edge encoder then runs inside that update)
+  const void *we_em0_acc = nullptr;
+  int grid_encupd = 0;
 };
 
 struct gnn_handle {
@@ -955,16 +959,20 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
       return fd.split ? launch_edge_split(mode, H, ea, grid, fd.prec, stream)
                       : launch_edge_f32(mode, H, ea, grid, stream);
     };
-    {
-      EdgeArgs ea = edge_args(w.pa, hd->edge_enc);
-      ea.e_out = (float *)w.e;
-      if (fd.split) {
-        ea.w2 = (const float *)fd.w2_ee;
-        ea.s1 = fd.s1_ee;
-        ea.s2 = fd.s2_ee;
-      }
+    // With fp16 weights the edge encoder runs inside the first update, so
+    // that e0 never goes to HBM and back (not for gnn_debug_stages, which
+    // copies e0 out when stop_iter is 0 and runs the two kernels apart).
+    const bool enc_in_upd = fd.prec == 2 && fused && T >= 1 && ro.stop_iter < 0;
+    EdgeArgs enc_a = edge_args(w.pa, hd->edge_enc);
+    enc_a.e_out = (float *)w.e;
+    if (fd.split) {
+      enc_a.w2 = (const float *)fd.w2_ee;
+      enc_a.s1 = fd.s1_ee;
+      enc_a.s2 = fd.s2_ee;
+    }
+    if (!enc_in_upd) {
       st.begin();
-      HIP_TRY(launch_edge(EdgeMode::Enc, ea, fd.grid_enc));
+      HIP_TRY(launch_edge(EdgeMode::Enc, enc_a, fd.grid_enc));
       st.end(GNN_STAGE_EDGE_ENC);
     }
     for (int t = 0; t < T; ++t) {
@@ -982,8 +990,24 @@ int run(gnn_handle *hd, const float *x, const int32_t *ei, int64_t N, int64_t E,
         ea.agg_out = w.aout;
         ea.agg_part = w.part;
       }
+      EdgeMode mode = fused ? EdgeMode::UpdAgg : EdgeMode::Upd;
+      int grid = fd.grid_upd;
+      if (t == 0 && enc_in_upd) {
+        ea.enc.P = enc_a.P;
+        ea.enc.w2 = enc_a.w2;
+        ea.enc.g1 = enc_a.g1;
+        ea.enc.beta1 = enc_a.beta1;
+        ea.enc.b2 = enc_a.b2;
+        ea.enc.g2 = enc_a.g2;
+        ea.enc.beta2 = enc_a.beta2;
+        ea.enc.s1 = enc_a.s1;
+        ea.enc.s2 = enc_a.s2;
+        ea.we = (const float *)fd.we_em0_acc;  // e0 from the accumulators
+        mode = EdgeMode::EncUpdAgg;
+        grid = fd.grid_encupd;
+      }
       st.begin(t == T / 2);
-      HIP_TRY(launch_edge(fused ? EdgeMode::UpdAgg : EdgeMode::Upd, ea, fd.grid_upd));
+      HIP_TRY(launch_edge(mode, ea, grid));
       st.end(GNN_STAGE_EDGE_UPDATE);
       st.begin(t == T / 2);
       if (fused)
@@ -1272,7 +1296,7 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
   std::vector<MlpOff> o_em(S), o_nm(S);
   const bool factored = !(d.flags & GNN_LITERAL_GATHER);
   const int T = d.n_iters;
-  size_t o_we_cls = 0, o_enc_stream = 0, o_w2_ee = 0;
+  size_t o_we_cls = 0, o_enc_stream = 0, o_w2_ee = 0, o_we_em0_acc = 0;
   std::vector<size_t> o_we_em(S), o_upd_stream(T), o_w2_em(S);
   bool split = false;
   FactDev fdh;  // scales of the split path (pointers are fixed up below)
@@ -1382,6 +1406,7 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
       }
       o_we_cls = add16(rec(c0, 2 * H, H, 0, fdh.s1_cls));
       o_w2_ee = add16(rec(b1, 0, H, -1, fdh.s2_ee));
+      if (f16w) o_we_em0_acc = add16(rec(e0s[0], 2 * H, H, -1, fdh.s1_em[0]));
       auto scale_of = [&](const BlobLayer &L) {
         if (&L == &c0) return fdh.s1_cls;
         for (int s = 0; s < S; ++s)
@@ -1522,6 +1547,10 @@ gnn_handle *gnn_create(const float *weights, const gnn_dims *dims) {
       fd.grid_enc = edge_split_grid(EdgeMode::Enc, H, fd.prec, n_cu);
       fd.grid_upd = edge_split_grid(EdgeMode::UpdAgg, H, fd.prec, n_cu);
       fd.grid_cls = edge_split_grid(EdgeMode::Cls, H, fd.prec, n_cu);
+      if (f16w) {
+        fd.we_em0_acc = base + o_we_em0_acc;
+        fd.grid_encupd = edge_split_grid(EdgeMode::EncUpdAgg, H, fd.prec, n_cu);
+      }
     } else {
       const int kg = H / 8;  // k-groups of one H-wide operand; 8 per chunk
       fd.enc_chunks = (kg + 4 * kg) / 8;

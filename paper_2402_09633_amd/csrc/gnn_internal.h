@@ -127,7 +127,9 @@ struct NodeArgs {
 // UpdAgg: the edge update that also sums its output rows per source node
 // (split kernels, fp32 or bf16 rows).  It needs the rows in source order:
 // every run of equal src_idx is one node's complete out-edge list.
-enum class EdgeMode : int { Enc = 0, Upd = 1, Cls = 2, UpdAgg = 3 };
+// EncUpdAgg (fp16 weights only): the edge encoder and the first UpdAgg in
+// one pass, e0 handed from one to the other in registers.
+enum class EdgeMode : int { Enc = 0, Upd = 1, Cls = 2, UpdAgg = 3, EncUpdAgg = 4 };
 
 struct EdgeArgs {
   int64_t n_rows = 0;
@@ -153,6 +155,14 @@ struct EdgeArgs {
   // run, continued in the next), H fp32 each, for launch_segsum_fused.
   void *agg_out = nullptr;
   float *agg_part = nullptr;
+  // EncUpdAgg: the edge encoder's projections, W2 records (B operand from
+  // the accumulators), LayerNorm parameters and first-layer / W2 scales.
+  // The update's W_e records (`we`) then read e0 from the accumulators too.
+  struct {
+    const float *P = nullptr, *w2 = nullptr;
+    const float *g1 = nullptr, *beta1 = nullptr, *b2 = nullptr, *g2 = nullptr, *beta2 = nullptr;
+    float s1 = 1.f, s2 = 1.f;
+  } enc;
 };
 
 hipError_t launch_node_f32(bool enc, int hidden, const NodeArgs &a, int grid,
@@ -174,7 +184,7 @@ hipError_t launch_node_split(bool enc, int hidden, const NodeArgs &a, int grid, 
 int node_split_chunks(bool enc, int hidden, int nproj, int prec);
 hipError_t launch_edge_split(EdgeMode mode, int hidden, const EdgeArgs &a, int grid, int prec,
                              hipStream_t stream);
-int edge_split_grid(EdgeMode mode, int hidden, int prec, int n_cu);
+int edge_split_grid(EdgeMode mode, int hidden, int prec, int n_cu);  // 0: no such kernel
 
 // Deterministic CSR segmented sums of the edge rows `e` ([n_edges][H]):
 // agg_in[v] = sum over p in [rp_in[v], rp_in[v+1]) of e[perm_in[p]], in

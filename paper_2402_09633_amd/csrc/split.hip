@@ -651,14 +651,21 @@ __global__ __launch_bounds__((64 * edge_waves<PREC, MODE>())) void edge_split(Ed
   using act_t = typename std::conditional<PREC == SPLIT, float, __bf16>::type;  // aggregates
   // edge rows: fp32, bf16, or bf16 values in fp16 encoding (F16W)
   using et_t = typename std::conditional<PREC == F16W, _Float16, act_t>::type;
-  constexpr bool HAS_E = MODE != (int)EdgeMode::Enc;
+  // ENC_UPD: the edge encoder, then the first update of the edges it
+  // encoded, each unit's e0 kept in registers between the two (fp16
+  // weights: their three H x H matrices fit in LDS together).
+  constexpr bool ENC_UPD = MODE == (int)EdgeMode::EncUpdAgg;
+  constexpr bool HAS_E = MODE != (int)EdgeMode::Enc && !ENC_UPD;  // e rows read from HBM
+  constexpr bool HAS_WE = MODE != (int)EdgeMode::Enc;             // a W_e product
   constexpr bool HAS_L2 = MODE != (int)EdgeMode::Cls;
-  constexpr bool FUSE = MODE == (int)EdgeMode::UpdAgg;
+  constexpr bool FUSE = MODE == (int)EdgeMode::UpdAgg || ENC_UPD;
   // The update always sums its rows per source here (UpdAgg); the plain
   // update is the fp32-matrix-core kernel's (factored.hip).
   static_assert(MODE != (int)EdgeMode::Upd, "split kernels have no plain update");
-  __shared__ h8 lds[(HAS_E ? NR : 0) + (HAS_L2 ? NR : 0)];
+  static_assert(!ENC_UPD || PREC == F16W, "the encoder runs inside the update with fp16 weights only");
+  __shared__ h8 lds[(HAS_WE ? NR : 0) + (HAS_L2 ? NR : 0) + (ENC_UPD ? NR : 0)];
   __shared__ float prm[6 * H];  // s1 b1, gamma1, beta1, s2 b2, gamma2, beta2
+  __shared__ float prm_enc[ENC_UPD ? 6 * H : 1];  // the same for the encoder
   const int lane = threadIdx.x & 63, hh = lane >> 5, n = lane & 31;
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
   const int wv = threadIdx.x >> 6;
@@ -717,13 +724,15 @@ __global__ __launch_bounds__((64 * edge_waves<PREC, MODE>())) void edge_split(Ed
   int64_t u = unit_at(0);
   if (u >= 0) {
     load_idx(u);
-    if constexpr (FUSE) load_e(row_of(u));
+    if constexpr (FUSE && HAS_E) load_e(row_of(u));
   }
   h8 *lw_e = lds;
-  h8 *lw_2 = lds + (HAS_E ? NR : 0);
+  h8 *lw_2 = lds + (HAS_WE ? NR : 0);
+  h8 *lw_2enc = lw_2 + NR;  // ENC_UPD: the encoder's W2
   for (int i = threadIdx.x; i < NR; i += 64 * EW) {
-    if constexpr (HAS_E) lw_e[i] = ((const h8 *)a.we)[i];
+    if constexpr (HAS_WE) lw_e[i] = ((const h8 *)a.we)[i];
     if constexpr (HAS_L2) lw_2[i] = ((const h8 *)a.w2)[i];
+    if constexpr (ENC_UPD) lw_2enc[i] = ((const h8 *)a.enc.w2)[i];
   }
   for (int i = threadIdx.x; i < H; i += 64 * EW) {
     prm[i] = 0.f;  // (layer-1 bias: inside the gathered P[src] rows)
@@ -735,6 +744,14 @@ __global__ __launch_bounds__((64 * edge_waves<PREC, MODE>())) void edge_split(Ed
       prm[5 * H + i] = a.beta2[i];
     } else {
       prm[3 * H + i] = ((const float *)a.w2)[i];  // classifier head row
+    }
+    if constexpr (ENC_UPD) {
+      prm_enc[i] = 0.f;
+      prm_enc[H + i] = a.enc.g1[i];
+      prm_enc[2 * H + i] = a.enc.beta1[i];
+      prm_enc[3 * H + i] = a.enc.b2[i] * a.enc.s2;
+      prm_enc[4 * H + i] = a.enc.g2[i];
+      prm_enc[5 * H + i] = a.enc.beta2[i];
     }
   }
   __syncthreads();
@@ -752,6 +769,7 @@ __global__ __launch_bounds__((64 * edge_waves<PREC, MODE>())) void edge_split(Ed
 
     // Layer 1 = s1 (P[src][0:H] + P[dst][H:2H] + W_e e) (+ s1 b1 in the LayerNorm).
     f16v acc[MB];
+    h8 xe[ENC_UPD ? G : 1];  // ENC_UPD: the unit's e0 as fp16 operands
     if constexpr (PREC == SPLIT) {
       const float *ps = a.P + s * 2 * H + 4 * hh;
       const float *pd = a.P + d * 2 * H + H + 4 * hh;
@@ -767,21 +785,68 @@ __global__ __launch_bounds__((64 * edge_waves<PREC, MODE>())) void edge_split(Ed
     } else {
       // fp16 rows in the order of store_block16: this lane's 16 values of
       // block mb are contiguous
-      const _Float16 *ps = (const _Float16 *)a.P + s * 2 * H + 16 * hh;
-      const _Float16 *pd = (const _Float16 *)a.P + d * 2 * H + H + 16 * hh;
+      // raw[mb] = this lane's 16 values of block mb of P[src][0:H] and of
+      // P[dst][H:2H]; sum16 adds them into acc[mb] in fp32
+      auto load16 = [&](const float *Pv, u4 (&raw)[MB][4]) {
+        const _Float16 *ps = (const _Float16 *)Pv + s * 2 * H + 16 * hh;
+        const _Float16 *pd = (const _Float16 *)Pv + d * 2 * H + H + 16 * hh;
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        const u4 s0 = *(const u4 *)(ps + 32 * mb), s1v = *(const u4 *)(ps + 32 * mb + 8);
-        const u4 d0 = *(const u4 *)(pd + 32 * mb), d1 = *(const u4 *)(pd + 32 * mb + 8);
+        for (int mb = 0; mb < MB; ++mb) {
+          raw[mb][0] = *(const u4 *)(ps + 32 * mb);
+          raw[mb][1] = *(const u4 *)(ps + 32 * mb + 8);
+          raw[mb][2] = *(const u4 *)(pd + 32 * mb);
+          raw[mb][3] = *(const u4 *)(pd + 32 * mb + 8);
+        }
+      };
+      auto sum16 = [&](const u4 (&raw)[MB][4], int mb) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const unsigned a0 = s0[j], b0 = d0[j], a1 = s1v[j], b1 = d1[j];
+          const unsigned a0 = raw[mb][0][j], b0 = raw[mb][2][j];
+          const unsigned a1 = raw[mb][1][j], b1 = raw[mb][3][j];
           acc[mb][2 * j] = add_f16<false>(a0, b0);
           acc[mb][2 * j + 1] = add_f16<true>(a0, b0);
           acc[mb][8 + 2 * j] = add_f16<false>(a1, b1);
           acc[mb][8 + 2 * j + 1] = add_f16<true>(a1, b1);
         }
+      };
+      u4 raw[MB][4];
+      if constexpr (ENC_UPD) {
+        // The encoder, e0 = LN/ReLU(W2 LN/ReLU(P_enc[src][0:H] +
+        // P_enc[dst][H:2H])), layer 2 untransposed: e0 ends in the layout
+        // of the next product's operand.
+        load16(a.enc.P, raw);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) sum16(raw, mb);
+        ln_relu_lds<MB, false>(acc, prm_enc, a.eps * a.enc.s1 * a.enc.s1, hh);
+        h8 xa[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) xa[g] = acc_to_h(acc_x<MB>(acc, g));
+        zero<MB>(acc);
+#pragma unroll
+        for (int g = 0; g < G; ++g) step_f<MB>(acc, lw_2enc + g * RP * MB * 64 + lane, xa[g]);
+        ln_relu_lds<MB>(acc, prm_enc + 3 * H, a.eps * a.enc.s2 * a.enc.s2, hh);
+        // The update's gathers.  Issued before that LayerNorm, to wait
+        // under it, they spill registers and cost more than they hide (full
+        // event 3.378 ms with the P[src] half there, 3.408 with both,
+        // against 3.363).
+        load16(a.P, raw);
+        // e0 rounded as the encoder stores it (bf16 values); block mb of
+        // the accumulators then takes the update's projections
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          xe[2 * mb] = acc_to_h(acc_x<MB>(acc, 2 * mb));
+          xe[2 * mb + 1] = acc_to_h(acc_x<MB>(acc, 2 * mb + 1));
+          sum16(raw, mb);
+        }
+      } else {
+        load16(a.P, raw);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) sum16(raw, mb);
       }
+    }
+    if constexpr (ENC_UPD) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) step_f<MB>(acc, lw_e + g * RP * MB * 64 + lane, xe[g]);
     }
     if constexpr (HAS_E) {
 #pragma unroll
@@ -923,7 +988,8 @@ __global__ __launch_bounds__((64 * edge_waves<PREC, MODE>())) void edge_split(Ed
           for (int p = 0; p < MB / 2; ++p) sum[p] = 0.f;
         }
       }
-      if (un >= 0) load_e(row_of(un));
+      if constexpr (HAS_E)
+        if (un >= 0) load_e(row_of(un));
       }
     }
     u = un;
@@ -959,6 +1025,12 @@ hipError_t edge_h(EdgeMode mode, const EdgeArgs &a, int grid, hipStream_t stream
     case EdgeMode::UpdAgg:
       if (!a.agg_out || !a.agg_part) return hipErrorInvalidValue;
       return edge_go<MB, PREC, 3>(a, grid, stream);
+    case EdgeMode::EncUpdAgg:
+      if constexpr (PREC == F16W) {
+        if (!a.agg_out || !a.agg_part || !a.enc.P || !a.enc.w2) return hipErrorInvalidValue;
+        return edge_go<MB, PREC, 4>(a, grid, stream);
+      }
+      return hipErrorInvalidValue;
   }
   return hipErrorInvalidValue;
 }
@@ -970,6 +1042,9 @@ const void *edge_fn_mb(EdgeMode mode) {
     case EdgeMode::Cls: return (const void *)edge_split<MB, 2, PREC>;
     case EdgeMode::Upd:  // not launched here (UpdAgg is)
     case EdgeMode::UpdAgg: return (const void *)edge_split<MB, 3, PREC>;
+    case EdgeMode::EncUpdAgg:
+      if constexpr (PREC == F16W) return (const void *)edge_split<MB, 4, PREC>;
+      return nullptr;
   }
   return (const void *)edge_split<MB, 3, PREC>;
 }
@@ -1025,10 +1100,11 @@ hipError_t launch_node_split(bool enc, int hidden, const NodeArgs &a, int grid, 
 int edge_split_grid(EdgeMode mode, int hidden, int prec, int n_cu) {
   const void *fn = prec == 2 ? edge_fn<F16W>(mode, hidden)
                              : prec == 1 ? edge_fn<BF16>(mode, hidden) : edge_fn<SPLIT>(mode, hidden);
-  const int m = mode == EdgeMode::Enc ? 0 : mode == EdgeMode::Cls ? 2 : 3;
+  if (!fn) return 0;  // (the fused encoder + update exists with fp16 weights only)
+  const int m = mode == EdgeMode::Enc ? 0 : mode == EdgeMode::Cls ? 2 : mode == EdgeMode::EncUpdAgg ? 4 : 3;
   auto waves = [&](auto pc) {
     constexpr int P = decltype(pc)::value;
-    return m == 0 ? edge_waves<P, 0>() : m == 2 ? edge_waves<P, 2>() : edge_waves<P, 3>();
+    return m == 0 ? edge_waves<P, 0>() : m == 2 ? edge_waves<P, 2>() : m == 4 ? edge_waves<P, 4>() : edge_waves<P, 3>();
   };
   const int threads = 64 * (prec == 2 ? waves(std::integral_constant<int, F16W>{})
                             : prec == 1 ? waves(std::integral_constant<int, BF16>{})

@@ -153,7 +153,7 @@ def test_full_bf16_scores_vs_stored_oracle(G, flags):
 
 @pytest.mark.parametrize("flags", BF16_PATHS)
 @pytest.mark.parametrize("H,T,S,noise", [(64, 2, 1, 0.0), (64, 2, 1, 0.3), (128, 3, 1, 0.3),
-                                         (64, 3, 3, 0.3), (128, 0, 1, 0.3)])
+                                         (64, 3, 3, 0.3), (128, 0, 1, 0.3), (128, 1, 1, 0.3)])
 def test_tiny_bf16_scores(G, oracle_mod, H, T, S, noise, flags):
     c = I.CONFIGS["tiny"]
     g = I.make_graph(c)
