@@ -50,9 +50,9 @@ TRAFFIC_SOURCES = {
 }
 # (path, source hash) -> (HBM bytes read, written) per edge-update launch on
 # the full event
-MEASURED_TRAFFIC = {("split", "0d0e0b302506faa5"): (1.137e9, 0.651e9),    # edge_split<4,3>
-                    ("bf16", "0d0e0b302506faa5"): (0.551e9, 0.342e9),     # edge_split<4,3,bf16>
-                    ("f16w", "0d0e0b302506faa5"): (0.593e9, 0.347e9)}     # edge_split<4,3,f16w>
+MEASURED_TRAFFIC = {("split", "b207f8ee01db6724"): (1.137e9, 0.651e9),    # edge_split<4,3>
+                    ("bf16", "b207f8ee01db6724"): (0.551e9, 0.342e9),     # edge_split<4,3,bf16>
+                    ("f16w", "b207f8ee01db6724"): (0.593e9, 0.347e9)}     # edge_split<4,3,f16w>
 
 
 def kernel_source_hash(path):
