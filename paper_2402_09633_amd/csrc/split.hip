@@ -784,9 +784,8 @@ __global__ __launch_bounds__((64 * edge_waves<PREC, MODE>())) void edge_split(Ed
         }
     } else {
       // fp16 rows in the order of store_block16: this lane's 16 values of
-      // block mb are contiguous
-      // raw[mb] = this lane's 16 values of block mb of P[src][0:H] and of
-      // P[dst][H:2H]; sum16 adds them into acc[mb] in fp32
+      // block mb are contiguous.  load16 fetches them from P[src][0:H] and
+      // P[dst][H:2H] into raw[mb]; sum16 adds the two into acc[mb] in fp32.
       auto load16 = [&](const float *Pv, u4 (&raw)[MB][4]) {
         const _Float16 *ps = (const _Float16 *)Pv + s * 2 * H + 16 * hh;
         const _Float16 *pd = (const _Float16 *)Pv + d * 2 * H + H + 16 * hh;
