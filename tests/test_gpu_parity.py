@@ -444,6 +444,39 @@ def test_hub_graph_long_segments(G, oracle_mod, flags):
     assert_logits_close(got, ref["logits"])
 
 
+@pytest.mark.parametrize("flags", BF16_PATHS)
+@pytest.mark.parametrize("H,n,e,seed", [(64, 50, 1, 0), (128, 50, 33, 2), (64, 1, 7, 4),
+                                        (128, 700, 129, 5)])
+def test_ragged_and_small_graphs_bf16(G, oracle_mod, H, n, e, seed, flags):
+    # the bf16 model's kernels (with fp16 weights the edge encoder runs inside
+    # the first edge update) on one edge, ragged last units and a self-loop
+    # graph of one node
+    x, ei = _tiny_random(seed, n, e, loops=(n == 1))
+    w = I.make_weights(3, H, 1, seed, affine_noise=0.3)
+    print(f"ragged bf16 H={H} n={n} e={e} flags={flags}", flush=True)
+    ref = oracle_mod.forward(w, x, ei, H, 2)
+    sc = run_model(G, w, G.make_dims(3, H, 2, dtype=G.GNN_BF16, flags=flags), x, ei, logits=False)
+    assert np.abs(sc - ref["scores"]).max() <= BF16_SCORE_ATOL
+
+
+@pytest.mark.parametrize("flags", BF16_PATHS)
+def test_hub_graph_long_segments_bf16(G, oracle_mod, flags):
+    # the hub graph of test_hub_graph_long_segments, H = 128, bf16 model
+    rng = np.random.default_rng(31)
+    n, e = 5000, 300_000
+    x = rng.normal(size=(n, 3)).astype(np.float32)
+    ei = rng.integers(0, n, size=(2, e)).astype(np.int32)
+    ei[1, rng.random(e) < 0.5] = 17
+    ei[0, rng.random(e) < 0.2] = 4999
+    w = I.make_weights(3, 128, 1, 31, affine_noise=0.2)
+    ref = oracle_mod.forward(w, x, ei, 128, 2)
+    sc = run_model(G, w, G.make_dims(3, 128, 2, dtype=G.GNN_BF16, flags=flags), x, ei,
+                   logits=False)
+    err = np.abs(sc - ref["scores"]).max()
+    print(f"hub bf16 flags={flags} max score error {err:.3e}", flush=True)
+    assert err <= BF16_SCORE_ATOL
+
+
 @pytest.mark.parametrize("flags", PATHS)
 def test_hidden64_many_tiles_per_workgroup(G, oracle_mod, flags):
     # 300k nodes: every persistent node workgroup walks several 256-node
