@@ -39,14 +39,15 @@ def _call(G, fn, handle, x, ei):
     return out.cpu().numpy()
 
 
-@pytest.mark.parametrize("dtype", [0, 1])
-def test_noalloc_equals_gnn_infer_two_calls_second_smaller(G, dtype):
+@pytest.mark.parametrize("dtype,flags", [(0, 0), (1, 0), (1, 8)])  # 8: fp16 weights
+def test_noalloc_equals_gnn_infer_two_calls_second_smaller(G, dtype, flags):
     c = I.CONFIGS["mid"]  # 50k hits, 329,756 edges: about 372 MB of fp32 workspace
     g = I.make_graph(c)
     w = I.make_weights(3, c.hidden, 1, c.weight_seed, affine_noise=0.1)
-    dims = G.make_dims(3, c.hidden, c.n_iters, dtype=dtype)
+    dims = G.make_dims(3, c.hidden, c.n_iters, dtype=dtype, flags=flags)
     events = [(dev(g.x), dev(g.edge_index)), _small_event(5, 3001, 8033)]
-    print(f"noalloc dtype={dtype}: events of {[e.shape[1] for _, e in events]} edges", flush=True)
+    print(f"noalloc dtype={dtype} flags={flags}: events of {[e.shape[1] for _, e in events]} edges",
+          flush=True)
     ref_model = G.Model(w, dims)
     m = G.Model(w, dims)  # used only through the no-allocation entry point
     try:
