@@ -50,9 +50,9 @@ TRAFFIC_SOURCES = {
 }
 # (path, source hash) -> (HBM bytes read, written) per edge-update launch on
 # the full event
-MEASURED_TRAFFIC = {("split", "306f3ecc6a16c2de"): (1.137e9, 0.651e9),    # edge_split<4,3>
-                    ("bf16", "306f3ecc6a16c2de"): (0.551e9, 0.342e9),     # edge_split<4,3,bf16>
-                    ("f16w", "306f3ecc6a16c2de"): (0.593e9, 0.347e9)}     # edge_split<4,3,f16w>
+MEASURED_TRAFFIC = {("split", "393e70c466c8f0c6"): (1.131e9, 0.651e9),    # edge_split<4,3>
+                    ("bf16", "393e70c466c8f0c6"): (0.551e9, 0.342e9),     # edge_split<4,3,bf16>
+                    ("f16w", "393e70c466c8f0c6"): (0.593e9, 0.347e9)}     # edge_split<4,3,f16w>
 
 
 def kernel_source_hash(path):
